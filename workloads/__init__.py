@@ -1,0 +1,174 @@
+"""Seeded synthetic inputs for single-query (L_Q = 1) decode attention.
+
+This module is shared by the fp64 oracle tests, the GPU parity tests and the
+benchmark.  It holds none of the attention arithmetic: it only draws seeded
+normal variates and rounds them to bf16 bit patterns, so that the oracle and
+the HIP path see exactly the same input bits.
+
+Workloads follow the shapes the paper measures (shape tuple
+(Batch, L_Q, L_K, H_Q, H_KV, D), bf16; Section 5.1 and Table 1) plus the
+MI355X workload set built around them:
+
+  1  MQA decode            B=1,  H_Q=8,  H_KV=1, L_K=128
+  2  Llama-3.1-70B GQA     B=1,  H_Q=64, H_KV=8, L_K in {128,256,384,512}
+  3  pure-MQA low-tile     B in {1,2,4} x L_K in {64,128,256,512}, H_Q=32, H_KV=1
+  4  varlen batched GQA    B=16, H_Q=32, H_KV=4, L_b ~ U[32,512] (cu_seqlens)
+  5  high-load             B=32, H_Q=64, H_KV=8, L_K=8192
+
+Recipe: NumPy PCG64 with seed = 1000 * config_id + shape_idx, draw order
+(varlen lengths) -> Q -> K -> V, each standard normal in float32, rounded to
+bf16 by round-to-nearest-even.  head_dim is 128 throughout.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+HEAD_DIM = 128
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (round-to-nearest-even); return uint16 bits.
+
+    Finite inputs only (the generators never produce NaN or Inf)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+@dataclass(frozen=True)
+class Shape:
+    """One decode-attention problem size (L_Q = 1)."""
+
+    config_id: int
+    shape_idx: int
+    B: int
+    H_Q: int
+    H_KV: int
+    L_K: int                      # fixed length, or max length when varlen
+    D: int = HEAD_DIM
+    varlen: bool = False
+    name: str = ""
+
+    @property
+    def seed(self) -> int:
+        return 1000 * self.config_id + self.shape_idx
+
+    @property
+    def group(self) -> int:
+        return self.H_Q // self.H_KV
+
+
+@dataclass
+class Inputs:
+    """bf16 bit patterns (uint16) of one problem, laid out as the C-ABI expects.
+
+    q:  [B, H_Q, D]
+    k,v: [B, L_K, H_KV, D] (fixed) or [sum L_b, H_KV, D] (varlen)
+    cu_seqlens_k: None (fixed) or int32 [B+1] prefix sums of the lengths
+    lengths: int64 [B], the per-sequence key counts in either layout
+    """
+
+    shape: Shape
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    lengths: np.ndarray
+    cu_seqlens_k: Optional[np.ndarray] = None
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def total_keys(self) -> int:
+        return int(self.lengths.sum())
+
+
+def _normal_bf16(rng: np.random.Generator, shape: Sequence[int], chunk_elems: int = 1 << 24) -> np.ndarray:
+    """Draw float32 N(0,1) of `shape` from `rng` and round to bf16 bits.
+
+    Drawn in consecutive chunks so the float32 staging stays small for the
+    1 GiB high-load KV cache; the stream of variates is the same as a single
+    draw of the whole array."""
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    pos = 0
+    while pos < n:
+        m = min(chunk_elems, n - pos)
+        out[pos:pos + m] = f32_to_bf16_bits(rng.standard_normal(m, dtype=np.float32))
+        pos += m
+    return out.reshape(shape)
+
+
+def make_inputs(shape: Shape, seed: Optional[int] = None,
+                lengths: Optional[Sequence[int]] = None) -> Inputs:
+    """Draw the inputs of `shape` from seed (default: the shape's own seed).
+
+    For varlen shapes the per-sequence lengths are drawn first from the same
+    stream as U[32, L_K] inclusive, unless `lengths` is given."""
+    rng = np.random.default_rng(shape.seed if seed is None else seed)
+    B, H_Q, H_KV, D = shape.B, shape.H_Q, shape.H_KV, shape.D
+    if shape.varlen:
+        if lengths is None:
+            lens = rng.integers(32, shape.L_K + 1, size=B).astype(np.int64)
+        else:
+            lens = np.asarray(lengths, dtype=np.int64)
+            assert lens.shape == (B,)
+        cu = np.zeros(B + 1, dtype=np.int32)
+        cu[1:] = np.cumsum(lens)
+        q = _normal_bf16(rng, (B, H_Q, D))
+        k = _normal_bf16(rng, (int(cu[-1]), H_KV, D))
+        v = _normal_bf16(rng, (int(cu[-1]), H_KV, D))
+        return Inputs(shape, q, k, v, lens, cu)
+    lens = np.full(B, shape.L_K, dtype=np.int64)
+    q = _normal_bf16(rng, (B, H_Q, D))
+    k = _normal_bf16(rng, (B, shape.L_K, H_KV, D))
+    v = _normal_bf16(rng, (B, shape.L_K, H_KV, D))
+    return Inputs(shape, q, k, v, lens, None)
+
+
+def custom_shape(B: int, H_Q: int, H_KV: int, L_K: int, D: int = HEAD_DIM,
+                 varlen: bool = False, name: str = "custom") -> Shape:
+    """A shape outside the fixed workload set (edge cases, tests)."""
+    return Shape(0, 0, B, H_Q, H_KV, L_K, D, varlen, name)
+
+
+def config_shapes(config_id: int) -> List[Shape]:
+    """The shapes of one workload, in shape_idx order."""
+    if config_id == 1:
+        return [Shape(1, 0, 1, 8, 1, 128, name="mqa_b1_h8_l128")]
+    if config_id == 2:
+        return [Shape(2, i, 1, 64, 8, L, name=f"llama70b_gqa_b1_l{L}")
+                for i, L in enumerate((128, 256, 384, 512))]
+    if config_id == 3:
+        out = []
+        idx = 0
+        for B in (1, 2, 4):
+            for L in (64, 128, 256, 512):
+                out.append(Shape(3, idx, B, 32, 1, L, name=f"mqa32_b{B}_l{L}"))
+                idx += 1
+        return out
+    if config_id == 4:
+        return [Shape(4, 0, 16, 32, 4, 512, varlen=True, name="varlen_gqa_b16_h32_kv4")]
+    if config_id == 5:
+        return [Shape(5, 0, 32, 64, 8, 8192, name="highload_b32_h64_kv8_l8192")]
+    raise ValueError(f"unknown config {config_id}")
+
+
+ALL_CONFIG_IDS = (1, 2, 3, 4, 5)
+
+
+def all_shapes() -> List[Shape]:
+    return [s for c in ALL_CONFIG_IDS for s in config_shapes(c)]
+
+
+def algorithmic_bytes(B: int, H_Q: int, H_KV: int, total_keys: int, D: int = HEAD_DIM,
+                      varlen: bool = False) -> int:
+    """Bytes the method must move once: K and V once, Q read, O written (bf16),
+    plus the cu_seqlens metadata for the varlen layout."""
+    kv = 2 * total_keys * H_KV * D * 2
+    qo = 2 * B * H_Q * D * 2
+    meta = 4 * (B + 1) if varlen else 0
+    return kv + qo + meta
