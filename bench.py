@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+One step is one call of the whole path -- plan (host), split-partial kernel
+with the in-kernel chunk merge -- over the Llama-3.1-70B-shaped GQA decode
+batch (B=1, H_Q=64, H_KV=8, D=128, L_K=512, bf16, synthetic N(0,1) inputs
+already resident in HBM).  K steps are captured in one HIP graph and
+replayed; HIP events on the replay stream bracket the timed replays (the
+paper times with CUDA-graph replay and A/B interleaving, Section 5).
+
+Printed: one JSON line.  `value` is microseconds per call for the planned
+num_splits (lower is better), next to num_splits=1, a split sweep, the
+cold-cache time, the high-load shape (B=32, H_Q=64, H_KV=8, L_K=8192, 1 GiB
+of KV) against the HBM roofline, and the fp64 oracle timed on the host cores
+(a reported baseline only).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode-attention µs/call + achieved HBM GB/s (% of peak), heuristic vs num_splits=1"
+HBM_PEAK_GBS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_00028_amd", "csrc", "decode_attn.hip")
+SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
+HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200, help="calls per timed replay")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--rounds", type=int, default=7, help="interleaved timed replays per variant")
+    ap.add_argument("--highload-steps", type=int, default=20)
+    ap.add_argument("--no-highload", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--full-sweep", action="store_true", help="sweep num_splits 1..64 on every config-2 length")
+    return ap.parse_args()
+
+
+class Variant:
+    """K calls of one launch configuration captured in a HIP graph."""
+
+    def __init__(self, name, da, torch, q, k, v, L, s, pack, steps, kv_copies=None):
+        self.name = name
+        B, H_Q, D = q.shape
+        H_KV = k.shape[2]
+        self.plan = da.da_make_plan(B, H_Q, H_KV, L, D, s, pack)
+        nbytes = da.da_workspace_bytes(B, H_Q, D, self.plan.num_splits)
+        self.ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device="cuda") if nbytes else None
+        self.out = torch.empty((B, H_Q, D), dtype=torch.bfloat16, device="cuda")
+        self.steps = steps
+        s_res, p_res = self.plan.num_splits, self.plan.pack_gqa
+        kvs = kv_copies if kv_copies else [(k, v)]
+
+        def call(i):
+            kk, vv = kvs[i % len(kvs)]
+            da.da_decode_attn(q, kk, vv, out=self.out, num_splits=s_res, pack_gqa=p_res, workspace=self.ws)
+
+        self.call = call
+        for i in range(3):
+            call(i)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            for i in range(steps):
+                call(i)
+        self.graph.replay()
+        torch.cuda.synchronize()
+        self.times = []
+
+    def timed(self, torch) -> float:
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        self.graph.replay()
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1000.0 / self.steps
+        self.times.append(us)
+        return us
+
+    @property
+    def median(self) -> float:
+        return statistics.median(self.times)
+
+
+def interleave(torch, variants, rounds):
+    for _ in range(rounds):
+        for var in variants:
+            var.timed(torch)
+
+
+def algorithmic_bytes(B, H_Q, H_KV, L, D=128):
+    from workloads import algorithmic_bytes as ab
+    return ab(B, H_Q, H_KV, B * L, D)
+
+
+def traffic_for(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    try:
+        with open(PROFILE_TRAFFIC) as f:
+            t = json.load(f)
+        sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        if t.get("kernel_source_sha256") != sha:
+            return None
+        w = t["workloads"][workload]
+        return int(w["fetch_bytes"] + w["write_bytes"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(inp, seconds: float):
+    """The fp64 oracle as it stands, on the host cores, on repeated calls of
+    the same problem for about `seconds`."""
+    import numpy as np
+    from oracle import decode_attention
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    decode_attention(inp.q, inp.k, inp.v)
+    n = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        decode_attention(inp.q, inp.k, inp.v)
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(dt / n * 1e6, 2), "unit": "us/call", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} full calls of the benchmarked shape (fp64 NumPy, {seconds:.0f} s budget)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode kernel shards by "
+              f"(sequence, KV head) with no exchange, so no multi-GPU figure is produced.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2604_00028_amd as da
+    from workloads import config_shapes, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    cus, is950 = da.da_device_info()
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    # ---------------- headline: Llama-3.1-70B GQA decode, B=1, L_K=512
+    shapes = {s.L_K: s for s in config_shapes(2)}
+    sh = shapes[512]
+    inp = make_inputs(sh)
+    q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
+    K = args.steps
+    log(f"device cus={cus} gfx950={is950}; headline {sh.name}, {K} calls per replay")
+    for _ in range(args.warmup):
+        da.da_decode_attn(q, k, v)
+    torch.cuda.synchronize()
+    heur = Variant("heuristic", da, torch, q, k, v, sh.L_K, 0, -1, K)
+    base = Variant("s1", da, torch, q, k, v, sh.L_K, 1, 1, K)
+    sweep = [Variant(f"s{s}", da, torch, q, k, v, sh.L_K, s, 1, K) for s in SWEEP if s != 1]
+    unpacked = [Variant("s1_unpacked", da, torch, q, k, v, sh.L_K, 1, 0, K),
+                Variant("heur_unpacked", da, torch, q, k, v, sh.L_K, heur.plan.num_splits, 0, K)]
+    # cold cache: cycle through 256 distinct KV copies (512 MiB > L2 + MALL)
+    ncopy = 256
+    copies = [(torch.randn_like(k, dtype=torch.float32).to(torch.bfloat16),
+               torch.randn_like(v, dtype=torch.float32).to(torch.bfloat16)) for _ in range(ncopy)]
+    cold_h = Variant("cold_heuristic", da, torch, q, k, v, sh.L_K, 0, -1, K, kv_copies=copies)
+    cold_1 = Variant("cold_s1", da, torch, q, k, v, sh.L_K, 1, 1, K, kv_copies=copies)
+    log("timing headline variants")
+    interleave(torch, [heur, base] + sweep + unpacked + [cold_h, cold_1], args.rounds)
+    value = heur.median
+    s1 = base.median
+    sweep_us = {1: round(s1, 3)}
+    for var in sweep:
+        sweep_us[var.plan.num_splits] = round(var.median, 3)
+    best_s = min(sweep_us, key=sweep_us.get)
+    bytes_call = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
+    achieved = bytes_call / (value * 1e-6) / 1e9
+    q25, q75 = np.percentile(heur.times, [25, 75])
+    cold = {"heuristic": round(cold_h.median, 3), "s1": round(cold_1.median, 3),
+            "speedup_vs_s1": round(cold_1.median / cold_h.median, 3)}
+    del copies, cold_h, cold_1
+
+    # other config-2 lengths: heuristic vs s=1 and a few fixed splits
+    other = {}
+    for L in (128, 256, 384):
+        shL = shapes[L]
+        inL = make_inputs(shL)
+        qL, kL, vL = dev(inL.q), dev(inL.k), dev(inL.v)
+        log(f"timing L_K={L}")
+        hv = Variant("h", da, torch, qL, kL, vL, L, 0, -1, K)
+        bv = Variant("1", da, torch, qL, kL, vL, L, 1, 1, K)
+        sv = [Variant(str(x), da, torch, qL, kL, vL, L, x, 1, K) for x in (2, 4, 8, 16)]
+        interleave(torch, [hv, bv] + sv, args.rounds)
+        sw = {1: round(bv.median, 3), **{x.plan.num_splits: round(x.median, 3) for x in sv}}
+        other[L] = {"heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
+                    "s1_us": round(bv.median, 3), "speedup_vs_s1": round(bv.median / hv.median, 3),
+                    "best_fixed": min(sw, key=sw.get), "best_fixed_us": min(sw.values())}
+
+    # ---------------- high load: B=32, H_Q=64, H_KV=8, L_K=8192 (1 GiB of KV)
+    high = None
+    if not args.no_highload:
+        shh = config_shapes(5)[0]
+        log(f"generating {shh.name}")
+        inh = make_inputs(shh)
+        qh, kh, vh = dev(inh.q), dev(inh.k), dev(inh.v)
+        del inh
+        Kh = args.highload_steps
+        hh = Variant("h", da, torch, qh, kh, vh, shh.L_K, 0, -1, Kh)
+        hs = [Variant(str(x), da, torch, qh, kh, vh, shh.L_K, x, 1, Kh) for x in HIGHLOAD_SWEEP]
+        log("timing high-load variants")
+        interleave(torch, [hh] + hs, max(3, args.rounds // 2))
+        hsw = {x.plan.num_splits: round(x.median, 2) for x in hs}
+        hbytes = algorithmic_bytes(shh.B, shh.H_Q, shh.H_KV, shh.L_K)
+        hgbs = hbytes / (hh.median * 1e-6) / 1e9
+        hbest = min(hsw, key=hsw.get)
+        high = {"workload": shh.name, "us_per_call": round(hh.median, 2), "num_splits": hh.plan.num_splits,
+                "s1_us": hsw[1], "best_fixed": hbest, "best_fixed_us": hsw[hbest],
+                "vs_best_fixed": round(hh.median / hsw[hbest], 3), "sweep_us": hsw,
+                "algorithmic_bytes": hbytes,
+                "roofline": {"bound": "hbm", "achieved": round(hgbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(hgbs / HBM_PEAK_GBS, 4), "traffic": traffic_for(shh.name)}}
+        del qh, kh, vh, hh, hs
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "us/call",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(value / 1000.0, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": sh.name, "B": sh.B, "H_Q": sh.H_Q, "H_KV": sh.H_KV, "head_dim": sh.D,
+                   "L_K": sh.L_K, "num_splits": heur.plan.num_splits, "pack_gqa": heur.plan.pack_gqa,
+                   "grid_workgroups": heur.plan.grid, "num_cus": cus},
+        "s1_us": round(s1, 3),
+        "speedup_vs_s1": round(s1 / value, 3),
+        "iqr_us": [round(q25, 3), round(q75, 3)],
+        "best_fixed_splits": best_s,
+        "vs_best_fixed": round(value / sweep_us[best_s], 3),
+        "sweep_us": sweep_us,
+        "unpacked_us": {"s1": round(unpacked[0].median, 3),
+                        f"s{heur.plan.num_splits}": round(unpacked[1].median, 3)},
+        "cold_us": cold,
+        "other_lk": other,
+        "high_load": high,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(sh.name)},
+        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(inp, args.cpu_seconds),
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * decode_attn.h - split-KV single-query decode attention on MI355X (gfx950).
+ *
+ * The operation (paper: Sections 2.1, 2.2, 3.1, 5.1): one decode step
+ * (L_Q = 1) of softmax attention for Batch sequences, H_Q query heads that
+ * share H_KV key/value heads (MQA when H_KV = 1, GQA otherwise; query head h
+ * reads KV head h / (H_Q / H_KV)), head dimension D, over a KV cache of L_K
+ * keys per sequence.  The sequence dimension is cut into num_splits chunks;
+ * each chunk yields a partial softmax state (running max m, sum l and
+ * unnormalised output Otilde) and a log-sum-exp combine merges them.  The
+ * scheduling knobs (num_splits, pack_gqa, cu_margin) never change the
+ * mathematical result (Section 3.1), only rounding order.
+ *
+ * Conventions for every entry point:
+ *   - Tensors are dense, row-major, in device memory (hipMalloc'd or torch
+ *     CUDA tensors), and owned by the caller.  The library never allocates or
+ *     frees device memory and keeps no pointer after a call returns.
+ *   - bf16 tensors are passed as raw 16-bit storage (IEEE bfloat16 bits).
+ *   - Device pointers to bf16 data, partial outputs and the workspace must be
+ *     16-byte aligned; fp32 lse/m/l pointers 4-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Work is
+ *     enqueued asynchronously with no allocation, no host synchronisation and
+ *     no device-to-host read, so calls can be captured in a HIP graph.
+ *   - Return value 0 (DA_OK) or a negative da_status.  All argument checks
+ *     run before any HIP call, so a rejected call touches no device state.
+ *     Kernel faults surface at the caller's next synchronisation.
+ *     da_last_error() gives a message for the calling thread's last failure.
+ *   - Only D = 128 and only gfx950 devices are supported.
+ */
+#ifndef DECODE_ATTN_H
+#define DECODE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DA_HEAD_DIM 128
+#define DA_MAX_SPLITS 64
+
+typedef enum da_status {
+  DA_OK = 0,
+  DA_ERR_NULL = -1,        /* a required pointer is NULL */
+  DA_ERR_SHAPE = -2,       /* B, H_Q, H_KV <= 0, H_Q % H_KV != 0, L_K_max < 0, sizes too large */
+  DA_ERR_UNSUPPORTED = -3, /* D != 128, or the current device is not gfx950 */
+  DA_ERR_SPLITS = -4,      /* num_splits > DA_MAX_SPLITS */
+  DA_ERR_ALIGN = -5,       /* a pointer violates the alignment rules above */
+  DA_ERR_WORKSPACE = -6,   /* workspace missing or smaller than da_workspace_bytes() */
+  DA_ERR_HIP = -7,         /* a HIP runtime call failed (device query or launch) */
+  DA_ERR_ARG = -8          /* another invalid argument (pack_gqa, policy, cu_margin, ...) */
+} da_status;
+
+typedef enum da_policy {
+  DA_POLICY_MI355X = 0, /* CU-aware cost model over num_splits in [1, 64] (default) */
+  DA_POLICY_PAPER = 1   /* the paper's rule (Section 4): 128-key blocks, Batch*H_KV tiles;
+                           at most 3 blocks -> 1; 4 blocks -> 1 with >= 4 tiles, else 3;
+                           longer contexts fall through to the MI355X cost model */
+} da_policy;
+
+/* A launch plan: the scheduler metadata decided on the host before launch
+ * (paper Section 5.1, precomputed scheduler metadata with an explicit
+ * num_splits; Section 3.1, num_splits / pack_gqa / sm_margin). */
+typedef struct da_plan {
+  int32_t num_splits;     /* chunks per sequence, 1..64 */
+  int32_t pack_gqa;       /* 1: one workgroup serves all query heads of a KV head */
+  int32_t heads_per_tile; /* query heads one workgroup serves (H_Q/H_KV packed, capped at 32; 1 unpacked) */
+  int32_t tiles;          /* work tiles = B * H_Q / heads_per_tile (Section 2.1: Batch x H_KV when packed) */
+  int32_t grid;           /* workgroups launched = tiles * num_splits */
+  int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
+} da_plan;
+
+/* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
+ * policy that counts work tiles against the available compute units).
+ *   L_K_max  longest sequence in the batch (host-known, as with precomputed
+ *            scheduler metadata, Section 5.1)
+ *   num_cus  compute units to plan for; 0 = query the current device (one
+ *            HIP attribute query, cached per device); > 0 = no device access
+ *   cu_margin compute units to leave free (the paper's sm_margin, Section 3.1)
+ *   policy   da_policy
+ * Host-only integer/float arithmetic; deterministic for equal arguments. */
+int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
+                     int cu_margin, int policy, da_plan* out);
+
+/* Same as da_choose_splits with num_splits and/or pack_gqa forced
+ * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy).
+ * Fills every field of `out` for the resulting launch. */
+int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
+                 int num_cus, int cu_margin, int policy, da_plan* out);
+
+/* Bytes of workspace da_decode_attn needs for num_splits chunks: 0 when
+ * num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
+ * [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q] | arrival counters
+ * uint32 [B*H_Q].  The counter region must be zero before the first call
+ * that uses the workspace; every call leaves it zero again. */
+size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
+
+/* Cut points of sequence chunking: chunk i of a sequence of L keys is
+ * [cuts[i], cuts[i+1]) with cuts[i] = floor(i*L/num_splits) (balanced,
+ * key-granular; empty chunks when num_splits > L).  cuts has num_splits+1
+ * entries, host memory.  The kernels partition each sequence this way. */
+int da_split_bounds(int L, int num_splits, int32_t* cuts);
+
+/* Decode attention, O = softmax(scale * q K^T) V per (sequence, query head)
+ * (Section 2.1), computed in num_splits chunks per sequence and merged by
+ * log-sum-exp (Sections 2.2, 3.1, 5.3).
+ *   q            bf16 [B, H_Q, d]
+ *   k, v         bf16 [B, L_K_max, H_KV, d] when cu_seqlens_k == NULL;
+ *                bf16 [sum_b L_b, H_KV, d] otherwise; may be NULL when
+ *                L_K_max == 0 (no key is read)
+ *   cu_seqlens_k NULL (every sequence has L_K_max keys) or device int32
+ *                [B+1] prefix sums: sequence b is rows [cu[b], cu[b+1]),
+ *                cu[0] = 0, non-decreasing, each length <= L_K_max
+ *   out          bf16 [B, H_Q, d], normalised output
+ *   lse_out      NULL or fp32 [B, H_Q]: natural-log log-sum-exp of the
+ *                scaled scores (-inf for an empty sequence, whose O is 0)
+ *   softmax_scale <= 0 selects 1/sqrt(d)
+ *   num_splits   <= 0: chosen by da_choose_splits (policy MI355X); else 1..64
+ *   pack_gqa     -1: chosen by the policy; 0 or 1 forced
+ *   workspace    device memory of workspace_bytes >= da_workspace_bytes(B,
+ *                H_Q, d, s) for the resolved s (unused when s == 1).  Calls
+ *                that share a workspace must not overlap in time.
+ * One kernel launch.  With s > 1 the last workgroup of each tile to finish
+ * merges the s partial states in split order, so results are bit-identical
+ * across runs for a fixed (num_splits, pack_gqa). */
+int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
+                   void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
+                   float softmax_scale, int num_splits, int pack_gqa, void* workspace,
+                   size_t workspace_bytes, void* stream);
+
+/* The split step alone: the partial softmax state of every chunk (the
+ * per-chunk max, sum and unnormalised output the paper's final reduction
+ * merges; Sections 3.1, 5.3).  Same inputs as da_decode_attn; num_splits
+ * must be 1..64 and pack_gqa 0 or 1 (no policy here).
+ *   o_part fp32 [num_splits, B, H_Q, d]: sum_j exp(s_j - m_i) v_j over chunk i
+ *   m_part fp32 [num_splits, B, H_Q]:    max scaled score of chunk i (natural
+ *                                        log units), -inf for an empty chunk
+ *   l_part fp32 [num_splits, B, H_Q]:    sum_j exp(s_j - m_i), 0 when empty
+ * Chunks follow da_split_bounds.  Feeding the result to da_combine_splits
+ * gives the same output as da_decode_attn up to rounding. */
+int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
+                      float* o_part, float* m_part, float* l_part, int B, int H_Q, int H_KV,
+                      int L_K_max, int d, float softmax_scale, int num_splits, int pack_gqa,
+                      void* stream);
+
+/* Log-sum-exp merge of num_splits partial states (the final reduction of
+ * Sections 3.1 and 5.3): M = max_i m_i over non-empty chunks, w_i =
+ * exp(m_i - M) (0 when l_i == 0), O = sum_i w_i Otilde_i / sum_i w_i l_i,
+ * lse = M + ln(sum_i w_i l_i); summed in chunk order i = 0..s-1.
+ * A row with every chunk empty gives O = 0 and lse = -inf.
+ *   o_part, m_part, l_part as written by da_split_partials (any producer of
+ *   that format works, e.g. partial states gathered from other devices)
+ *   out bf16 [B, H_Q, d]; lse_out NULL or fp32 [B, H_Q].  One kernel launch. */
+int da_combine_splits(const float* o_part, const float* m_part, const float* l_part, void* out,
+                      float* lse_out, int num_splits, int B, int H_Q, int d, void* stream);
+
+/* Compute units of the current device (hipDeviceAttributeMultiprocessorCount,
+ * cached per device) and whether it is gfx950. */
+int da_device_info(int* num_cus, int* is_gfx950);
+
+/* Static text for a da_status code. */
+const char* da_strerror(int code);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char* da_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DECODE_ATTN_H */

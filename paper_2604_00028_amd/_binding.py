@@ -1,0 +1,276 @@
+"""ctypes binding of libdecode_attn.so: argument marshalling only.
+
+Every function has the name of the C entry point it calls.  torch supplies
+device memory (tensors), their data pointers and the current HIP stream;
+every step of the computation runs in the library's HIP kernels.  torch is
+imported before the library is loaded so that both resolve the same HIP
+runtime (libamdhip64.so.7).  A missing library raises; there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdecode_attn.so")
+HEAD_DIM = 128
+MAX_SPLITS = 64
+
+DA_OK = 0
+DA_ERR_NULL = -1
+DA_ERR_SHAPE = -2
+DA_ERR_UNSUPPORTED = -3
+DA_ERR_SPLITS = -4
+DA_ERR_ALIGN = -5
+DA_ERR_WORKSPACE = -6
+DA_ERR_HIP = -7
+DA_ERR_ARG = -8
+
+POLICY_MI355X = 0
+POLICY_PAPER = 1
+
+# Every symbol include/decode_attn.h declares.
+EXPORTS = (
+    "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
+    "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror", "da_last_error",
+)
+
+
+class DaPlan(ctypes.Structure):
+    _fields_ = [
+        ("num_splits", ctypes.c_int32),
+        ("pack_gqa", ctypes.c_int32),
+        ("heads_per_tile", ctypes.c_int32),
+        ("tiles", ctypes.c_int32),
+        ("grid", ctypes.c_int32),
+        ("num_cus", ctypes.c_int32),
+    ]
+
+    def as_dict(self) -> dict:
+        return {name: int(getattr(self, name)) for name, _ in self._fields_}
+
+
+class DecodeAttnError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{message} (code {code})")
+        self.code = code
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+_I = ctypes.c_int
+_P = ctypes.c_void_p
+_F = ctypes.c_float
+_Z = ctypes.c_size_t
+
+
+def _hip_runtimes_loaded() -> List[str]:
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64.so" in line:
+                    paths.add(line.split()[-1])
+    except OSError:
+        pass
+    return sorted(paths)
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2604_00028_amd.build` "
+                           "(there is no fallback implementation)")
+    lib = ctypes.CDLL(LIB_PATH)
+    runtimes = _hip_runtimes_loaded()
+    if len(runtimes) > 1:
+        raise RuntimeError(f"two HIP runtimes are loaded ({runtimes}); torch must be imported first")
+    lib.da_choose_splits.argtypes = [_I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(DaPlan)]
+    lib.da_choose_splits.restype = _I
+    lib.da_make_plan.argtypes = [_I, _I, _I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(DaPlan)]
+    lib.da_make_plan.restype = _I
+    lib.da_workspace_bytes.argtypes = [_I, _I, _I, _I]
+    lib.da_workspace_bytes.restype = _Z
+    lib.da_split_bounds.argtypes = [_I, _I, ctypes.POINTER(ctypes.c_int32)]
+    lib.da_split_bounds.restype = _I
+    lib.da_decode_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _I, _P, _Z, _P]
+    lib.da_decode_attn.restype = _I
+    lib.da_split_partials.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _I, _P]
+    lib.da_split_partials.restype = _I
+    lib.da_combine_splits.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _P]
+    lib.da_combine_splits.restype = _I
+    lib.da_device_info.argtypes = [ctypes.POINTER(_I), ctypes.POINTER(_I)]
+    lib.da_device_info.restype = _I
+    lib.da_strerror.argtypes = [_I]
+    lib.da_strerror.restype = ctypes.c_char_p
+    lib.da_last_error.argtypes = []
+    lib.da_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(rc: int) -> None:
+    if rc != DA_OK:
+        lib = load()
+        msg = (lib.da_last_error() or b"").decode() or lib.da_strerror(rc).decode()
+        raise DecodeAttnError(rc, msg)
+
+
+def da_strerror(code: int) -> str:
+    return load().da_strerror(code).decode()
+
+
+def da_last_error() -> str:
+    return (load().da_last_error() or b"").decode()
+
+
+def da_device_info() -> Tuple[int, bool]:
+    cus, is950 = _I(0), _I(0)
+    _check(load().da_device_info(ctypes.byref(cus), ctypes.byref(is950)))
+    return cus.value, bool(is950.value)
+
+
+def da_choose_splits(B: int, H_Q: int, H_KV: int, L_K_max: int, d: int = HEAD_DIM, num_cus: int = 0,
+                     cu_margin: int = 0, policy: int = POLICY_MI355X) -> DaPlan:
+    plan = DaPlan()
+    _check(load().da_choose_splits(B, H_Q, H_KV, L_K_max, d, num_cus, cu_margin, policy, ctypes.byref(plan)))
+    return plan
+
+
+def da_make_plan(B: int, H_Q: int, H_KV: int, L_K_max: int, d: int = HEAD_DIM, num_splits: int = 0,
+                 pack_gqa: int = -1, num_cus: int = 0, cu_margin: int = 0, policy: int = POLICY_MI355X) -> DaPlan:
+    plan = DaPlan()
+    _check(load().da_make_plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, num_cus, cu_margin, policy,
+                               ctypes.byref(plan)))
+    return plan
+
+
+def da_workspace_bytes(B: int, H_Q: int, d: int, num_splits: int) -> int:
+    return int(load().da_workspace_bytes(B, H_Q, d, num_splits))
+
+
+def da_split_bounds(L: int, num_splits: int) -> List[int]:
+    cuts = (ctypes.c_int32 * (num_splits + 1))() if num_splits >= 0 else None
+    _check(load().da_split_bounds(L, num_splits, cuts))
+    return list(cuts)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    # an empty tensor has no storage: NULL (the library reads nothing there)
+    return None if t is None or t.numel() == 0 else t.data_ptr()
+
+
+def _stream(dev: torch.device, stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream(dev).cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _shapes(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu: Optional[torch.Tensor],
+            L_K_max: Optional[int]) -> Tuple[int, int, int, int, int]:
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous bfloat16 CUDA tensor")
+    if k.shape != v.shape:
+        raise ValueError("k and v shapes differ")
+    B, H_Q, d = q.shape
+    if cu is None:
+        if k.dim() != 4 or k.shape[0] != B or k.shape[3] != d:
+            raise ValueError("k must be [B, L_K, H_KV, d]")
+        L = k.shape[1]
+        H_KV = k.shape[2]
+        if L_K_max is not None and L_K_max != L:
+            raise ValueError("L_K_max must equal k.shape[1] for the fixed layout")
+        L_K_max = L
+    else:
+        if cu.dtype != torch.int32 or not cu.is_contiguous() or cu.numel() != B + 1 or not cu.is_cuda:
+            raise ValueError("cu_seqlens_k must be a contiguous int32 CUDA tensor of B+1 entries")
+        if k.dim() != 3 or k.shape[2] != d:
+            raise ValueError("varlen k must be [sum L_b, H_KV, d]")
+        H_KV = k.shape[1]
+        if L_K_max is None:
+            raise ValueError("L_K_max (the host-known longest sequence) is required with cu_seqlens_k")
+    return B, H_Q, H_KV, int(L_K_max), d
+
+
+_workspaces: Dict[Tuple[int, int], torch.Tensor] = {}
+
+
+def workspace_for(dev: torch.device, stream_handle: int, nbytes: int) -> torch.Tensor:
+    """A zero-initialised workspace of at least nbytes, cached per (device,
+    stream).  The library leaves its arrival counters at zero after every
+    call, so the cached buffer stays valid for later calls on that stream."""
+    key = (dev.index if dev.index is not None else torch.cuda.current_device(), stream_handle)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        _workspaces[key] = ws
+    return ws
+
+
+def da_decode_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens_k: Optional[torch.Tensor] = None,
+                   out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None, *,
+                   L_K_max: Optional[int] = None, softmax_scale: float = 0.0, num_splits: int = 0,
+                   pack_gqa: int = -1, workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """O = softmax(scale q K^T) V for one decode step; returns `out`."""
+    B, H_Q, H_KV, L, d = _shapes(q, k, v, cu_seqlens_k, L_K_max)
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
+    s_handle = _stream(dev, stream)
+    if workspace is None:
+        plan = da_make_plan(B, H_Q, H_KV, L, d, num_splits, pack_gqa)
+        nbytes = da_workspace_bytes(B, H_Q, d, plan.num_splits)
+        if nbytes:
+            workspace = workspace_for(dev, s_handle, nbytes)
+    ws_ptr = _ptr(workspace)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().da_decode_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),
+                                 B, H_Q, H_KV, L, d, float(softmax_scale), int(num_splits), int(pack_gqa),
+                                 ws_ptr, ws_bytes, s_handle))
+    return out
+
+
+def da_split_partials(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                      cu_seqlens_k: Optional[torch.Tensor] = None, o_part: Optional[torch.Tensor] = None,
+                      m_part: Optional[torch.Tensor] = None, l_part: Optional[torch.Tensor] = None, *,
+                      num_splits: int, pack_gqa: int, L_K_max: Optional[int] = None,
+                      softmax_scale: float = 0.0, stream=None):
+    """Per-chunk partial states (o_part [s,B,H_Q,d], m_part, l_part [s,B,H_Q])."""
+    B, H_Q, H_KV, L, d = _shapes(q, k, v, cu_seqlens_k, L_K_max)
+    dev = q.device
+    if o_part is None:
+        o_part = torch.empty((num_splits, B, H_Q, d), dtype=torch.float32, device=dev)
+    if m_part is None:
+        m_part = torch.empty((num_splits, B, H_Q), dtype=torch.float32, device=dev)
+    if l_part is None:
+        l_part = torch.empty((num_splits, B, H_Q), dtype=torch.float32, device=dev)
+    _check(load().da_split_partials(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(o_part), _ptr(m_part),
+                                    _ptr(l_part), B, H_Q, H_KV, L, d, float(softmax_scale), int(num_splits),
+                                    int(pack_gqa), _stream(dev, stream)))
+    return o_part, m_part, l_part
+
+
+def da_combine_splits(o_part: torch.Tensor, m_part: torch.Tensor, l_part: torch.Tensor,
+                      out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None, *,
+                      stream=None) -> torch.Tensor:
+    """Log-sum-exp merge of partial states; returns `out` (bf16 [B,H_Q,d])."""
+    for name, t in (("o_part", o_part), ("m_part", m_part), ("l_part", l_part)):
+        if t.dtype != torch.float32 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous float32 CUDA tensor")
+    s, B, H_Q, d = o_part.shape
+    if tuple(m_part.shape) != (s, B, H_Q) or tuple(l_part.shape) != (s, B, H_Q):
+        raise ValueError("m_part and l_part must be [s, B, H_Q]")
+    dev = o_part.device
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
+    _check(load().da_combine_splits(_ptr(o_part), _ptr(m_part), _ptr(l_part), _ptr(out), _ptr(lse_out), s, B, H_Q,
+                                    d, _stream(dev, stream)))
+    return out

@@ -1,0 +1,618 @@
+// Split-KV single-query decode attention for MI355X (gfx950): the split
+// partial kernel (with an optional in-kernel log-sum-exp merge), the
+// standalone combine kernel, and the C-ABI launch entry points.
+//
+// What one workgroup computes (paper Sections 2.1, 2.2, 3.1): for one work
+// tile -- a sequence b and the query heads that share one KV head when GQA
+// packing is on (Sections 3.1 and 4: Batch x H_KV tiles for L_Q = 1), or a
+// single query head when it is off -- and one chunk of that sequence's keys,
+// the partial softmax state (running max m, sum l, unnormalised output
+// Otilde).  With one split the state is normalised and written as the
+// output; with several, the last workgroup of a tile to finish merges the
+// chunk states in chunk order (the paper's final reduction, Sections 3.1 and
+// 5.3), so one launch covers the whole call.
+//
+// gfx950 mapping:
+//  * 256 threads = 4 wave64s.  The chunk is cut into 4 contiguous key ranges,
+//    one per wave; each wave walks its range in tiles of 32 keys and the 4
+//    wave states are merged through LDS in wave order.
+//  * Scores S^T[key, head] = K . Q^T on MFMA v_mfma_f32_16x16x32_bf16: keys
+//    are the 16 rows, the packed query heads the 16 columns (two column
+//    tiles when a KV head serves up to 32 query heads).  K is fetched
+//    straight into the MFMA A-operand layout: lane (row r, group q) loads the
+//    64 contiguous bytes of dims [32q, 32q+32) of key r.
+//  * Online softmax on the MFMA result layout: every lane holds 8 scores of
+//    one head column; the tile max needs two cross-lane steps (lanes ^16,
+//    ^32); exp2 on the hardware v_exp_f32 with the scale folded as
+//    scale*log2(e); fp32 running state.
+//  * Output O^T[dim, head] += V^T . P^T on the same MFMA: the P operand is
+//    the lane's own 8 probabilities (bf16), so softmax never moves data
+//    across lanes; V^T comes from a per-wave LDS tile of 32 keys (16-byte
+//    coalesced loads, 272-byte row pitch, 16-bit transposing reads).
+//  * K/V loads are raw buffer loads bounded by the sequence: keys outside the
+//    wave's range use an out-of-range offset, which returns zeros without
+//    touching memory, so ragged tails cost no traffic.
+//  * Workgroup ids are remapped so consecutive tiles land on the same XCD
+//    (dispatch is round-robin over the 8 XCDs): with packing off, the query
+//    heads of one KV head then share that XCD's L2.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "decode_attn.h"
+#include "plan.h"
+
+namespace {
+
+constexpr int D = DA_HEAD_DIM;
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kKeysPerTile = 32;
+constexpr int kVPitch = 272;                                  // bytes per staged V row
+constexpr int kStageBytes = kWaves * kKeysPerTile * kVPitch;  // V staging, all waves
+constexpr int kMergeBytes = kWaves * D * 16 * 4;              // wave O^T states, one head tile
+constexpr int kStatBytes = 2 * kWaves * 16 * 4;               // wave m and l, one head tile
+constexpr int kSmemBytes = (kStageBytes > kMergeBytes ? kStageBytes : kMergeBytes) + kStatBytes;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+enum Mode : int { kDirect = 0, kPartials = 1, kMerged = 2 };
+
+struct Params {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* cu;    // nullable: fixed layout
+  uint16_t* out;        // bf16 [B, H_Q, D]        (kDirect, kMerged)
+  float* lse;           // nullable, [B, H_Q]      (kDirect, kMerged)
+  float* o_part;        // [s, B, H_Q, D]          (kPartials, kMerged)
+  float* m_part;        // [s, B, H_Q]
+  float* l_part;        // [s, B, H_Q]
+  uint32_t* counters;   // [tiles]                 (kMerged)
+  int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
+  float scale_log2;     // softmax scale * log2(e)
+};
+
+__device__ __forceinline__ float wave_max_rows(float x) {
+  // max over lanes {l, l^16, l^32, l^48}: the 4 row groups of one column
+  x = fmaxf(x, __shfl_xor(x, 16));
+  x = fmaxf(x, __shfl_xor(x, 32));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum_rows(float x) {
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  __bf16 a = (__bf16)lo;
+  __bf16 b = (__bf16)hi;
+  uint16_t ua, ub;
+  memcpy(&ua, &a, 2);
+  memcpy(&ub, &b, 2);
+  return (uint32_t)ua | ((uint32_t)ub << 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
+
+// Normalise 8 output columns of one head by the softmax sum and store them as
+// bf16; M is the row max in natural-log units, for the log-sum-exp.
+__device__ __forceinline__ void finish_row(float M, float Lsum, const float* o8, uint16_t* out_row,
+                                           float* lse_slot) {
+  const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
+  u32x4 w;
+  w.x = pack_bf16x2(o8[0] * inv, o8[1] * inv);
+  w.y = pack_bf16x2(o8[2] * inv, o8[3] * inv);
+  w.z = pack_bf16x2(o8[4] * inv, o8[5] * inv);
+  w.w = pack_bf16x2(o8[6] * inv, o8[7] * inv);
+  *reinterpret_cast<u32x4*>(out_row) = w;
+  if (lse_slot) *lse_slot = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
+}
+
+template <int NT>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+split_partial_kernel(Params p) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int col = lane & 15;   // MFMA column: head within a 16-head tile
+  const int quad = lane >> 4;  // MFMA row group
+
+  // ---- which tile and chunk this workgroup owns
+  const int nwg = p.tiles * p.s;
+  const int bid = blockIdx.x;
+  const int logical = (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
+  const int tile = logical / p.s;
+  const int split = logical - tile * p.s;
+  const int b = tile / p.tiles_per_seq;
+  const int head0 = (tile - b * p.tiles_per_seq) * p.hpt;
+  const int kvh = head0 / p.g;
+
+  int64_t row0;
+  int L;
+  if (p.cu) {
+    row0 = p.cu[b];
+    L = p.cu[b + 1] - p.cu[b];
+    L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
+  } else {
+    row0 = (int64_t)b * p.L_K;
+    L = p.L_K;
+  }
+  const int c0 = (int)(((int64_t)L * split) / p.s);
+  const int c1 = (int)(((int64_t)L * (split + 1)) / p.s);
+  const int n = c1 - c0;
+  const int key_lo = c0 + (int)(((int64_t)n * wave) / kWaves);
+  const int key_hi = c0 + (int)(((int64_t)n * (wave + 1)) / kWaves);
+
+  // ---- buffer resources over this (sequence, KV head): rows of H_KV*256 bytes
+  const uint32_t rs = (uint32_t)p.H_KV * (D * 2);
+  const int64_t base_elems = (row0 * p.H_KV + kvh) * D;
+  const uint32_t nrec = (uint32_t)L * rs;
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + base_elems), (short)0, (int)nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + base_elems), (short)0, (int)nrec, 0x00020000);
+
+  // ---- Q^T as the MFMA B operand: lane holds dims [32*quad + 8j, +8) of
+  //      head column `col` for k-step j (zeros for padding columns)
+  bf16x8 qreg[NT][4];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int h = nt * 16 + col;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u32x4 x = {0u, 0u, 0u, 0u};
+      if (h < p.hpt)
+        x = *reinterpret_cast<const u32x4*>(p.q + ((int64_t)b * p.H_Q + head0 + h) * D + 32 * quad + 8 * j);
+      qreg[nt][j] = as_bf16x8(x);
+    }
+  }
+
+  float m_run[NT], l_run[NT];
+  f32x4 acc_o[NT][8];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    m_run[nt] = -INFINITY;
+    l_run[nt] = 0.f;
+#pragma unroll
+    for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  unsigned char* vstage = smem + wave * (kKeysPerTile * kVPitch);
+  const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
+
+  u32x4 kreg[2][4], vreg[8];
+  auto load_tile = [&](int kb) {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const int key = kb + mt * 16 + col;
+      const uint32_t off = key < key_hi ? (uint32_t)key * rs + 64u * quad : nrec;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u * j, 0, 0);
+    }
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      const int key = kb + 4 * jj + quad;
+      const uint32_t off = key < key_hi ? (uint32_t)key * rs + 16u * col : nrec;
+      vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
+    }
+  };
+
+  if (ntiles > 0) load_tile(key_lo);
+  for (int t = 0; t < ntiles; ++t) {
+    const int kb = key_lo + t * kKeysPerTile;
+    const int nvalid = key_hi - kb;  // >= 1
+
+    // scores for this tile: S^T[16 keys x 16 heads] per (mt, nt)
+    f32x4 sc[NT][2];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[mt][j]), qreg[nt][j], acc, 0, 0, 0);
+        sc[nt][mt] = acc;
+      }
+
+    // stage V rows in LDS (row-major, padded pitch)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj)
+      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
+
+    // prefetch the next tile while this one is reduced
+    if (t + 1 < ntiles) load_tile(kb + kKeysPerTile);
+
+    // online softmax per head column
+    bf16x8 pb[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float x[8];
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kl = mt * 16 + quad * 4 + i;
+          const float s2 = kl < nvalid ? sc[nt][mt][i] * p.scale_log2 : -INFINITY;
+          x[mt * 4 + i] = s2;
+          tmax = fmaxf(tmax, s2);
+        }
+      tmax = wave_max_rows(tmax);
+      const float m_new = fmaxf(m_run[nt], tmax);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[nt] - m_new);
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x[e] = __builtin_amdgcn_exp2f(x[e] - m_new);
+        psum += x[e];
+      }
+      l_run[nt] = l_run[nt] * alpha + psum;
+      m_run[nt] = m_new;
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] *= alpha;
+      u32x4 pk;
+      pk.x = pack_bf16x2(x[0], x[1]);
+      pk.y = pack_bf16x2(x[2], x[3]);
+      pk.z = pack_bf16x2(x[4], x[5]);
+      pk.w = pack_bf16x2(x[6], x[7]);
+      pb[nt] = as_bf16x8(pk);
+    }
+
+    __builtin_amdgcn_wave_barrier();
+    // O^T[16 dims x 16 heads] += V^T[16 dims x 32 keys] . P^T[32 keys x 16 heads]
+    // The k index 8*quad + 4*mt + i of the product stands for key
+    // 16*mt + 4*quad + i, matching the score layout above.
+#pragma unroll
+    for (int nn = 0; nn < 8; ++nn) {
+      const unsigned char* vcol = vstage + 2 * (16 * nn + col);
+      uint16_t e[8];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          e[mt * 4 + i] = *reinterpret_cast<const uint16_t*>(vcol + (mt * 16 + quad * 4 + i) * kVPitch);
+      u32x4 a;
+      a.x = (uint32_t)e[0] | ((uint32_t)e[1] << 16);
+      a.y = (uint32_t)e[2] | ((uint32_t)e[3] << 16);
+      a.z = (uint32_t)e[4] | ((uint32_t)e[5] << 16);
+      a.w = (uint32_t)e[6] | ((uint32_t)e[7] << 16);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), pb[nt], acc_o[nt][nn], 0, 0, 0);
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+
+  // ---- merge the 4 wave states through LDS, one 16-head tile at a time
+  float* sm_o = reinterpret_cast<float*>(smem);                 // [wave][dim][16]
+  float* sm_m = reinterpret_cast<float*>(smem + kSmemBytes - kStatBytes);
+  float* sm_l = sm_m + kWaves * 16;
+  const int64_t rows = (int64_t)p.B * p.H_Q;
+
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float lsum = wave_sum_rows(l_run[nt]);
+    __syncthreads();
+#pragma unroll
+    for (int nn = 0; nn < 8; ++nn)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm_o[(wave * D + 16 * nn + 4 * quad + i) * 16 + col] = acc_o[nt][nn][i];
+    if (quad == 0) {
+      sm_m[wave * 16 + col] = m_run[nt];
+      sm_l[wave * 16 + col] = lsum;
+    }
+    __syncthreads();
+
+    const int hcount = min(16, p.hpt - nt * 16);
+    for (int it = tid; it < hcount * 16; it += kThreads) {
+      const int hc = it >> 4;          // head within this 16-head tile
+      const int d8 = (it & 15) * 8;    // first of 8 dims
+      float M2 = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w)
+        if (sm_l[w * 16 + hc] > 0.f) M2 = fmaxf(M2, sm_m[w * 16 + hc]);
+      float Lsum = 0.f;
+      float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float lw = sm_l[w * 16 + hc];
+        if (lw > 0.f) {
+          const float wt = __builtin_amdgcn_exp2f(sm_m[w * 16 + hc] - M2);
+          Lsum += wt * lw;
+#pragma unroll
+          for (int dd = 0; dd < 8; ++dd) o8[dd] += wt * sm_o[(w * D + d8 + dd) * 16 + hc];
+        }
+      }
+      const int64_t row = (int64_t)b * p.H_Q + head0 + nt * 16 + hc;
+      if (p.mode == kDirect) {
+        finish_row(M2 * kLn2, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+      } else {
+        float* dst = p.o_part + ((int64_t)split * rows + row) * D + d8;
+        *reinterpret_cast<f32x4*>(dst) = f32x4{o8[0], o8[1], o8[2], o8[3]};
+        *reinterpret_cast<f32x4*>(dst + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
+        if (d8 == 0) {
+          p.m_part[split * rows + row] = Lsum > 0.f ? M2 * kLn2 : -INFINITY;
+          p.l_part[split * rows + row] = Lsum;
+        }
+      }
+    }
+  }
+  if (p.mode != kMerged) return;
+
+  // ---- in-kernel merge: the last workgroup of this tile to arrive merges
+  //      the s chunk states in chunk order.  Release before the arrival
+  //      count, acquire after it; agent scope because the chunks of one tile
+  //      run on different XCDs with separate L2s.
+  __shared__ int sh_last;
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const uint32_t prev = __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = prev == (uint32_t)(p.s - 1);
+    if (last) __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sh_last = last;
+  }
+  __syncthreads();
+  if (!sh_last) return;
+  __threadfence();
+
+  for (int it = tid; it < p.hpt * 16; it += kThreads) {
+    const int h = it >> 4;
+    const int d8 = (it & 15) * 8;
+    const int64_t row = (int64_t)b * p.H_Q + head0 + h;
+    float M = -INFINITY;
+    for (int i = 0; i < p.s; ++i) {
+      const float li = __hip_atomic_load(p.l_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float mi = __hip_atomic_load(p.m_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (li > 0.f) M = fmaxf(M, mi);
+    }
+    float Lsum = 0.f;
+    float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < p.s; ++i) {
+      const float li = __hip_atomic_load(p.l_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (li > 0.f) {
+        const float mi = __hip_atomic_load(p.m_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const float wt = __builtin_amdgcn_exp2f((mi - M) * kLog2e);
+        Lsum += wt * li;
+        const float* src = p.o_part + ((int64_t)i * rows + row) * D + d8;
+        const f32x4 a = *reinterpret_cast<const f32x4*>(src);
+        const f32x4 c = *reinterpret_cast<const f32x4*>(src + 4);
+        o8[0] += wt * a.x; o8[1] += wt * a.y; o8[2] += wt * a.z; o8[3] += wt * a.w;
+        o8[4] += wt * c.x; o8[5] += wt * c.y; o8[6] += wt * c.z; o8[7] += wt * c.w;
+      }
+    }
+    finish_row(M, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+  }
+}
+
+// Standalone log-sum-exp combine: one wave64 per (b, h) row, 2 dims per
+// lane, chunks merged in index order.
+__global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
+                                                            const float* __restrict__ m_part,
+                                                            const float* __restrict__ l_part,
+                                                            uint16_t* __restrict__ out, float* __restrict__ lse,
+                                                            int s, int64_t rows) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  float M = -INFINITY;
+  for (int i = 0; i < s; ++i)
+    if (l_part[i * rows + row] > 0.f) M = fmaxf(M, m_part[i * rows + row]);
+  float Lsum = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int i = 0; i < s; ++i) {
+    const float li = l_part[i * rows + row];
+    if (li > 0.f) {
+      const float wt = __builtin_amdgcn_exp2f((m_part[i * rows + row] - M) * kLog2e);
+      Lsum += wt * li;
+      const float2 x = *reinterpret_cast<const float2*>(o_part + ((int64_t)i * rows + row) * D + 2 * lane);
+      o0 += wt * x.x;
+      o1 += wt * x.y;
+    }
+  }
+  const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
+  *reinterpret_cast<uint32_t*>(out + row * D + 2 * lane) = pack_bf16x2(o0 * inv, o1 * inv);
+  if (lse && lane == 0) lse[row] = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
+}
+
+// ---------------------------------------------------------------- host side
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+std::atomic<int> g_is950[kMaxDevices];  // 0 unknown, 1 yes, 2 no
+
+int query_device(int* cus, int* is950) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return da::fail(DA_ERR_UNSUPPORTED, "device index %d", dev);
+  if (g_is950[dev].load() == 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return da::fail(DA_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    g_cus[dev].store(prop.multiProcessorCount);
+    g_is950[dev].store(strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2);
+  }
+  *cus = g_cus[dev].load();
+  *is950 = g_is950[dev].load() == 1;
+  return DA_OK;
+}
+
+bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
+
+int check_inputs(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q,
+                 int H_KV, int L_K_max, int d, float** lse_check) {
+  (void)lse_check;
+  int rc = da::check_shape(B, H_Q, H_KV, L_K_max, d);
+  if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
+  // With L_K_max == 0 no key is ever read, so an empty cache may be NULL.
+  if ((!k || !v) && !(rc == DA_OK && L_K_max == 0)) return da::fail(DA_ERR_NULL, "k and v must be non-NULL");
+  if (rc) return rc;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16))
+    return da::fail(DA_ERR_ALIGN, "q, k and v must be 16-byte aligned");
+  if (cu && !aligned(cu, 4)) return da::fail(DA_ERR_ALIGN, "cu_seqlens_k must be 4-byte aligned");
+  return DA_OK;
+}
+
+int ensure_gfx950() {
+  int cus = 0, is950 = 0;
+  int rc = query_device(&cus, &is950);
+  if (rc) return rc;
+  if (!is950) return da::fail(DA_ERR_UNSUPPORTED, "current device is not gfx950");
+  return DA_OK;
+}
+
+int launch_partial(const Params& prm, int hpt, int grid, hipStream_t stream) {
+  void* args[] = {const_cast<Params*>(&prm)};
+  const void* fn = hpt <= 16 ? reinterpret_cast<const void*>(&split_partial_kernel<1>)
+                             : reinterpret_cast<const void*>(&split_partial_kernel<2>);
+  hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, kSmemBytes, stream);
+  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "split partial launch: %s", hipGetErrorString(e));
+  return DA_OK;
+}
+
+Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q,
+                   int H_KV, int L_K_max, float scale, const da_plan& pl) {
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.cu = cu;
+  p.B = B;
+  p.H_Q = H_Q;
+  p.H_KV = H_KV;
+  p.L_K = L_K_max;
+  p.g = H_Q / H_KV;
+  p.hpt = pl.heads_per_tile;
+  p.tiles_per_seq = H_Q / pl.heads_per_tile;
+  p.tiles = pl.tiles;
+  p.s = pl.num_splits;
+  const float sigma = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
+  p.scale_log2 = sigma * kLog2e;
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+int da_device_info(int* num_cus, int* is_gfx950) {
+  if (!num_cus || !is_gfx950) return da::fail(DA_ERR_NULL, "output pointers must be non-NULL");
+  return query_device(num_cus, is_gfx950);
+}
+
+int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, void* out,
+                   float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
+                   int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d, nullptr);
+  if (rc) return rc;
+  if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
+  if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
+  if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
+  if (num_splits > DA_MAX_SPLITS)
+    return da::fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, DA_MAX_SPLITS);
+  if (pack_gqa < -1 || pack_gqa > 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
+
+  int cus = 1;
+  if (num_splits <= 0 || pack_gqa < 0) {
+    int is950 = 0;
+    rc = query_device(&cus, &is950);
+    if (rc) return rc;
+  }
+  da_plan pl;
+  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+  if (rc) return rc;
+  const int s = pl.num_splits;
+  const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
+  if (s > 1 && (!workspace || workspace_bytes < wl.total))
+    return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, wl.total,
+                    workspace ? workspace_bytes : (size_t)0);
+  rc = ensure_gfx950();
+  if (rc) return rc;
+
+  Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
+  p.out = static_cast<uint16_t*>(out);
+  p.lse = lse_out;
+  if (s == 1) {
+    p.mode = kDirect;
+  } else {
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    p.mode = kMerged;
+    p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
+    p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
+    p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
+    p.counters = reinterpret_cast<uint32_t*>(ws + wl.cnt_off);
+  }
+  return launch_partial(p, pl.heads_per_tile, pl.grid, static_cast<hipStream_t>(stream));
+}
+
+int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, float* o_part,
+                      float* m_part, float* l_part, int B, int H_Q, int H_KV, int L_K_max, int d,
+                      float softmax_scale, int num_splits, int pack_gqa, void* stream) {
+  da::clear_error();
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d, nullptr);
+  if (rc) return rc;
+  if (!o_part || !m_part || !l_part) return da::fail(DA_ERR_NULL, "o_part, m_part and l_part must be non-NULL");
+  if (!aligned(o_part, 16) || !aligned(m_part, 4) || !aligned(l_part, 4))
+    return da::fail(DA_ERR_ALIGN, "o_part must be 16-byte and m_part/l_part 4-byte aligned");
+  if (num_splits < 1 || num_splits > DA_MAX_SPLITS)
+    return da::fail(DA_ERR_SPLITS, "num_splits=%d not in [1, %d]", num_splits, DA_MAX_SPLITS);
+  if (pack_gqa != 0 && pack_gqa != 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {0,1}", pack_gqa);
+  da_plan pl;
+  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 1, 0, DA_POLICY_MI355X, &pl);
+  if (rc) return rc;
+  rc = ensure_gfx950();
+  if (rc) return rc;
+  Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
+  p.mode = kPartials;
+  p.o_part = o_part;
+  p.m_part = m_part;
+  p.l_part = l_part;
+  return launch_partial(p, pl.heads_per_tile, pl.grid, static_cast<hipStream_t>(stream));
+}
+
+int da_combine_splits(const float* o_part, const float* m_part, const float* l_part, void* out, float* lse_out,
+                      int num_splits, int B, int H_Q, int d, void* stream) {
+  da::clear_error();
+  if (!o_part || !m_part || !l_part || !out)
+    return da::fail(DA_ERR_NULL, "o_part, m_part, l_part and out must be non-NULL");
+  if (d != D) return da::fail(DA_ERR_UNSUPPORTED, "head dim %d unsupported (only %d)", d, D);
+  if (B <= 0 || H_Q <= 0) return da::fail(DA_ERR_SHAPE, "B=%d H_Q=%d must be positive", B, H_Q);
+  if (num_splits < 1 || num_splits > DA_MAX_SPLITS)
+    return da::fail(DA_ERR_SPLITS, "num_splits=%d not in [1, %d]", num_splits, DA_MAX_SPLITS);
+  if (!aligned(o_part, 8) || !aligned(m_part, 4) || !aligned(l_part, 4) || !aligned(out, 4) ||
+      (lse_out && !aligned(lse_out, 4)))
+    return da::fail(DA_ERR_ALIGN, "misaligned combine operand");
+  int rc = ensure_gfx950();
+  if (rc) return rc;
+  const int64_t rows = (int64_t)B * H_Q;
+  const int grid = (int)((rows + 3) / 4);
+  int s = num_splits;
+  const float* a0 = o_part;
+  const float* a1 = m_part;
+  const float* a2 = l_part;
+  uint16_t* a3 = static_cast<uint16_t*>(out);
+  float* a4 = lse_out;
+  int64_t a6 = rows;
+  void* args[] = {&a0, &a1, &a2, &a3, &a4, &s, &a6};
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&split_combine_kernel), dim3(grid), dim3(256), args,
+                                 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+  return DA_OK;
+}
+
+}  // extern "C"

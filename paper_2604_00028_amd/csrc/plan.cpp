@@ -1,0 +1,208 @@
+// Host-side planning: split policy (paper Section 4 and the MI355X cost
+// model), the sequence partition, workspace sizing and error reporting.
+#include "plan.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+namespace da {
+
+namespace {
+thread_local char g_last_error[512] = "";
+}
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+void clear_error() { g_last_error[0] = '\0'; }
+
+int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
+  if (!pack_gqa) return 1;
+  const int g = H_Q / H_KV;
+  if (g <= kMaxHeadsPerTile) return g;
+  for (int h = kMaxHeadsPerTile; h > 1; --h)
+    if (g % h == 0) return h;
+  return 1;
+}
+
+// Constants measured on MI355X (see the calibration notes that accompany the
+// split sweeps).  Units: microseconds and bytes per microsecond.
+const CostModel& mi355x_model() {
+  static const CostModel m = {
+      /*t_wg=*/1.5,
+      /*wg_rate=*/40.0e3,
+      /*hbm_rate=*/5.0e6,
+      /*t_merge=*/1.0,
+      /*t_dispatch=*/0.004,
+      /*wgs_per_cu=*/2,
+      /*tie=*/0.02,
+  };
+  return m;
+}
+
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus) {
+  const double row_bytes = 2.0 * kHeadDim * 2.0;              // K and V row of one KV head
+  const int64_t tiles = (int64_t)B * H_Q / hpt;
+  const int64_t wgs = tiles * s;
+  const double slots = (double)cus * m.wgs_per_cu;
+  const double rounds = ceil((double)wgs / slots);
+  const double chunk = ceil((double)L_K / s) * row_bytes;
+  const double per_round = m.t_wg + chunk / m.wg_rate;
+  double bytes = (double)B * L_K * H_KV * row_bytes + 4.0 * B * H_Q * kHeadDim;
+  if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
+  const double stream = bytes / m.hbm_rate;
+  double t = rounds * per_round;
+  if (stream > t) t = stream;
+  t += m.t_dispatch * (double)wgs;
+  if (s > 1) t += m.t_merge;
+  return t;
+}
+
+static int mi355x_splits(int B, int H_Q, int H_KV, int L_K, int hpt, int cus) {
+  if (L_K <= 0) return 1;
+  const CostModel& m = mi355x_model();
+  double best = 0.0;
+  double times[kMaxSplits + 1];
+  for (int s = 1; s <= kMaxSplits; ++s) {
+    times[s] = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus);
+    if (s == 1 || times[s] < best) best = times[s];
+  }
+  // Smallest split count whose modelled time is within the tie tolerance of
+  // the best one (the paper, Section 5.2, likewise keeps the smallest split
+  // that reaches the low-latency plateau).
+  for (int s = 1; s <= kMaxSplits; ++s)
+    if (times[s] <= best * (1.0 + m.tie)) return s;
+  return 1;
+}
+
+// The paper's rule (Section 4): 128-key blocks, Batch * H_KV tiles.
+static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
+  const int blocks = (L_K + 127) / 128;
+  const int64_t tiles = (int64_t)B * H_KV;
+  if (blocks <= 3) return 1;                 // short contexts stay unsplit
+  if (blocks == 4) return tiles >= 4 ? 1 : 3;  // saturated vs low-tile boundary bucket
+  // Longer contexts: the paper defers to the stack's own long-context path,
+  // which here is the MI355X cost model.
+  return mi355x_splits(B, H_Q, H_KV, L_K, hpt, cus);
+}
+
+int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
+  if (d != kHeadDim) return fail(DA_ERR_UNSUPPORTED, "head dim %d unsupported (only %d)", d, kHeadDim);
+  if (B <= 0 || H_Q <= 0 || H_KV <= 0)
+    return fail(DA_ERR_SHAPE, "B=%d H_Q=%d H_KV=%d must be positive", B, H_Q, H_KV);
+  if (H_Q % H_KV != 0) return fail(DA_ERR_SHAPE, "H_Q=%d is not a multiple of H_KV=%d", H_Q, H_KV);
+  if (L_K_max < 0) return fail(DA_ERR_SHAPE, "L_K_max=%d is negative", L_K_max);
+  // Per-sequence K/V byte offsets must fit the 32-bit buffer offsets the
+  // kernels use; B*H_Q rows must fit a 32-bit grid.
+  const int64_t seq_bytes = (int64_t)L_K_max * H_KV * kHeadDim * 2;
+  if (seq_bytes >= ((int64_t)1 << 31))
+    return fail(DA_ERR_SHAPE, "one sequence spans %lld bytes of K (limit 2 GiB)", (long long)seq_bytes);
+  if ((int64_t)B * H_Q > (1 << 24)) return fail(DA_ERR_SHAPE, "B*H_Q=%lld too large", (long long)B * H_Q);
+  return DA_OK;
+}
+
+int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
+         int cu_margin, int policy, da_plan* out) {
+  if (!out) return fail(DA_ERR_NULL, "plan output is NULL");
+  int rc = check_shape(B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  if (num_splits > kMaxSplits) return fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, kMaxSplits);
+  if (pack_gqa < -1 || pack_gqa > 1) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (policy != DA_POLICY_MI355X && policy != DA_POLICY_PAPER)
+    return fail(DA_ERR_ARG, "unknown policy %d", policy);
+  if (num_cus <= 0) return fail(DA_ERR_ARG, "num_cus=%d must be positive here", num_cus);
+  if (cu_margin < 0 || cu_margin >= num_cus)
+    return fail(DA_ERR_ARG, "cu_margin=%d must be in [0, %d)", cu_margin, num_cus);
+  const int cus = num_cus - cu_margin;
+  const int g = H_Q / H_KV;
+  const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
+  const int hpt = heads_per_tile(H_Q, H_KV, pack);
+  int s = num_splits;
+  if (s <= 0)
+    s = policy == DA_POLICY_PAPER ? paper_splits(B, H_KV, L_K_max, H_Q, hpt, cus)
+                                  : mi355x_splits(B, H_Q, H_KV, L_K_max, hpt, cus);
+  out->num_splits = s;
+  out->pack_gqa = pack;
+  out->heads_per_tile = hpt;
+  out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
+  out->grid = (int32_t)((int64_t)out->tiles * s);
+  out->num_cus = cus;
+  return DA_OK;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s) {
+  WorkspaceLayout w{};
+  const size_t rows = (size_t)B * H_Q;
+  w.o_off = 0;
+  w.m_off = align256(w.o_off + (size_t)s * rows * d * sizeof(float));
+  w.l_off = align256(w.m_off + (size_t)s * rows * sizeof(float));
+  w.cnt_off = align256(w.l_off + (size_t)s * rows * sizeof(float));
+  w.total = align256(w.cnt_off + rows * sizeof(uint32_t));
+  return w;
+}
+
+}  // namespace da
+
+extern "C" {
+
+int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus, int cu_margin,
+                     int policy, da_plan* out) {
+  if (num_cus <= 0) {
+    int is950 = 0;
+    int rc = da_device_info(&num_cus, &is950);
+    if (rc) return rc;
+  }
+  return da::plan(B, H_Q, H_KV, L_K_max, d, 0, -1, num_cus, cu_margin, policy, out);
+}
+
+int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
+                 int num_cus, int cu_margin, int policy, da_plan* out) {
+  if (num_cus <= 0 && (num_splits <= 0 || pack_gqa < 0)) {
+    int is950 = 0;
+    int rc = da_device_info(&num_cus, &is950);
+    if (rc) return rc;
+  }
+  if (num_cus <= 0) num_cus = 1;  // forced plan: the CU count is not used
+  return da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, num_cus, cu_margin, policy, out);
+}
+
+size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits) {
+  if (B <= 0 || H_Q <= 0 || d <= 0 || num_splits <= 1) return 0;
+  return da::workspace_layout(B, H_Q, d, num_splits).total;
+}
+
+int da_split_bounds(int L, int num_splits, int32_t* cuts) {
+  if (!cuts) return da::fail(DA_ERR_NULL, "cuts is NULL");
+  if (L < 0) return da::fail(DA_ERR_SHAPE, "L=%d is negative", L);
+  if (num_splits <= 0 || num_splits > da::kMaxSplits)
+    return da::fail(DA_ERR_SPLITS, "num_splits=%d not in [1, %d]", num_splits, da::kMaxSplits);
+  for (int i = 0; i <= num_splits; ++i) cuts[i] = (int32_t)da::chunk_start(L, num_splits, i);
+  return DA_OK;
+}
+
+const char* da_strerror(int code) {
+  switch (code) {
+    case DA_OK: return "ok";
+    case DA_ERR_NULL: return "null pointer";
+    case DA_ERR_SHAPE: return "invalid shape";
+    case DA_ERR_UNSUPPORTED: return "unsupported head dim or device";
+    case DA_ERR_SPLITS: return "num_splits out of range";
+    case DA_ERR_ALIGN: return "misaligned pointer";
+    case DA_ERR_WORKSPACE: return "workspace missing or too small";
+    case DA_ERR_HIP: return "HIP runtime error";
+    case DA_ERR_ARG: return "invalid argument";
+    default: return "unknown error";
+  }
+}
+
+const char* da_last_error(void) { return da::g_last_error; }
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// Host-side planning shared by the C-ABI entry points: error state, the split
+// policy, the sequence partition and workspace sizing.  No HIP calls here.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "decode_attn.h"
+
+namespace da {
+
+constexpr int kHeadDim = DA_HEAD_DIM;
+constexpr int kMaxSplits = DA_MAX_SPLITS;
+constexpr int kMaxHeadsPerTile = 32;   // two 16-column MFMA head tiles per workgroup
+
+// Records a printf-style message for da_last_error() and returns `code`.
+int fail(int code, const char* fmt, ...);
+void clear_error();
+
+// Query heads one workgroup serves.  Packed: the whole GQA group of a KV head
+// when it fits in 32 columns, else the largest divisor of the group <= 32.
+// Unpacked: one.
+int heads_per_tile(int H_Q, int H_KV, int pack_gqa);
+
+// First key of chunk i when L keys are cut into s balanced chunks.
+inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
+
+// Policy knobs of the MI355X cost model (times in microseconds, rates in
+// bytes per microsecond).  Exposed so that tests can check its properties.
+struct CostModel {
+  double t_wg;        // fixed latency of one workgroup: first loads, epilogue
+  double wg_rate;     // KV bytes per microsecond one 4-wave workgroup streams
+  double hbm_rate;    // sustained HBM bytes per microsecond for the whole chip
+  double t_merge;     // extra latency of the in-kernel split merge (s > 1)
+  double t_dispatch;  // dispatch cost per workgroup launched
+  int wgs_per_cu;     // workgroups resident per CU
+  double tie;         // relative tolerance: take the smallest s within it
+};
+const CostModel& mi355x_model();
+
+// Modelled time (us) of one call with s splits (policy MI355X).
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus);
+
+int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
+         int cu_margin, int policy, da_plan* out);
+
+// Argument checks shared by the launch entry points (no HIP calls).
+int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d);
+
+struct WorkspaceLayout {
+  size_t o_off, m_off, l_off, cnt_off, total;
+};
+WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s);
+
+}  // namespace da

@@ -1,0 +1,197 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and
+its host-side logic (argument checks, planner, partition, workspace sizing)
+behaves as documented.  No kernel runs here; every call below returns before
+any HIP call."""
+
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2604_00028_amd as da
+from paper_2604_00028_amd import _binding as bnd
+from oracle import even_bounds, paper_split_policy
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "decode_attn.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden", "paper_policy.json")
+
+FAKE = 0x100000          # 16-byte aligned stand-in device address (never dereferenced)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(da_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declarations_are_exported(lib):
+    names = declared_functions()
+    assert names, "no declarations found"
+    assert sorted(bnd.EXPORTS) == names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_strerror_covers_every_code(lib):
+    for code in range(-8, 1):
+        assert da.da_strerror(code) not in ("", "unknown error")
+    assert da.da_strerror(-99) == "unknown error"
+
+
+def call_decode(lib, q=FAKE, k=FAKE, v=FAKE, cu=None, out=FAKE, lse=None, B=1, H_Q=8, H_KV=1, L=128, d=128,
+                scale=0.0, s=1, pack=1, ws=None, ws_bytes=0):
+    return lib.da_decode_attn(q, k, v, cu, out, lse, B, H_Q, H_KV, L, d, scale, s, pack, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), bnd.DA_ERR_NULL),
+    (dict(k=None), bnd.DA_ERR_NULL),
+    (dict(v=None), bnd.DA_ERR_NULL),
+    (dict(out=None), bnd.DA_ERR_NULL),
+    (dict(B=0), bnd.DA_ERR_SHAPE),
+    (dict(H_Q=0), bnd.DA_ERR_SHAPE),
+    (dict(H_KV=0), bnd.DA_ERR_SHAPE),
+    (dict(H_Q=8, H_KV=3), bnd.DA_ERR_SHAPE),
+    (dict(L=-1), bnd.DA_ERR_SHAPE),
+    (dict(L=1 << 22, H_KV=8), bnd.DA_ERR_SHAPE),
+    (dict(d=64), bnd.DA_ERR_UNSUPPORTED),
+    (dict(s=65), bnd.DA_ERR_SPLITS),
+    (dict(pack=2), bnd.DA_ERR_ARG),
+    (dict(pack=-2), bnd.DA_ERR_ARG),
+    (dict(q=FAKE + 2), bnd.DA_ERR_ALIGN),
+    (dict(k=FAKE + 8), bnd.DA_ERR_ALIGN),
+    (dict(out=FAKE + 4), bnd.DA_ERR_ALIGN),
+    (dict(lse=FAKE + 1), bnd.DA_ERR_ALIGN),
+    (dict(cu=FAKE + 2), bnd.DA_ERR_ALIGN),
+    (dict(s=4), bnd.DA_ERR_WORKSPACE),
+    (dict(s=4, ws=FAKE, ws_bytes=100), bnd.DA_ERR_WORKSPACE),
+    (dict(s=4, ws=FAKE + 4, ws_bytes=1 << 20), bnd.DA_ERR_ALIGN),
+])
+def test_decode_attn_argument_errors(lib, kw, code):
+    assert call_decode(lib, **kw) == code
+    assert da.da_last_error() != ""
+
+
+def test_split_partials_and_combine_argument_errors(lib):
+    sp = lib.da_split_partials
+    ok = dict(q=FAKE, k=FAKE, v=FAKE)
+    args = lambda **o: [o.get("q", FAKE), o.get("k", FAKE), o.get("v", FAKE), None, o.get("op", FAKE),
+                        o.get("mp", FAKE), o.get("lp", FAKE), 1, 8, 1, 128, 128, 0.0, o.get("s", 2),
+                        o.get("pack", 1), None]
+    assert sp(*args(op=None)) == bnd.DA_ERR_NULL
+    assert sp(*args(s=0)) == bnd.DA_ERR_SPLITS
+    assert sp(*args(s=65)) == bnd.DA_ERR_SPLITS
+    assert sp(*args(pack=-1)) == bnd.DA_ERR_ARG
+    assert sp(*args(op=FAKE + 4)) == bnd.DA_ERR_ALIGN
+    cs = lib.da_combine_splits
+    assert cs(None, FAKE, FAKE, FAKE, None, 2, 1, 8, 128, None) == bnd.DA_ERR_NULL
+    assert cs(FAKE, FAKE, FAKE, FAKE, None, 0, 1, 8, 128, None) == bnd.DA_ERR_SPLITS
+    assert cs(FAKE, FAKE, FAKE, FAKE, None, 2, 0, 8, 128, None) == bnd.DA_ERR_SHAPE
+    assert cs(FAKE, FAKE, FAKE, FAKE, None, 2, 1, 8, 64, None) == bnd.DA_ERR_UNSUPPORTED
+    assert cs(FAKE + 4, FAKE, FAKE, FAKE, None, 2, 1, 8, 128, None) == bnd.DA_ERR_ALIGN
+
+
+@pytest.mark.parametrize("L,s", [(0, 1), (1, 1), (5, 8), (45, 7), (512, 3), (8192, 64), (100, 64)])
+def test_split_bounds_match_the_oracle_partition(L, s):
+    assert da.da_split_bounds(L, s) == even_bounds(L, s)
+
+
+def test_split_bounds_errors():
+    with pytest.raises(da.DecodeAttnError):
+        da.da_split_bounds(10, 0)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_split_bounds(10, 65)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_split_bounds(-1, 2)
+
+
+def test_workspace_bytes():
+    assert da.da_workspace_bytes(1, 64, 128, 1) == 0
+    for B, H, s in [(1, 8, 2), (32, 64, 8), (16, 32, 64)]:
+        n = da.da_workspace_bytes(B, H, 128, s)
+        need = s * B * H * 128 * 4 + 2 * s * B * H * 4 + B * H * 4
+        assert need <= n <= need + 4 * 256 and n % 256 == 0
+
+
+# ------------------------------------------------------------------ planner
+
+def test_paper_policy_reproduces_the_paper_table():
+    table = json.load(open(GOLDEN))
+    for c in table["cases"]:
+        H_Q = 8 * c["H_KV"]
+        plan = da.da_choose_splits(c["B"], H_Q, c["H_KV"], c["L_K"], num_cus=256, policy=da.POLICY_PAPER)
+        if c["s"] is not None:
+            assert plan.num_splits == c["s"], c
+        else:
+            mi = da.da_choose_splits(c["B"], H_Q, c["H_KV"], c["L_K"], num_cus=256, policy=da.POLICY_MI355X)
+            assert plan.num_splits == mi.num_splits, c
+
+
+def test_paper_policy_matches_the_oracle_rule_on_a_grid():
+    for B in (1, 2, 4, 8):
+        for H_KV in (1, 2, 4, 8, 32):
+            for L in (1, 64, 128, 129, 256, 384, 385, 448, 512, 513, 640, 1024, 8192):
+                want = paper_split_policy(L, B, H_KV)
+                plan = da.da_choose_splits(B, 8 * H_KV, H_KV, L, num_cus=132, policy=da.POLICY_PAPER)
+                if want is not None:
+                    assert plan.num_splits == want, (B, H_KV, L)
+
+
+def test_plan_fields_and_packing():
+    p = da.da_choose_splits(1, 64, 8, 512, num_cus=256)
+    assert p.pack_gqa == 1 and p.heads_per_tile == 8 and p.tiles == 8
+    assert p.grid == p.tiles * p.num_splits and p.num_cus == 256
+    p = da.da_make_plan(1, 64, 8, 512, num_splits=4, pack_gqa=0, num_cus=256)
+    assert (p.num_splits, p.pack_gqa, p.heads_per_tile, p.tiles, p.grid) == (4, 0, 1, 64, 256)
+    p = da.da_choose_splits(4, 32, 1, 256, num_cus=256)          # g = 32: one tile per KV head
+    assert p.heads_per_tile == 32 and p.tiles == 4
+    p = da.da_make_plan(2, 128, 2, 64, num_splits=1, pack_gqa=1, num_cus=256)  # g = 64 -> 2 tiles per KV head
+    assert p.heads_per_tile == 32 and p.tiles == 8
+    p = da.da_make_plan(1, 12, 4, 64, num_splits=1, pack_gqa=1, num_cus=256)   # g = 3
+    assert p.heads_per_tile == 3 and p.tiles == 4
+    p = da.da_choose_splits(1, 8, 8, 64, num_cus=256)              # MHA: nothing to pack
+    assert p.pack_gqa == 0 and p.heads_per_tile == 1
+
+
+def test_mi355x_policy_properties():
+    for B, H_Q, H_KV in [(1, 8, 1), (1, 64, 8), (4, 32, 1), (16, 32, 4), (32, 64, 8), (8, 256, 32)]:
+        prev_tiles_s = None
+        for L in (1, 32, 64, 128, 256, 512, 1024, 4096, 8192):
+            p = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256)
+            assert 1 <= p.num_splits <= 64
+            again = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256)
+            assert again.as_dict() == p.as_dict()           # deterministic
+    # a grid that already fills the chip is not split further
+    p = da.da_choose_splits(64, 64, 8, 8192, num_cus=256)
+    assert p.num_splits <= 2
+    # a starved grid on a long sequence is split
+    p = da.da_choose_splits(1, 8, 1, 8192, num_cus=256)
+    assert p.num_splits > 1
+    # fewer compute units never asks for more splits
+    for L in (512, 4096):
+        a = da.da_choose_splits(1, 64, 8, L, num_cus=256).num_splits
+        b = da.da_choose_splits(1, 64, 8, L, num_cus=64).num_splits
+        assert b <= a
+
+
+def test_cu_margin_and_plan_errors():
+    p = da.da_choose_splits(1, 8, 1, 4096, num_cus=256, cu_margin=200)
+    assert p.num_cus == 56
+    with pytest.raises(da.DecodeAttnError):
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, cu_margin=256)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=7)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_choose_splits(1, 8, 3, 512, num_cus=256)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_make_plan(1, 8, 1, 512, num_splits=65, pack_gqa=1, num_cus=256)
+
+
+def test_binding_refuses_bad_tensors():
+    import torch
+    q = torch.zeros(1, 8, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        da.da_decode_attn(q, q, q)            # CPU tensors are refused before any call
