@@ -53,7 +53,9 @@ def parse():
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--full-sweep", action="store_true", help="sweep num_splits 1..64 on every config-2 length")
+    ap.add_argument("--only", choices=("headline", "highload"), default=None,
+                    help="time only the planned launch of one workload (for profiler runs)")
+    ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
     return ap.parse_args()
 
 
@@ -152,6 +154,24 @@ def cpu_baseline(inp, seconds: float):
             "sample": f"{n} full calls of the benchmarked shape (fp64 NumPy, {seconds:.0f} s budget)"}
 
 
+def only_run(args, da, torch, np, dev):
+    """Planned (or forced) launch of one workload, nothing else: the command
+    the rocprofv3 summaries are taken from."""
+    from workloads import config_shapes, make_inputs
+    sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
+    inp = make_inputs(sh)
+    q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
+    del inp
+    K = args.steps if args.only == "headline" else args.highload_steps
+    var = Variant(args.only, da, torch, q, k, v, sh.L_K, args.num_splits, -1, K)
+    interleave(torch, [var], args.rounds)
+    nbytes = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
+    gbs = nbytes / (var.median * 1e-6) / 1e9
+    print(json.dumps({"workload": sh.name, "us_per_call": round(var.median, 3), "num_splits": var.plan.num_splits,
+                      "calls": K * (args.rounds + 1) + 3, "achieved_gbps": round(gbs, 1),
+                      "frac": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -170,6 +190,9 @@ def main():
     torch.cuda.set_device(0)
     cus, is950 = da.da_device_info()
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    if args.only:
+        only_run(args, da, torch, np, dev)
+        return
 
     # ---------------- headline: Llama-3.1-70B GQA decode, B=1, L_K=512
     shapes = {s.L_K: s for s in config_shapes(2)}

@@ -90,10 +90,12 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
                  int num_cus, int cu_margin, int policy, da_plan* out);
 
 /* Bytes of workspace da_decode_attn needs for num_splits chunks: 0 when
- * num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
- * [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q] | arrival counters
- * uint32 [B*H_Q].  The counter region must be zero before the first call
- * that uses the workspace; every call leaves it zero again. */
+ * num_splits == 1.  Layout (each region 256-byte aligned): arrival counters
+ * uint32 [B*H_Q] | Otilde fp32 [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32
+ * [s,B,H_Q].  The counter region (the first B*H_Q*4 bytes) must be zero
+ * before the first call that uses the workspace; every call leaves it zero
+ * again, so a workspace can be reused by later calls with the same B*H_Q and
+ * any num_splits without clearing it. */
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
 
 /* Cut points of sequence chunking: chunk i of a sequence of L keys is

@@ -28,7 +28,8 @@
 //  * Output O^T[dim, head] += V^T . P^T on the same MFMA: the P operand is
 //    the lane's own 8 probabilities (bf16), so softmax never moves data
 //    across lanes; V^T comes from a per-wave LDS tile of 32 keys (16-byte
-//    coalesced loads, 272-byte row pitch, 16-bit transposing reads).
+//    coalesced loads, 288-byte row pitch, ds_read_b64_tr_b16 transposing
+//    reads: two per 16 output dims).
 //  * K/V loads are raw buffer loads bounded by the sequence: keys outside the
 //    wave's range use an out-of-range offset, which returns zeros without
 //    touching memory, so ragged tails cost no traffic.
@@ -51,11 +52,14 @@ constexpr int D = DA_HEAD_DIM;
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kKeysPerTile = 32;
-constexpr int kVPitch = 272;                                  // bytes per staged V row
+constexpr int kMergeBatch = 8;                               // chunk states loaded per batch in a merge
+constexpr int kVPitch = 288;                                  // bytes per staged V row
 constexpr int kStageBytes = kWaves * kKeysPerTile * kVPitch;  // V staging, all waves
 constexpr int kMergeBytes = kWaves * D * 16 * 4;              // wave O^T states, one head tile
 constexpr int kStatBytes = 2 * kWaves * 16 * 4;               // wave m and l, one head tile
 constexpr int kSmemBytes = (kStageBytes > kMergeBytes ? kStageBytes : kMergeBytes) + kStatBytes;
+static_assert(2 * da::kMaxHeadsPerTile * DA_MAX_SPLITS * 4 + da::kMaxHeadsPerTile * 8 <= kSmemBytes,
+              "merge scratch must fit the workgroup's LDS");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -63,6 +67,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 enum Mode : int { kDirect = 0, kPartials = 1, kMerged = 2 };
 
@@ -105,6 +111,38 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
+// Chunk states shared between workgroups of one launch.  An agent-scope
+// fence on gfx950 writes back and invalidates the whole L2 of the XCD, which
+// costs microseconds per workgroup.  Instead the states are written and read
+// with agent-scope relaxed atomics, which go through to the point of
+// coherence shared by all XCDs, and the fences below only order them:
+// wait until this wave's memory operations have completed (s_waitcnt with
+// vmcnt = 0; expcnt = 7 and lgkmcnt = 15 leave those counters unchecked).
+__device__ __forceinline__ void store_shared(float* dst, float v) {
+  __hip_atomic_store(dst, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_shared2(float* dst, float a, float b) {
+  const uint64_t bits = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(dst), bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_shared(const float* src) {
+  return __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void load_shared2(const float* src, float& a, float& b) {
+  const uint64_t bits =
+      __hip_atomic_load(reinterpret_cast<const uint64_t*>(src), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  a = __uint_as_float((uint32_t)bits);
+  b = __uint_as_float((uint32_t)(bits >> 32));
+}
+__device__ __forceinline__ void order_after_memory_ops() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+__device__ __forceinline__ void order_before_memory_ops() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 // Normalise 8 output columns of one head by the softmax sum and store them as
 // bf16; M is the row max in natural-log units, for the log-sum-exp.
 __device__ __forceinline__ void finish_row(float M, float Lsum, const float* o8, uint16_t* out_row,
@@ -119,7 +157,27 @@ __device__ __forceinline__ void finish_row(float M, float Lsum, const float* o8,
   if (lse_slot) *lse_slot = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
 }
 
-template <int NT>
+// Chunk weights of one (sequence, head) row from its s chunk states:
+// M = max m_i over non-empty chunks (l_i > 0), w_i = exp(m_i - M) (0 for an
+// empty chunk), L = sum_i w_i l_i accumulated in chunk order.  m holds the
+// maxima on entry and the weights on return; ML receives (M, L).
+__device__ __forceinline__ void merge_weights(float* m, const float* l, int s, float* ML) {
+  float M = -INFINITY;
+  for (int i = 0; i < s; ++i)
+    if (l[i] > 0.f) M = fmaxf(M, m[i]);
+  float L = 0.f;
+  for (int i = 0; i < s; ++i) {
+    const float w = l[i] > 0.f ? __builtin_amdgcn_exp2f((m[i] - M) * kLog2e) : 0.f;
+    m[i] = w;
+    L = fmaf(w, l[i], L);
+  }
+  ML[0] = M;
+  ML[1] = L;
+}
+
+// NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
+// 32).  PF: 32-key tiles of K/V loads each wave keeps in flight.
+template <int NT, int PF>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -192,25 +250,27 @@ split_partial_kernel(Params p) {
   unsigned char* vstage = smem + wave * (kKeysPerTile * kVPitch);
   const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
 
-  u32x4 kreg[2][4], vreg[8];
-  auto load_tile = [&](int kb) {
+  // K/V of one 32-key tile: K in the MFMA A layout (two 16-key row blocks x
+  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.
+  auto load_tile = [&](u32x4 (&kr)[2][4], u32x4 (&vr)[8], int kb) {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
       const int key = kb + mt * 16 + col;
       const uint32_t off = key < key_hi ? (uint32_t)key * rs + 64u * quad : nrec;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u * j, 0, 0);
+      for (int j = 0; j < 4; ++j) kr[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u * j, 0, 0);
     }
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) {
       const int key = kb + 4 * jj + quad;
       const uint32_t off = key < key_hi ? (uint32_t)key * rs + 16u * col : nrec;
-      vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
+      vr[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
     }
   };
 
-  if (ntiles > 0) load_tile(key_lo);
-  for (int t = 0; t < ntiles; ++t) {
+  // One tile: scores, V to LDS, refill the registers with tile t + PF,
+  // online softmax, then the PV product.
+  auto process = [&](u32x4 (&kr)[2][4], u32x4 (&vr)[8], int t) {
     const int kb = key_lo + t * kKeysPerTile;
     const int nvalid = key_hi - kb;  // >= 1
 
@@ -223,17 +283,20 @@ split_partial_kernel(Params p) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[mt][j]), qreg[nt][j], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[mt][j]), qreg[nt][j], acc, 0, 0, 0);
         sc[nt][mt] = acc;
       }
 
     // stage V rows in LDS (row-major, padded pitch)
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj)
-      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
+      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vr[jj];
 
-    // prefetch the next tile while this one is reduced
-    if (t + 1 < ntiles) load_tile(kb + kKeysPerTile);
+    // refill: keep PF tiles of loads in flight while this one is reduced.
+    // Unconditional on purpose: past the wave's range every offset is out of
+    // range (zeros, no memory traffic), and branch-free loads let the
+    // compiler wait for exactly the tile it needs instead of for all loads.
+    load_tile(kr, vr, kb + PF * kKeysPerTile);
 
     // online softmax per head column
     bf16x8 pb[NT];
@@ -274,26 +337,39 @@ split_partial_kernel(Params p) {
     __builtin_amdgcn_wave_barrier();
     // O^T[16 dims x 16 heads] += V^T[16 dims x 32 keys] . P^T[32 keys x 16 heads]
     // The k index 8*quad + 4*mt + i of the product stands for key
-    // 16*mt + 4*quad + i, matching the score layout above.
+    // 16*mt + 4*quad + i, matching the score layout above.  The V^T operand
+    // comes from transposing LDS reads (ds_read_b64_tr_b16): within each
+    // 16-lane group, output lane j receives element j%4 of the 8-byte chunks
+    // that lanes 4k + j/4 point at, k = 0..3.  Lane (quad, 4k + m) therefore
+    // points at dims [16nn + 4m, +4) of key 16mt + 4quad + k, and lane
+    // (quad, col) receives V[16mt + 4quad + k][16nn + col] for k = 0..3.
+    const unsigned char* vrow = vstage + (quad * 4 + (col >> 2)) * kVPitch + 8 * (col & 3);
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn) {
-      const unsigned char* vcol = vstage + 2 * (16 * nn + col);
-      uint16_t e[8];
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          e[mt * 4 + i] = *reinterpret_cast<const uint16_t*>(vcol + (mt * 16 + quad * 4 + i) * kVPitch);
-      u32x4 a;
-      a.x = (uint32_t)e[0] | ((uint32_t)e[1] << 16);
-      a.y = (uint32_t)e[2] | ((uint32_t)e[3] << 16);
-      a.z = (uint32_t)e[4] | ((uint32_t)e[5] << 16);
-      a.w = (uint32_t)e[6] | ((uint32_t)e[7] << 16);
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
+      const bf16x8 a = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+          lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), pb[nt], acc_o[nt][nn], 0, 0, 0);
+        acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], acc_o[nt][nn], 0, 0, 0);
     }
     __builtin_amdgcn_wave_barrier();
+  };
+
+  u32x4 kA[2][4], vA[8];
+  load_tile(kA, vA, key_lo);
+  if constexpr (PF == 1) {
+    for (int t = 0; t < ntiles; ++t) process(kA, vA, t);
+  } else {
+    u32x4 kB[2][4], vB[8];
+    load_tile(kB, vB, key_lo + kKeysPerTile);
+    int t = 0;
+    for (; t + 1 < ntiles; t += 2) {
+      process(kA, vA, t);
+      process(kB, vB, t + 1);
+    }
+    if (t < ntiles) process(kA, vA, t);
   }
 
   // ---- merge the 4 wave states through LDS, one 16-head tile at a time
@@ -341,11 +417,21 @@ split_partial_kernel(Params p) {
         finish_row(M2 * kLn2, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
       } else {
         float* dst = p.o_part + ((int64_t)split * rows + row) * D + d8;
-        *reinterpret_cast<f32x4*>(dst) = f32x4{o8[0], o8[1], o8[2], o8[3]};
-        *reinterpret_cast<f32x4*>(dst + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
-        if (d8 == 0) {
-          p.m_part[split * rows + row] = Lsum > 0.f ? M2 * kLn2 : -INFINITY;
-          p.l_part[split * rows + row] = Lsum;
+        const float mval = Lsum > 0.f ? M2 * kLn2 : -INFINITY;
+        if (p.mode == kPartials) {
+          *reinterpret_cast<f32x4*>(dst) = f32x4{o8[0], o8[1], o8[2], o8[3]};
+          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
+          if (d8 == 0) {
+            p.m_part[split * rows + row] = mval;
+            p.l_part[split * rows + row] = Lsum;
+          }
+        } else {
+#pragma unroll
+          for (int dd = 0; dd < 8; dd += 2) store_shared2(dst + dd, o8[dd], o8[dd + 1]);
+          if (d8 == 0) {
+            store_shared(p.m_part + split * rows + row, mval);
+            store_shared(p.l_part + split * rows + row, Lsum);
+          }
         }
       }
     }
@@ -353,75 +439,111 @@ split_partial_kernel(Params p) {
   if (p.mode != kMerged) return;
 
   // ---- in-kernel merge: the last workgroup of this tile to arrive merges
-  //      the s chunk states in chunk order.  Release before the arrival
-  //      count, acquire after it; agent scope because the chunks of one tile
-  //      run on different XCDs with separate L2s.
+  //      the s chunk states in chunk order.  The chunks of one tile run on
+  //      different XCDs with separate L2s, so the states travel through
+  //      agent-coherent stores and loads; the arrival count is an
+  //      agent-scope atomic issued only after every state store completed.
   __shared__ int sh_last;
-  __threadfence();
-  __syncthreads();
+  order_after_memory_ops();   // this wave's state stores have completed
+  __syncthreads();            // ... and so have every other wave's
   if (tid == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t prev = __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int last = prev == (uint32_t)(p.s - 1);
     if (last) __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     sh_last = last;
+    order_before_memory_ops();
   }
   __syncthreads();
   if (!sh_last) return;
-  __threadfence();
+
+  // phase 1: every chunk max and sum of this tile's heads, all loads issued
+  // at once; phase 2: chunk weights per head; phase 3: weighted sum of the
+  // chunk outputs in chunk order.
+  float* sw = reinterpret_cast<float*>(smem);             // [hpt][kMaxSplits]: m, then weight
+  float* sl = sw + da::kMaxHeadsPerTile * DA_MAX_SPLITS;  // [hpt][kMaxSplits]: l
+  float* sML = sl + da::kMaxHeadsPerTile * DA_MAX_SPLITS; // [hpt][2]: M, L
+  const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
+  for (int it = tid; it < p.hpt * p.s; it += kThreads) {
+    const int h = it / p.s;
+    const int i = it - h * p.s;
+    const int64_t idx = (int64_t)i * rows + row0_tile + h;
+    sw[h * DA_MAX_SPLITS + i] = load_shared(p.m_part + idx);
+    sl[h * DA_MAX_SPLITS + i] = load_shared(p.l_part + idx);
+  }
+  __syncthreads();
+  if (tid < p.hpt) merge_weights(sw + tid * DA_MAX_SPLITS, sl + tid * DA_MAX_SPLITS, p.s, sML + 2 * tid);
+  __syncthreads();
 
   for (int it = tid; it < p.hpt * 16; it += kThreads) {
     const int h = it >> 4;
     const int d8 = (it & 15) * 8;
-    const int64_t row = (int64_t)b * p.H_Q + head0 + h;
-    float M = -INFINITY;
-    for (int i = 0; i < p.s; ++i) {
-      const float li = __hip_atomic_load(p.l_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float mi = __hip_atomic_load(p.m_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (li > 0.f) M = fmaxf(M, mi);
-    }
-    float Lsum = 0.f;
+    const int64_t row = row0_tile + h;
+    const float* w = sw + h * DA_MAX_SPLITS;
+    const float* l = sl + h * DA_MAX_SPLITS;
+    const float* src = p.o_part + row * D + d8;
+    const int64_t stride = rows * D;
     float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int i = 0; i < p.s; ++i) {
-      const float li = __hip_atomic_load(p.l_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (li > 0.f) {
-        const float mi = __hip_atomic_load(p.m_part + i * rows + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const float wt = __builtin_amdgcn_exp2f((mi - M) * kLog2e);
-        Lsum += wt * li;
-        const float* src = p.o_part + ((int64_t)i * rows + row) * D + d8;
-        const f32x4 a = *reinterpret_cast<const f32x4*>(src);
-        const f32x4 c = *reinterpret_cast<const f32x4*>(src + 4);
-        o8[0] += wt * a.x; o8[1] += wt * a.y; o8[2] += wt * a.z; o8[3] += wt * a.w;
-        o8[4] += wt * c.x; o8[5] += wt * c.y; o8[6] += wt * c.z; o8[7] += wt * c.w;
-      }
+    for (int i0 = 0; i0 < p.s; i0 += kMergeBatch) {
+      float a[kMergeBatch][8];
+#pragma unroll
+      for (int u = 0; u < kMergeBatch; ++u)
+        if (i0 + u < p.s)
+#pragma unroll
+          for (int dd = 0; dd < 8; dd += 2) load_shared2(src + (i0 + u) * stride + dd, a[u][dd], a[u][dd + 1]);
+#pragma unroll
+      for (int u = 0; u < kMergeBatch; ++u)
+        if (i0 + u < p.s) {
+          const float wi = w[i0 + u];
+          const bool live = l[i0 + u] > 0.f;
+#pragma unroll
+          for (int dd = 0; dd < 8; ++dd) o8[dd] = fmaf(wi, live ? a[u][dd] : 0.f, o8[dd]);
+        }
     }
-    finish_row(M, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+    finish_row(sML[2 * h], sML[2 * h + 1], o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
   }
 }
 
 // Standalone log-sum-exp combine: one wave64 per (b, h) row, 2 dims per
-// lane, chunks merged in index order.
+// lane.  Same three phases and the same arithmetic as the in-kernel merge,
+// so both produce identical bits for identical chunk states.
 __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
                                                             const float* __restrict__ m_part,
                                                             const float* __restrict__ l_part,
                                                             uint16_t* __restrict__ out, float* __restrict__ lse,
                                                             int s, int64_t rows) {
+  __shared__ float sw[4][DA_MAX_SPLITS];
+  __shared__ float sl[4][DA_MAX_SPLITS];
+  __shared__ float sML[4][2];
   const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  float M = -INFINITY;
-  for (int i = 0; i < s; ++i)
-    if (l_part[i * rows + row] > 0.f) M = fmaxf(M, m_part[i * rows + row]);
-  float Lsum = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int i = 0; i < s; ++i) {
-    const float li = l_part[i * rows + row];
-    if (li > 0.f) {
-      const float wt = __builtin_amdgcn_exp2f((m_part[i * rows + row] - M) * kLog2e);
-      Lsum += wt * li;
-      const float2 x = *reinterpret_cast<const float2*>(o_part + ((int64_t)i * rows + row) * D + 2 * lane);
-      o0 += wt * x.x;
-      o1 += wt * x.y;
-    }
+  const int w = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;  // waves are independent: no workgroup barrier below
+  for (int i = lane; i < s; i += 64) {
+    sw[w][i] = m_part[i * rows + row];
+    sl[w][i] = l_part[i * rows + row];
   }
+  __builtin_amdgcn_wave_barrier();
+  if (lane == 0) merge_weights(sw[w], sl[w], s, sML[w]);
+  __builtin_amdgcn_wave_barrier();
+  const float* src = o_part + row * D + 2 * lane;
+  const int64_t stride = rows * D;
+  float o0 = 0.f, o1 = 0.f;
+  for (int i0 = 0; i0 < s; i0 += kMergeBatch) {
+    float2 a[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u)
+      if (i0 + u < s) a[u] = *reinterpret_cast<const float2*>(src + (i0 + u) * stride);
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u)
+      if (i0 + u < s) {
+        const float wi = sw[w][i0 + u];
+        const bool live = sl[w][i0 + u] > 0.f;
+        o0 = fmaf(wi, live ? a[u].x : 0.f, o0);
+        o1 = fmaf(wi, live ? a[u].y : 0.f, o1);
+      }
+  }
+  const float M = sML[w][0];
+  const float Lsum = sML[w][1];
   const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
   *reinterpret_cast<uint32_t*>(out + row * D + 2 * lane) = pack_bf16x2(o0 * inv, o1 * inv);
   if (lse && lane == 0) lse[row] = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
@@ -476,8 +598,8 @@ int ensure_gfx950() {
 
 int launch_partial(const Params& prm, int hpt, int grid, hipStream_t stream) {
   void* args[] = {const_cast<Params*>(&prm)};
-  const void* fn = hpt <= 16 ? reinterpret_cast<const void*>(&split_partial_kernel<1>)
-                             : reinterpret_cast<const void*>(&split_partial_kernel<2>);
+  const void* fn = hpt <= 16 ? reinterpret_cast<const void*>(&split_partial_kernel<1, 2>)
+                             : reinterpret_cast<const void*>(&split_partial_kernel<2, 1>);
   hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, kSmemBytes, stream);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "split partial launch: %s", hipGetErrorString(e));
   return DA_OK;

@@ -141,11 +141,13 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s) {
   WorkspaceLayout w{};
   const size_t rows = (size_t)B * H_Q;
-  w.o_off = 0;
+  // Counters first: their place depends only on B*H_Q, so one workspace
+  // can serve calls with any split count without clearing it again.
+  w.cnt_off = 0;
+  w.o_off = align256(rows * sizeof(uint32_t));
   w.m_off = align256(w.o_off + (size_t)s * rows * d * sizeof(float));
   w.l_off = align256(w.m_off + (size_t)s * rows * sizeof(float));
-  w.cnt_off = align256(w.l_off + (size_t)s * rows * sizeof(float));
-  w.total = align256(w.cnt_off + rows * sizeof(uint32_t));
+  w.total = align256(w.l_off + (size_t)s * rows * sizeof(float));
   return w;
 }
 

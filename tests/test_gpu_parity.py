@@ -250,3 +250,24 @@ def test_graph_replay_matches_eager(s):
         # eager work between replays
         again, _ = run(q, k, v, cu, sh.L_K, s, 1)
         assert torch.equal(again.view(torch.int16), eager.view(torch.int16))
+
+
+def test_workspace_reused_across_split_counts():
+    """One workspace serves calls with different split counts back to back:
+    the arrival counters sit at an offset that depends only on B*H_Q."""
+    sh = config_shapes(2)[3]
+    inp = make_inputs(sh)
+    O, _ = decode_attention(inp.q, inp.k, inp.v)
+    q, k, v, cu = dev_inputs(inp)
+    ws = torch.zeros(da.da_workspace_bytes(sh.B, sh.H_Q, 128, 64), dtype=torch.uint8, device="cuda")
+    outs = {}
+    for s in (64, 8, 2, 5, 8, 64, 3):
+        say(f"shared workspace s={s}")
+        out = da.da_decode_attn(q, k, v, num_splits=s, pack_gqa=1, workspace=ws)
+        torch.cuda.synchronize()
+        assert_parity(out, O, f"shared workspace s={s}")
+        if s in outs:
+            assert torch.equal(out.view(torch.int16), outs[s].view(torch.int16))
+        outs[s] = out
+    nrows = sh.B * sh.H_Q
+    assert torch.all(ws[: nrows * 4] == 0)        # counters left at zero
