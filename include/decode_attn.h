@@ -69,6 +69,7 @@ typedef struct da_plan {
   int32_t tiles;          /* work tiles = B * H_Q / heads_per_tile (Section 2.1: Batch x H_KV when packed) */
   int32_t grid;           /* workgroups launched = tiles * num_splits */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
+  int32_t group_waves;    /* wave64s per workgroup (4 or 8); each takes a contiguous part of the chunk */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split

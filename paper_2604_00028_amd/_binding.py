@@ -48,6 +48,7 @@ class DaPlan(ctypes.Structure):
         ("tiles", ctypes.c_int32),
         ("grid", ctypes.c_int32),
         ("num_cus", ctypes.c_int32),
+        ("group_waves", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

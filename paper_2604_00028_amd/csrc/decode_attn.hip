@@ -13,26 +13,27 @@
 // 5.3), so one launch covers the whole call.
 //
 // gfx950 mapping:
-//  * 256 threads = 4 wave64s.  The chunk is cut into 4 contiguous key ranges,
-//    one per wave; each wave walks its range in tiles of 32 keys and the 4
-//    wave states are merged through LDS in wave order.
+//  * W = 4 wave64s per workgroup, one per SIMD.  The chunk is cut into W
+//    contiguous key ranges, one per wave; each wave walks its range in tiles
+//    of 32 keys and the W wave states are merged through LDS in wave order.
 //  * Scores S^T[key, head] = K . Q^T on MFMA v_mfma_f32_16x16x32_bf16: keys
 //    are the 16 rows, the packed query heads the 16 columns (two column
 //    tiles when a KV head serves up to 32 query heads).  K is fetched
 //    straight into the MFMA A-operand layout: lane (row r, group q) loads the
 //    64 contiguous bytes of dims [32q, 32q+32) of key r.
 //  * Online softmax on the MFMA result layout: every lane holds 8 scores of
-//    one head column; the tile max needs two cross-lane steps (lanes ^16,
-//    ^32); exp2 on the hardware v_exp_f32 with the scale folded as
-//    scale*log2(e); fp32 running state.
+//    one head column; the tile max and sum over the 4 row groups take two
+//    v_permlane16/32_swap steps; exp2 on the hardware v_exp_f32 with the
+//    scale folded as scale*log2(e); fp32 running state; the output is only
+//    rescaled when some column's running max moved.
 //  * Output O^T[dim, head] += V^T . P^T on the same MFMA: the P operand is
 //    the lane's own 8 probabilities (bf16), so softmax never moves data
 //    across lanes; V^T comes from a per-wave LDS tile of 32 keys (16-byte
 //    coalesced loads, 288-byte row pitch, ds_read_b64_tr_b16 transposing
 //    reads: two per 16 output dims).
-//  * K/V loads are raw buffer loads bounded by the sequence: keys outside the
-//    wave's range use an out-of-range offset, which returns zeros without
-//    touching memory, so ragged tails cost no traffic.
+//  * K/V loads are raw buffer loads whose record count ends at the wave's
+//    last key: keys past it read as zeros without touching memory, so ragged
+//    tails cost no traffic and no load needs a mask or a branch.
 //  * Workgroup ids are remapped so consecutive tiles land on the same XCD
 //    (dispatch is round-robin over the 8 XCDs): with packing off, the query
 //    heads of one KV head then share that XCD's L2.
@@ -42,6 +43,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "decode_attn.h"
 #include "plan.h"
@@ -49,16 +51,19 @@
 namespace {
 
 constexpr int D = DA_HEAD_DIM;
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kKeysPerTile = 32;
-constexpr int kMergeBatch = 8;                               // chunk states loaded per batch in a merge
-constexpr int kVPitch = 288;                                  // bytes per staged V row
-constexpr int kStageBytes = kWaves * kKeysPerTile * kVPitch;  // V staging, all waves
-constexpr int kMergeBytes = kWaves * D * 16 * 4;              // wave O^T states, one head tile
-constexpr int kStatBytes = 2 * kWaves * 16 * 4;               // wave m and l, one head tile
-constexpr int kSmemBytes = (kStageBytes > kMergeBytes ? kStageBytes : kMergeBytes) + kStatBytes;
-static_assert(2 * da::kMaxHeadsPerTile * DA_MAX_SPLITS * 4 + da::kMaxHeadsPerTile * 8 <= kSmemBytes,
+constexpr int kVPitch = 288;                 // bytes per staged V row (256 + 32 pad)
+constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
+constexpr int kCoherent = 16;                // buffer cache policy: sc1 (agent coherence)
+constexpr int kGroupWaves = 4;               // wave64s per workgroup (one per SIMD of a CU)
+
+// LDS of one workgroup of W waves: the per-wave V stage, reused for the
+// wave-state merge ([W][128 dims][16 heads] fp32) and its per-wave m and l.
+constexpr int smem_bytes(int W) {
+  return (W * kKeysPerTile * kVPitch > W * D * 16 * 4 ? W * kKeysPerTile * kVPitch : W * D * 16 * 4) +
+         2 * W * 16 * 4;
+}
+static_assert(2 * da::kMaxHeadsPerTile * DA_MAX_SPLITS * 4 + da::kMaxHeadsPerTile * 8 <= smem_bytes(4),
               "merge scratch must fit the workgroup's LDS");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -66,8 +71,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 enum Mode : int { kDirect = 0, kPartials = 1, kMerged = 2 };
@@ -87,17 +92,22 @@ struct Params {
   float scale_log2;     // softmax scale * log2(e)
 };
 
-__device__ __forceinline__ float wave_max_rows(float x) {
-  // max over lanes {l, l^16, l^32, l^48}: the 4 row groups of one column
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
+// Max and sum over lanes {l, l^16, l^32, l^48}: the 4 row groups of one MFMA
+// column.  permlane16_swap(x, x) hands every lane the pair (x[l], x[l^16])
+// and permlane32_swap(x, x) the pair (x[l], x[l^32]), in the same order on
+// both lanes of a pair, so every lane of a column ends with identical bits.
+__device__ __forceinline__ float max_rows(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto c = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(c[0]), __uint_as_float(c[1]));
 }
 
-__device__ __forceinline__ float wave_sum_rows(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
+__device__ __forceinline__ float sum_rows(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto c = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(c[0]) + __uint_as_float(c[1]);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -111,29 +121,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
-// Chunk states shared between workgroups of one launch.  An agent-scope
-// fence on gfx950 writes back and invalidates the whole L2 of the XCD, which
-// costs microseconds per workgroup.  Instead the states are written and read
-// with agent-scope relaxed atomics, which go through to the point of
-// coherence shared by all XCDs, and the fences below only order them:
-// wait until this wave's memory operations have completed (s_waitcnt with
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Chunk states shared between the workgroups of one launch travel through
+// memory with the sc1 cache policy (coherent at agent scope: written through
+// and read past the XCD-private L2s).  An agent-scope fence would instead
+// write back and invalidate the whole L2 of the XCD, which costs microseconds
+// per workgroup on gfx950.  The fences below therefore only order: they wait
+// until this wave's memory operations have completed (s_waitcnt with
 // vmcnt = 0; expcnt = 7 and lgkmcnt = 15 leave those counters unchecked).
-__device__ __forceinline__ void store_shared(float* dst, float v) {
-  __hip_atomic_store(dst, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void store_shared2(float* dst, float a, float b) {
-  const uint64_t bits = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(dst), bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_shared(const float* src) {
-  return __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void load_shared2(const float* src, float& a, float& b) {
-  const uint64_t bits =
-      __hip_atomic_load(reinterpret_cast<const uint64_t*>(src), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  a = __uint_as_float((uint32_t)bits);
-  b = __uint_as_float((uint32_t)(bits >> 32));
-}
 __device__ __forceinline__ void order_after_memory_ops() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -143,17 +141,21 @@ __device__ __forceinline__ void order_before_memory_ops() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Normalise 8 output columns of one head by the softmax sum and store them as
-// bf16; M is the row max in natural-log units, for the log-sum-exp.
-__device__ __forceinline__ void finish_row(float M, float Lsum, const float* o8, uint16_t* out_row,
+// Normalise N output columns of one head by the softmax sum and store them
+// as bf16; M is the row max in natural-log units, for the log-sum-exp.
+template <int N>
+__device__ __forceinline__ void finish_row(float M, float Lsum, const float* o, uint16_t* out_row,
                                            float* lse_slot) {
   const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
-  u32x4 w;
-  w.x = pack_bf16x2(o8[0] * inv, o8[1] * inv);
-  w.y = pack_bf16x2(o8[2] * inv, o8[3] * inv);
-  w.z = pack_bf16x2(o8[4] * inv, o8[5] * inv);
-  w.w = pack_bf16x2(o8[6] * inv, o8[7] * inv);
-  *reinterpret_cast<u32x4*>(out_row) = w;
+  uint32_t w[N / 2];
+#pragma unroll
+  for (int j = 0; j < N / 2; ++j) w[j] = pack_bf16x2(o[2 * j] * inv, o[2 * j + 1] * inv);
+  if constexpr (N == 8) {
+    *reinterpret_cast<u32x4*>(out_row) = u32x4{w[0], w[1], w[2], w[3]};
+  } else {
+    static_assert(N == 4, "4 or 8 columns");
+    *reinterpret_cast<uint2*>(out_row) = make_uint2(w[0], w[1]);
+  }
   if (lse_slot) *lse_slot = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
 }
 
@@ -176,14 +178,16 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
 }
 
 // NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
-// 32).  PF: 32-key tiles of K/V loads each wave keeps in flight.
-template <int NT, int PF>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+// 32).  W: waves per workgroup.
+template <int NT, int W>
+__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
+  constexpr int kThreads = 64 * W;
+  constexpr int kSmem = smem_bytes(W);
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;   // MFMA column: head within a 16-head tile
   const int quad = lane >> 4;  // MFMA row group
 
@@ -210,20 +214,24 @@ split_partial_kernel(Params p) {
   const int c0 = (int)(((int64_t)L * split) / p.s);
   const int c1 = (int)(((int64_t)L * (split + 1)) / p.s);
   const int n = c1 - c0;
-  const int key_lo = c0 + (int)(((int64_t)n * wave) / kWaves);
-  const int key_hi = c0 + (int)(((int64_t)n * (wave + 1)) / kWaves);
+  const int key_lo = c0 + (int)(((int64_t)n * wave) / W);
+  const int key_hi = c0 + (int)(((int64_t)n * (wave + 1)) / W);
 
-  // ---- buffer resources over this (sequence, KV head): rows of H_KV*256 bytes
+  // ---- buffer resources over this (sequence, KV head), rows of H_KV*256
+  //      bytes, ending at this wave's last key: any key >= key_hi is out of
+  //      range and reads as zeros without touching memory, so no load needs
+  //      a mask and ragged tails cost no traffic
   const uint32_t rs = (uint32_t)p.H_KV * (D * 2);
   const int64_t base_elems = (row0 * p.H_KV + kvh) * D;
-  const uint32_t nrec = (uint32_t)L * rs;
-  const __amdgpu_buffer_rsrc_t krs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(p.k + base_elems), (short)0, (int)nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(p.v + base_elems), (short)0, (int)nrec, 0x00020000);
+  const uint32_t lim = (uint32_t)key_hi * rs;
+  const __amdgpu_buffer_rsrc_t krs = make_rsrc(p.k + base_elems, lim);
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(p.v + base_elems, lim);
 
-  // ---- Q^T as the MFMA B operand: lane holds dims [32*quad + 8j, +8) of
-  //      head column `col` for k-step j (zeros for padding columns)
+  // ---- Q^T as the MFMA B operand.  The reduction index of the product may
+  //      map to head dims in any order as long as K and Q agree: k-step j,
+  //      lane group `quad` covers dims [32j + 8*quad, +8), so each K load
+  //      instruction reads one contiguous 64-byte segment of every row.
+  //      Lane holds those dims of head column `col` (zeros for padding).
   bf16x8 qreg[NT][4];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -232,7 +240,7 @@ split_partial_kernel(Params p) {
     for (int j = 0; j < 4; ++j) {
       u32x4 x = {0u, 0u, 0u, 0u};
       if (h < p.hpt)
-        x = *reinterpret_cast<const u32x4*>(p.q + ((int64_t)b * p.H_Q + head0 + h) * D + 32 * quad + 8 * j);
+        x = *reinterpret_cast<const u32x4*>(p.q + ((int64_t)b * p.H_Q + head0 + h) * D + 32 * j + 8 * quad);
       qreg[nt][j] = as_bf16x8(x);
     }
   }
@@ -251,26 +259,27 @@ split_partial_kernel(Params p) {
   const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
 
   // K/V of one 32-key tile: K in the MFMA A layout (two 16-key row blocks x
-  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.
-  auto load_tile = [&](u32x4 (&kr)[2][4], u32x4 (&vr)[8], int kb) {
+  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.  Per-lane byte
+  // offsets of the wave's first tile; tile t adds t*32 rows.
+  const uint32_t koff0 = (uint32_t)(key_lo + col) * rs + 16u * quad;
+  const uint32_t voff0 = (uint32_t)(key_lo + quad) * rs + 16u * col;
+  const uint32_t tile_step = kKeysPerTile * rs;
+  u32x4 kreg[2][4], vreg[8];
+  auto load_tile = [&](int t) {
+    const uint32_t adv = (uint32_t)t * tile_step;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      const int key = kb + mt * 16 + col;
-      const uint32_t off = key < key_hi ? (uint32_t)key * rs + 64u * quad : nrec;
+      const uint32_t off = koff0 + adv + (uint32_t)mt * 16u * rs;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kr[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u * j, 0, 0);
+      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 64u * j, 0, 0);
     }
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      const int key = kb + 4 * jj + quad;
-      const uint32_t off = key < key_hi ? (uint32_t)key * rs + 16u * col : nrec;
-      vr[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off, 0, 0);
-    }
+    for (int jj = 0; jj < 8; ++jj)
+      vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff0 + adv + (uint32_t)jj * 4u * rs, 0, 0);
   };
 
-  // One tile: scores, V to LDS, refill the registers with tile t + PF,
-  // online softmax, then the PV product.
-  auto process = [&](u32x4 (&kr)[2][4], u32x4 (&vr)[8], int t) {
+  load_tile(0);
+  for (int t = 0; t < ntiles; ++t) {
     const int kb = key_lo + t * kKeysPerTile;
     const int nvalid = key_hi - kb;  // >= 1
 
@@ -283,20 +292,19 @@ split_partial_kernel(Params p) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[mt][j]), qreg[nt][j], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[mt][j]), qreg[nt][j], acc, 0, 0, 0);
         sc[nt][mt] = acc;
       }
 
     // stage V rows in LDS (row-major, padded pitch)
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj)
-      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vr[jj];
+      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
 
-    // refill: keep PF tiles of loads in flight while this one is reduced.
-    // Unconditional on purpose: past the wave's range every offset is out of
-    // range (zeros, no memory traffic), and branch-free loads let the
-    // compiler wait for exactly the tile it needs instead of for all loads.
-    load_tile(kr, vr, kb + PF * kKeysPerTile);
+    // prefetch the next tile while this one is reduced; unconditional, so
+    // the compiler waits for exactly the tile in use (past the wave's range
+    // every offset is out of range: zeros, no memory traffic)
+    load_tile(t + 1);
 
     // online softmax per head column
     bf16x8 pb[NT];
@@ -313,7 +321,7 @@ split_partial_kernel(Params p) {
           x[mt * 4 + i] = s2;
           tmax = fmaxf(tmax, s2);
         }
-      tmax = wave_max_rows(tmax);
+      tmax = max_rows(tmax);
       const float m_new = fmaxf(m_run[nt], tmax);
       const float alpha = __builtin_amdgcn_exp2f(m_run[nt] - m_new);
       float psum = 0.f;
@@ -324,8 +332,12 @@ split_partial_kernel(Params p) {
       }
       l_run[nt] = l_run[nt] * alpha + psum;
       m_run[nt] = m_new;
+      // alpha == 1 exactly when the column max did not move: skip the
+      // multiply by one (a wave-uniform branch)
+      if (__any(alpha != 1.0f)) {
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] *= alpha;
+        for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] *= alpha;
+      }
       u32x4 pk;
       pk.x = pack_bf16x2(x[0], x[1]);
       pk.y = pack_bf16x2(x[2], x[3]);
@@ -348,39 +360,27 @@ split_partial_kernel(Params p) {
     for (int nn = 0; nn < 8; ++nn) {
       const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
       const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
-      const bf16x8 a = __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
-          lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+      const bf16x8 a = __builtin_bit_cast(bf16x8, s16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
         acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], acc_o[nt][nn], 0, 0, 0);
     }
     __builtin_amdgcn_wave_barrier();
-  };
-
-  u32x4 kA[2][4], vA[8];
-  load_tile(kA, vA, key_lo);
-  if constexpr (PF == 1) {
-    for (int t = 0; t < ntiles; ++t) process(kA, vA, t);
-  } else {
-    u32x4 kB[2][4], vB[8];
-    load_tile(kB, vB, key_lo + kKeysPerTile);
-    int t = 0;
-    for (; t + 1 < ntiles; t += 2) {
-      process(kA, vA, t);
-      process(kB, vB, t + 1);
-    }
-    if (t < ntiles) process(kA, vA, t);
   }
 
-  // ---- merge the 4 wave states through LDS, one 16-head tile at a time
+  // ---- merge the W wave states through LDS, one 16-head tile at a time
   float* sm_o = reinterpret_cast<float*>(smem);                 // [wave][dim][16]
-  float* sm_m = reinterpret_cast<float*>(smem + kSmemBytes - kStatBytes);
-  float* sm_l = sm_m + kWaves * 16;
+  float* sm_m = reinterpret_cast<float*>(smem + kSmem - 2 * W * 16 * 4);
+  float* sm_l = sm_m + W * 16;
   const int64_t rows = (int64_t)p.B * p.H_Q;
+  const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
+  // chunk-state outputs of this workgroup: uniform base, small per-lane offsets
+  const __amdgpu_buffer_rsrc_t ors =
+      make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
 
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const float lsum = wave_sum_rows(l_run[nt]);
+    const float lsum = sum_rows(l_run[nt]);
     __syncthreads();
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn)
@@ -398,12 +398,12 @@ split_partial_kernel(Params p) {
       const int d8 = (it & 15) * 8;    // first of 8 dims
       float M2 = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w)
+      for (int w = 0; w < W; ++w)
         if (sm_l[w * 16 + hc] > 0.f) M2 = fmaxf(M2, sm_m[w * 16 + hc]);
       float Lsum = 0.f;
       float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
+      for (int w = 0; w < W; ++w) {
         const float lw = sm_l[w * 16 + hc];
         if (lw > 0.f) {
           const float wt = __builtin_amdgcn_exp2f(sm_m[w * 16 + hc] - M2);
@@ -412,25 +412,30 @@ split_partial_kernel(Params p) {
           for (int dd = 0; dd < 8; ++dd) o8[dd] += wt * sm_o[(w * D + d8 + dd) * 16 + hc];
         }
       }
-      const int64_t row = (int64_t)b * p.H_Q + head0 + nt * 16 + hc;
+      const int h = nt * 16 + hc;
+      const int64_t row = row0_tile + h;
       if (p.mode == kDirect) {
-        finish_row(M2 * kLn2, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+        finish_row<8>(M2 * kLn2, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
       } else {
-        float* dst = p.o_part + ((int64_t)split * rows + row) * D + d8;
         const float mval = Lsum > 0.f ? M2 * kLn2 : -INFINITY;
+        const u32x4 lo = {__float_as_uint(o8[0]), __float_as_uint(o8[1]), __float_as_uint(o8[2]),
+                          __float_as_uint(o8[3])};
+        const u32x4 hi = {__float_as_uint(o8[4]), __float_as_uint(o8[5]), __float_as_uint(o8[6]),
+                          __float_as_uint(o8[7])};
+        const uint32_t off = (uint32_t)(h * D + d8) * 4u;
         if (p.mode == kPartials) {
-          *reinterpret_cast<f32x4*>(dst) = f32x4{o8[0], o8[1], o8[2], o8[3]};
-          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{o8[4], o8[5], o8[6], o8[7]};
+          __builtin_amdgcn_raw_buffer_store_b128(lo, ors, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(hi, ors, off + 16u, 0, 0);
           if (d8 == 0) {
             p.m_part[split * rows + row] = mval;
             p.l_part[split * rows + row] = Lsum;
           }
         } else {
-#pragma unroll
-          for (int dd = 0; dd < 8; dd += 2) store_shared2(dst + dd, o8[dd], o8[dd + 1]);
+          __builtin_amdgcn_raw_buffer_store_b128(lo, ors, off, 0, kCoherent);
+          __builtin_amdgcn_raw_buffer_store_b128(hi, ors, off + 16u, 0, kCoherent);
           if (d8 == 0) {
-            store_shared(p.m_part + split * rows + row, mval);
-            store_shared(p.l_part + split * rows + row, Lsum);
+            __hip_atomic_store(p.m_part + split * rows + row, mval, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(p.l_part + split * rows + row, Lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
         }
       }
@@ -456,56 +461,131 @@ split_partial_kernel(Params p) {
   __syncthreads();
   if (!sh_last) return;
 
-  // phase 1: every chunk max and sum of this tile's heads, all loads issued
-  // at once; phase 2: chunk weights per head; phase 3: weighted sum of the
-  // chunk outputs in chunk order.
+  // All loads of the merge are issued before any of them is waited for: the
+  // chunk maxima and sums of this tile's heads, and the first batch of
+  // chunk outputs of this thread's (head, 4 dims) items.  Then the weights
+  // per head (one thread per head, chunk order), then the weighted sums.
   float* sw = reinterpret_cast<float*>(smem);             // [hpt][kMaxSplits]: m, then weight
   float* sl = sw + da::kMaxHeadsPerTile * DA_MAX_SPLITS;  // [hpt][kMaxSplits]: l
   float* sML = sl + da::kMaxHeadsPerTile * DA_MAX_SPLITS; // [hpt][2]: M, L
-  const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
-  for (int it = tid; it < p.hpt * p.s; it += kThreads) {
-    const int h = it / p.s;
-    const int i = it - h * p.s;
-    const int64_t idx = (int64_t)i * rows + row0_tile + h;
-    sw[h * DA_MAX_SPLITS + i] = load_shared(p.m_part + idx);
-    sl[h * DA_MAX_SPLITS + i] = load_shared(p.l_part + idx);
+  const int nml = p.hpt * p.s;
+  constexpr int kMlPerThread = (da::kMaxHeadsPerTile * DA_MAX_SPLITS + kThreads - 1) / kThreads;
+  float mv[kMlPerThread], lv[kMlPerThread];
+#pragma unroll
+  for (int u = 0; u < kMlPerThread; ++u) {
+    const int it = tid + u * kThreads;
+    if (it < nml) {
+      const int h = it / p.s;
+      const int i = it - h * p.s;
+      const int64_t idx = (int64_t)i * rows + row0_tile + h;
+      mv[u] = __hip_atomic_load(p.m_part + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      lv[u] = __hip_atomic_load(p.l_part + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  // This thread's items: (head, 4 dims); an item sits at byte 16*item of a
+  // chunk's state rows, chunk i at byte i*split_stride.  Loads for all of a
+  // thread's items are in flight together: with one item per thread a batch
+  // covers 16 chunks, with up to kMaxItems items it covers 16/kMaxItems
+  // chunks of each.  The first batch is issued before the weights exist.
+  constexpr int kMaxItems = (da::kMaxHeadsPerTile * (D / 4) + kThreads - 1) / kThreads;
+  constexpr int kMultiBatch = kMergeBatch / kMaxItems;
+  const int nitems = p.hpt * (D / 4);
+  const uint32_t split_stride = (uint32_t)(rows * D * 4);
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(p.o_part + row0_tile * D, (uint32_t)p.s * split_stride);
+  auto state_load = [&](int it, int i) {
+    return __builtin_amdgcn_raw_buffer_load_b128(mrs, (uint32_t)it * 16u + (uint32_t)i * split_stride, 0, kCoherent);
+  };
+  const bool one_item = nitems <= kThreads;
+  u32x4 ob[kMergeBatch];
+  if (one_item) {
+    if (tid < nitems) {
+#pragma unroll
+      for (int u = 0; u < kMergeBatch; ++u)
+        if (u < p.s) ob[u] = state_load(tid, u);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kMaxItems; ++r)
+#pragma unroll
+      for (int u = 0; u < kMultiBatch; ++u)
+        if (tid + r * kThreads < nitems && u < p.s) ob[r * kMultiBatch + u] = state_load(tid + r * kThreads, u);
+  }
+#pragma unroll
+  for (int u = 0; u < kMlPerThread; ++u) {
+    const int it = tid + u * kThreads;
+    if (it < nml) {
+      const int h = it / p.s;
+      const int i = it - h * p.s;
+      sw[h * DA_MAX_SPLITS + i] = mv[u];
+      sl[h * DA_MAX_SPLITS + i] = lv[u];
+    }
   }
   __syncthreads();
   if (tid < p.hpt) merge_weights(sw + tid * DA_MAX_SPLITS, sl + tid * DA_MAX_SPLITS, p.s, sML + 2 * tid);
   __syncthreads();
 
-  for (int it = tid; it < p.hpt * 16; it += kThreads) {
-    const int h = it >> 4;
-    const int d8 = (it & 15) * 8;
-    const int64_t row = row0_tile + h;
-    const float* w = sw + h * DA_MAX_SPLITS;
-    const float* l = sl + h * DA_MAX_SPLITS;
-    const float* src = p.o_part + row * D + d8;
-    const int64_t stride = rows * D;
-    float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int i0 = 0; i0 < p.s; i0 += kMergeBatch) {
-      float a[kMergeBatch][8];
+  // weighted sum of one item over chunks [i0, i0 + N) clipped to s, from
+  // registers (compile-time indices only, so `src` stays in registers)
+  auto accumulate = [&](auto n_tag, int it, float (&o4)[4], const u32x4* src, int i0) {
+    constexpr int N = decltype(n_tag)::value;
+    const float* w = sw + (it >> 5) * DA_MAX_SPLITS;
+    const float* l = sl + (it >> 5) * DA_MAX_SPLITS;
 #pragma unroll
-      for (int u = 0; u < kMergeBatch; ++u)
-        if (i0 + u < p.s)
+    for (int u = 0; u < N; ++u) {
+      if (i0 + u < p.s) {
+        const float wi = w[i0 + u];
+        const bool live = l[i0 + u] > 0.f;
 #pragma unroll
-          for (int dd = 0; dd < 8; dd += 2) load_shared2(src + (i0 + u) * stride + dd, a[u][dd], a[u][dd + 1]);
-#pragma unroll
-      for (int u = 0; u < kMergeBatch; ++u)
-        if (i0 + u < p.s) {
-          const float wi = w[i0 + u];
-          const bool live = l[i0 + u] > 0.f;
-#pragma unroll
-          for (int dd = 0; dd < 8; ++dd) o8[dd] = fmaf(wi, live ? a[u][dd] : 0.f, o8[dd]);
-        }
+        for (int dd = 0; dd < 4; ++dd) o4[dd] = fmaf(wi, live ? __uint_as_float(src[u][dd]) : 0.f, o4[dd]);
+      }
     }
-    finish_row(sML[2 * h], sML[2 * h + 1], o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+  };
+  auto finish_item = [&](int it, const float (&o4)[4]) {
+    const int h = it >> 5;
+    const int d4 = (it & 31) * 4;
+    const int64_t row = row0_tile + h;
+    finish_row<4>(sML[2 * h], sML[2 * h + 1], o4, p.out + row * D + d4, (p.lse && d4 == 0) ? p.lse + row : nullptr);
+  };
+
+  if (one_item) {
+    if (tid < nitems) {
+      float o4[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int i0 = 0; i0 < p.s; i0 += kMergeBatch) {
+        if (i0 > 0) {
+#pragma unroll
+          for (int u = 0; u < kMergeBatch; ++u)
+            if (i0 + u < p.s) ob[u] = state_load(tid, i0 + u);
+        }
+        accumulate(std::integral_constant<int, kMergeBatch>{}, tid, o4, ob, i0);
+      }
+      finish_item(tid, o4);
+    }
+  } else {
+    float o4[kMaxItems][4] = {};
+    for (int i0 = 0; i0 < p.s; i0 += kMultiBatch) {
+      if (i0 > 0) {
+#pragma unroll
+        for (int r = 0; r < kMaxItems; ++r)
+#pragma unroll
+          for (int u = 0; u < kMultiBatch; ++u)
+            if (tid + r * kThreads < nitems && i0 + u < p.s)
+              ob[r * kMultiBatch + u] = state_load(tid + r * kThreads, i0 + u);
+      }
+#pragma unroll
+      for (int r = 0; r < kMaxItems; ++r)
+        if (tid + r * kThreads < nitems)
+          accumulate(std::integral_constant<int, kMultiBatch>{}, tid + r * kThreads, o4[r], ob + r * kMultiBatch, i0);
+    }
+#pragma unroll
+    for (int r = 0; r < kMaxItems; ++r)
+      if (tid + r * kThreads < nitems) finish_item(tid + r * kThreads, o4[r]);
   }
 }
 
 // Standalone log-sum-exp combine: one wave64 per (b, h) row, 2 dims per
-// lane.  Same three phases and the same arithmetic as the in-kernel merge,
-// so both produce identical bits for identical chunk states.
+// lane.  Same phases and the same arithmetic as the in-kernel merge (loads
+// issued together, weights in chunk order, weighted sum in chunk order), so
+// both produce identical bits for identical chunk states.
 __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
                                                             const float* __restrict__ m_part,
                                                             const float* __restrict__ l_part,
@@ -518,6 +598,12 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
   const int w = threadIdx.x >> 6;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;  // waves are independent: no workgroup barrier below
+  const float* src = o_part + row * D + 2 * lane;
+  const int64_t stride = rows * D;
+  float2 a[kMergeBatch];
+#pragma unroll
+  for (int u = 0; u < kMergeBatch; ++u)
+    if (u < s) a[u] = *reinterpret_cast<const float2*>(src + u * stride);
   for (int i = lane; i < s; i += 64) {
     sw[w][i] = m_part[i * rows + row];
     sl[w][i] = l_part[i * rows + row];
@@ -525,14 +611,13 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
   __builtin_amdgcn_wave_barrier();
   if (lane == 0) merge_weights(sw[w], sl[w], s, sML[w]);
   __builtin_amdgcn_wave_barrier();
-  const float* src = o_part + row * D + 2 * lane;
-  const int64_t stride = rows * D;
   float o0 = 0.f, o1 = 0.f;
   for (int i0 = 0; i0 < s; i0 += kMergeBatch) {
-    float2 a[kMergeBatch];
+    if (i0 > 0) {
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u)
-      if (i0 + u < s) a[u] = *reinterpret_cast<const float2*>(src + (i0 + u) * stride);
+      for (int u = 0; u < kMergeBatch; ++u)
+        if (i0 + u < s) a[u] = *reinterpret_cast<const float2*>(src + (i0 + u) * stride);
+    }
 #pragma unroll
     for (int u = 0; u < kMergeBatch; ++u)
       if (i0 + u < s) {
@@ -574,9 +659,8 @@ int query_device(int* cus, int* is950) {
 
 bool aligned(const void* ptr, uintptr_t a) { return ((uintptr_t)ptr & (a - 1)) == 0; }
 
-int check_inputs(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q,
-                 int H_KV, int L_K_max, int d, float** lse_check) {
-  (void)lse_check;
+int check_inputs(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q, int H_KV,
+                 int L_K_max, int d) {
   int rc = da::check_shape(B, H_Q, H_KV, L_K_max, d);
   if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
   // With L_K_max == 0 no key is ever read, so an empty cache may be NULL.
@@ -588,6 +672,14 @@ int check_inputs(const void* q, const void* k, const void* v, const int32_t* cu,
   return DA_OK;
 }
 
+// Chunk states are addressed with 32-bit buffer offsets.
+int check_state_size(int B, int H_Q, int s) {
+  if ((int64_t)s * B * H_Q * D * 4 >= ((int64_t)1 << 31))
+    return da::fail(DA_ERR_SHAPE, "num_splits*B*H_Q*D*4 = %lld bytes of chunk state exceed 2 GiB",
+                    (long long)s * B * H_Q * D * 4);
+  return DA_OK;
+}
+
 int ensure_gfx950() {
   int cus = 0, is950 = 0;
   int rc = query_device(&cus, &is950);
@@ -596,17 +688,23 @@ int ensure_gfx950() {
   return DA_OK;
 }
 
-int launch_partial(const Params& prm, int hpt, int grid, hipStream_t stream) {
+template <int NT, int W>
+const void* kernel_ptr() {
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W>);
+}
+
+int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
+  constexpr int W = kGroupWaves;
+  if (pl.group_waves != W) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", pl.group_waves);
+  const void* fn = pl.heads_per_tile <= 16 ? kernel_ptr<1, W>() : kernel_ptr<2, W>();
   void* args[] = {const_cast<Params*>(&prm)};
-  const void* fn = hpt <= 16 ? reinterpret_cast<const void*>(&split_partial_kernel<1, 2>)
-                             : reinterpret_cast<const void*>(&split_partial_kernel<2, 1>);
-  hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(kThreads), args, kSmemBytes, stream);
+  hipError_t e = hipLaunchKernel(fn, dim3(pl.grid), dim3(64 * W), args, smem_bytes(W), stream);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "split partial launch: %s", hipGetErrorString(e));
   return DA_OK;
 }
 
-Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q,
-                   int H_KV, int L_K_max, float scale, const da_plan& pl) {
+Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q, int H_KV,
+                   int L_K_max, float scale, const da_plan& pl) {
   Params p{};
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k);
@@ -639,7 +737,7 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
                    float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
                    int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
   da::clear_error();
-  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d, nullptr);
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
   if (rc) return rc;
   if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
   if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
@@ -649,20 +747,18 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   if (pack_gqa < -1 || pack_gqa > 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
   if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
 
-  int cus = 1;
-  if (num_splits <= 0 || pack_gqa < 0) {
-    int is950 = 0;
-    rc = query_device(&cus, &is950);
-    if (rc) return rc;
-  }
   da_plan pl;
-  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+  rc = da_make_plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 0, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   const int s = pl.num_splits;
   const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
-  if (s > 1 && (!workspace || workspace_bytes < wl.total))
-    return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, wl.total,
-                    workspace ? workspace_bytes : (size_t)0);
+  if (s > 1) {
+    if (!workspace || workspace_bytes < wl.total)
+      return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, wl.total,
+                      workspace ? workspace_bytes : (size_t)0);
+    rc = check_state_size(B, H_Q, s);
+    if (rc) return rc;
+  }
   rc = ensure_gfx950();
   if (rc) return rc;
 
@@ -679,14 +775,14 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
     p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
     p.counters = reinterpret_cast<uint32_t*>(ws + wl.cnt_off);
   }
-  return launch_partial(p, pl.heads_per_tile, pl.grid, static_cast<hipStream_t>(stream));
+  return launch_partial(p, pl, static_cast<hipStream_t>(stream));
 }
 
 int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, float* o_part,
                       float* m_part, float* l_part, int B, int H_Q, int H_KV, int L_K_max, int d,
                       float softmax_scale, int num_splits, int pack_gqa, void* stream) {
   da::clear_error();
-  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d, nullptr);
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
   if (rc) return rc;
   if (!o_part || !m_part || !l_part) return da::fail(DA_ERR_NULL, "o_part, m_part and l_part must be non-NULL");
   if (!aligned(o_part, 16) || !aligned(m_part, 4) || !aligned(l_part, 4))
@@ -694,8 +790,10 @@ int da_split_partials(const void* q, const void* k, const void* v, const int32_t
   if (num_splits < 1 || num_splits > DA_MAX_SPLITS)
     return da::fail(DA_ERR_SPLITS, "num_splits=%d not in [1, %d]", num_splits, DA_MAX_SPLITS);
   if (pack_gqa != 0 && pack_gqa != 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {0,1}", pack_gqa);
+  rc = check_state_size(B, H_Q, num_splits);
+  if (rc) return rc;
   da_plan pl;
-  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 1, 0, DA_POLICY_MI355X, &pl);
+  rc = da_make_plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 0, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   rc = ensure_gfx950();
   if (rc) return rc;
@@ -704,7 +802,7 @@ int da_split_partials(const void* q, const void* k, const void* v, const int32_t
   p.o_part = o_part;
   p.m_part = m_part;
   p.l_part = l_part;
-  return launch_partial(p, pl.heads_per_tile, pl.grid, static_cast<hipStream_t>(stream));
+  return launch_partial(p, pl, static_cast<hipStream_t>(stream));
 }
 
 int da_combine_splits(const float* o_part, const float* m_part, const float* l_part, void* out, float* lse_out,

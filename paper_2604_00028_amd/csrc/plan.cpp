@@ -31,36 +31,44 @@ int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
   return 1;
 }
 
-// Constants measured on MI355X (see the calibration notes that accompany the
-// split sweeps).  Units: microseconds and bytes per microsecond.
+// MI355X constants, fitted (log-error least squares over launches within
+// 1.6x of each shape's best) to a sweep of num_splits in
+// {1,2,3,4,6,8,12,16,24,32,48,64} over B in {1,2,4,8,16,32}, H_KV in {1,4,8},
+// g in {8,32} and L_K from 64 to 8192, timed with HIP-graph replay.
 const CostModel& mi355x_model() {
   static const CostModel m = {
-      /*t_wg=*/1.5,
-      /*wg_rate=*/40.0e3,
-      /*hbm_rate=*/5.0e6,
-      /*t_merge=*/1.0,
-      /*t_dispatch=*/0.004,
-      /*wgs_per_cu=*/2,
-      /*tie=*/0.02,
+      /*base=*/{4.01, 7.33},
+      /*t_tile=*/{1.105, 1.091},
+      /*merge0=*/2.25,
+      /*merge1=*/{0.443, 1.179},
+      /*hbm_rate=*/5.94e6,
+      /*hbm0=*/2.41,
+      /*tie=*/0.03,
   };
   return m;
 }
 
+// Time of one call with s chunks per sequence:
+//   compute = base + (workgroups per CU) x (32-key tiles per wave) x t_tile
+//   stream  = hbm0 + (K/V bytes + chunk-state traffic) / hbm_rate
+//   T = max(compute, stream) + [s > 1] (merge0 + merge1 s)
+// Every workgroup has four waves, one per SIMD, and walks a quarter of its
+// chunk each; workgroups that share a CU share its SIMDs.
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus) {
-  const double row_bytes = 2.0 * kHeadDim * 2.0;              // K and V row of one KV head
+  const int wide = hpt > 16 ? 1 : 0;
+  const double row_bytes = 2.0 * kHeadDim * 2.0;  // K and V row of one KV head
   const int64_t tiles = (int64_t)B * H_Q / hpt;
   const int64_t wgs = tiles * s;
-  const double slots = (double)cus * m.wgs_per_cu;
-  const double rounds = ceil((double)wgs / slots);
-  const double chunk = ceil((double)L_K / s) * row_bytes;
-  const double per_round = m.t_wg + chunk / m.wg_rate;
-  double bytes = (double)B * L_K * H_KV * row_bytes + 4.0 * B * H_Q * kHeadDim;
+  const int64_t chunk = ((int64_t)L_K + s - 1) / s;
+  const int64_t per_wave = (chunk + 3) / 4;
+  const int64_t tiles_per_wave = (per_wave + 31) / 32;
+  const int64_t per_cu = (wgs + cus - 1) / cus;
+  const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * m.t_tile[wide];
+  double bytes = (double)B * L_K * H_KV * row_bytes;
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
-  const double stream = bytes / m.hbm_rate;
-  double t = rounds * per_round;
-  if (stream > t) t = stream;
-  t += m.t_dispatch * (double)wgs;
-  if (s > 1) t += m.t_merge;
+  const double stream = m.hbm0 + bytes / m.hbm_rate;
+  double t = compute > stream ? compute : stream;
+  if (s > 1) t += m.merge0 + m.merge1[wide] * s;
   return t;
 }
 
@@ -90,6 +98,15 @@ static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
   // Longer contexts: the paper defers to the stack's own long-context path,
   // which here is the MI355X cost model.
   return mi355x_splits(B, H_Q, H_KV, L_K, hpt, cus);
+}
+
+int group_waves(int L_K_max, int s) {
+  // Four wave64s, one per SIMD.  Measured on MI355X, eight waves per
+  // workgroup were slower at every chunk length: the tile loop is bound by
+  // issue on its SIMD, so a second wave per SIMD only shares it.
+  (void)L_K_max;
+  (void)s;
+  return 4;
 }
 
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
@@ -133,6 +150,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
   out->grid = (int32_t)((int64_t)out->tiles * s);
   out->num_cus = cus;
+  out->group_waves = group_waves(L_K_max, s);
   return DA_OK;
 }
 

@@ -25,21 +25,26 @@ int heads_per_tile(int H_Q, int H_KV, int pack_gqa);
 // First key of chunk i when L keys are cut into s balanced chunks.
 inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
 
-// Policy knobs of the MI355X cost model (times in microseconds, rates in
-// bytes per microsecond).  Exposed so that tests can check its properties.
+// Constants of the MI355X cost model (times in microseconds, rates in bytes
+// per microsecond), fitted to a measured split sweep over 72 shapes
+// (B, H_Q, H_KV, L_K) x 12 split counts.  Exposed so tests can check the
+// model's properties.
 struct CostModel {
-  double t_wg;        // fixed latency of one workgroup: first loads, epilogue
-  double wg_rate;     // KV bytes per microsecond one 4-wave workgroup streams
-  double hbm_rate;    // sustained HBM bytes per microsecond for the whole chip
-  double t_merge;     // extra latency of the in-kernel split merge (s > 1)
-  double t_dispatch;  // dispatch cost per workgroup launched
-  int wgs_per_cu;     // workgroups resident per CU
+  double base[2];     // launch, first loads and epilogue (16-column / 32-column head tiles)
+  double t_tile[2];   // one 32-key tile on one wave
+  double merge0;      // in-kernel merge of the chunk states, fixed part (s > 1)
+  double merge1[2];   // ... per chunk
+  double hbm_rate;    // sustained HBM bytes per microsecond, whole chip
+  double hbm0;        // fixed part of the streaming bound
   double tie;         // relative tolerance: take the smallest s within it
 };
 const CostModel& mi355x_model();
 
 // Modelled time (us) of one call with s splits (policy MI355X).
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus);
+
+// Waves per workgroup for chunks of about L_K_max / s keys.
+int group_waves(int L_K_max, int s);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);
