@@ -53,9 +53,13 @@ def parse():
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--only", choices=("headline", "highload"), default=None,
-                    help="time only the planned launch of one workload (for profiler runs)")
+    ap.add_argument("--only", choices=("headline", "highload", "copy"), default=None,
+                    help="time only the planned launch of one workload, or a plain 1 GiB device copy "
+                         "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
+    ap.add_argument("--traffic-summary", metavar="DIR", default=None,
+                    help="derive per-launch HBM traffic from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE output "
+                         "directories DIR/pmc_<COUNTER>_<workload> and write profiles/traffic.json")
     return ap.parse_args()
 
 
@@ -154,10 +158,34 @@ def cpu_baseline(inp, seconds: float):
             "sample": f"{n} full calls of the benchmarked shape (fp64 NumPy, {seconds:.0f} s budget)"}
 
 
+def copy_run(args, torch):
+    """A plain device-to-device copy of 1 GiB (torch's copy kernel), steps
+    times: bytes read and written per launch are known exactly."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    steps = max(1, args.highload_steps)
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) * 1000.0 / steps
+    print(json.dumps({"workload": "copy_1GiB", "bytes_read": n, "bytes_written": n, "launches": steps,
+                      "us_per_copy": round(us, 2), "gbps": round(2 * n / (us * 1e-6) / 1e9, 1)}), flush=True)
+
+
 def only_run(args, da, torch, np, dev):
     """Planned (or forced) launch of one workload, nothing else: the command
     the rocprofv3 summaries are taken from."""
     from workloads import config_shapes, make_inputs
+    if args.only == "copy":
+        copy_run(args, torch)
+        return
     sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
     inp = make_inputs(sh)
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
@@ -172,8 +200,48 @@ def only_run(args, da, torch, np, dev):
                       "frac": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
 
+TRAFFIC_WORKLOADS = {"headline": "llama70b_gqa_b1_l512", "highload": "highload_b32_h64_kv8_l8192"}
+
+
+def counter_avg(path: str, kernel_prefix: str, counter: str) -> float:
+    """Mean per-dispatch value (KiB) of one counter for kernels whose name
+    starts with kernel_prefix, from a rocprofv3 counter_collection.csv."""
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if r["Kernel_Name"].startswith(kernel_prefix) and r["Counter_Name"] == counter]
+    if not vals:
+        raise ValueError(f"no {counter} rows for {kernel_prefix} in {path}")
+    return sum(vals) / len(vals)
+
+
+def traffic_summary(d: str) -> None:
+    """Scale each counter by what it reads for a plain copy of known size
+    (1 GiB read, 1 GiB written per launch), then write profiles/traffic.json."""
+    f = lambda c, w: os.path.join(d, f"pmc_{c}_{w}", "run_counter_collection.csv")
+    copy_kib = float(1 << 20)
+    fetch_scale = copy_kib / counter_avg(f("FETCH_SIZE", "copy"), "__amd_rocclr_copyBuffer", "FETCH_SIZE")
+    write_scale = copy_kib / counter_avg(f("WRITE_SIZE", "copy"), "__amd_rocclr_copyBuffer", "WRITE_SIZE")
+    out = {"kernel_source_sha256": hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest(),
+           "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
+           "command": "rocprofv3 --pmc <FETCH_SIZE|WRITE_SIZE> --output-format csv -d DIR/pmc_<counter>_<w> -o run "
+                      "-- python3 bench.py --only <w> --steps 20 --rounds 1 --highload-steps 3",
+           "workloads": {}}
+    for w, name in TRAFFIC_WORKLOADS.items():
+        fk = counter_avg(f("FETCH_SIZE", w), "void (anonymous namespace)::split_partial_kernel", "FETCH_SIZE")
+        wk = counter_avg(f("WRITE_SIZE", w), "void (anonymous namespace)::split_partial_kernel", "WRITE_SIZE")
+        out["workloads"][name] = {"fetch_kib_counter": round(fk, 2), "write_kib_counter": round(wk, 2),
+                                  "fetch_bytes": int(fk * 1024 * fetch_scale), "write_bytes": int(wk * 1024 * write_scale)}
+    with open(PROFILE_TRAFFIC, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode kernel shards by "
               f"(sequence, KV head) with no exchange, so no multi-GPU figure is produced.", file=sys.stderr)
