@@ -91,12 +91,9 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
                  int num_cus, int cu_margin, int policy, da_plan* out);
 
 /* Bytes of workspace da_decode_attn needs for num_splits chunks: 0 when
- * num_splits == 1.  Layout (each region 256-byte aligned): arrival counters
- * uint32 [B*H_Q] | Otilde fp32 [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32
- * [s,B,H_Q].  The counter region (the first B*H_Q*4 bytes) must be zero
- * before the first call that uses the workspace; every call leaves it zero
- * again, so a workspace can be reused by later calls with the same B*H_Q and
- * any num_splits without clearing it. */
+ * num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
+ * [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q].  No initialisation is
+ * needed; every call overwrites what it reads. */
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
 
 /* Cut points of sequence chunking: chunk i of a sequence of L keys is
@@ -124,9 +121,10 @@ int da_split_bounds(int L, int num_splits, int32_t* cuts);
  *   workspace    device memory of workspace_bytes >= da_workspace_bytes(B,
  *                H_Q, d, s) for the resolved s (unused when s == 1).  Calls
  *                that share a workspace must not overlap in time.
- * One kernel launch.  With s > 1 the last workgroup of each tile to finish
- * merges the s partial states in split order, so results are bit-identical
- * across runs for a fixed (num_splits, pack_gqa). */
+ * s == 1: one kernel launch.  s > 1: the split kernel writes the chunk
+ * states to the workspace and the combine kernel merges them in chunk order
+ * (exactly da_split_partials followed by da_combine_splits), so results are
+ * bit-identical across runs for a fixed (num_splits, pack_gqa). */
 int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                    void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                    float softmax_scale, int num_splits, int pack_gqa, void* workspace,

@@ -201,18 +201,17 @@ def _shapes(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu: Optional[torc
     return B, H_Q, H_KV, int(L_K_max), d
 
 
-_workspaces: Dict[Tuple[int, int, int], torch.Tensor] = {}
+_workspaces: Dict[Tuple[int, int], torch.Tensor] = {}
 
 
-def workspace_for(dev: torch.device, stream_handle: int, rows: int, nbytes: int) -> torch.Tensor:
-    """A zero-initialised workspace of at least nbytes, cached per (device,
-    stream, B*H_Q).  The library leaves the arrival counters (the first
-    B*H_Q*4 bytes) at zero after every call, so the cached buffer stays valid
-    for later calls with the same B*H_Q and any split count on that stream."""
-    key = (dev.index if dev.index is not None else torch.cuda.current_device(), stream_handle, rows)
+def workspace_for(dev: torch.device, stream_handle: int, nbytes: int) -> torch.Tensor:
+    """A workspace of at least nbytes, cached per (device, stream).  Calls on
+    one stream run in order, so they can share it; the library overwrites
+    whatever it reads, so it needs no initialisation."""
+    key = (dev.index if dev.index is not None else torch.cuda.current_device(), stream_handle)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
         _workspaces[key] = ws
     return ws
 
@@ -231,7 +230,7 @@ def da_decode_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens
         plan = da_make_plan(B, H_Q, H_KV, L, d, num_splits, pack_gqa)
         nbytes = da_workspace_bytes(B, H_Q, d, plan.num_splits)
         if nbytes:
-            workspace = workspace_for(dev, s_handle, B * H_Q, nbytes)
+            workspace = workspace_for(dev, s_handle, nbytes)
     ws_ptr = _ptr(workspace)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(load().da_decode_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),

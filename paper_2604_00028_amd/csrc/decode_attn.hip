@@ -1,6 +1,6 @@
 // Split-KV single-query decode attention for MI355X (gfx950): the split
-// partial kernel (with an optional in-kernel log-sum-exp merge), the
-// standalone combine kernel, and the C-ABI launch entry points.
+// partial kernel, the log-sum-exp combine kernel, and the C-ABI launch entry
+// points.
 //
 // What one workgroup computes (paper Sections 2.1, 2.2, 3.1): for one work
 // tile -- a sequence b and the query heads that share one KV head when GQA
@@ -8,9 +8,9 @@
 // single query head when it is off -- and one chunk of that sequence's keys,
 // the partial softmax state (running max m, sum l, unnormalised output
 // Otilde).  With one split the state is normalised and written as the
-// output; with several, the last workgroup of a tile to finish merges the
-// chunk states in chunk order (the paper's final reduction, Sections 3.1 and
-// 5.3), so one launch covers the whole call.
+// output; with several, the chunk states go to the workspace and the combine
+// kernel merges them in chunk order (the paper's final reduction, Sections
+// 3.1 and 5.3).
 //
 // gfx950 mapping:
 //  * W = 4 wave64s per workgroup, one per SIMD.  The chunk is cut into W
@@ -54,7 +54,6 @@ constexpr int D = DA_HEAD_DIM;
 constexpr int kKeysPerTile = 32;
 constexpr int kVPitch = 288;                 // bytes per staged V row (256 + 32 pad)
 constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
-constexpr int kCoherent = 16;                // buffer cache policy: sc1 (agent coherence)
 constexpr int kGroupWaves = 4;               // wave64s per workgroup (one per SIMD of a CU)
 
 // LDS of one workgroup of W waves: the per-wave V stage, reused for the
@@ -75,19 +74,18 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-enum Mode : int { kDirect = 0, kPartials = 1, kMerged = 2 };
+enum Mode : int { kDirect = 0, kPartials = 1 };
 
 struct Params {
   const uint16_t* q;
   const uint16_t* k;
   const uint16_t* v;
   const int32_t* cu;    // nullable: fixed layout
-  uint16_t* out;        // bf16 [B, H_Q, D]        (kDirect, kMerged)
-  float* lse;           // nullable, [B, H_Q]      (kDirect, kMerged)
-  float* o_part;        // [s, B, H_Q, D]          (kPartials, kMerged)
+  uint16_t* out;        // bf16 [B, H_Q, D]        (kDirect)
+  float* lse;           // nullable, [B, H_Q]      (kDirect)
+  float* o_part;        // [s, B, H_Q, D]          (kPartials)
   float* m_part;        // [s, B, H_Q]
   float* l_part;        // [s, B, H_Q]
-  uint32_t* counters;   // [tiles]                 (kMerged)
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
   float scale_log2;     // softmax scale * log2(e)
 };
@@ -110,53 +108,18 @@ __device__ __forceinline__ float sum_rows(float x) {
   return __uint_as_float(c[0]) + __uint_as_float(c[1]);
 }
 
+// Two floats to bf16 (round to nearest even), packed low/high in one dword:
+// a single v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo;
-  __bf16 b = (__bf16)hi;
-  uint16_t ua, ub;
-  memcpy(&ua, &a, 2);
-  memcpy(&ub, &b, 2);
-  return (uint32_t)ua | ((uint32_t)ub << 16);
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-// Chunk states shared between the workgroups of one launch travel through
-// memory with the sc1 cache policy (coherent at agent scope: written through
-// and read past the XCD-private L2s).  An agent-scope fence would instead
-// write back and invalidate the whole L2 of the XCD, which costs microseconds
-// per workgroup on gfx950.  The fences below therefore only order: they wait
-// until this wave's memory operations have completed (s_waitcnt with
-// vmcnt = 0; expcnt = 7 and lgkmcnt = 15 leave those counters unchecked).
-__device__ __forceinline__ void order_after_memory_ops() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-}
-__device__ __forceinline__ void order_before_memory_ops() {
-  __builtin_amdgcn_s_waitcnt(0x0F70);
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-
-// Normalise N output columns of one head by the softmax sum and store them
-// as bf16; M is the row max in natural-log units, for the log-sum-exp.
-template <int N>
-__device__ __forceinline__ void finish_row(float M, float Lsum, const float* o, uint16_t* out_row,
-                                           float* lse_slot) {
-  const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
-  uint32_t w[N / 2];
-#pragma unroll
-  for (int j = 0; j < N / 2; ++j) w[j] = pack_bf16x2(o[2 * j] * inv, o[2 * j + 1] * inv);
-  if constexpr (N == 8) {
-    *reinterpret_cast<u32x4*>(out_row) = u32x4{w[0], w[1], w[2], w[3]};
-  } else {
-    static_assert(N == 4, "4 or 8 columns");
-    *reinterpret_cast<uint2*>(out_row) = make_uint2(w[0], w[1]);
-  }
-  if (lse_slot) *lse_slot = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
 }
 
 // Chunk weights of one (sequence, head) row from its s chunk states:
@@ -182,8 +145,6 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
 template <int NT, int W>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
-  constexpr int kThreads = 64 * W;
-  constexpr int kSmem = smem_bytes(W);
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -224,8 +185,6 @@ split_partial_kernel(Params p) {
   const uint32_t rs = (uint32_t)p.H_KV * (D * 2);
   const int64_t base_elems = (row0 * p.H_KV + kvh) * D;
   const uint32_t lim = (uint32_t)key_hi * rs;
-  const __amdgpu_buffer_rsrc_t krs = make_rsrc(p.k + base_elems, lim);
-  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(p.v + base_elems, lim);
 
   // ---- Q^T as the MFMA B operand.  The reduction index of the product may
   //      map to head dims in any order as long as K and Q agree: k-step j,
@@ -259,27 +218,39 @@ split_partial_kernel(Params p) {
   const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
 
   // K/V of one 32-key tile: K in the MFMA A layout (two 16-key row blocks x
-  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.  Per-lane byte
-  // offsets of the wave's first tile; tile t adds t*32 rows.
-  const uint32_t koff0 = (uint32_t)(key_lo + col) * rs + 16u * quad;
-  const uint32_t voff0 = (uint32_t)(key_lo + quad) * rs + 16u * col;
+  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.  The per-lane
+  // byte offsets are fixed; tile t moves the descriptor base by t*32 rows
+  // and shrinks its record count to match (scalar work only).
   const uint32_t tile_step = kKeysPerTile * rs;
-  u32x4 kreg[2][4], vreg[8];
-  auto load_tile = [&](int t) {
-    const uint32_t adv = (uint32_t)t * tile_step;
+  const uint32_t koff[2] = {(uint32_t)(key_lo + col) * rs + 16u * quad,
+                            (uint32_t)(key_lo + 16 + col) * rs + 16u * quad};
+  uint32_t voff[8];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      const uint32_t off = koff0 + adv + (uint32_t)mt * 16u * rs;
+  for (int jj = 0; jj < 8; ++jj) voff[jj] = (uint32_t)(key_lo + 4 * jj + quad) * rs + 16u * col;
+  auto load_tile = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t) {
+    // wave-uniform by construction; readfirstlane tells the compiler so the
+    // descriptor stays in scalar registers
+    const uint32_t adv = __builtin_amdgcn_readfirstlane((uint32_t)t * tile_step);
+    const uint32_t left = __builtin_amdgcn_readfirstlane(lim > adv ? lim - adv : 0u);
+    const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + base_elems + (int64_t)adv / 2, left);
+    const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + base_elems + (int64_t)adv / 2, left);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + 64u * j, 0, 0);
-    }
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
-      vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vrs, voff0 + adv + (uint32_t)jj * 4u * rs, 0, 0);
+      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, 0);
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, 0);
   };
 
-  load_tile(0);
-  for (int t = 0; t < ntiles; ++t) {
+  // One tile held in (kreg, vreg).  `prefetch`: refill those registers with
+  // tile t + 1 while this one is reduced (the loop refills unconditionally,
+  // so the compiler waits for exactly the tile in use; the final tile does
+  // not refill).  A second tile in flight per wave was measured slower at
+  // every length: with one workgroup per CU, the CU's memory pipeline rather
+  // than the wave bounds the short-sequence tile rate.
+  // `last`: only the final tile can be shorter than 32 keys and needs its
+  // scores masked.
+  auto process = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t, auto prefetch, auto last) {
     const int kb = key_lo + t * kKeysPerTile;
     const int nvalid = key_hi - kb;  // >= 1
 
@@ -301,33 +272,31 @@ split_partial_kernel(Params p) {
     for (int jj = 0; jj < 8; ++jj)
       *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
 
-    // prefetch the next tile while this one is reduced; unconditional, so
-    // the compiler waits for exactly the tile in use (past the wave's range
-    // every offset is out of range: zeros, no memory traffic)
-    load_tile(t + 1);
+    if constexpr (decltype(prefetch)::value) load_tile(kreg, vreg, t + 1);
 
-    // online softmax per head column
+    // online softmax per head column, in log2 units of the scaled score:
+    // the max is taken on raw scores (the scale is positive) and each
+    // exponent is one fma, raw * scale*log2(e) - running max
     bf16x8 pb[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       float x[8];
-      float tmax = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int kl = mt * 16 + quad * 4 + i;
-          const float s2 = kl < nvalid ? sc[nt][mt][i] * p.scale_log2 : -INFINITY;
-          x[mt * 4 + i] = s2;
-          tmax = fmaxf(tmax, s2);
+          float r = sc[nt][mt][i];
+          if constexpr (decltype(last)::value) r = (mt * 16 + quad * 4 + i) < nvalid ? r : -INFINITY;
+          x[mt * 4 + i] = r;
         }
-      tmax = max_rows(tmax);
-      const float m_new = fmaxf(m_run[nt], tmax);
+      const float rmax = max_rows(fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                                        fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7]))));
+      const float m_new = fmaxf(m_run[nt], rmax * p.scale_log2);
       const float alpha = __builtin_amdgcn_exp2f(m_run[nt] - m_new);
       float psum = 0.f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        x[e] = __builtin_amdgcn_exp2f(x[e] - m_new);
+        x[e] = __builtin_amdgcn_exp2f(fmaf(x[e], p.scale_log2, -m_new));
         psum += x[e];
       }
       l_run[nt] = l_run[nt] * alpha + psum;
@@ -360,232 +329,118 @@ split_partial_kernel(Params p) {
     for (int nn = 0; nn < 8; ++nn) {
       const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
       const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
-      const bf16x8 a = __builtin_bit_cast(bf16x8, s16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
         acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], acc_o[nt][nn], 0, 0, 0);
     }
     __builtin_amdgcn_wave_barrier();
-  }
+  };
 
-  // ---- merge the W wave states through LDS, one 16-head tile at a time
-  float* sm_o = reinterpret_cast<float*>(smem);                 // [wave][dim][16]
-  float* sm_m = reinterpret_cast<float*>(smem + kSmem - 2 * W * 16 * 4);
-  float* sm_l = sm_m + W * 16;
+  constexpr std::true_type yes{};
+  constexpr std::false_type no{};
+  u32x4 kreg[2][4], vreg[8];
+  load_tile(kreg, vreg, 0);
+  int t = 0;
+  for (; t + 1 < ntiles; ++t) process(kreg, vreg, t, yes, no);
+  if (t < ntiles) process(kreg, vreg, t, no, yes);
+
+  // ---- merge the W wave states: ((w0 + w1) + (w2 + w3)), in registers.
+  //      Every wave holds its state in the same lane layout (per head column:
+  //      running max, row-summed l, 8 x 4 output values), so a partner's
+  //      state passes through LDS value-major ([value][lane], conflict-free)
+  //      and is absorbed lane by lane.  Wave 0 ends with the workgroup state.
+  static_assert(W == 4, "the merge tree below is written for four waves");
+  constexpr int kVals = 2 + 32;                         // m, l, 8 x 4 outputs
+  float lsum[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) lsum[nt] = sum_rows(l_run[nt]);
+  float* slot_a = reinterpret_cast<float*>(smem);
+  float* slot_b = slot_a + NT * kVals * 64;
+  auto publish = [&](float* slot) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float* v = slot + nt * kVals * 64 + lane;
+      v[0] = m_run[nt];
+      v[64] = lsum[nt];
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[(2 + nn * 4 + i) * 64] = acc_o[nt][nn][i];
+    }
+  };
+  auto absorb = [&](const float* slot) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float* v = slot + nt * kVals * 64 + lane;
+      const float mo = v[0];
+      const float lo = v[64];
+      const float M = fmaxf(m_run[nt], mo);
+      const bool empty = M == -INFINITY;  // both states empty: stay empty
+      const float as = empty ? 0.f : __builtin_amdgcn_exp2f(m_run[nt] - M);
+      const float ao = empty ? 0.f : __builtin_amdgcn_exp2f(mo - M);
+      lsum[nt] = lsum[nt] * as + lo * ao;
+      m_run[nt] = M;
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc_o[nt][nn][i] = acc_o[nt][nn][i] * as + v[(2 + nn * 4 + i) * 64] * ao;
+    }
+  };
+  __syncthreads();                                   // every wave is done with its V stage
+  if (wave == 1) publish(slot_a);
+  if (wave == 3) publish(slot_b);
+  __syncthreads();
+  if (wave == 0) absorb(slot_a);
+  if (wave == 2) absorb(slot_b);
+  __syncthreads();
+  if (wave == 2) publish(slot_a);
+  __syncthreads();
+
   const int64_t rows = (int64_t)p.B * p.H_Q;
   const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
-  // chunk-state outputs of this workgroup: uniform base, small per-lane offsets
-  const __amdgpu_buffer_rsrc_t ors =
-      make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
-
+  if (wave == 0) {
+    absorb(slot_a);
+    // lane (col, quad) owns dims 16nn + 4quad + [0, 4) of head 16nt + col
+    const __amdgpu_buffer_rsrc_t ors =
+        make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const float lsum = sum_rows(l_run[nt]);
-    __syncthreads();
-#pragma unroll
-    for (int nn = 0; nn < 8; ++nn)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sm_o[(wave * D + 16 * nn + 4 * quad + i) * 16 + col] = acc_o[nt][nn][i];
-    if (quad == 0) {
-      sm_m[wave * 16 + col] = m_run[nt];
-      sm_l[wave * 16 + col] = lsum;
-    }
-    __syncthreads();
-
-    const int hcount = min(16, p.hpt - nt * 16);
-    for (int it = tid; it < hcount * 16; it += kThreads) {
-      const int hc = it >> 4;          // head within this 16-head tile
-      const int d8 = (it & 15) * 8;    // first of 8 dims
-      float M2 = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < W; ++w)
-        if (sm_l[w * 16 + hc] > 0.f) M2 = fmaxf(M2, sm_m[w * 16 + hc]);
-      float Lsum = 0.f;
-      float o8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int w = 0; w < W; ++w) {
-        const float lw = sm_l[w * 16 + hc];
-        if (lw > 0.f) {
-          const float wt = __builtin_amdgcn_exp2f(sm_m[w * 16 + hc] - M2);
-          Lsum += wt * lw;
-#pragma unroll
-          for (int dd = 0; dd < 8; ++dd) o8[dd] += wt * sm_o[(w * D + d8 + dd) * 16 + hc];
-        }
-      }
-      const int h = nt * 16 + hc;
+    for (int nt = 0; nt < NT; ++nt) {
+      const int h = nt * 16 + col;
+      if (h >= p.hpt) continue;
       const int64_t row = row0_tile + h;
+      const float lw = lsum[nt];
+      const float mval = lw > 0.f ? m_run[nt] * kLn2 : -INFINITY;
       if (p.mode == kDirect) {
-        finish_row<8>(M2 * kLn2, Lsum, o8, p.out + row * D + d8, (p.lse && d8 == 0) ? p.lse + row : nullptr);
+        const float inv = lw > 0.f ? 1.0f / lw : 0.f;
+#pragma unroll
+        for (int nn = 0; nn < 8; ++nn) {
+          const f32x4 a = acc_o[nt][nn];
+          *reinterpret_cast<uint2*>(p.out + row * D + 16 * nn + 4 * quad) =
+              make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
+        }
+        if (p.lse && quad == 0) p.lse[row] = lw > 0.f ? mval + logf(lw) : -INFINITY;
       } else {
-        const float mval = Lsum > 0.f ? M2 * kLn2 : -INFINITY;
-        const u32x4 lo = {__float_as_uint(o8[0]), __float_as_uint(o8[1]), __float_as_uint(o8[2]),
-                          __float_as_uint(o8[3])};
-        const u32x4 hi = {__float_as_uint(o8[4]), __float_as_uint(o8[5]), __float_as_uint(o8[6]),
-                          __float_as_uint(o8[7])};
-        const uint32_t off = (uint32_t)(h * D + d8) * 4u;
-        if (p.mode == kPartials) {
-          __builtin_amdgcn_raw_buffer_store_b128(lo, ors, off, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b128(hi, ors, off + 16u, 0, 0);
-          if (d8 == 0) {
-            p.m_part[split * rows + row] = mval;
-            p.l_part[split * rows + row] = Lsum;
-          }
-        } else {
-          __builtin_amdgcn_raw_buffer_store_b128(lo, ors, off, 0, kCoherent);
-          __builtin_amdgcn_raw_buffer_store_b128(hi, ors, off + 16u, 0, kCoherent);
-          if (d8 == 0) {
-            __hip_atomic_store(p.m_part + split * rows + row, mval, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(p.l_part + split * rows + row, Lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
+#pragma unroll
+        for (int nn = 0; nn < 8; ++nn) {
+          const f32x4 a = acc_o[nt][nn];
+          const u32x4 bits = {__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
+                              __float_as_uint(a[3])};
+          __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0, 0);
+        }
+        if (quad == 0) {
+          p.m_part[split * rows + row] = mval;
+          p.l_part[split * rows + row] = lw;
         }
       }
     }
-  }
-  if (p.mode != kMerged) return;
-
-  // ---- in-kernel merge: the last workgroup of this tile to arrive merges
-  //      the s chunk states in chunk order.  The chunks of one tile run on
-  //      different XCDs with separate L2s, so the states travel through
-  //      agent-coherent stores and loads; the arrival count is an
-  //      agent-scope atomic issued only after every state store completed.
-  __shared__ int sh_last;
-  order_after_memory_ops();   // this wave's state stores have completed
-  __syncthreads();            // ... and so have every other wave's
-  if (tid == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(p.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int last = prev == (uint32_t)(p.s - 1);
-    if (last) __hip_atomic_store(p.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sh_last = last;
-    order_before_memory_ops();
-  }
-  __syncthreads();
-  if (!sh_last) return;
-
-  // All loads of the merge are issued before any of them is waited for: the
-  // chunk maxima and sums of this tile's heads, and the first batch of
-  // chunk outputs of this thread's (head, 4 dims) items.  Then the weights
-  // per head (one thread per head, chunk order), then the weighted sums.
-  float* sw = reinterpret_cast<float*>(smem);             // [hpt][kMaxSplits]: m, then weight
-  float* sl = sw + da::kMaxHeadsPerTile * DA_MAX_SPLITS;  // [hpt][kMaxSplits]: l
-  float* sML = sl + da::kMaxHeadsPerTile * DA_MAX_SPLITS; // [hpt][2]: M, L
-  const int nml = p.hpt * p.s;
-  constexpr int kMlPerThread = (da::kMaxHeadsPerTile * DA_MAX_SPLITS + kThreads - 1) / kThreads;
-  float mv[kMlPerThread], lv[kMlPerThread];
-#pragma unroll
-  for (int u = 0; u < kMlPerThread; ++u) {
-    const int it = tid + u * kThreads;
-    if (it < nml) {
-      const int h = it / p.s;
-      const int i = it - h * p.s;
-      const int64_t idx = (int64_t)i * rows + row0_tile + h;
-      mv[u] = __hip_atomic_load(p.m_part + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      lv[u] = __hip_atomic_load(p.l_part + idx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
-  // This thread's items: (head, 4 dims); an item sits at byte 16*item of a
-  // chunk's state rows, chunk i at byte i*split_stride.  Loads for all of a
-  // thread's items are in flight together: with one item per thread a batch
-  // covers 16 chunks, with up to kMaxItems items it covers 16/kMaxItems
-  // chunks of each.  The first batch is issued before the weights exist.
-  constexpr int kMaxItems = (da::kMaxHeadsPerTile * (D / 4) + kThreads - 1) / kThreads;
-  constexpr int kMultiBatch = kMergeBatch / kMaxItems;
-  const int nitems = p.hpt * (D / 4);
-  const uint32_t split_stride = (uint32_t)(rows * D * 4);
-  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(p.o_part + row0_tile * D, (uint32_t)p.s * split_stride);
-  auto state_load = [&](int it, int i) {
-    return __builtin_amdgcn_raw_buffer_load_b128(mrs, (uint32_t)it * 16u + (uint32_t)i * split_stride, 0, kCoherent);
-  };
-  const bool one_item = nitems <= kThreads;
-  u32x4 ob[kMergeBatch];
-  if (one_item) {
-    if (tid < nitems) {
-#pragma unroll
-      for (int u = 0; u < kMergeBatch; ++u)
-        if (u < p.s) ob[u] = state_load(tid, u);
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < kMaxItems; ++r)
-#pragma unroll
-      for (int u = 0; u < kMultiBatch; ++u)
-        if (tid + r * kThreads < nitems && u < p.s) ob[r * kMultiBatch + u] = state_load(tid + r * kThreads, u);
-  }
-#pragma unroll
-  for (int u = 0; u < kMlPerThread; ++u) {
-    const int it = tid + u * kThreads;
-    if (it < nml) {
-      const int h = it / p.s;
-      const int i = it - h * p.s;
-      sw[h * DA_MAX_SPLITS + i] = mv[u];
-      sl[h * DA_MAX_SPLITS + i] = lv[u];
-    }
-  }
-  __syncthreads();
-  if (tid < p.hpt) merge_weights(sw + tid * DA_MAX_SPLITS, sl + tid * DA_MAX_SPLITS, p.s, sML + 2 * tid);
-  __syncthreads();
-
-  // weighted sum of one item over chunks [i0, i0 + N) clipped to s, from
-  // registers (compile-time indices only, so `src` stays in registers)
-  auto accumulate = [&](auto n_tag, int it, float (&o4)[4], const u32x4* src, int i0) {
-    constexpr int N = decltype(n_tag)::value;
-    const float* w = sw + (it >> 5) * DA_MAX_SPLITS;
-    const float* l = sl + (it >> 5) * DA_MAX_SPLITS;
-#pragma unroll
-    for (int u = 0; u < N; ++u) {
-      if (i0 + u < p.s) {
-        const float wi = w[i0 + u];
-        const bool live = l[i0 + u] > 0.f;
-#pragma unroll
-        for (int dd = 0; dd < 4; ++dd) o4[dd] = fmaf(wi, live ? __uint_as_float(src[u][dd]) : 0.f, o4[dd]);
-      }
-    }
-  };
-  auto finish_item = [&](int it, const float (&o4)[4]) {
-    const int h = it >> 5;
-    const int d4 = (it & 31) * 4;
-    const int64_t row = row0_tile + h;
-    finish_row<4>(sML[2 * h], sML[2 * h + 1], o4, p.out + row * D + d4, (p.lse && d4 == 0) ? p.lse + row : nullptr);
-  };
-
-  if (one_item) {
-    if (tid < nitems) {
-      float o4[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int i0 = 0; i0 < p.s; i0 += kMergeBatch) {
-        if (i0 > 0) {
-#pragma unroll
-          for (int u = 0; u < kMergeBatch; ++u)
-            if (i0 + u < p.s) ob[u] = state_load(tid, i0 + u);
-        }
-        accumulate(std::integral_constant<int, kMergeBatch>{}, tid, o4, ob, i0);
-      }
-      finish_item(tid, o4);
-    }
-  } else {
-    float o4[kMaxItems][4] = {};
-    for (int i0 = 0; i0 < p.s; i0 += kMultiBatch) {
-      if (i0 > 0) {
-#pragma unroll
-        for (int r = 0; r < kMaxItems; ++r)
-#pragma unroll
-          for (int u = 0; u < kMultiBatch; ++u)
-            if (tid + r * kThreads < nitems && i0 + u < p.s)
-              ob[r * kMultiBatch + u] = state_load(tid + r * kThreads, i0 + u);
-      }
-#pragma unroll
-      for (int r = 0; r < kMaxItems; ++r)
-        if (tid + r * kThreads < nitems)
-          accumulate(std::integral_constant<int, kMultiBatch>{}, tid + r * kThreads, o4[r], ob + r * kMultiBatch, i0);
-    }
-#pragma unroll
-    for (int r = 0; r < kMaxItems; ++r)
-      if (tid + r * kThreads < nitems) finish_item(tid + r * kThreads, o4[r]);
   }
 }
 
-// Standalone log-sum-exp combine: one wave64 per (b, h) row, 2 dims per
-// lane.  Same phases and the same arithmetic as the in-kernel merge (loads
-// issued together, weights in chunk order, weighted sum in chunk order), so
-// both produce identical bits for identical chunk states.
+// Log-sum-exp combine: one wave64 per (b, h) row, 2 dims per lane.  The
+// first 16 chunk outputs are loaded before the weights are known; weights
+// and the weighted sum are taken in chunk order, so the result is
+// bit-identical across runs and producers of the same chunk states.
 __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
                                                             const float* __restrict__ m_part,
                                                             const float* __restrict__ l_part,
@@ -703,6 +558,16 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   return DA_OK;
 }
 
+int launch_combine(const float* o_part, const float* m_part, const float* l_part, uint16_t* out, float* lse,
+                   int s, int64_t rows, hipStream_t stream) {
+  const int grid = (int)((rows + 3) / 4);
+  void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows};
+  hipError_t e =
+      hipLaunchKernel(reinterpret_cast<const void*>(&split_combine_kernel), dim3(grid), dim3(256), args, 0, stream);
+  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
+  return DA_OK;
+}
+
 Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q, int H_KV,
                    int L_K_max, float scale, const da_plan& pl) {
   Params p{};
@@ -763,19 +628,22 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   if (rc) return rc;
 
   Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
-  p.out = static_cast<uint16_t*>(out);
-  p.lse = lse_out;
   if (s == 1) {
     p.mode = kDirect;
-  } else {
-    unsigned char* ws = static_cast<unsigned char*>(workspace);
-    p.mode = kMerged;
-    p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
-    p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
-    p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
-    p.counters = reinterpret_cast<uint32_t*>(ws + wl.cnt_off);
+    p.out = static_cast<uint16_t*>(out);
+    p.lse = lse_out;
+    return launch_partial(p, pl, static_cast<hipStream_t>(stream));
   }
-  return launch_partial(p, pl, static_cast<hipStream_t>(stream));
+  // s > 1: chunk states into the workspace, then the log-sum-exp combine.
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  p.mode = kPartials;
+  p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
+  p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
+  p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
+  rc = launch_partial(p, pl, static_cast<hipStream_t>(stream));
+  if (rc) return rc;
+  return launch_combine(p.o_part, p.m_part, p.l_part, static_cast<uint16_t*>(out), lse_out, s, (int64_t)B * H_Q,
+                        static_cast<hipStream_t>(stream));
 }
 
 int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, float* o_part,
@@ -819,20 +687,8 @@ int da_combine_splits(const float* o_part, const float* m_part, const float* l_p
     return da::fail(DA_ERR_ALIGN, "misaligned combine operand");
   int rc = ensure_gfx950();
   if (rc) return rc;
-  const int64_t rows = (int64_t)B * H_Q;
-  const int grid = (int)((rows + 3) / 4);
-  int s = num_splits;
-  const float* a0 = o_part;
-  const float* a1 = m_part;
-  const float* a2 = l_part;
-  uint16_t* a3 = static_cast<uint16_t*>(out);
-  float* a4 = lse_out;
-  int64_t a6 = rows;
-  void* args[] = {&a0, &a1, &a2, &a3, &a4, &s, &a6};
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&split_combine_kernel), dim3(grid), dim3(256), args,
-                                 0, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
-  return DA_OK;
+  return launch_combine(o_part, m_part, l_part, static_cast<uint16_t*>(out), lse_out, num_splits, (int64_t)B * H_Q,
+                        static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -32,7 +32,7 @@ inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
 struct CostModel {
   double base[2];     // launch, first loads and epilogue (16-column / 32-column head tiles)
   double t_tile[2];   // one 32-key tile on one wave
-  double merge0;      // in-kernel merge of the chunk states, fixed part (s > 1)
+  double merge0;      // second launch that combines the chunk states, fixed part (s > 1)
   double merge1[2];   // ... per chunk
   double hbm_rate;    // sustained HBM bytes per microsecond, whole chip
   double hbm0;        // fixed part of the streaming bound
@@ -53,7 +53,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d);
 
 struct WorkspaceLayout {
-  size_t o_off, m_off, l_off, cnt_off, total;
+  size_t o_off, m_off, l_off, total;
 };
 WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s);
 

@@ -208,7 +208,7 @@ def test_combine_of_oracle_partials():
 
 
 @pytest.mark.parametrize("s,pack", [(2, 1), (5, 1), (64, 1), (3, 0)])
-def test_single_launch_merge_equals_split_then_combine(s, pack):
+def test_decode_attn_equals_split_then_combine(s, pack):
     sh = config_shapes(4)[0]
     inp = make_inputs(sh)
     q, k, v, cu = dev_inputs(inp)
@@ -253,13 +253,12 @@ def test_graph_replay_matches_eager(s):
 
 
 def test_workspace_reused_across_split_counts():
-    """One workspace serves calls with different split counts back to back:
-    the arrival counters sit at an offset that depends only on B*H_Q."""
+    """One workspace serves calls with different split counts back to back."""
     sh = config_shapes(2)[3]
     inp = make_inputs(sh)
     O, _ = decode_attention(inp.q, inp.k, inp.v)
     q, k, v, cu = dev_inputs(inp)
-    ws = torch.zeros(da.da_workspace_bytes(sh.B, sh.H_Q, 128, 64), dtype=torch.uint8, device="cuda")
+    ws = torch.full((da.da_workspace_bytes(sh.B, sh.H_Q, 128, 64),), 255, dtype=torch.uint8, device="cuda")
     outs = {}
     for s in (64, 8, 2, 5, 8, 64, 3):
         say(f"shared workspace s={s}")
@@ -269,5 +268,3 @@ def test_workspace_reused_across_split_counts():
         if s in outs:
             assert torch.equal(out.view(torch.int16), outs[s].view(torch.int16))
         outs[s] = out
-    nrows = sh.B * sh.H_Q
-    assert torch.all(ws[: nrows * 4] == 0)        # counters left at zero
