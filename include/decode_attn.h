@@ -69,7 +69,9 @@ typedef struct da_plan {
   int32_t tiles;          /* work tiles = B * H_Q / heads_per_tile (Section 2.1: Batch x H_KV when packed) */
   int32_t grid;           /* workgroups launched = tiles * num_splits */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
-  int32_t group_waves;    /* wave64s per workgroup (4 or 8); each takes a contiguous part of the chunk */
+  int32_t group_waves;    /* wave64s per workgroup (4); each takes a contiguous part of the chunk */
+  int32_t k_staged;       /* 1: K tiles are fetched row-contiguous and pass through LDS;
+                             0: K is fetched straight into the matrix-core operand layout */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
@@ -86,7 +88,8 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
 
 /* Same as da_choose_splits with num_splits and/or pack_gqa forced
  * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy).
- * Fills every field of `out` for the resulting launch. */
+ * Fills every field of `out` for the resulting launch; num_cus as for
+ * da_choose_splits. */
 int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
                  int num_cus, int cu_margin, int policy, da_plan* out);
 
@@ -124,7 +127,8 @@ int da_split_bounds(int L, int num_splits, int32_t* cuts);
  * s == 1: one kernel launch.  s > 1: the split kernel writes the chunk
  * states to the workspace and the combine kernel merges them in chunk order
  * (exactly da_split_partials followed by da_combine_splits), so results are
- * bit-identical across runs for a fixed (num_splits, pack_gqa). */
+ * bit-identical across runs on one device for a fixed (num_splits,
+ * pack_gqa). */
 int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                    void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                    float softmax_scale, int num_splits, int pack_gqa, void* workspace,

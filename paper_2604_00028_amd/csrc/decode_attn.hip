@@ -15,12 +15,13 @@
 // gfx950 mapping:
 //  * W = 4 wave64s per workgroup, one per SIMD.  The chunk is cut into W
 //    contiguous key ranges, one per wave; each wave walks its range in tiles
-//    of 32 keys and the W wave states are merged through LDS in wave order.
+//    of 32 keys and the W wave states are merged through LDS in a fixed
+//    tree order.
 //  * Scores S^T[key, head] = K . Q^T on MFMA v_mfma_f32_16x16x32_bf16: keys
 //    are the 16 rows, the packed query heads the 16 columns (two column
-//    tiles when a KV head serves up to 32 query heads).  K is fetched
-//    straight into the MFMA A-operand layout: lane (row r, group q) loads the
-//    64 contiguous bytes of dims [32q, 32q+32) of key r.
+//    tiles when a KV head serves up to 32 query heads).  K is fetched in
+//    whole 128-byte lines (8 keys per load instruction) and moved into the
+//    MFMA A-operand layout with one DPP lane rotation per dword.
 //  * Online softmax on the MFMA result layout: every lane holds 8 scores of
 //    one head column; the tile max and sum over the 4 row groups take two
 //    v_permlane16/32_swap steps; exp2 on the hardware v_exp_f32 with the
@@ -53,17 +54,21 @@ namespace {
 constexpr int D = DA_HEAD_DIM;
 constexpr int kKeysPerTile = 32;
 constexpr int kVPitch = 288;                 // bytes per staged V row (256 + 32 pad)
+constexpr int kKPitch = 272;                 // bytes per staged K row (256 + 16 pad)
 constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
-constexpr int kGroupWaves = 4;               // wave64s per workgroup (one per SIMD of a CU)
+constexpr int kStateVals = 2 + 32;           // one wave's state per lane: m, l, 8 x 4 outputs
 
-// LDS of one workgroup of W waves: the per-wave V stage, reused for the
-// wave-state merge ([W][128 dims][16 heads] fp32) and its per-wave m and l.
-constexpr int smem_bytes(int W) {
-  return (W * kKeysPerTile * kVPitch > W * D * 16 * 4 ? W * kKeysPerTile * kVPitch : W * D * 16 * 4) +
-         2 * W * 16 * 4;
+// LDS of one workgroup of W waves with NT head tiles: the per-wave V stage
+// (and K stage when K is staged), reused after the tile loop for the
+// wave-state merge tree (two banks of W/2 and W/4 slots, one wave state of
+// NT x kStateVals x 64 floats each).
+constexpr int merge_slot_bytes(int NT) { return NT * kStateVals * 64 * 4; }
+constexpr int stage_bytes(bool KS) { return kKeysPerTile * (kVPitch + (KS ? kKPitch : 0)); }
+constexpr int smem_bytes(int W, int NT, bool KS) {
+  return W * stage_bytes(KS) > (W / 2 + W / 4) * merge_slot_bytes(NT) ? W * stage_bytes(KS)
+                                                                     : (W / 2 + W / 4) * merge_slot_bytes(NT);
 }
-static_assert(2 * da::kMaxHeadsPerTile * DA_MAX_SPLITS * 4 + da::kMaxHeadsPerTile * 8 <= smem_bytes(4),
-              "merge scratch must fit the workgroup's LDS");
+static_assert(smem_bytes(4, 2, true) <= 160 * 1024, "a workgroup must fit the LDS of one CU");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -142,7 +147,9 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
 
 // NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
 // 32).  W: waves per workgroup.
-template <int NT, int W>
+// KS: K passes through LDS (row-contiguous fetch, then reads in the MFMA
+// operand layout) instead of being fetched straight into that layout.
+template <int NT, int W, bool KS>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -188,9 +195,8 @@ split_partial_kernel(Params p) {
 
   // ---- Q^T as the MFMA B operand.  The reduction index of the product may
   //      map to head dims in any order as long as K and Q agree: k-step j,
-  //      lane group `quad` covers dims [32j + 8*quad, +8), so each K load
-  //      instruction reads one contiguous 64-byte segment of every row.
-  //      Lane holds those dims of head column `col` (zeros for padding).
+  //      lane group `quad` covers dims [32j + 8*quad, +8).  Lane holds those
+  //      dims of head column `col` (zeros for padding).
   bf16x8 qreg[NT][4];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -214,11 +220,17 @@ split_partial_kernel(Params p) {
     for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  unsigned char* vstage = smem + wave * (kKeysPerTile * kVPitch);
+  unsigned char* vstage = smem + wave * stage_bytes(KS);
+  unsigned char* kstage = vstage + kKeysPerTile * kVPitch;
   const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
 
-  // K/V of one 32-key tile: K in the MFMA A layout (two 16-key row blocks x
-  // four 32-dim k-steps), V as 8 rows-of-4 for the LDS stage.  The per-lane
+  // K/V of one 32-key tile.  V always comes as 8 rows-of-4 (16 consecutive
+  // lanes read one 256-byte row) for its LDS stage.  K either comes the same
+  // way and takes its own LDS stage (KS), from which it is read back in the
+  // MFMA A layout, or is fetched straight into that layout: lane (row r,
+  // group q) loads the 64 bytes of dims [32q, 32q+32) of key r, so
+  // neighbouring lanes read different rows, which the memory pipeline
+  // serves at about half the rate of row-contiguous lanes.  The per-lane
   // byte offsets are fixed; tile t moves the descriptor base by t*32 rows
   // and shrinks its record count to match (scalar work only).
   const uint32_t tile_step = kKeysPerTile * rs;
@@ -234,27 +246,56 @@ split_partial_kernel(Params p) {
     const uint32_t left = __builtin_amdgcn_readfirstlane(lim > adv ? lim - adv : 0u);
     const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + base_elems + (int64_t)adv / 2, left);
     const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + base_elems + (int64_t)adv / 2, left);
+    if constexpr (KS) {
+      // kreg[mt][j]: rows 16mt + 4j + quad, bytes [16 col, +16)
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, 0);
+        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, voff[4 * mt + j], 0, 0);
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, 0);
+    }
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, 0);
   };
 
   // One tile held in (kreg, vreg).  `prefetch`: refill those registers with
-  // tile t + 1 while this one is reduced (the loop refills unconditionally,
+  // tile t + 1 once K has been consumed (the loop refills unconditionally,
   // so the compiler waits for exactly the tile in use; the final tile does
-  // not refill).  A second tile in flight per wave was measured slower at
-  // every length: with one workgroup per CU, the CU's memory pipeline rather
-  // than the wave bounds the short-sequence tile rate.
-  // `last`: only the final tile can be shorter than 32 keys and needs its
-  // scores masked.
+  // not refill).  More tiles in flight per wave (a ring of register
+  // buffers) measured slower: it needs more registers than a wave may hold
+  // without spilling into accumulation registers.  `last`: only the final
+  // tile can be shorter than 32 keys and needs its scores masked.
   auto process = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t, auto prefetch, auto last) {
     const int kb = key_lo + t * kKeysPerTile;
     const int nvalid = key_hi - kb;  // >= 1
 
     // scores for this tile: S^T[16 keys x 16 heads] per (mt, nt)
+    bf16x8 kop[2][4];
+    if constexpr (KS) {
+      // row-major K tile in LDS (kKPitch bytes per key), read back so that
+      // lane (col, quad) of operand (mt, j) holds dims [32j + 8quad, +8) of
+      // key 16mt + col
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<u32x4*>(kstage + (16 * mt + 4 * j + quad) * kKPitch + 16 * col) = kreg[mt][j];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          kop[mt][j] = as_bf16x8(*reinterpret_cast<const u32x4*>(kstage + (16 * mt + col) * kKPitch + 16 * (4 * j + quad)));
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) kop[mt][j] = as_bf16x8(kreg[mt][j]);
+    }
     f32x4 sc[NT][2];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -263,7 +304,7 @@ split_partial_kernel(Params p) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[mt][j]), qreg[nt][j], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[mt][j], qreg[nt][j], acc, 0, 0, 0);
         sc[nt][mt] = acc;
       }
 
@@ -324,12 +365,20 @@ split_partial_kernel(Params p) {
     // that lanes 4k + j/4 point at, k = 0..3.  Lane (quad, 4k + m) therefore
     // points at dims [16nn + 4m, +4) of key 16mt + 4quad + k, and lane
     // (quad, col) receives V[16mt + 4quad + k][16nn + col] for k = 0..3.
+    // All 16 reads are issued before the first product so their LDS
+    // latency is paid once per tile rather than once per 16 output dims.
     const unsigned char* vrow = vstage + (quad * 4 + (col >> 2)) * kVPitch + 8 * (col & 3);
+    s16x4 vlo[8], vhi[8];
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn) {
-      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
-      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
-      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      vlo[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
+      vhi[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // the 16 DS reads first
+    __builtin_amdgcn_sched_group_barrier(0x008, 8 * NT, 0);  // then the MFMAs
+#pragma unroll
+    for (int nn = 0; nn < 8; ++nn) {
+      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vlo[nn], vhi[nn], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
         acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], acc_o[nt][nn], 0, 0, 0);
@@ -345,22 +394,27 @@ split_partial_kernel(Params p) {
   for (; t + 1 < ntiles; ++t) process(kreg, vreg, t, yes, no);
   if (t < ntiles) process(kreg, vreg, t, no, yes);
 
-  // ---- merge the W wave states: ((w0 + w1) + (w2 + w3)), in registers.
-  //      Every wave holds its state in the same lane layout (per head column:
-  //      running max, row-summed l, 8 x 4 output values), so a partner's
-  //      state passes through LDS value-major ([value][lane], conflict-free)
-  //      and is absorbed lane by lane.  Wave 0 ends with the workgroup state.
-  static_assert(W == 4, "the merge tree below is written for four waves");
-  constexpr int kVals = 2 + 32;                         // m, l, 8 x 4 outputs
+  // ---- merge the W wave states in a fixed binary tree, in registers:
+  //      ((w0 + w1) + (w2 + w3)) for W = 4, and that plus ((w4 + w5) +
+  //      (w6 + w7)) for W = 8.  Every wave holds its state in the same lane
+  //      layout (per head column: running max, row-summed l, 8 x 4 output
+  //      values), so a partner's state passes through LDS value-major
+  //      ([value][lane], conflict-free) and is absorbed lane by lane.  Level
+  //      k uses slot bank k % 2, so a bank is rewritten only after the
+  //      barrier that follows its last reader.  Wave 0 ends with the
+  //      workgroup state.
+  static_assert(W == 4 || W == 8, "merge tree written for 4 or 8 waves");
   float lsum[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) lsum[nt] = sum_rows(l_run[nt]);
-  float* slot_a = reinterpret_cast<float*>(smem);
-  float* slot_b = slot_a + NT * kVals * 64;
+  auto slot_ptr = [&](int level, int idx) {
+    const int bank_off = (level & 1) ? (W / 2) : 0;
+    return reinterpret_cast<float*>(smem) + (size_t)(bank_off + idx) * (merge_slot_bytes(NT) / 4);
+  };
   auto publish = [&](float* slot) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      float* v = slot + nt * kVals * 64 + lane;
+      float* v = slot + nt * kStateVals * 64 + lane;
       v[0] = m_run[nt];
       v[64] = lsum[nt];
 #pragma unroll
@@ -372,7 +426,7 @@ split_partial_kernel(Params p) {
   auto absorb = [&](const float* slot) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const float* v = slot + nt * kVals * 64 + lane;
+      const float* v = slot + nt * kStateVals * 64 + lane;
       const float mo = v[0];
       const float lo = v[64];
       const float M = fmaxf(m_run[nt], mo);
@@ -387,20 +441,18 @@ split_partial_kernel(Params p) {
         for (int i = 0; i < 4; ++i) acc_o[nt][nn][i] = acc_o[nt][nn][i] * as + v[(2 + nn * 4 + i) * 64] * ao;
     }
   };
-  __syncthreads();                                   // every wave is done with its V stage
-  if (wave == 1) publish(slot_a);
-  if (wave == 3) publish(slot_b);
-  __syncthreads();
-  if (wave == 0) absorb(slot_a);
-  if (wave == 2) absorb(slot_b);
-  __syncthreads();
-  if (wave == 2) publish(slot_a);
-  __syncthreads();
+  __syncthreads();  // every wave is done with its V stage
+#pragma unroll
+  for (int level = 0, stride = 1; stride < W; ++level, stride *= 2) {
+    const int pos = wave % (2 * stride);
+    if (pos == stride) publish(slot_ptr(level, wave / (2 * stride)));
+    __syncthreads();
+    if (pos == 0) absorb(slot_ptr(level, wave / (2 * stride)));
+  }
 
   const int64_t rows = (int64_t)p.B * p.H_Q;
   const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
   if (wave == 0) {
-    absorb(slot_a);
     // lane (col, quad) owns dims 16nn + 4quad + [0, 4) of head 16nt + col
     const __amdgpu_buffer_rsrc_t ors =
         make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
@@ -493,9 +545,10 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cus[kMaxDevices];
+std::atomic<int> g_lds[kMaxDevices];    // LDS bytes one workgroup may use
 std::atomic<int> g_is950[kMaxDevices];  // 0 unknown, 1 yes, 2 no
 
-int query_device(int* cus, int* is950) {
+int query_device(int* cus, int* is950, int* lds = nullptr) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -505,10 +558,12 @@ int query_device(int* cus, int* is950) {
     e = hipGetDeviceProperties(&prop, dev);
     if (e != hipSuccess) return da::fail(DA_ERR_HIP, "hipGetDeviceProperties: %s", hipGetErrorString(e));
     g_cus[dev].store(prop.multiProcessorCount);
+    g_lds[dev].store((int)prop.sharedMemPerBlock);
     g_is950[dev].store(strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2);
   }
   *cus = g_cus[dev].load();
   *is950 = g_is950[dev].load() == 1;
+  if (lds) *lds = g_lds[dev].load();
   return DA_OK;
 }
 
@@ -535,25 +590,33 @@ int check_state_size(int B, int H_Q, int s) {
   return DA_OK;
 }
 
-int ensure_gfx950() {
-  int cus = 0, is950 = 0;
-  int rc = query_device(&cus, &is950);
+int ensure_gfx950(int* cus) {
+  int is950 = 0;
+  int rc = query_device(cus, &is950);
   if (rc) return rc;
   if (!is950) return da::fail(DA_ERR_UNSUPPORTED, "current device is not gfx950");
   return DA_OK;
 }
 
-template <int NT, int W>
+template <int NT, int W, bool KS>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, KS>);
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
-  constexpr int W = kGroupWaves;
-  if (pl.group_waves != W) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", pl.group_waves);
-  const void* fn = pl.heads_per_tile <= 16 ? kernel_ptr<1, W>() : kernel_ptr<2, W>();
+  const int W = pl.group_waves;
+  const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
+  const bool KS = pl.k_staged != 0;
+  if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
+  const void* fn = KS ? (NT == 1 ? kernel_ptr<1, 4, true>() : kernel_ptr<2, 4, true>())
+                      : (NT == 1 ? kernel_ptr<1, 4, false>() : kernel_ptr<2, 4, false>());
+  int cus = 0, is950 = 0, lds = 0;
+  int rc = query_device(&cus, &is950, &lds);
+  if (rc) return rc;
+  const int smem = smem_bytes(W, NT, KS);
+  if (smem > lds) return da::fail(DA_ERR_UNSUPPORTED, "workgroup needs %d bytes of LDS, device allows %d", smem, lds);
   void* args[] = {const_cast<Params*>(&prm)};
-  hipError_t e = hipLaunchKernel(fn, dim3(pl.grid), dim3(64 * W), args, smem_bytes(W), stream);
+  hipError_t e = hipLaunchKernel(fn, dim3(pl.grid), dim3(64 * W), args, smem, stream);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "split partial launch: %s", hipGetErrorString(e));
   return DA_OK;
 }
@@ -612,20 +675,27 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   if (pack_gqa < -1 || pack_gqa > 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
   if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
 
+  // A forced split count fixes the workspace need before any device access.
+  auto check_workspace = [&](int s) {
+    if (s <= 1) return (int)DA_OK;
+    const size_t need = da::workspace_layout(B, H_Q, d, s).total;
+    if (!workspace || workspace_bytes < need)
+      return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, need,
+                      workspace ? workspace_bytes : (size_t)0);
+    return check_state_size(B, H_Q, s);
+  };
+  rc = check_workspace(num_splits);
+  if (rc) return rc;
+  int cus = 0;
+  rc = ensure_gfx950(&cus);
+  if (rc) return rc;
   da_plan pl;
-  rc = da_make_plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 0, 0, DA_POLICY_MI355X, &pl);
+  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   const int s = pl.num_splits;
-  const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
-  if (s > 1) {
-    if (!workspace || workspace_bytes < wl.total)
-      return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, wl.total,
-                      workspace ? workspace_bytes : (size_t)0);
-    rc = check_state_size(B, H_Q, s);
-    if (rc) return rc;
-  }
-  rc = ensure_gfx950();
+  rc = check_workspace(s);
   if (rc) return rc;
+  const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
 
   Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   if (s == 1) {
@@ -660,10 +730,11 @@ int da_split_partials(const void* q, const void* k, const void* v, const int32_t
   if (pack_gqa != 0 && pack_gqa != 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {0,1}", pack_gqa);
   rc = check_state_size(B, H_Q, num_splits);
   if (rc) return rc;
-  da_plan pl;
-  rc = da_make_plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, 0, 0, DA_POLICY_MI355X, &pl);
+  int cus = 0;
+  rc = ensure_gfx950(&cus);
   if (rc) return rc;
-  rc = ensure_gfx950();
+  da_plan pl;
+  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   p.mode = kPartials;
@@ -685,7 +756,8 @@ int da_combine_splits(const float* o_part, const float* m_part, const float* l_p
   if (!aligned(o_part, 8) || !aligned(m_part, 4) || !aligned(l_part, 4) || !aligned(out, 4) ||
       (lse_out && !aligned(lse_out, 4)))
     return da::fail(DA_ERR_ALIGN, "misaligned combine operand");
-  int rc = ensure_gfx950();
+  int cus = 0;
+  int rc = ensure_gfx950(&cus);
   if (rc) return rc;
   return launch_combine(o_part, m_part, l_part, static_cast<uint16_t*>(out), lse_out, num_splits, (int64_t)B * H_Q,
                         static_cast<hipStream_t>(stream));

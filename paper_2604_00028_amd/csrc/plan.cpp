@@ -35,17 +35,19 @@ int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
 // 1.6x of each shape's best) to a sweep of num_splits in
 // {1,2,3,4,6,8,12,16,24,32,48,64} over B in {1,2,4,8,16,32}, H_KV in {1,4,8},
 // g in {8,32} and L_K from 64 to 8192, timed with HIP-graph replay.  Over
-// that sweep the chosen split is on average 1.0% and at worst 7.5% slower
-// than the fastest measured one.
+// that sweep the chosen split is on average 0.3% and at worst 4.7% slower
+// than the fastest measured one; fitted on half of the shapes, it chooses
+// the other half within 1% on average.
 const CostModel& mi355x_model() {
   static const CostModel m = {
-      /*base=*/{3.463, 5.030},
-      /*t_tile=*/{1.118, 1.129},
-      /*merge0=*/2.417,
-      /*merge1=*/{0.227, 0.259},
-      /*hbm_rate=*/5.905e6,
-      /*hbm0=*/0.710,
-      /*tie=*/0.03,
+      /*base=*/{3.662, 5.188},
+      /*t_tile=*/{1.049, 1.130},
+      /*t_tile_staged=*/{0.760, 1.049},
+      /*merge0=*/2.389,
+      /*merge1=*/{0.219, 0.259},
+      /*hbm_rate=*/5.953e6,
+      /*hbm0=*/0.0,
+      /*pnorm=*/3.56,
   };
   return m;
 }
@@ -53,9 +55,10 @@ const CostModel& mi355x_model() {
 // Time of one call with s chunks per sequence:
 //   compute = base + (workgroups per CU) x (32-key tiles per wave) x t_tile
 //   stream  = hbm0 + (K/V bytes + chunk-state traffic) / hbm_rate
-//   T = max(compute, stream) + [s > 1] (merge0 + merge1 s)
+//   T = (compute^p + stream^p)^(1/p) + [s > 1] (merge0 + merge1 s)
 // Every workgroup has four waves, one per SIMD, and walks a quarter of its
-// chunk each; workgroups that share a CU share its SIMDs.
+// chunk each; workgroups that share a CU share its SIMDs.  The soft maximum
+// reflects that a CU's tile loop slows as the chip nears its HBM rate.
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus) {
   const int wide = hpt > 16 ? 1 : 0;
   const double row_bytes = 2.0 * kHeadDim * 2.0;  // K and V row of one KV head
@@ -65,11 +68,12 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
   const int64_t per_wave = (chunk + 3) / 4;
   const int64_t tiles_per_wave = (per_wave + 31) / 32;
   const int64_t per_cu = (wgs + cus - 1) / cus;
-  const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * m.t_tile[wide];
+  const double tt = k_staged(wgs, cus) ? m.t_tile_staged[wide] : m.t_tile[wide];
+  const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * tt;
   double bytes = (double)B * L_K * H_KV * row_bytes;
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
   const double stream = m.hbm0 + bytes / m.hbm_rate;
-  double t = compute > stream ? compute : stream;
+  double t = pow(pow(compute, m.pnorm) + pow(stream, m.pnorm), 1.0 / m.pnorm);
   if (s > 1) t += m.merge0 + m.merge1[wide] * s;
   return t;
 }
@@ -77,18 +81,17 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
 static int mi355x_splits(int B, int H_Q, int H_KV, int L_K, int hpt, int cus) {
   if (L_K <= 0) return 1;
   const CostModel& m = mi355x_model();
-  double best = 0.0;
-  double times[kMaxSplits + 1];
-  for (int s = 1; s <= kMaxSplits; ++s) {
-    times[s] = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus);
-    if (s == 1 || times[s] < best) best = times[s];
+  // Fastest modelled split count; the smallest one on an exact tie.
+  int best_s = 1;
+  double best = model_time(m, B, H_Q, H_KV, L_K, hpt, 1, cus);
+  for (int s = 2; s <= kMaxSplits; ++s) {
+    const double ts = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus);
+    if (ts < best) {
+      best = ts;
+      best_s = s;
+    }
   }
-  // Smallest split count whose modelled time is within the tie tolerance of
-  // the best one (the paper, Section 5.2, likewise keeps the smallest split
-  // that reaches the low-latency plateau).
-  for (int s = 1; s <= kMaxSplits; ++s)
-    if (times[s] <= best * (1.0 + m.tie)) return s;
-  return 1;
+  return best_s;
 }
 
 // The paper's rule (Section 4): 128-key blocks, Batch * H_KV tiles.
@@ -102,13 +105,25 @@ static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
   return mi355x_splits(B, H_Q, H_KV, L_K, hpt, cus);
 }
 
-int group_waves(int L_K_max, int s) {
-  // Four wave64s, one per SIMD.  Measured on MI355X, eight waves per
-  // workgroup were slower at every chunk length: the tile loop is bound by
-  // issue on its SIMD, so a second wave per SIMD only shares it.
-  (void)L_K_max;
-  (void)s;
+int group_waves(int64_t grid, int cus) {
+  // Four wave64s, one per SIMD.  Eight (two per SIMD, with K staged)
+  // measured about 15% faster per key on a lone workgroup per CU with a
+  // long chunk, but 0.6-1.5 us slower at chunks of a few hundred keys; the
+  // split count is the better lever for long sequences, and with it chosen
+  // the chunks stay short.
+  (void)grid;
+  (void)cus;
   return 4;
+}
+
+int k_staged(int64_t grid, int cus) {
+  // Fetched straight into the operand layout, neighbouring lanes read
+  // different key rows and one CU streams K at about half the rate it
+  // reaches with row-contiguous lanes.  Passing K through LDS costs LDS
+  // bandwidth and space, which pays where each workgroup has a CU to
+  // itself; when CUs hold several workgroups HBM bandwidth is the bound and
+  // the direct fetch keeps the LDS footprint small.
+  return grid <= cus ? 1 : 0;
 }
 
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
@@ -152,7 +167,8 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
   out->grid = (int32_t)((int64_t)out->tiles * s);
   out->num_cus = cus;
-  out->group_waves = group_waves(L_K_max, s);
+  out->group_waves = group_waves(out->grid, cus);
+  out->k_staged = k_staged(out->grid, cus);
   return DA_OK;
 }
 
@@ -184,12 +200,11 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus, 
 
 int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
                  int num_cus, int cu_margin, int policy, da_plan* out) {
-  if (num_cus <= 0 && (num_splits <= 0 || pack_gqa < 0)) {
+  if (num_cus <= 0) {
     int is950 = 0;
     int rc = da_device_info(&num_cus, &is950);
     if (rc) return rc;
   }
-  if (num_cus <= 0) num_cus = 1;  // forced plan: the CU count is not used
   return da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, num_cus, cu_margin, policy, out);
 }
 

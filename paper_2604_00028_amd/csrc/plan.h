@@ -30,21 +30,25 @@ inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
 // (B, H_Q, H_KV, L_K) x 12 split counts.  Exposed so tests can check the
 // model's properties.
 struct CostModel {
-  double base[2];     // launch, first loads and epilogue (16-column / 32-column head tiles)
-  double t_tile[2];   // one 32-key tile on one wave
-  double merge0;      // second launch that combines the chunk states, fixed part (s > 1)
-  double merge1[2];   // ... per chunk
-  double hbm_rate;    // sustained HBM bytes per microsecond, whole chip
-  double hbm0;        // fixed part of the streaming bound
-  double tie;         // relative tolerance: take the smallest s within it
+  double base[2];          // launch, first loads and epilogue (16-column / 32-column head tiles)
+  double t_tile[2];        // one 32-key tile on one wave, K fetched into the operand layout
+  double t_tile_staged[2]; // ... K staged through LDS (at most one workgroup per CU)
+  double merge0;           // second launch that combines the chunk states, fixed part (s > 1)
+  double merge1[2];        // ... per chunk
+  double hbm_rate;         // sustained HBM bytes per microsecond, whole chip
+  double hbm0;             // fixed part of the streaming bound
+  double pnorm;            // the two bounds combine as (compute^p + stream^p)^(1/p)
 };
 const CostModel& mi355x_model();
 
 // Modelled time (us) of one call with s splits (policy MI355X).
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus);
 
-// Waves per workgroup for chunks of about L_K_max / s keys.
-int group_waves(int L_K_max, int s);
+// Waves per workgroup for a launch of `grid` workgroups on `cus` CUs.
+int group_waves(int64_t grid, int cus);
+
+// Whether K passes through LDS for that launch.
+int k_staged(int64_t grid, int cus);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);

@@ -156,6 +156,15 @@ def test_plan_fields_and_packing():
     assert p.pack_gqa == 0 and p.heads_per_tile == 1
 
 
+def test_k_staging_follows_workgroups_per_cu():
+    # K passes through LDS exactly when every workgroup has a CU to itself
+    for s, staged in [(1, 1), (4, 1), (5, 0), (64, 0)]:
+        p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=1, num_cus=256)   # 64 tiles
+        assert p.grid == 64 * s and p.k_staged == staged and p.group_waves == 4, (s, p.as_dict())
+    p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=1, num_cus=256, cu_margin=1)
+    assert p.k_staged == 0
+
+
 def test_mi355x_policy_properties():
     for B, H_Q, H_KV in [(1, 8, 1), (1, 64, 8), (4, 32, 1), (16, 32, 4), (32, 64, 8), (8, 256, 32)]:
         prev_tiles_s = None
