@@ -37,6 +37,7 @@ PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_00028_amd", "csrc", "decode_attn.hip")
 SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
+LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
 
 
 def log(msg: str) -> None:
@@ -51,6 +52,7 @@ def parse():
     ap.add_argument("--rounds", type=int, default=7, help="interleaved timed replays per variant")
     ap.add_argument("--highload-steps", type=int, default=20)
     ap.add_argument("--no-highload", action="store_true")
+    ap.add_argument("--no-long", action="store_true", help="skip the L_K = 1024/2048/8192 block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=("headline", "highload", "copy"), default=None,
@@ -182,7 +184,7 @@ def copy_run(args, torch):
 def only_run(args, da, torch, np, dev):
     """Planned (or forced) launch of one workload, nothing else: the command
     the rocprofv3 summaries are taken from."""
-    from workloads import config_shapes, make_inputs
+    from workloads import config_shapes, custom_shape, make_inputs
     if args.only == "copy":
         copy_run(args, torch)
         return
@@ -250,7 +252,7 @@ def main():
     import torch
 
     import paper_2604_00028_amd as da
-    from workloads import config_shapes, make_inputs
+    from workloads import config_shapes, custom_shape, make_inputs
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -314,6 +316,24 @@ def main():
                     "s1_us": round(bv.median, 3), "speedup_vs_s1": round(bv.median / hv.median, 3),
                     "best_fixed": min(sw, key=sw.get), "best_fixed_us": min(sw.values())}
 
+    # longer Llama GQA contexts at B=1, where splitting pays on MI355X
+    longer = {}
+    if not args.no_long:
+        for L in (1024, 2048, 8192):
+            shL = custom_shape(1, 64, 8, L)
+            inL = make_inputs(shL, seed=3000 + L)
+            qL, kL, vL = dev(inL.q), dev(inL.k), dev(inL.v)
+            log(f"timing L_K={L}")
+            hv = Variant("h", da, torch, qL, kL, vL, L, 0, -1, K)
+            sv = [Variant(str(x), da, torch, qL, kL, vL, L, x, 1, K) for x in LONG_SWEEP]
+            interleave(torch, [hv] + sv, args.rounds)
+            sw = {x.plan.num_splits: round(x.median, 3) for x in sv}
+            longer[L] = {"heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
+                         "s1_us": sw[1], "speedup_vs_s1": round(sw[1] / hv.median, 3),
+                         "best_fixed": min(sw, key=sw.get), "best_fixed_us": min(sw.values()),
+                         "vs_best_fixed": round(hv.median / min(sw.values()), 3), "sweep_us": sw}
+            del qL, kL, vL, hv, sv
+
     # ---------------- high load: B=32, H_Q=64, H_KV=8, L_K=8192 (1 GiB of KV)
     high = None
     if not args.no_highload:
@@ -365,6 +385,7 @@ def main():
                         f"s{heur.plan.num_splits}": round(unpacked[1].median, 3)},
         "cold_us": cold,
         "other_lk": other,
+        "long_lk": longer,
         "high_load": high,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(sh.name)},
