@@ -54,7 +54,7 @@ namespace {
 constexpr int D = DA_HEAD_DIM;
 constexpr int kKeysPerTile = 32;
 constexpr int kVPitch = 288;                 // bytes per staged V row (256 + 32 pad)
-constexpr int kKPitch = 272;                 // bytes per staged K row (256 + 16 pad)
+constexpr int kKPitch = 288;                 // bytes per staged K row (256 + 32 pad)
 constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
 constexpr int kStateVals = 2 + 32;           // one wave's state per lane: m, l, 8 x 4 outputs
 
@@ -179,11 +179,13 @@ split_partial_kernel(Params p) {
     row0 = (int64_t)b * p.L_K;
     L = p.L_K;
   }
-  const int c0 = (int)(((int64_t)L * split) / p.s);
-  const int c1 = (int)(((int64_t)L * (split + 1)) / p.s);
+  // L < 2^23 (one sequence's K spans < 2 GiB) and split < 64, so the
+  // products fit 32 bits and the divisions stay 32-bit
+  const int c0 = (int)(((uint32_t)L * (uint32_t)split) / (uint32_t)p.s);
+  const int c1 = (int)(((uint32_t)L * (uint32_t)(split + 1)) / (uint32_t)p.s);
   const int n = c1 - c0;
-  const int key_lo = c0 + (int)(((int64_t)n * wave) / W);
-  const int key_hi = c0 + (int)(((int64_t)n * (wave + 1)) / W);
+  const int key_lo = c0 + (int)(((uint32_t)n * (uint32_t)wave) / W);
+  const int key_hi = c0 + (int)(((uint32_t)n * (uint32_t)(wave + 1)) / W);
 
   // ---- buffer resources over this (sequence, KV head), rows of H_KV*256
   //      bytes, ending at this wave's last key: any key >= key_hi is out of
