@@ -49,7 +49,7 @@ class DaPlan(ctypes.Structure):
         ("grid", ctypes.c_int32),
         ("num_cus", ctypes.c_int32),
         ("group_waves", ctypes.c_int32),
-        ("k_staged", ctypes.c_int32),
+        ("kv_fetch", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

@@ -58,17 +58,36 @@ constexpr int kKPitch = 288;                 // bytes per staged K row (256 + 32
 constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
 constexpr int kStateVals = 2 + 32;           // one wave's state per lane: m, l, 8 x 4 outputs
 
-// LDS of one workgroup of W waves with NT head tiles: the per-wave V stage
-// (and K stage when K is staged), reused after the tile loop for the
-// wave-state merge tree (two banks of W/2 and W/4 slots, one wave state of
-// NT x kStateVals x 64 floats each).
+// How a tile's K and V reach the matrix cores.
+enum Fetch : int {
+  kFetchDirect = 0,  // K straight into the MFMA operand layout; V via registers to LDS
+  kFetchStaged = 1,  // K and V row-contiguous into registers, then through LDS
+  kFetchLds = 2,     // K and V row-contiguous straight into LDS (buffer_load ... lds), two stages
+};
+
+// Direct-to-LDS tiles: an instruction writes 64 lanes x 16 bytes = 4 rows
+// contiguously, so a 32-key tile is 8 such blocks.  Blocks sit kBlockStride
+// bytes apart (64 bytes of padding), and within a block the 16-byte chunks
+// of a row are permuted by an XOR with the row (K) or twice the row (V), so
+// that the operand reads below hit distinct LDS banks.
+constexpr int kBlockStride = 1024 + 64;
+constexpr int kLdsTileBytes = 8 * kBlockStride;                 // one K or V tile
+constexpr int kLdsStageBytes = 2 * kLdsTileBytes;                // K and V of one tile
+
+// LDS of one workgroup of W waves with NT head tiles: the per-wave stages,
+// reused after the tile loop for the wave-state merge tree (two banks of
+// W/2 and W/4 slots, one wave state of NT x kStateVals x 64 floats each).
 constexpr int merge_slot_bytes(int NT) { return NT * kStateVals * 64 * 4; }
-constexpr int stage_bytes(bool KS) { return kKeysPerTile * (kVPitch + (KS ? kKPitch : 0)); }
-constexpr int smem_bytes(int W, int NT, bool KS) {
-  return W * stage_bytes(KS) > (W / 2 + W / 4) * merge_slot_bytes(NT) ? W * stage_bytes(KS)
-                                                                     : (W / 2 + W / 4) * merge_slot_bytes(NT);
+constexpr int stage_bytes(int FETCH) {
+  return FETCH == kFetchLds ? 2 * kLdsStageBytes
+                            : kKeysPerTile * (kVPitch + (FETCH == kFetchStaged ? kKPitch : 0));
 }
-static_assert(smem_bytes(4, 2, true) <= 160 * 1024, "a workgroup must fit the LDS of one CU");
+constexpr int smem_bytes(int W, int NT, int FETCH) {
+  return W * stage_bytes(FETCH) > (W / 2 + W / 4) * merge_slot_bytes(NT) ? W * stage_bytes(FETCH)
+                                                                        : (W / 2 + W / 4) * merge_slot_bytes(NT);
+}
+static_assert(smem_bytes(4, 2, kFetchLds) <= 160 * 1024, "a workgroup must fit the LDS of one CU");
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -78,6 +97,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 enum Mode : int { kDirect = 0, kPartials = 1 };
 
@@ -123,6 +143,11 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
 
+// Byte offset of a shared-memory pointer within the workgroup's LDS.
+__device__ __forceinline__ uint32_t lds_offset(const void* ptr) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) unsigned char*)ptr;
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
@@ -147,9 +172,8 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
 
 // NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
 // 32).  W: waves per workgroup.
-// KS: K passes through LDS (row-contiguous fetch, then reads in the MFMA
-// operand layout) instead of being fetched straight into that layout.
-template <int NT, int W, bool KS>
+// FETCH: a Fetch value.
+template <int NT, int W, int FETCH>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -222,7 +246,8 @@ split_partial_kernel(Params p) {
     for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  unsigned char* vstage = smem + wave * stage_bytes(KS);
+  constexpr bool KS = FETCH == kFetchStaged;
+  unsigned char* vstage = smem + wave * stage_bytes(FETCH);
   unsigned char* kstage = vstage + kKeysPerTile * kVPitch;
   const int ntiles = (key_hi - key_lo + kKeysPerTile - 1) / kKeysPerTile;
 
@@ -264,41 +289,8 @@ split_partial_kernel(Params p) {
     for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, 0);
   };
 
-  // One tile held in (kreg, vreg).  `prefetch`: refill those registers with
-  // tile t + 1 once K has been consumed (the loop refills unconditionally,
-  // so the compiler waits for exactly the tile in use; the final tile does
-  // not refill).  More tiles in flight per wave (a ring of register
-  // buffers) measured slower: it needs more registers than a wave may hold
-  // without spilling into accumulation registers.  `last`: only the final
-  // tile can be shorter than 32 keys and needs its scores masked.
-  auto process = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t, auto prefetch, auto last) {
-    const int kb = key_lo + t * kKeysPerTile;
-    const int nvalid = key_hi - kb;  // >= 1
-
-    // scores for this tile: S^T[16 keys x 16 heads] per (mt, nt)
-    bf16x8 kop[2][4];
-    if constexpr (KS) {
-      // row-major K tile in LDS (kKPitch bytes per key), read back so that
-      // lane (col, quad) of operand (mt, j) holds dims [32j + 8quad, +8) of
-      // key 16mt + col
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<u32x4*>(kstage + (16 * mt + 4 * j + quad) * kKPitch + 16 * col) = kreg[mt][j];
-      __builtin_amdgcn_wave_barrier();
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          kop[mt][j] = as_bf16x8(*reinterpret_cast<const u32x4*>(kstage + (16 * mt + col) * kKPitch + 16 * (4 * j + quad)));
-    } else {
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) kop[mt][j] = as_bf16x8(kreg[mt][j]);
-    }
-    f32x4 sc[NT][2];
+  // S^T[16 keys x 16 heads] per (mt, nt) from the tile's 8 K operands.
+  auto scores = [&](const bf16x8 (&kop)[2][4], f32x4 (&sc)[NT][2]) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -309,18 +301,13 @@ split_partial_kernel(Params p) {
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[mt][j], qreg[nt][j], acc, 0, 0, 0);
         sc[nt][mt] = acc;
       }
+  };
 
-    // stage V rows in LDS (row-major, padded pitch)
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
-      *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
-
-    if constexpr (decltype(prefetch)::value) load_tile(kreg, vreg, t + 1);
-
-    // online softmax per head column, in log2 units of the scaled score:
-    // the max is taken on raw scores (the scale is positive) and each
-    // exponent is one fma, raw * scale*log2(e) - running max
-    bf16x8 pb[NT];
+  // Online softmax per head column, in log2 units of the scaled score: the
+  // max is taken on raw scores (the scale is positive) and each exponent is
+  // one fma, raw * scale*log2(e) - running max.  `last`: only the final tile
+  // can be shorter than 32 keys and needs its scores masked.
+  auto softmax = [&](f32x4 (&sc)[NT][2], int nvalid, auto last, bf16x8 (&pb)[NT]) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       float x[8];
@@ -357,26 +344,47 @@ split_partial_kernel(Params p) {
       pk.w = pack_bf16x2(x[6], x[7]);
       pb[nt] = as_bf16x8(pk);
     }
+  };
 
-    __builtin_amdgcn_wave_barrier();
-    // O^T[16 dims x 16 heads] += V^T[16 dims x 32 keys] . P^T[32 keys x 16 heads]
-    // The k index 8*quad + 4*mt + i of the product stands for key
-    // 16*mt + 4*quad + i, matching the score layout above.  The V^T operand
-    // comes from transposing LDS reads (ds_read_b64_tr_b16): within each
-    // 16-lane group, output lane j receives element j%4 of the 8-byte chunks
-    // that lanes 4k + j/4 point at, k = 0..3.  Lane (quad, 4k + m) therefore
-    // points at dims [16nn + 4m, +4) of key 16mt + 4quad + k, and lane
-    // (quad, col) receives V[16mt + 4quad + k][16nn + col] for k = 0..3.
-    // All 16 reads are issued before the first product so their LDS
-    // latency is paid once per tile rather than once per 16 output dims.
-    const unsigned char* vrow = vstage + (quad * 4 + (col >> 2)) * kVPitch + 8 * (col & 3);
+  // O^T[16 dims x 16 heads] += V^T[16 dims x 32 keys] . P^T[32 keys x 16 heads]
+  // The k index 8*quad + 4*mt + i of the product stands for key
+  // 16*mt + 4*quad + i, matching the score layout.  The V^T operand comes
+  // from transposing LDS reads (ds_read_b64_tr_b16): within each 16-lane
+  // group, output lane j receives element j%4 of the 8-byte chunks that
+  // lanes 4k + j/4 point at, k = 0..3.  Lane (quad, 4k + m) therefore points
+  // at dims [16nn + 4m, +4) of key 16mt + 4quad + k -- vaddr(mt, nn) gives
+  // that address for the stage layout in use -- and lane (quad, col)
+  // receives V[16mt + 4quad + k][16nn + col] for k = 0..3.  All 16 reads are
+  // issued before the first product so their LDS latency is paid once per
+  // tile rather than once per 16 output dims.
+  // With direct-to-LDS loads in flight (`opaque`; vaddr then gives LDS byte
+  // offsets), the reads are written as inline assembly followed by an
+  // explicit wait: the compiler cannot tell that they touch the other stage
+  // and would otherwise drain every outstanding load before them.
+  auto pv = [&](const bf16x8 (&pb)[NT], auto vaddr, auto opaque) {
     s16x4 vlo[8], vhi[8];
+    if constexpr (decltype(opaque)::value) {
 #pragma unroll
-    for (int nn = 0; nn < 8; ++nn) {
-      vlo[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 32 * nn));
-      vhi[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vrow + 16 * kVPitch + 32 * nn));
+      for (int nn = 0; nn < 8; ++nn) {
+        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(vlo[nn]) : "v"((uint32_t)vaddr(0, nn)) : "memory");
+        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(vhi[nn]) : "v"((uint32_t)vaddr(1, nn)) : "memory");
+      }
+      // The wait names every result as an operand it updates, so nothing
+      // that reads them can be scheduled before it.
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(vlo[0]), "+v"(vlo[1]), "+v"(vlo[2]), "+v"(vlo[3]), "+v"(vlo[4]), "+v"(vlo[5]),
+                     "+v"(vlo[6]), "+v"(vlo[7]), "+v"(vhi[0]), "+v"(vhi[1]), "+v"(vhi[2]), "+v"(vhi[3]),
+                     "+v"(vhi[4]), "+v"(vhi[5]), "+v"(vhi[6]), "+v"(vhi[7])
+                   :
+                   : "memory");
+    } else {
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) {
+        vlo[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)vaddr(0, nn));
+        vhi[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)vaddr(1, nn));
+      }
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);  // the 16 DS reads first
+    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);      // the 16 DS reads first
     __builtin_amdgcn_sched_group_barrier(0x008, 8 * NT, 0);  // then the MFMAs
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn) {
@@ -385,16 +393,165 @@ split_partial_kernel(Params p) {
       for (int nt = 0; nt < NT; ++nt)
         acc_o[nt][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[nt], acc_o[nt][nn], 0, 0, 0);
     }
-    __builtin_amdgcn_wave_barrier();
   };
 
   constexpr std::true_type yes{};
   constexpr std::false_type no{};
-  u32x4 kreg[2][4], vreg[8];
-  load_tile(kreg, vreg, 0);
-  int t = 0;
-  for (; t + 1 < ntiles; ++t) process(kreg, vreg, t, yes, no);
-  if (t < ntiles) process(kreg, vreg, t, no, yes);
+  if constexpr (FETCH != kFetchLds) {
+    // One tile held in (kreg, vreg).  `prefetch`: refill those registers
+    // with tile t + 1 once K has been consumed (the loop refills
+    // unconditionally, so the compiler waits for exactly the tile in use; the
+    // final tile does not refill).  More tiles in flight per wave (a ring of
+    // register buffers) measured slower: it needs more registers than a wave
+    // may hold without spilling into accumulation registers.
+    auto process = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t, auto prefetch, auto last) {
+      const int nvalid = key_hi - (key_lo + t * kKeysPerTile);  // >= 1
+      bf16x8 kop[2][4];
+      if constexpr (KS) {
+        // row-major K tile in LDS (kKPitch bytes per key), read back so that
+        // lane (col, quad) of operand (mt, j) holds dims [32j + 8quad, +8) of
+        // key 16mt + col
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<u32x4*>(kstage + (16 * mt + 4 * j + quad) * kKPitch + 16 * col) = kreg[mt][j];
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            kop[mt][j] =
+                as_bf16x8(*reinterpret_cast<const u32x4*>(kstage + (16 * mt + col) * kKPitch + 16 * (4 * j + quad)));
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) kop[mt][j] = as_bf16x8(kreg[mt][j]);
+      }
+      f32x4 sc[NT][2];
+      scores(kop, sc);
+
+      // stage V rows in LDS (row-major, padded pitch)
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj)
+        *reinterpret_cast<u32x4*>(vstage + (4 * jj + quad) * kVPitch + 16 * col) = vreg[jj];
+
+      if constexpr (decltype(prefetch)::value) load_tile(kreg, vreg, t + 1);
+
+      bf16x8 pb[NT];
+      softmax(sc, nvalid, last, pb);
+      __builtin_amdgcn_wave_barrier();
+      const unsigned char* vrow = vstage + (quad * 4 + (col >> 2)) * kVPitch + 8 * (col & 3);
+      pv(pb, [&](int mt, int nn) { return vrow + mt * 16 * kVPitch + 32 * nn; }, no);
+      __builtin_amdgcn_wave_barrier();
+    };
+
+    u32x4 kreg[2][4], vreg[8];
+    load_tile(kreg, vreg, 0);
+    int t = 0;
+    for (; t + 1 < ntiles; ++t) process(kreg, vreg, t, yes, no);
+    if (t < ntiles) process(kreg, vreg, t, no, yes);
+  } else {
+    // Direct-to-LDS: each wave has two stages; tile t + 1 streams into one
+    // while tile t is reduced from the other.  Lane l of a load instruction
+    // for block b (rows 4b + l/16 of the tile) takes the 16-byte chunk at
+    // position l%16 of its row, XOR-permuted by the row within the block:
+    // K chunk (l%16) ^ r, V chunk (l%16) ^ 2r, r = l/16.  Each group of 8
+    // lanes still reads one aligned 128-byte line.
+    const int rr = lane >> 4;
+    const int cp = lane & 15;
+    uint32_t kdoff[8], vdoff[8];
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) {
+      const uint32_t row = (uint32_t)(key_lo + 4 * blk + rr) * rs;
+      kdoff[blk] = row + 16u * (uint32_t)(cp ^ rr);
+      vdoff[blk] = row + 16u * (uint32_t)(cp ^ (2 * rr));
+    }
+    unsigned char* const sbase = smem + wave * stage_bytes(FETCH);
+    auto dma_tile = [&](int stage, int t) {
+      const uint32_t adv = __builtin_amdgcn_readfirstlane((uint32_t)t * tile_step);
+      const uint32_t left = __builtin_amdgcn_readfirstlane(lim > adv ? lim - adv : 0u);
+      const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + base_elems + (int64_t)adv / 2, left);
+      const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + base_elems + (int64_t)adv / 2, left);
+      unsigned char* ks = sbase + stage * kLdsStageBytes;
+      unsigned char* vs = ks + kLdsTileBytes;
+#pragma unroll
+      for (int blk = 0; blk < 8; ++blk)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, kdoff[blk], 0, 0, 0);
+#pragma unroll
+      for (int blk = 0; blk < 8; ++blk)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, vdoff[blk], 0, 0, 0);
+    };
+    // Operand reads.  K operand (mt, j), lane (col, quad): key 16mt + col is
+    // row col%4 of block 4mt + col/4, dims [32j + 8quad, +8) are its chunk
+    // 4j + quad.  V (see pv): key 16mt + 4quad + k is row k of block
+    // 4mt + quad, dims [16nn + 4m, +4) sit in chunk 2nn + m/2.  The permuted
+    // offsets differ per lane and per operand, so they are computed once.
+    uint32_t kro[2][4], vro[2][8];
+    {
+      const int kr = col & 3;
+      const int vk = col >> 2;
+      const int vm = col & 3;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          kro[mt][j] = lds_offset(sbase) + (uint32_t)((4 * mt + (col >> 2)) * kBlockStride + kr * 256 +
+                                                      16 * ((4 * j + quad) ^ kr));
+#pragma unroll
+        for (int nn = 0; nn < 8; ++nn)
+          vro[mt][nn] = lds_offset(sbase) + (uint32_t)(kLdsTileBytes + (4 * mt + quad) * kBlockStride + vk * 256 +
+                                                       32 * (nn ^ vk) + 8 * vm);
+      }
+    }
+    // `stage` is a compile-time constant, so its offset folds into the LDS
+    // instructions' immediate field.
+    auto reduce = [&](auto stage, int t, auto last) {
+      constexpr uint32_t so = decltype(stage)::value * kLdsStageBytes;
+      bf16x8 kop[2][4];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          kop[mt][j] = as_bf16x8(*reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(
+              (uintptr_t)(kro[mt][j] + so)));
+      f32x4 sc[NT][2];
+      scores(kop, sc);
+      bf16x8 pb[NT];
+      softmax(sc, key_hi - (key_lo + t * kKeysPerTile), last, pb);
+      pv(pb, [&](int mt, int nn) { return vro[mt][nn] + so; }, yes);
+    };
+    // The compiler cannot see that the LDS reads depend on the direct-to-LDS
+    // loads, so the waits are explicit: 16 loads per tile, completing in
+    // issue order.  Tile t lives in stage t % 2; the loop takes tiles in
+    // pairs so that each stage is known at compile time.
+    constexpr std::integral_constant<int, 0> s0{};
+    constexpr std::integral_constant<int, 1> s1{};
+    if (ntiles > 0) dma_tile(0, 0);
+    int t = 0;
+    for (; t + 2 < ntiles; t += 2) {
+      dma_tile(1, t + 1);
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      reduce(s0, t, no);
+      dma_tile(0, t + 2);
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      reduce(s1, t + 1, no);
+    }
+    if (t + 1 < ntiles) {
+      dma_tile(1, t + 1);
+      asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+      reduce(s0, t, no);
+      ++t;
+    }
+    if (t < ntiles) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (t & 1)
+        reduce(s1, t, yes);
+      else
+        reduce(s0, t, yes);
+    }
+  }
 
   // ---- merge the W wave states in a fixed binary tree, in registers:
   //      ((w0 + w1) + (w2 + w3)) for W = 4, and that plus ((w4 + w5) +
@@ -600,22 +757,30 @@ int ensure_gfx950(int* cus) {
   return DA_OK;
 }
 
-template <int NT, int W, bool KS>
+template <int NT, int W, int FETCH>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, KS>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH>);
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   const int W = pl.group_waves;
   const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
-  const bool KS = pl.k_staged != 0;
+  const int FETCH = pl.kv_fetch;
   if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
-  const void* fn = KS ? (NT == 1 ? kernel_ptr<1, 4, true>() : kernel_ptr<2, 4, true>())
-                      : (NT == 1 ? kernel_ptr<1, 4, false>() : kernel_ptr<2, 4, false>());
+  const void* fn = nullptr;
+  switch (FETCH * 2 + NT - 1) {
+    case 0: fn = kernel_ptr<1, 4, kFetchDirect>(); break;
+    case 1: fn = kernel_ptr<2, 4, kFetchDirect>(); break;
+    case 2: fn = kernel_ptr<1, 4, kFetchStaged>(); break;
+    case 3: fn = kernel_ptr<2, 4, kFetchStaged>(); break;
+    case 4: fn = kernel_ptr<1, 4, kFetchLds>(); break;
+    case 5: fn = kernel_ptr<2, 4, kFetchLds>(); break;
+    default: return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
+  }
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
   if (rc) return rc;
-  const int smem = smem_bytes(W, NT, KS);
+  const int smem = smem_bytes(W, NT, FETCH);
   if (smem > lds) return da::fail(DA_ERR_UNSUPPORTED, "workgroup needs %d bytes of LDS, device allows %d", smem, lds);
   void* args[] = {const_cast<Params*>(&prm)};
   hipError_t e = hipLaunchKernel(fn, dim3(pl.grid), dim3(64 * W), args, smem, stream);

@@ -68,7 +68,7 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
   const int64_t per_wave = (chunk + 3) / 4;
   const int64_t tiles_per_wave = (per_wave + 31) / 32;
   const int64_t per_cu = (wgs + cus - 1) / cus;
-  const double tt = k_staged(wgs, cus) ? m.t_tile_staged[wide] : m.t_tile[wide];
+  const double tt = kv_fetch(wgs, cus) ? m.t_tile_staged[wide] : m.t_tile[wide];
   const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * tt;
   double bytes = (double)B * L_K * H_KV * row_bytes;
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
@@ -116,14 +116,14 @@ int group_waves(int64_t grid, int cus) {
   return 4;
 }
 
-int k_staged(int64_t grid, int cus) {
+int kv_fetch(int64_t grid, int cus) {
   // Fetched straight into the operand layout, neighbouring lanes read
   // different key rows and one CU streams K at about half the rate it
   // reaches with row-contiguous lanes.  Passing K through LDS costs LDS
   // bandwidth and space, which pays where each workgroup has a CU to
   // itself; when CUs hold several workgroups HBM bandwidth is the bound and
   // the direct fetch keeps the LDS footprint small.
-  return grid <= cus ? 1 : 0;
+  return grid <= cus ? kLoneFetch : 0;
 }
 
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
@@ -168,7 +168,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   out->grid = (int32_t)((int64_t)out->tiles * s);
   out->num_cus = cus;
   out->group_waves = group_waves(out->grid, cus);
-  out->k_staged = k_staged(out->grid, cus);
+  out->kv_fetch = kv_fetch(out->grid, cus);
   return DA_OK;
 }
 

@@ -47,8 +47,10 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
 // Waves per workgroup for a launch of `grid` workgroups on `cus` CUs.
 int group_waves(int64_t grid, int cus);
 
-// Whether K passes through LDS for that launch.
-int k_staged(int64_t grid, int cus);
+// How K/V tiles reach the matrix cores for that launch (da_plan.kv_fetch);
+// kLoneFetch is the mode used when every workgroup has a CU to itself.
+constexpr int kLoneFetch = 2;
+int kv_fetch(int64_t grid, int cus);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);

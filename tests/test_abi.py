@@ -156,13 +156,13 @@ def test_plan_fields_and_packing():
     assert p.pack_gqa == 0 and p.heads_per_tile == 1
 
 
-def test_k_staging_follows_workgroups_per_cu():
+def test_fetch_mode_follows_workgroups_per_cu():
     # K passes through LDS exactly when every workgroup has a CU to itself
     for s, staged in [(1, 1), (4, 1), (5, 0), (64, 0)]:
         p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=1, num_cus=256)   # 64 tiles
-        assert p.grid == 64 * s and p.k_staged == staged and p.group_waves == 4, (s, p.as_dict())
+        assert p.grid == 64 * s and (p.kv_fetch > 0) == bool(staged) and p.group_waves == 4, (s, p.as_dict())
     p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=1, num_cus=256, cu_margin=1)
-    assert p.k_staged == 0
+    assert p.kv_fetch == 0
 
 
 def test_mi355x_policy_properties():
