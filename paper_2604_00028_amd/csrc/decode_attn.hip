@@ -15,8 +15,8 @@
 // gfx950 mapping:
 //  * W = 4 wave64s per workgroup, one per SIMD.  The chunk is cut into W
 //    contiguous key ranges, one per wave; each wave walks its range in tiles
-//    of 32 keys and the W wave states are merged through LDS in a fixed
-//    tree order.
+//    of 32 keys, and the W wave states are merged through LDS in one step,
+//    each wave producing a quarter of the output dims.
 //  * Scores S^T[key, head] = K . Q^T on MFMA v_mfma_f32_16x16x32_bf16: keys
 //    are the 16 rows, the packed query heads the 16 columns (two column
 //    tiles when a KV head serves up to 32 query heads).  K is fetched in
@@ -67,24 +67,24 @@ enum Fetch : int {
 
 // Direct-to-LDS tiles: an instruction writes 64 lanes x 16 bytes = 4 rows
 // contiguously, so a 32-key tile is 8 such blocks.  Blocks sit kBlockStride
-// bytes apart (64 bytes of padding), and within a block the 16-byte chunks
-// of a row are permuted by an XOR with the row (K) or twice the row (V), so
-// that the operand reads below hit distinct LDS banks.
-constexpr int kBlockStride = 1024 + 64;
+// bytes apart and within a block the 16-byte chunks of row r are rotated
+// by 2r positions, which places every chunk on the LDS banks a 288-byte row
+// pitch would (the pitch the register-staged path uses): the operand reads
+// below then measure no bank conflicts.
+constexpr int kBlockStride = 4 * 288;
 constexpr int kLdsTileBytes = 8 * kBlockStride;                 // one K or V tile
 constexpr int kLdsStageBytes = 2 * kLdsTileBytes;                // K and V of one tile
 
 // LDS of one workgroup of W waves with NT head tiles: the per-wave stages,
-// reused after the tile loop for the wave-state merge tree (two banks of
-// W/2 and W/4 slots, one wave state of NT x kStateVals x 64 floats each).
+// reused after the tile loop for the wave-state merge (W slots, one wave
+// state of NT x kStateVals x 64 floats each).
 constexpr int merge_slot_bytes(int NT) { return NT * kStateVals * 64 * 4; }
 constexpr int stage_bytes(int FETCH) {
   return FETCH == kFetchLds ? 2 * kLdsStageBytes
                             : kKeysPerTile * (kVPitch + (FETCH == kFetchStaged ? kKPitch : 0));
 }
 constexpr int smem_bytes(int W, int NT, int FETCH) {
-  return W * stage_bytes(FETCH) > (W / 2 + W / 4) * merge_slot_bytes(NT) ? W * stage_bytes(FETCH)
-                                                                        : (W / 2 + W / 4) * merge_slot_bytes(NT);
+  return W * stage_bytes(FETCH) > W * merge_slot_bytes(NT) ? W * stage_bytes(FETCH) : W * merge_slot_bytes(NT);
 }
 static_assert(smem_bytes(4, 2, kFetchLds) <= 160 * 1024, "a workgroup must fit the LDS of one CU");
 
@@ -455,19 +455,14 @@ split_partial_kernel(Params p) {
   } else {
     // Direct-to-LDS: each wave has two stages; tile t + 1 streams into one
     // while tile t is reduced from the other.  Lane l of a load instruction
-    // for block b (rows 4b + l/16 of the tile) takes the 16-byte chunk at
-    // position l%16 of its row, XOR-permuted by the row within the block:
-    // K chunk (l%16) ^ r, V chunk (l%16) ^ 2r, r = l/16.  Each group of 8
-    // lanes still reads one aligned 128-byte line.
+    // for block b (rows 4b + l/16 of the tile) fills position l%16 of its
+    // row, which holds chunk (l%16 - 2r) mod 16, r = l/16.
     const int rr = lane >> 4;
     const int cp = lane & 15;
-    uint32_t kdoff[8], vdoff[8];
+    uint32_t dmaoff[8];
 #pragma unroll
-    for (int blk = 0; blk < 8; ++blk) {
-      const uint32_t row = (uint32_t)(key_lo + 4 * blk + rr) * rs;
-      kdoff[blk] = row + 16u * (uint32_t)(cp ^ rr);
-      vdoff[blk] = row + 16u * (uint32_t)(cp ^ (2 * rr));
-    }
+    for (int blk = 0; blk < 8; ++blk)
+      dmaoff[blk] = (uint32_t)(key_lo + 4 * blk + rr) * rs + 16u * (uint32_t)((cp - 2 * rr) & 15);
     unsigned char* const sbase = smem + wave * stage_bytes(FETCH);
     auto dma_tile = [&](int stage, int t) {
       const uint32_t adv = __builtin_amdgcn_readfirstlane((uint32_t)t * tile_step);
@@ -478,15 +473,15 @@ split_partial_kernel(Params p) {
       unsigned char* vs = ks + kLdsTileBytes;
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, kdoff[blk], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0, 0);
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, vdoff[blk], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0, 0);
     };
     // Operand reads.  K operand (mt, j), lane (col, quad): key 16mt + col is
     // row col%4 of block 4mt + col/4, dims [32j + 8quad, +8) are its chunk
     // 4j + quad.  V (see pv): key 16mt + 4quad + k is row k of block
-    // 4mt + quad, dims [16nn + 4m, +4) sit in chunk 2nn + m/2.  The permuted
+    // 4mt + quad, dims [16nn + 4m, +4) sit in chunk 2nn + m/2.  The rotated
     // offsets differ per lane and per operand, so they are computed once.
     uint32_t kro[2][4], vro[2][8];
     {
@@ -498,11 +493,11 @@ split_partial_kernel(Params p) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           kro[mt][j] = lds_offset(sbase) + (uint32_t)((4 * mt + (col >> 2)) * kBlockStride + kr * 256 +
-                                                      16 * ((4 * j + quad) ^ kr));
+                                                      16 * ((4 * j + quad + 2 * kr) & 15));
 #pragma unroll
         for (int nn = 0; nn < 8; ++nn)
           vro[mt][nn] = lds_offset(sbase) + (uint32_t)(kLdsTileBytes + (4 * mt + quad) * kBlockStride + vk * 256 +
-                                                       32 * (nn ^ vk) + 8 * vm);
+                                                       16 * ((2 * nn + (vm >> 1) + 2 * vk) & 15) + 8 * (vm & 1));
       }
     }
     // `stage` is a compile-time constant, so its offset folds into the LDS
@@ -553,27 +548,25 @@ split_partial_kernel(Params p) {
     }
   }
 
-  // ---- merge the W wave states in a fixed binary tree, in registers:
-  //      ((w0 + w1) + (w2 + w3)) for W = 4, and that plus ((w4 + w5) +
-  //      (w6 + w7)) for W = 8.  Every wave holds its state in the same lane
-  //      layout (per head column: running max, row-summed l, 8 x 4 output
-  //      values), so a partner's state passes through LDS value-major
-  //      ([value][lane], conflict-free) and is absorbed lane by lane.  Level
-  //      k uses slot bank k % 2, so a bank is rewritten only after the
-  //      barrier that follows its last reader.  Wave 0 ends with the
-  //      workgroup state.
-  static_assert(W == 4 || W == 8, "merge tree written for 4 or 8 waves");
+  // ---- merge the W wave states in one step.  Every wave publishes its
+  //      state (per head column: running max, row-summed l, 8 x 4 output
+  //      values; all waves share one lane layout) to LDS value-major
+  //      ([value][lane], conflict-free).  After one barrier, wave w merges
+  //      the W states for its 8/W blocks of 16 output dims -- maximum,
+  //      weights, then sums taken in wave order, so the result is the same
+  //      on every run -- and writes that slice of the output.
+  static_assert(8 % W == 0, "each wave merges a whole number of 16-dim blocks");
+  constexpr int NBW = 8 / W;
   float lsum[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) lsum[nt] = sum_rows(l_run[nt]);
-  auto slot_ptr = [&](int level, int idx) {
-    const int bank_off = (level & 1) ? (W / 2) : 0;
-    return reinterpret_cast<float*>(smem) + (size_t)(bank_off + idx) * (merge_slot_bytes(NT) / 4);
-  };
-  auto publish = [&](float* slot) {
+  auto slot = [&](int w) { return reinterpret_cast<float*>(smem) + (size_t)w * (merge_slot_bytes(NT) / 4); };
+  __syncthreads();  // every wave is done with its stages
+  {
+    float* v0 = slot(wave) + lane;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      float* v = slot + nt * kStateVals * 64 + lane;
+      float* v = v0 + nt * kStateVals * 64;
       v[0] = m_run[nt];
       v[64] = lsum[nt];
 #pragma unroll
@@ -581,68 +574,64 @@ split_partial_kernel(Params p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[(2 + nn * 4 + i) * 64] = acc_o[nt][nn][i];
     }
-  };
-  auto absorb = [&](const float* slot) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const float* v = slot + nt * kStateVals * 64 + lane;
-      const float mo = v[0];
-      const float lo = v[64];
-      const float M = fmaxf(m_run[nt], mo);
-      const bool empty = M == -INFINITY;  // both states empty: stay empty
-      const float as = empty ? 0.f : __builtin_amdgcn_exp2f(m_run[nt] - M);
-      const float ao = empty ? 0.f : __builtin_amdgcn_exp2f(mo - M);
-      lsum[nt] = lsum[nt] * as + lo * ao;
-      m_run[nt] = M;
-#pragma unroll
-      for (int nn = 0; nn < 8; ++nn)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc_o[nt][nn][i] = acc_o[nt][nn][i] * as + v[(2 + nn * 4 + i) * 64] * ao;
-    }
-  };
-  __syncthreads();  // every wave is done with its V stage
-#pragma unroll
-  for (int level = 0, stride = 1; stride < W; ++level, stride *= 2) {
-    const int pos = wave % (2 * stride);
-    if (pos == stride) publish(slot_ptr(level, wave / (2 * stride)));
-    __syncthreads();
-    if (pos == 0) absorb(slot_ptr(level, wave / (2 * stride)));
   }
+  __syncthreads();
 
   const int64_t rows = (int64_t)p.B * p.H_Q;
   const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
-  if (wave == 0) {
+  const __amdgpu_buffer_rsrc_t ors =
+      make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float mk[W], wk[W];
+    float M = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < W; ++k) {
+      mk[k] = slot(k)[nt * kStateVals * 64 + lane];
+      M = fmaxf(M, mk[k]);
+    }
+    float Lw = 0.f;
+#pragma unroll
+    for (int k = 0; k < W; ++k) {
+      wk[k] = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mk[k] - M);  // all empty: stays empty
+      Lw = fmaf(wk[k], slot(k)[(nt * kStateVals + 1) * 64 + lane], Lw);
+    }
     // lane (col, quad) owns dims 16nn + 4quad + [0, 4) of head 16nt + col
-    const __amdgpu_buffer_rsrc_t ors =
-        make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
+    f32x4 o[NBW];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int h = nt * 16 + col;
-      if (h >= p.hpt) continue;
-      const int64_t row = row0_tile + h;
-      const float lw = lsum[nt];
-      const float mval = lw > 0.f ? m_run[nt] * kLn2 : -INFINITY;
-      if (p.mode == kDirect) {
-        const float inv = lw > 0.f ? 1.0f / lw : 0.f;
+    for (int bb = 0; bb < NBW; ++bb) {
+      const int nn = wave * NBW + bb;
+      o[bb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int nn = 0; nn < 8; ++nn) {
-          const f32x4 a = acc_o[nt][nn];
-          *reinterpret_cast<uint2*>(p.out + row * D + 16 * nn + 4 * quad) =
-              make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
-        }
-        if (p.lse && quad == 0) p.lse[row] = lw > 0.f ? mval + logf(lw) : -INFINITY;
-      } else {
+      for (int k = 0; k < W; ++k)
 #pragma unroll
-        for (int nn = 0; nn < 8; ++nn) {
-          const f32x4 a = acc_o[nt][nn];
-          const u32x4 bits = {__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
-                              __float_as_uint(a[3])};
-          __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0, 0);
-        }
-        if (quad == 0) {
-          p.m_part[split * rows + row] = mval;
-          p.l_part[split * rows + row] = lw;
-        }
+        for (int i = 0; i < 4; ++i)
+          o[bb][i] = fmaf(wk[k], slot(k)[(nt * kStateVals + 2 + nn * 4 + i) * 64 + lane], o[bb][i]);
+    }
+    const int h = nt * 16 + col;
+    if (h >= p.hpt) continue;
+    const int64_t row = row0_tile + h;
+    const float mval = Lw > 0.f ? M * kLn2 : -INFINITY;
+    if (p.mode == kDirect) {
+      const float inv = Lw > 0.f ? 1.0f / Lw : 0.f;
+#pragma unroll
+      for (int bb = 0; bb < NBW; ++bb) {
+        const int nn = wave * NBW + bb;
+        *reinterpret_cast<uint2*>(p.out + row * D + 16 * nn + 4 * quad) =
+            make_uint2(pack_bf16x2(o[bb][0] * inv, o[bb][1] * inv), pack_bf16x2(o[bb][2] * inv, o[bb][3] * inv));
+      }
+      if (p.lse && wave == 0 && quad == 0) p.lse[row] = Lw > 0.f ? mval + logf(Lw) : -INFINITY;
+    } else {
+#pragma unroll
+      for (int bb = 0; bb < NBW; ++bb) {
+        const int nn = wave * NBW + bb;
+        const u32x4 bits = {__float_as_uint(o[bb][0]), __float_as_uint(o[bb][1]), __float_as_uint(o[bb][2]),
+                            __float_as_uint(o[bb][3])};
+        __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0, 0);
+      }
+      if (wave == 0 && quad == 0) {
+        p.m_part[split * rows + row] = mval;
+        p.l_part[split * rows + row] = Lw;
       }
     }
   }
