@@ -32,7 +32,7 @@ inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
 struct CostModel {
   double base[2];          // launch, first loads and epilogue (16-column / 32-column head tiles)
   double t_tile[2];        // one 32-key tile on one wave, K fetched into the operand layout
-  double t_tile_staged[2]; // ... K staged through LDS (at most one workgroup per CU)
+  double t_tile_staged[2]; // ... K and V fetched straight into LDS (at most one workgroup per CU)
   double merge0;           // second launch that combines the chunk states, fixed part (s > 1)
   double merge1[2];        // ... per chunk
   double hbm_rate;         // sustained HBM bytes per microsecond, whole chip
