@@ -38,6 +38,12 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_00028_amd", "csrc", "decode_attn.
 SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
 LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
+# The paper's regression matrix (Section 5.3): Batch x L_K x H_KV, here with H_Q = 8 * H_KV.
+REG_B = (1, 2, 4, 8)
+REG_L = (128, 256, 384, 512, 1024, 2048, 4096, 8192)
+REG_HKV = (1, 2, 4, 8, 32)
+REG_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)
+PROFILE_REGRESSION = os.path.join(ROOT, "profiles", "regression_160_configs.md")
 
 
 def log(msg: str) -> None:
@@ -59,6 +65,11 @@ def parse():
                     help="time only the planned launch of one workload, or a plain 1 GiB device copy "
                          "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
+    ap.add_argument("--regression", metavar="OUT_JSON", default=None,
+                    help="time the paper's 160-configuration regression matrix (heuristic, num_splits=1, the "
+                         "paper's policy and fixed splits) and write the results to OUT_JSON")
+    ap.add_argument("--regression-summary", metavar="IN_JSON", default=None,
+                    help="summarise a --regression result into profiles/regression_160_configs.md")
     ap.add_argument("--traffic-summary", metavar="DIR", default=None,
                     help="derive per-launch HBM traffic from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE output "
                          "directories DIR/pmc_<COUNTER>_<workload> and write profiles/traffic.json")
@@ -239,10 +250,97 @@ def traffic_summary(d: str) -> None:
     print(json.dumps(out))
 
 
+def regression_run(args, da, torch) -> None:
+    """Every configuration of the matrix: the MI355X heuristic, num_splits = 1, the paper's policy and a
+    fixed-split sweep, each as graph-replayed calls interleaved over rounds (synthetic inputs)."""
+    results = []
+    gen = torch.Generator(device="cuda")
+    for B in REG_B:
+        for H_KV in REG_HKV:
+            H_Q = 8 * H_KV
+            for L in REG_L:
+                gen.manual_seed(B * 100000 + H_KV * 10000 + L)
+                q = torch.randn((B, H_Q, 128), generator=gen, device="cuda").to(torch.bfloat16)
+                k = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
+                v = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
+                est_us = 5.0 + 2.0 * B * L * H_KV * 256 / 5e6
+                K = int(max(10, min(100, 2000.0 / est_us)))
+                # each distinct launch (split count, packing on) is timed once; the heuristic and the
+                # paper's policy reuse the sweep's timing when they pick a split it already covers
+                paper_s = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER).num_splits
+                heur_s = da.da_choose_splits(B, H_Q, H_KV, L).num_splits
+                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s, paper_s})
+                variants = {s: Variant(str(s), da, torch, q, k, v, L, s, 1, K) for s in splits}
+                interleave(torch, list(variants.values()), args.rounds)
+                sw = {s: round(x.median, 3) for s, x in variants.items() if s in REG_SWEEP}
+                best = min(sw, key=sw.get)
+                row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L,
+                       "heuristic_splits": heur_s, "heuristic_us": round(variants[heur_s].median, 3),
+                       "paper_splits": paper_s, "paper_us": round(variants[paper_s].median, 3),
+                       "s1_us": sw[1], "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
+                results.append(row)
+                log(f"B={B} H_KV={H_KV} L_K={L}: heuristic s={row['heuristic_splits']} {row['heuristic_us']} us, "
+                    f"s=1 {row['s1_us']}, paper s={row['paper_splits']} {row['paper_us']}, "
+                    f"best s={best} {sw[best]}")
+                del q, k, v, variants
+    json.dump({"configs": results}, open(args.regression, "w"), indent=1)
+    worst_s1 = max(r["heuristic_us"] / r["s1_us"] for r in results)
+    worst_best = max(r["heuristic_us"] / r["best_fixed_us"] for r in results)
+    print(json.dumps({"regression_configs": len(results), "worst_heuristic_over_s1": round(worst_s1, 3),
+                      "worst_heuristic_over_best_fixed": round(worst_best, 3)}), flush=True)
+
+
+def regression_summary(path: str) -> None:
+    rows = json.load(open(path))["configs"]
+    n = len(rows)
+    r_s1 = [r["heuristic_us"] / r["s1_us"] for r in rows]
+    r_best = [r["heuristic_us"] / r["best_fixed_us"] for r in rows]
+    r_paper = [r["heuristic_us"] / r["paper_us"] for r in rows]
+    faster = sum(x < 0.99 for x in r_s1)
+    slower = [r for r, x in zip(rows, r_s1) if x > 1 / 0.99]
+    over5 = [r for r, x in zip(rows, r_best) if x > 1.05]
+    lines = [
+        "# Regression matrix: 160 decode shapes (the paper's Section 5.3 sweep) on MI355X",
+        "",
+        "Batch in {1, 2, 4, 8} x L_K in {128, 256, 384, 512, 1024, 2048, 4096, 8192} x H_KV in {1, 2, 4, 8, 32},",
+        "H_Q = 8 * H_KV, D = 128, bf16, synthetic inputs. Each shape times the MI355X heuristic, num_splits = 1,",
+        "the paper's policy (policy PAPER) and fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8),",
+        "as graph-replayed calls interleaved over rounds (median). Each distinct launch is timed once: a policy",
+        "that picks a split of the sweep shares that split's timing.",
+        "",
+        "Command (MI355X, one GPU):",
+        "",
+        "```",
+        "python3 bench.py --regression gpurun_out/regression.json --rounds 5",
+        "python3 bench.py --regression-summary gpurun_out/regression.json   # writes this file",
+        "```",
+        "",
+        f"* Shapes: {n}.",
+        f"* Heuristic vs num_splits = 1: at least 0.99x its speed in {n - len(slower)} of {n} shapes; worst "
+        f"{max(r_s1):.3f}x the time of s = 1; faster by more than 1% in {faster}.",
+        f"* Heuristic vs the best fixed split: within 5% in {n - len(over5)} of {n}; worst {max(r_best):.3f}x, "
+        f"mean {statistics.mean(r_best):.3f}x.",
+        f"* Heuristic vs the paper's policy: mean {statistics.mean(r_paper):.3f}x its time, "
+        f"best {min(r_paper):.3f}x, worst {max(r_paper):.3f}x.",
+        "",
+        "| B | H_KV | L_K | heuristic s | us | s = 1 us | vs s = 1 | paper s | paper us | best s | best us | vs best |",
+        "|---|---|---|---|---|---|---|---|---|---|---|---|",
+    ]
+    for r, a, c in zip(rows, r_s1, r_best):
+        lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_splits']} | {r['heuristic_us']} | "
+                     f"{r['s1_us']} | {1 / a:.2f}x | {r['paper_splits']} | {r['paper_us']} | {r['best_fixed']} | "
+                     f"{r['best_fixed_us']} | {c:.3f} |")
+    open(PROFILE_REGRESSION, "w").write("\n".join(lines) + "\n")
+    print(f"wrote {PROFILE_REGRESSION}")
+
+
 def main():
     args = parse()
     if args.traffic_summary:
         traffic_summary(args.traffic_summary)
+        return
+    if args.regression_summary:
+        regression_summary(args.regression_summary)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode kernel shards by "
@@ -262,6 +360,9 @@ def main():
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
     if args.only:
         only_run(args, da, torch, np, dev)
+        return
+    if args.regression:
+        regression_run(args, da, torch)
         return
 
     # ---------------- headline: Llama-3.1-70B GQA decode, B=1, L_K=512

