@@ -268,8 +268,9 @@ def regression_run(args, da, torch) -> None:
                 # each distinct launch (split count, packing on) is timed once; the heuristic and the
                 # paper's policy reuse the sweep's timing when they pick a split it already covers
                 paper_s = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER).num_splits
+                evolved_s = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_EVOLVED).num_splits
                 heur_s = da.da_choose_splits(B, H_Q, H_KV, L).num_splits
-                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s, paper_s})
+                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s, paper_s, evolved_s})
                 variants = {s: Variant(str(s), da, torch, q, k, v, L, s, 1, K) for s in splits}
                 interleave(torch, list(variants.values()), args.rounds)
                 sw = {s: round(x.median, 3) for s, x in variants.items() if s in REG_SWEEP}
@@ -277,6 +278,7 @@ def regression_run(args, da, torch) -> None:
                 row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L,
                        "heuristic_splits": heur_s, "heuristic_us": round(variants[heur_s].median, 3),
                        "paper_splits": paper_s, "paper_us": round(variants[paper_s].median, 3),
+                       "evolved_splits": evolved_s, "evolved_us": round(variants[evolved_s].median, 3),
                        "s1_us": sw[1], "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
                 results.append(row)
                 log(f"B={B} H_KV={H_KV} L_K={L}: heuristic s={row['heuristic_splits']} {row['heuristic_us']} us, "
@@ -296,6 +298,7 @@ def regression_summary(path: str) -> None:
     r_s1 = [r["heuristic_us"] / r["s1_us"] for r in rows]
     r_best = [r["heuristic_us"] / r["best_fixed_us"] for r in rows]
     r_paper = [r["heuristic_us"] / r["paper_us"] for r in rows]
+    r_evo = [r["heuristic_us"] / r["evolved_us"] for r in rows if r["B"] == 1]
     faster = sum(x < 0.99 for x in r_s1)
     slower = [r for r, x in zip(rows, r_s1) if x > 1 / 0.99]
     over5 = [r for r, x in zip(rows, r_best) if x > 1.05]
@@ -304,7 +307,8 @@ def regression_summary(path: str) -> None:
         "",
         "Batch in {1, 2, 4, 8} x L_K in {128, 256, 384, 512, 1024, 2048, 4096, 8192} x H_KV in {1, 2, 4, 8, 32},",
         "H_Q = 8 * H_KV, D = 128, bf16, synthetic inputs. Each shape times the MI355X heuristic, num_splits = 1,",
-        "the paper's policy (policy PAPER) and fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8),",
+        "the paper's policy (policy PAPER), the evolved single-batch setting of its Fig. 1 (policy EVOLVED) and",
+        "fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8),",
         "as graph-replayed calls interleaved over rounds (median). Each distinct launch is timed once: a policy",
         "that picks a split of the sweep shares that split's timing.",
         "",
@@ -322,14 +326,17 @@ def regression_summary(path: str) -> None:
         f"mean {statistics.mean(r_best):.3f}x.",
         f"* Heuristic vs the paper's policy: mean {statistics.mean(r_paper):.3f}x its time, "
         f"best {min(r_paper):.3f}x, worst {max(r_paper):.3f}x.",
+        f"* Heuristic vs the evolved single-batch setting (Fig. 1; batch 1 only, {len(r_evo)} shapes): mean "
+        f"{statistics.mean(r_evo):.3f}x its time, best {min(r_evo):.3f}x, worst {max(r_evo):.3f}x.",
         "",
-        "| B | H_KV | L_K | heuristic s | us | s = 1 us | vs s = 1 | paper s | paper us | best s | best us | vs best |",
-        "|---|---|---|---|---|---|---|---|---|---|---|---|",
+        "| B | H_KV | L_K | heuristic s | us | s = 1 us | vs s = 1 | paper s | paper us | evolved s | evolved us "
+        "| best s | best us | vs best |",
+        "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
     ]
     for r, a, c in zip(rows, r_s1, r_best):
         lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_splits']} | {r['heuristic_us']} | "
-                     f"{r['s1_us']} | {1 / a:.2f}x | {r['paper_splits']} | {r['paper_us']} | {r['best_fixed']} | "
-                     f"{r['best_fixed_us']} | {c:.3f} |")
+                     f"{r['s1_us']} | {1 / a:.2f}x | {r['paper_splits']} | {r['paper_us']} | {r['evolved_splits']} | "
+                     f"{r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
     open(PROFILE_REGRESSION, "w").write("\n".join(lines) + "\n")
     print(f"wrote {PROFILE_REGRESSION}")
 
@@ -479,6 +486,11 @@ def main():
         "s1_us": round(s1, 3),
         "speedup_vs_s1": round(s1 / value, 3),
         "iqr_us": [round(q25, 3), round(q75, 3)],
+        "policies": {name: {"num_splits": s_pol, "us": sweep_us.get(s_pol)}
+                     for name, s_pol in (("paper", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
+                                                                       policy=da.POLICY_PAPER).num_splits),
+                                         ("evolved", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
+                                                                         policy=da.POLICY_EVOLVED).num_splits))},
         "best_fixed_splits": best_s,
         "vs_best_fixed": round(value / sweep_us[best_s], 3),
         "sweep_us": sweep_us,

@@ -54,9 +54,12 @@ typedef enum da_status {
 
 typedef enum da_policy {
   DA_POLICY_MI355X = 0, /* CU-aware cost model over num_splits in [1, 64] (default) */
-  DA_POLICY_PAPER = 1   /* the paper's rule (Section 4): 128-key blocks, Batch*H_KV tiles;
+  DA_POLICY_PAPER = 1,  /* the paper's rule (Section 4): 128-key blocks, Batch*H_KV tiles;
                            at most 3 blocks -> 1; 4 blocks -> 1 with >= 4 tiles, else 3;
                            longer contexts fall through to the MI355X cost model */
+  DA_POLICY_EVOLVED = 2 /* the evolved single-batch setting the paper's search found (Section 3,
+                           Fig. 1): batch 1 -> 12 splits, 16 below 256 keys, GQA packing on;
+                           larger batches use the MI355X cost model */
 } da_policy;
 
 /* A launch plan: the scheduler metadata decided on the host before launch

@@ -21,7 +21,7 @@ force, closed forms, invariants, library routines, the paper's table).
 
 from .attention import (bf16_bits_to_f64, combine_partials, decode_attention,
                         even_bounds, split_partials)
-from .policy import paper_split_policy
+from .policy import evolved_split_policy, paper_split_policy
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -30,4 +30,5 @@ __all__ = [
     "even_bounds",
     "split_partials",
     "paper_split_policy",
+    "evolved_split_policy",
 ]

@@ -1,6 +1,8 @@
-"""The paper's sequence-aware split rule, written from its prose (Section 4).
+"""The paper's sequence-aware split rule, written from its prose (Section 4),
+and the evolved single-batch setting its search found (Section 3, Fig. 1).
 
-TEST INFRASTRUCTURE ONLY.  It pins the planner's PAPER policy mode.
+TEST INFRASTRUCTURE ONLY.  It pins the planner's PAPER and EVOLVED policy
+modes.
 
 The rule works on two quantities: the number of key blocks of the sequence
 (blocks of 128 keys on the paper's stack, so L_K <= 384 is at most 3 blocks
@@ -32,3 +34,15 @@ def paper_split_policy(L_K: int, B: int, H_KV: int, block_keys: int = 128) -> Op
     if blocks == 4:
         return 1 if tiles >= 4 else 3
     return None
+
+
+def evolved_split_policy(L_K: int, B: int) -> Optional[int]:
+    """num_splits of the evolved heuristic fragment (Section 3, Fig. 1): for a
+    single sequence, twelve splits, or sixteen below 256 keys, with GQA
+    packing on and no reserved compute units.  The fragment covers batch 1
+    only; None for larger batches (the stack's own choice applies)."""
+    if L_K <= 0 or B <= 0:
+        raise ValueError("L_K and B must be positive")
+    if B != 1:
+        return None
+    return 16 if L_K < 256 else 12

@@ -4,13 +4,13 @@ The computation lives in the HIP library libdecode_attn.so (C-ABI declared
 in include/decode_attn.h); this package is its Python binding.
 """
 
-from ._binding import (DA_OK, EXPORTS, POLICY_MI355X, POLICY_PAPER, DaPlan, DecodeAttnError,
+from ._binding import (DA_OK, EXPORTS, POLICY_EVOLVED, POLICY_MI355X, POLICY_PAPER, DaPlan, DecodeAttnError,
                        da_choose_splits, da_combine_splits, da_decode_attn, da_device_info,
                        da_last_error, da_make_plan, da_split_bounds, da_split_partials,
                        da_strerror, da_workspace_bytes, load)
 
 __all__ = [
-    "DA_OK", "EXPORTS", "POLICY_MI355X", "POLICY_PAPER", "DaPlan", "DecodeAttnError",
+    "DA_OK", "EXPORTS", "POLICY_EVOLVED", "POLICY_MI355X", "POLICY_PAPER", "DaPlan", "DecodeAttnError",
     "da_choose_splits", "da_combine_splits", "da_decode_attn", "da_device_info", "da_last_error",
     "da_make_plan", "da_split_bounds", "da_split_partials", "da_strerror", "da_workspace_bytes", "load",
 ]

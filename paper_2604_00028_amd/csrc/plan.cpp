@@ -148,7 +148,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   if (rc) return rc;
   if (num_splits > kMaxSplits) return fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, kMaxSplits);
   if (pack_gqa < -1 || pack_gqa > 1) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
-  if (policy != DA_POLICY_MI355X && policy != DA_POLICY_PAPER)
+  if (policy != DA_POLICY_MI355X && policy != DA_POLICY_PAPER && policy != DA_POLICY_EVOLVED)
     return fail(DA_ERR_ARG, "unknown policy %d", policy);
   if (num_cus <= 0) return fail(DA_ERR_ARG, "num_cus=%d must be positive here", num_cus);
   if (cu_margin < 0 || cu_margin >= num_cus)
@@ -158,9 +158,14 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
   const int hpt = heads_per_tile(H_Q, H_KV, pack);
   int s = num_splits;
-  if (s <= 0)
-    s = policy == DA_POLICY_PAPER ? paper_splits(B, H_KV, L_K_max, H_Q, hpt, cus)
-                                  : mi355x_splits(B, H_Q, H_KV, L_K_max, hpt, cus);
+  if (s <= 0) {
+    if (policy == DA_POLICY_PAPER)
+      s = paper_splits(B, H_KV, L_K_max, H_Q, hpt, cus);
+    else if (policy == DA_POLICY_EVOLVED && B == 1)
+      s = L_K_max < 256 ? 16 : 12;  // Fig. 1: the evolved single-batch setting
+    else
+      s = mi355x_splits(B, H_Q, H_KV, L_K_max, hpt, cus);
+  }
   out->num_splits = s;
   out->pack_gqa = pack;
   out->heads_per_tile = hpt;

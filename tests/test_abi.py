@@ -12,7 +12,7 @@ import pytest
 
 import paper_2604_00028_amd as da
 from paper_2604_00028_amd import _binding as bnd
-from oracle import even_bounds, paper_split_policy
+from oracle import even_bounds, evolved_split_policy, paper_split_policy
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "decode_attn.h")
@@ -130,6 +130,23 @@ def test_paper_policy_reproduces_the_paper_table():
             assert plan.num_splits == mi.num_splits, c
 
 
+def test_evolved_policy_reproduces_the_paper_figure():
+    table = json.load(open(os.path.join(ROOT, "tests", "golden", "evolved_policy.json")))
+    for c in table["cases"]:
+        plan = da.da_choose_splits(c["B"], 64, 8, c["L_K"], num_cus=256, policy=da.POLICY_EVOLVED)
+        if c["s"] is not None:
+            assert plan.num_splits == c["s"] and plan.pack_gqa == 1, c
+        else:
+            mi = da.da_choose_splits(c["B"], 64, 8, c["L_K"], num_cus=256, policy=da.POLICY_MI355X)
+            assert plan.num_splits == mi.num_splits, c
+    for B in (1, 2, 4):
+        for L in (1, 100, 255, 256, 511, 4096):
+            want = evolved_split_policy(L, B)
+            plan = da.da_choose_splits(B, 8, 1, L, num_cus=256, policy=da.POLICY_EVOLVED)
+            if want is not None:
+                assert plan.num_splits == want, (B, L)
+
+
 def test_paper_policy_matches_the_oracle_rule_on_a_grid():
     for B in (1, 2, 4, 8):
         for H_KV in (1, 2, 4, 8, 32):
@@ -193,6 +210,8 @@ def test_cu_margin_and_plan_errors():
         da.da_choose_splits(1, 8, 1, 512, num_cus=256, cu_margin=256)
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=7)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=3)
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 3, 512, num_cus=256)
     with pytest.raises(da.DecodeAttnError):

@@ -13,7 +13,7 @@ import pytest
 import torch
 
 from oracle import (bf16_bits_to_f64, combine_partials, decode_attention, even_bounds,
-                    paper_split_policy, split_partials)
+                    evolved_split_policy, paper_split_policy, split_partials)
 from oracle.brute import brute_attention
 from workloads import config_shapes, custom_shape, f32_to_bf16_bits, make_inputs
 
@@ -300,6 +300,13 @@ def test_paper_policy_matches_table():
         table = json.load(f)
     for c in table["cases"]:
         assert paper_split_policy(c["L_K"], c["B"], c["H_KV"], table["block_keys"]) == c["s"], c
+
+
+def test_evolved_policy_matches_figure():
+    with open(os.path.join(GOLDEN, "evolved_policy.json")) as f:
+        table = json.load(f)
+    for c in table["cases"]:
+        assert evolved_split_policy(c["L_K"], c["B"]) == c["s"], c
 
 
 # ---------------------------------------------------------- input recipe
