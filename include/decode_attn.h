@@ -139,6 +139,30 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
                    float softmax_scale, int num_splits, int pack_gqa, void* workspace,
                    size_t workspace_bytes, void* stream);
 
+/* Decode attention over a paged KV cache: the same computation as
+ * da_decode_attn, with sequence b's keys held in fixed-size pages (the
+ * serving layout whose per-batch scheduling metadata the paper's
+ * deployment path precomputes, Section 5.1).
+ *   k_cache, v_cache bf16 [num_pages, page_size, H_KV, d]: page n holds
+ *                page_size consecutive keys of some sequence
+ *   block_table  device int32 [B, max_pages]: key j of sequence b lives in
+ *                page block_table[b*max_pages + j/page_size], row
+ *                j % page_size; entries past the sequence are not read; a
+ *                page id outside [0, num_pages) reads as zero keys/values
+ *   seq_lens     device int32 [B]: sequence lengths, each clamped to
+ *                [0, L_K_max]
+ *   page_size    multiple of 32 (one 32-key tile never spans two pages)
+ *   max_pages    columns of block_table; max_pages * page_size >= L_K_max
+ * Chunks (and each workgroup's wave ranges) are cut at 32-key boundaries,
+ * ceil(i * T / s) style over the T = ceil(L_b / 32) tiles, rather than at
+ * da_split_bounds; the result does not depend on the cut.  Other arguments,
+ * the workspace, error codes and launches are as for da_decode_attn. */
+int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache,
+                         const int32_t* block_table, const int32_t* seq_lens, void* out,
+                         float* lse_out, int B, int H_Q, int H_KV, int page_size, int max_pages,
+                         int num_pages, int L_K_max, int d, float softmax_scale, int num_splits,
+                         int pack_gqa, void* workspace, size_t workspace_bytes, void* stream);
+
 /* The split step alone: the partial softmax state of every chunk (the
  * per-chunk max, sum and unnormalised output the paper's final reduction
  * merges; Sections 3.1, 5.3).  Same inputs as da_decode_attn; num_splits

@@ -113,6 +113,9 @@ struct Params {
   float* o_part;        // [s, B, H_Q, D]          (kPartials)
   float* m_part;        // [s, B, H_Q]
   float* l_part;        // [s, B, H_Q]
+  const int32_t* block_table;  // paged layout: [B, max_pages] page ids
+  const int32_t* seq_lens;     // paged layout: [B] sequence lengths
+  int page_size, max_pages, num_pages;
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
   int xcd_group;        // 1: consecutive tiles share an XCD (packing off)
   float scale_log2;     // softmax scale * log2(e)
@@ -174,9 +177,11 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
 }
 
 // NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
-// 32).  W: waves per workgroup.
-// FETCH: a Fetch value.
-template <int NT, int W, int FETCH>
+// 32).  W: waves per workgroup.  FETCH: a Fetch value.  PG: paged K/V cache
+// (pages of page_size rows, page_size a multiple of 32; chunks and wave
+// ranges are then cut at 32-key tile boundaries, so every tile lies in one
+// page).
+template <int NT, int W, int FETCH, bool PG>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -196,31 +201,79 @@ split_partial_kernel(Params p) {
   const int head0 = (tile - b * p.tiles_per_seq) * p.hpt;
   const int kvh = head0 / p.g;
 
-  int64_t row0;
+  int64_t row0 = 0;
   int L;
-  if (p.cu) {
-    row0 = p.cu[b];
-    L = p.cu[b + 1] - p.cu[b];
+  int key_lo, key_hi;
+  if constexpr (PG) {
+    L = p.seq_lens[b];
     L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
+    // tiles of 32 keys cut into s chunks, each chunk's tiles into W ranges
+    const uint32_t T = (uint32_t)(L + kKeysPerTile - 1) / kKeysPerTile;
+    const uint32_t t0 = T * (uint32_t)split / (uint32_t)p.s;
+    const uint32_t nt = T * (uint32_t)(split + 1) / (uint32_t)p.s - t0;
+    key_lo = kKeysPerTile * (int)(t0 + nt * (uint32_t)wave / W);
+    key_hi = kKeysPerTile * (int)(t0 + nt * (uint32_t)(wave + 1) / W);
+    key_hi = key_hi < L ? key_hi : L;
+    key_lo = key_lo < key_hi ? key_lo : key_hi;
   } else {
-    row0 = (int64_t)b * p.L_K;
-    L = p.L_K;
+    if (p.cu) {
+      row0 = p.cu[b];
+      L = p.cu[b + 1] - p.cu[b];
+      L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
+    } else {
+      row0 = (int64_t)b * p.L_K;
+      L = p.L_K;
+    }
+    // L < 2^23 (one sequence's K spans < 2 GiB) and split < 64, so the
+    // products fit 32 bits and the divisions stay 32-bit
+    const int c0 = (int)(((uint32_t)L * (uint32_t)split) / (uint32_t)p.s);
+    const int c1 = (int)(((uint32_t)L * (uint32_t)(split + 1)) / (uint32_t)p.s);
+    const int n = c1 - c0;
+    key_lo = c0 + (int)(((uint32_t)n * (uint32_t)wave) / W);
+    key_hi = c0 + (int)(((uint32_t)n * (uint32_t)(wave + 1)) / W);
   }
-  // L < 2^23 (one sequence's K spans < 2 GiB) and split < 64, so the
-  // products fit 32 bits and the divisions stay 32-bit
-  const int c0 = (int)(((uint32_t)L * (uint32_t)split) / (uint32_t)p.s);
-  const int c1 = (int)(((uint32_t)L * (uint32_t)(split + 1)) / (uint32_t)p.s);
-  const int n = c1 - c0;
-  const int key_lo = c0 + (int)(((uint32_t)n * (uint32_t)wave) / W);
-  const int key_hi = c0 + (int)(((uint32_t)n * (uint32_t)(wave + 1)) / W);
 
-  // ---- buffer resources over this (sequence, KV head), rows of H_KV*256
-  //      bytes, ending at this wave's last key: any key >= key_hi is out of
-  //      range and reads as zeros without touching memory, so no load needs
-  //      a mask and ragged tails cost no traffic
+  // ---- K/V tile addressing.  Tile t holds keys [key_lo + 32t, +32) of this
+  //      (sequence, KV head); its buffer resource starts at that tile's first
+  //      row (rows of H_KV*256 bytes) and ends at this wave's last key: any
+  //      key >= key_hi is out of range and reads as zeros without touching
+  //      memory, so no load needs a mask and ragged tails cost no traffic.
+  //      Per-lane offsets below are relative to the tile's first row.
   const uint32_t rs = (uint32_t)p.H_KV * (D * 2);
   const int64_t base_elems = (row0 * p.H_KV + kvh) * D;
-  const uint32_t lim = (uint32_t)key_hi * rs;
+  // paged: this wave's page ids, 64 at a time, one per lane
+  int pg_first = 0, pg_last = -1, pg_win = 0, pg_ids = 0;
+  if constexpr (PG) {
+    if (key_hi > key_lo) {
+      pg_first = key_lo / p.page_size;
+      pg_last = (key_hi - 1) / p.page_size;
+    }
+    pg_win = pg_first;
+    const int j = pg_win + lane;
+    pg_ids = j <= pg_last ? p.block_table[(int64_t)b * p.max_pages + j] : 0;
+  }
+  // element offset of tile t's first row and its record count in bytes
+  auto tile_place = [&](int t, int64_t& elems, uint32_t& bytes) {
+    const int first = key_lo + t * kKeysPerTile;
+    const int rows = key_hi - first;
+    bytes = (uint32_t)__builtin_amdgcn_readfirstlane(rows > 0 ? (uint32_t)rows * rs : 0u);
+    if constexpr (PG) {
+      const int j = first / p.page_size;
+      if (j - pg_win >= 64 && rows > 0) {  // next window of page ids (wave-uniform)
+        pg_win = j;
+        const int jj = pg_win + lane;
+        pg_ids = jj <= pg_last ? p.block_table[(int64_t)b * p.max_pages + jj] : 0;
+      }
+      const int page = __builtin_amdgcn_readlane(pg_ids, (j - pg_win) & 63);
+      // a page id outside the cache reads as zero keys and values
+      if (page < 0 || page >= p.num_pages) bytes = 0u;
+      const int64_t prow = (page < 0 || page >= p.num_pages ? 0 : (int64_t)page) * p.page_size +
+                           first % p.page_size;
+      elems = (prow * p.H_KV + kvh) * D;
+    } else {
+      elems = base_elems + (int64_t)first * p.H_KV * D;
+    }
+  };
 
   // ---- Q^T as the MFMA B operand.  The reduction index of the product may
   //      map to head dims in any order as long as K and Q agree: k-step j,
@@ -263,19 +316,16 @@ split_partial_kernel(Params p) {
   // serves at about half the rate of row-contiguous lanes.  The per-lane
   // byte offsets are fixed; tile t moves the descriptor base by t*32 rows
   // and shrinks its record count to match (scalar work only).
-  const uint32_t tile_step = kKeysPerTile * rs;
-  const uint32_t koff[2] = {(uint32_t)(key_lo + col) * rs + 16u * quad,
-                            (uint32_t)(key_lo + 16 + col) * rs + 16u * quad};
+  const uint32_t koff[2] = {(uint32_t)col * rs + 16u * quad, (uint32_t)(16 + col) * rs + 16u * quad};
   uint32_t voff[8];
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj) voff[jj] = (uint32_t)(key_lo + 4 * jj + quad) * rs + 16u * col;
+  for (int jj = 0; jj < 8; ++jj) voff[jj] = (uint32_t)(4 * jj + quad) * rs + 16u * col;
   auto load_tile = [&](u32x4 (&kreg)[2][4], u32x4 (&vreg)[8], int t) {
-    // wave-uniform by construction; readfirstlane tells the compiler so the
-    // descriptor stays in scalar registers
-    const uint32_t adv = __builtin_amdgcn_readfirstlane((uint32_t)t * tile_step);
-    const uint32_t left = __builtin_amdgcn_readfirstlane(lim > adv ? lim - adv : 0u);
-    const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + base_elems + (int64_t)adv / 2, left);
-    const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + base_elems + (int64_t)adv / 2, left);
+    int64_t elems;
+    uint32_t left;
+    tile_place(t, elems, left);
+    const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + elems, left);
+    const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + elems, left);
     if constexpr (KS) {
       // kreg[mt][j]: rows 16mt + 4j + quad, bytes [16 col, +16)
 #pragma unroll
@@ -465,13 +515,14 @@ split_partial_kernel(Params p) {
     uint32_t dmaoff[8];
 #pragma unroll
     for (int blk = 0; blk < 8; ++blk)
-      dmaoff[blk] = (uint32_t)(key_lo + 4 * blk + rr) * rs + 16u * (uint32_t)((cp - 2 * rr) & 15);
+      dmaoff[blk] = (uint32_t)(4 * blk + rr) * rs + 16u * (uint32_t)((cp - 2 * rr) & 15);
     unsigned char* const sbase = smem + wave * stage_bytes(FETCH);
     auto dma_tile = [&](int stage, int t) {
-      const uint32_t adv = __builtin_amdgcn_readfirstlane((uint32_t)t * tile_step);
-      const uint32_t left = __builtin_amdgcn_readfirstlane(lim > adv ? lim - adv : 0u);
-      const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + base_elems + (int64_t)adv / 2, left);
-      const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + base_elems + (int64_t)adv / 2, left);
+      int64_t elems;
+      uint32_t left;
+      tile_place(t, elems, left);
+      const __amdgpu_buffer_rsrc_t kt = make_rsrc(p.k + elems, left);
+      const __amdgpu_buffer_rsrc_t vt = make_rsrc(p.v + elems, left);
       unsigned char* ks = sbase + stage * kLdsStageBytes;
       unsigned char* vs = ks + kLdsTileBytes;
 #pragma unroll
@@ -749,9 +800,22 @@ int ensure_gfx950(int* cus) {
   return DA_OK;
 }
 
-template <int NT, int W, int FETCH>
+template <int NT, int W, int FETCH, bool PG>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG>);
+}
+
+template <bool PG>
+const void* pick_kernel(int NT, int FETCH) {
+  switch (FETCH * 2 + NT - 1) {
+    case 0: return kernel_ptr<1, 4, kFetchDirect, PG>();
+    case 1: return kernel_ptr<2, 4, kFetchDirect, PG>();
+    case 2: return kernel_ptr<1, 4, kFetchStaged, PG>();
+    case 3: return kernel_ptr<2, 4, kFetchStaged, PG>();
+    case 4: return kernel_ptr<1, 4, kFetchLds, PG>();
+    case 5: return kernel_ptr<2, 4, kFetchLds, PG>();
+    default: return nullptr;
+  }
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
@@ -759,16 +823,8 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
   const int FETCH = pl.kv_fetch;
   if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
-  const void* fn = nullptr;
-  switch (FETCH * 2 + NT - 1) {
-    case 0: fn = kernel_ptr<1, 4, kFetchDirect>(); break;
-    case 1: fn = kernel_ptr<2, 4, kFetchDirect>(); break;
-    case 2: fn = kernel_ptr<1, 4, kFetchStaged>(); break;
-    case 3: fn = kernel_ptr<2, 4, kFetchStaged>(); break;
-    case 4: fn = kernel_ptr<1, 4, kFetchLds>(); break;
-    case 5: fn = kernel_ptr<2, 4, kFetchLds>(); break;
-    default: return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
-  }
+  const void* fn = prm.block_table ? pick_kernel<true>(NT, FETCH) : pick_kernel<false>(NT, FETCH);
+  if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
   if (rc) return rc;
@@ -790,13 +846,9 @@ int launch_combine(const float* o_part, const float* m_part, const float* l_part
   return DA_OK;
 }
 
-Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q, int H_KV,
-                   int L_K_max, float scale, const da_plan& pl) {
-  Params p{};
-  p.q = static_cast<const uint16_t*>(q);
-  p.k = static_cast<const uint16_t*>(k);
-  p.v = static_cast<const uint16_t*>(v);
-  p.cu = cu;
+// Shape and plan fields of the kernel arguments (the K/V layout fields are
+// set by the caller).
+void fill_params(Params& p, int B, int H_Q, int H_KV, int L_K_max, float scale, const da_plan& pl) {
   p.B = B;
   p.H_Q = H_Q;
   p.H_KV = H_KV;
@@ -809,24 +861,24 @@ Params make_params(const void* q, const void* k, const void* v, const int32_t* c
   p.xcd_group = pl.heads_per_tile < p.g ? 1 : 0;  // several workgroups read each KV head
   const float sigma = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
   p.scale_log2 = sigma * kLog2e;
+}
+
+Params make_params(const void* q, const void* k, const void* v, const int32_t* cu, int B, int H_Q, int H_KV,
+                   int L_K_max, float scale, const da_plan& pl) {
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.cu = cu;
+  fill_params(p, B, H_Q, H_KV, L_K_max, scale, pl);
   return p;
 }
 
-}  // namespace
-
-extern "C" {
-
-int da_device_info(int* num_cus, int* is_gfx950) {
-  if (!num_cus || !is_gfx950) return da::fail(DA_ERR_NULL, "output pointers must be non-NULL");
-  return query_device(num_cus, is_gfx950);
-}
-
-int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, void* out,
-                   float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
-                   int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
-  da::clear_error();
-  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
-  if (rc) return rc;
+// What the decode entry points share once their inputs are checked: the
+// plan, the workspace check, then one launch (s == 1) or the chunk states
+// followed by the log-sum-exp combine.  `p` carries the K/V layout.
+int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale, int num_splits,
+               int pack_gqa, void* out, float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
   if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
   if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
   if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
@@ -844,7 +896,7 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
                       workspace ? workspace_bytes : (size_t)0);
     return check_state_size(B, H_Q, s);
   };
-  rc = check_workspace(num_splits);
+  int rc = check_workspace(num_splits);
   if (rc) return rc;
   int cus = 0;
   rc = ensure_gfx950(&cus);
@@ -857,14 +909,13 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   if (rc) return rc;
   const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
 
-  Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
+  fill_params(p, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   if (s == 1) {
     p.mode = kDirect;
     p.out = static_cast<uint16_t*>(out);
     p.lse = lse_out;
     return launch_partial(p, pl, static_cast<hipStream_t>(stream));
   }
-  // s > 1: chunk states into the workspace, then the log-sum-exp combine.
   unsigned char* ws = static_cast<unsigned char*>(workspace);
   p.mode = kPartials;
   p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
@@ -874,6 +925,67 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   if (rc) return rc;
   return launch_combine(p.o_part, p.m_part, p.l_part, static_cast<uint16_t*>(out), lse_out, s, (int64_t)B * H_Q,
                         static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int da_device_info(int* num_cus, int* is_gfx950) {
+  if (!num_cus || !is_gfx950) return da::fail(DA_ERR_NULL, "output pointers must be non-NULL");
+  return query_device(num_cus, is_gfx950);
+}
+
+int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, void* out,
+                   float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
+                   int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.cu = cu_seqlens_k;
+  return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, num_splits, pack_gqa, out, lse_out, workspace,
+                    workspace_bytes, stream);
+}
+
+int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+                         const int32_t* seq_lens, void* out, float* lse_out, int B, int H_Q, int H_KV,
+                         int page_size, int max_pages, int num_pages, int L_K_max, int d, float softmax_scale,
+                         int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  int rc = da::check_shape(B, H_Q, H_KV, L_K_max, d);
+  if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
+  if (!block_table || !seq_lens) return da::fail(DA_ERR_NULL, "block_table and seq_lens must be non-NULL");
+  if ((!k_cache || !v_cache) && !(rc == DA_OK && L_K_max == 0))
+    return da::fail(DA_ERR_NULL, "k_cache and v_cache must be non-NULL");
+  if (rc) return rc;
+  if (page_size < kKeysPerTile || page_size % kKeysPerTile != 0 || page_size > (1 << 20))
+    return da::fail(DA_ERR_UNSUPPORTED, "page_size=%d must be a multiple of %d (at most 2^20)", page_size,
+                    kKeysPerTile);
+  if (max_pages < 1 || num_pages < 0 || (int64_t)max_pages * page_size < L_K_max)
+    return da::fail(DA_ERR_SHAPE, "max_pages=%d pages of %d keys cannot hold L_K_max=%d (num_pages=%d)",
+                    max_pages, page_size, L_K_max, num_pages);
+  if ((int64_t)B * max_pages >= ((int64_t)1 << 31))
+    return da::fail(DA_ERR_SHAPE, "block table of B*max_pages=%lld entries is too large",
+                    (long long)B * max_pages);
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+    return da::fail(DA_ERR_ALIGN, "q, k_cache and v_cache must be 16-byte aligned");
+  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
+    return da::fail(DA_ERR_ALIGN, "block_table and seq_lens must be 4-byte aligned");
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.page_size = page_size;
+  p.max_pages = max_pages;
+  p.num_pages = num_pages;
+  return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, num_splits, pack_gqa, out, lse_out, workspace,
+                    workspace_bytes, stream);
 }
 
 int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, float* o_part,

@@ -75,6 +75,37 @@ def test_decode_attn_argument_errors(lib, kw, code):
     assert da.da_last_error() != ""
 
 
+def call_paged(lib, q=FAKE, k=FAKE, v=FAKE, bt=FAKE, sl=FAKE, out=FAKE, B=1, H_Q=8, H_KV=1, page=64, max_pages=4,
+               num_pages=4, L=128, d=128, s=1, pack=1, ws=None, ws_bytes=0):
+    return lib.da_decode_attn_paged(q, k, v, bt, sl, out, None, B, H_Q, H_KV, page, max_pages, num_pages, L, d, 0.0,
+                                    s, pack, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), bnd.DA_ERR_NULL),
+    (dict(k=None), bnd.DA_ERR_NULL),
+    (dict(bt=None), bnd.DA_ERR_NULL),
+    (dict(sl=None), bnd.DA_ERR_NULL),
+    (dict(out=None), bnd.DA_ERR_NULL),
+    (dict(page=16), bnd.DA_ERR_UNSUPPORTED),
+    (dict(page=48), bnd.DA_ERR_UNSUPPORTED),
+    (dict(page=0), bnd.DA_ERR_UNSUPPORTED),
+    (dict(max_pages=1, L=128), bnd.DA_ERR_SHAPE),
+    (dict(max_pages=0), bnd.DA_ERR_SHAPE),
+    (dict(num_pages=-1), bnd.DA_ERR_SHAPE),
+    (dict(H_Q=8, H_KV=3), bnd.DA_ERR_SHAPE),
+    (dict(d=64), bnd.DA_ERR_UNSUPPORTED),
+    (dict(bt=FAKE + 2), bnd.DA_ERR_ALIGN),
+    (dict(sl=FAKE + 1), bnd.DA_ERR_ALIGN),
+    (dict(k=FAKE + 8), bnd.DA_ERR_ALIGN),
+    (dict(s=65), bnd.DA_ERR_SPLITS),
+    (dict(s=4), bnd.DA_ERR_WORKSPACE),
+])
+def test_paged_argument_errors(lib, kw, code):
+    assert call_paged(lib, **kw) == code
+    assert da.da_last_error() != ""
+
+
 def test_split_partials_and_combine_argument_errors(lib):
     sp = lib.da_split_partials
     ok = dict(q=FAKE, k=FAKE, v=FAKE)

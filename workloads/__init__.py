@@ -129,6 +129,71 @@ def make_inputs(shape: Shape, seed: Optional[int] = None,
     return Inputs(shape, q, k, v, lens, None)
 
 
+@dataclass
+class PagedInputs:
+    """The keys of an Inputs scattered into a pool of fixed-size pages.
+
+    k_cache, v_cache: uint16 bf16 bits [num_pages, page_size, H_KV, D]
+    block_table: int32 [B, max_pages]; key j of sequence b sits in page
+        block_table[b, j // page_size], row j % page_size
+    seq_lens: int32 [B]
+    Rows and pages that hold no key of any sequence, and table entries past a
+    sequence's last page, hold seeded noise (valid page ids of other
+    sequences' pages), so a kernel that reads them gives a wrong answer."""
+
+    k_cache: np.ndarray
+    v_cache: np.ndarray
+    block_table: np.ndarray
+    seq_lens: np.ndarray
+    page_size: int
+
+    @property
+    def num_pages(self) -> int:
+        return int(self.k_cache.shape[0])
+
+    @property
+    def max_pages(self) -> int:
+        return int(self.block_table.shape[1])
+
+
+def sequence_rows(inp: Inputs, b: int, which: str = "k") -> np.ndarray:
+    """Sequence b's key (or value) rows [L_b, H_KV, D] in either layout."""
+    x = inp.k if which == "k" else inp.v
+    if inp.cu_seqlens_k is None:
+        return x[b]
+    return x[int(inp.cu_seqlens_k[b]):int(inp.cu_seqlens_k[b + 1])]
+
+
+def paged_layout(inp: Inputs, page_size: int, seed: int, spare_pages: int = 3,
+                 max_pages: Optional[int] = None) -> PagedInputs:
+    """Scatter the keys and values of `inp` into pages in a seeded random order.
+
+    Draw order from PCG64(seed): K noise, V noise, page permutation, noise
+    table entries.  Pure data movement: no attention arithmetic."""
+    rng = np.random.default_rng(seed)
+    B, H_KV, D = inp.shape.B, inp.shape.H_KV, inp.shape.D
+    need = [-(-int(L) // page_size) for L in inp.lengths]
+    mp = max(max(need, default=0), 1) if max_pages is None else max_pages
+    assert mp >= max(need, default=0)
+    n_pages = sum(need) + spare_pages
+    k_cache = _normal_bf16(rng, (n_pages, page_size, H_KV, D))
+    v_cache = _normal_bf16(rng, (n_pages, page_size, H_KV, D))
+    order = rng.permutation(n_pages)
+    table = rng.integers(0, n_pages, size=(B, mp)).astype(np.int32)
+    pos = 0
+    for b in range(B):
+        kr, vr = sequence_rows(inp, b, "k"), sequence_rows(inp, b, "v")
+        for j in range(need[b]):
+            pid = int(order[pos])
+            pos += 1
+            table[b, j] = pid
+            rows = slice(j * page_size, min((j + 1) * page_size, kr.shape[0]))
+            n = rows.stop - rows.start
+            k_cache[pid, :n] = kr[rows]
+            v_cache[pid, :n] = vr[rows]
+    return PagedInputs(k_cache, v_cache, table, inp.lengths.astype(np.int32), page_size)
+
+
 def custom_shape(B: int, H_Q: int, H_KV: int, L_K: int, D: int = HEAD_DIM,
                  varlen: bool = False, name: str = "custom") -> Shape:
     """A shape outside the fixed workload set (edge cases, tests)."""
