@@ -163,6 +163,86 @@ int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache
                          int num_pages, int L_K_max, int d, float softmax_scale, int num_splits,
                          int pack_gqa, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Per-sequence scheduler metadata: the precomputed scheduling of Section 5.1
+ * carried down to one split count per sequence, so that in a batch of mixed
+ * lengths long sequences are cut into more chunks than short ones (the
+ * sequence-aware rule of Section 4 applied to each sequence's own length).
+ * Built on the host from host-known lengths; the caller copies the metadata
+ * bytes to device memory and passes both to da_decode_attn_scheduled. */
+typedef struct da_schedule {
+  int32_t B, H_Q, H_KV, L_K_max; /* the shape it was made for */
+  int32_t pack_gqa;              /* as in da_plan */
+  int32_t heads_per_tile;        /* as in da_plan */
+  int32_t tiles;                 /* head tiles = B * H_Q / heads_per_tile */
+  int32_t num_items;             /* workgroups launched */
+  int32_t chunk_tiles;           /* target chunk length in 32-key tiles */
+  int32_t max_splits;            /* largest per-sequence split count (1..64) */
+  int32_t state_rows;            /* chunk-state rows: sum of s_b over sequences with s_b > 1 */
+  int32_t num_cus;               /* compute units planned for (after cu_margin) */
+  int32_t kv_fetch;              /* as in da_plan */
+  int32_t seq_offset;            /* byte offset of the per-sequence table in the metadata */
+  int32_t meta_bytes;            /* metadata bytes written */
+  int32_t reserved;
+} da_schedule;
+
+/* Upper bound on the metadata bytes da_make_schedule writes for this shape
+ * (every sequence at 64 chunks). */
+size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa);
+
+/* Build the per-sequence schedule.
+ *   seq_lens   host int32 [B]: key counts, each in [0, L_K_max]
+ *   pack_gqa   -1 (chosen as by the policy) or 0/1
+ *   num_cus    0 = query the current device, > 0 = no device access
+ *   cu_margin  compute units to leave to concurrent work (Section 3.1's
+ *              sm_margin): the schedule is sized for num_cus - cu_margin
+ *   chunk_tiles <= 0: chosen by the MI355X cost model; > 0: every sequence
+ *              is cut into ceil(T_b / chunk_tiles) chunks (at most 64), T_b
+ *              = ceil(L_b / 32)
+ *   meta       host buffer of meta_bytes >= the bytes needed (at most
+ *              da_schedule_max_bytes); receives, 16-byte aligned:
+ *                items int32x4 [num_items]: {head tile, first tile, end
+ *                  tile, state row (-1: the chunk is the whole sequence and
+ *                  writes the output directly)}, with the 32-key tile range
+ *                  [first, end) of that workgroup's chunk
+ *                sequences int32x2 [B] at seq_offset: {first state row or
+ *                  -1, split count s_b}
+ *   out        filled on success
+ * Host-only; deterministic for equal arguments.  Errors: DA_ERR_NULL,
+ * DA_ERR_SHAPE (a length outside [0, L_K_max]), DA_ERR_ARG (cu_margin,
+ * pack_gqa), DA_ERR_WORKSPACE (meta_bytes too small; out->meta_bytes then
+ * holds the size needed). */
+int da_make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d,
+                     int pack_gqa, int num_cus, int cu_margin, int chunk_tiles, void* meta,
+                     size_t meta_bytes, da_schedule* out);
+
+/* Workspace bytes da_decode_attn_scheduled needs for `sched`: 0 when no
+ * sequence is split.  Layout (256-byte aligned regions): Otilde fp32
+ * [state_rows, H_Q, D] | m fp32 [state_rows, H_Q] | l fp32 [state_rows, H_Q]. */
+size_t da_schedule_workspace_bytes(const da_schedule* sched);
+
+/* Decode attention driven by a per-sequence schedule: the same result as
+ * da_decode_attn (or da_decode_attn_paged) up to rounding order.
+ *   K/V layout: block_table == NULL -> contiguous (k, v, cu_seqlens_k as for
+ *     da_decode_attn; page_size, max_pages, num_pages, seq_lens ignored);
+ *     block_table != NULL -> paged (k, v are the page pools, with
+ *     block_table, seq_lens, page_size, max_pages, num_pages as for
+ *     da_decode_attn_paged; cu_seqlens_k ignored)
+ *   sched      host struct from da_make_schedule for this B, H_Q, H_KV,
+ *              L_K_max
+ *   meta_dev   device copy of the metadata bytes (16-byte aligned); the
+ *              kernel reads the lengths on the device, so a length that
+ *              differs from the one scheduled changes only the balance
+ *   workspace  >= da_schedule_workspace_bytes(sched)
+ * At most two launches (the combine only when some sequence is split), no
+ * allocation, graph-capturable; results bit-identical across runs for a
+ * fixed schedule. */
+int da_decode_attn_scheduled(const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens_k, const int32_t* block_table,
+                             const int32_t* seq_lens, int page_size, int max_pages, int num_pages,
+                             void* out, float* lse_out, int d, float softmax_scale,
+                             const da_schedule* sched, const void* meta_dev, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
 /* The split step alone: the partial softmax state of every chunk (the
  * per-chunk max, sum and unnormalised output the paper's final reduction
  * merges; Sections 3.1, 5.3).  Same inputs as da_decode_attn; num_splits

@@ -37,7 +37,9 @@ POLICY_EVOLVED = 2
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (
     "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
-    "da_decode_attn_paged", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror", "da_last_error",
+    "da_decode_attn_paged", "da_schedule_max_bytes", "da_make_schedule", "da_schedule_workspace_bytes",
+    "da_decode_attn_scheduled", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror",
+    "da_last_error",
 )
 
 
@@ -52,6 +54,15 @@ class DaPlan(ctypes.Structure):
         ("group_waves", ctypes.c_int32),
         ("kv_fetch", ctypes.c_int32),
     ]
+
+    def as_dict(self) -> dict:
+        return {name: int(getattr(self, name)) for name, _ in self._fields_}
+
+
+class DaSchedule(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "B", "H_Q", "H_KV", "L_K_max", "pack_gqa", "heads_per_tile", "tiles", "num_items", "chunk_tiles",
+        "max_splits", "state_rows", "num_cus", "kv_fetch", "seq_offset", "meta_bytes", "reserved")]
 
     def as_dict(self) -> dict:
         return {name: int(getattr(self, name)) for name, _ in self._fields_}
@@ -108,6 +119,15 @@ def load() -> ctypes.CDLL:
     lib.da_decode_attn_paged.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
                                          _P, _Z, _P]
     lib.da_decode_attn_paged.restype = _I
+    lib.da_schedule_max_bytes.argtypes = [_I, _I, _I, _I]
+    lib.da_schedule_max_bytes.restype = _Z
+    lib.da_make_schedule.argtypes = [_P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _Z, ctypes.POINTER(DaSchedule)]
+    lib.da_make_schedule.restype = _I
+    lib.da_schedule_workspace_bytes.argtypes = [ctypes.POINTER(DaSchedule)]
+    lib.da_schedule_workspace_bytes.restype = _Z
+    lib.da_decode_attn_scheduled.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _P, _P, _I, _F,
+                                             ctypes.POINTER(DaSchedule), _P, _P, _Z, _P]
+    lib.da_decode_attn_scheduled.restype = _I
     lib.da_split_partials.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _I, _P]
     lib.da_split_partials.restype = _I
     lib.da_combine_splits.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _P]
@@ -278,6 +298,74 @@ def da_decode_attn_paged(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
                                        _ptr(out), _ptr(lse_out), B, H_Q, H_KV, page_size, max_pages, num_pages,
                                        int(L_K_max), d, float(softmax_scale), int(num_splits), int(pack_gqa),
                                        _ptr(workspace), ws_bytes, s_handle))
+    return out
+
+
+def da_schedule_max_bytes(B: int, H_Q: int, H_KV: int, pack_gqa: int = -1) -> int:
+    return int(load().da_schedule_max_bytes(B, H_Q, H_KV, pack_gqa))
+
+
+def da_make_schedule(seq_lens: Sequence[int], H_Q: int, H_KV: int, L_K_max: Optional[int] = None,
+                     d: int = HEAD_DIM, pack_gqa: int = -1, num_cus: int = 0, cu_margin: int = 0,
+                     chunk_tiles: int = 0) -> Tuple[DaSchedule, torch.Tensor]:
+    """Per-sequence schedule from host-known lengths: (DaSchedule, metadata
+    bytes as a CPU uint8 tensor to copy to the device)."""
+    lens = torch.as_tensor(list(seq_lens) if not isinstance(seq_lens, torch.Tensor) else seq_lens.cpu(),
+                           dtype=torch.int32).contiguous()
+    B = lens.numel()
+    if L_K_max is None:
+        L_K_max = int(lens.max()) if B else 0
+    cap = da_schedule_max_bytes(B, H_Q, H_KV, pack_gqa)
+    meta = torch.zeros(max(cap, 16), dtype=torch.uint8)
+    sched = DaSchedule()
+    _check(load().da_make_schedule(lens.data_ptr() if B else None, B, H_Q, H_KV, int(L_K_max), d, pack_gqa,
+                                   num_cus, cu_margin, chunk_tiles, meta.data_ptr(), meta.numel(),
+                                   ctypes.byref(sched)))
+    return sched, meta[: sched.meta_bytes].clone()
+
+
+def da_schedule_workspace_bytes(sched: DaSchedule) -> int:
+    return int(load().da_schedule_workspace_bytes(ctypes.byref(sched)))
+
+
+def da_decode_attn_scheduled(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, sched: DaSchedule,
+                             meta_dev: torch.Tensor, cu_seqlens_k: Optional[torch.Tensor] = None,
+                             block_table: Optional[torch.Tensor] = None, seq_lens: Optional[torch.Tensor] = None,
+                             out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None, *,
+                             softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None,
+                             stream=None) -> torch.Tensor:
+    """Decode attention driven by a per-sequence schedule; returns `out`.
+    Contiguous K/V (fixed, or varlen with cu_seqlens_k) when block_table is
+    None, else paged: k, v [num_pages, page_size, H_KV, d] with block_table
+    [B, max_pages] and seq_lens [B]."""
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"{name} must be a contiguous bfloat16 CUDA tensor")
+    if meta_dev.dtype != torch.uint8 or not meta_dev.is_cuda or meta_dev.numel() < sched.meta_bytes:
+        raise ValueError("meta_dev must be a CUDA uint8 tensor holding the schedule's metadata")
+    B, H_Q, d = q.shape
+    if B != sched.B or H_Q != sched.H_Q:
+        raise ValueError("q does not match the schedule")
+    page_size = max_pages = num_pages = 0
+    if block_table is not None:
+        for name, t in (("block_table", block_table), ("seq_lens", seq_lens)):
+            if t is None or t.dtype != torch.int32 or not t.is_contiguous() or not t.is_cuda:
+                raise ValueError(f"{name} must be a contiguous int32 CUDA tensor")
+        num_pages, page_size = k.shape[0], k.shape[1]
+        max_pages = block_table.shape[1]
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
+    s_handle = _stream(dev, stream)
+    if workspace is None:
+        nbytes = da_schedule_workspace_bytes(sched)
+        if nbytes:
+            workspace = workspace_for(dev, s_handle, nbytes)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().da_decode_attn_scheduled(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(block_table),
+                                           _ptr(seq_lens), page_size, max_pages, num_pages, _ptr(out),
+                                           _ptr(lse_out), d, float(softmax_scale), ctypes.byref(sched),
+                                           _ptr(meta_dev), _ptr(workspace), ws_bytes, s_handle))
     return out
 
 

@@ -116,6 +116,8 @@ struct Params {
   const int32_t* block_table;  // paged layout: [B, max_pages] page ids
   const int32_t* seq_lens;     // paged layout: [B] sequence lengths
   int page_size, max_pages, num_pages;
+  const int32_t* work;  // nullable: per-sequence schedule, int32x4 {tile, first, end, state row} per workgroup
+  int state_rows;       // chunk-state rows of the schedule
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
   int xcd_group;        // 1: consecutive tiles share an XCD (packing off)
   float scale_log2;     // softmax scale * log2(e)
@@ -192,38 +194,58 @@ split_partial_kernel(Params p) {
   const int quad = lane >> 4;  // MFMA row group
 
   // ---- which tile and chunk this workgroup owns
-  const int nwg = p.tiles * p.s;
   const int bid = blockIdx.x;
-  const int logical = (p.xcd_group && nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
-  const int tile = logical / p.s;
-  const int split = logical - tile * p.s;
+  int tile, split = 0, prow = -1, w_first = 0, w_end = 0;
+  if (p.work) {
+    // scheduled: this workgroup's head tile, 32-key tile range and state row
+    tile = p.work[4 * bid];
+    w_first = p.work[4 * bid + 1];
+    w_end = p.work[4 * bid + 2];
+    prow = p.work[4 * bid + 3];
+    if (tile < 0 || tile >= p.tiles || prow >= p.state_rows) return;  // not a schedule of this shape
+  } else {
+    const int nwg = p.tiles * p.s;
+    const int logical = (p.xcd_group && nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
+    tile = logical / p.s;
+    split = logical - tile * p.s;
+  }
   const int b = tile / p.tiles_per_seq;
   const int head0 = (tile - b * p.tiles_per_seq) * p.hpt;
   const int kvh = head0 / p.g;
 
   int64_t row0 = 0;
   int L;
-  int key_lo, key_hi;
   if constexpr (PG) {
     L = p.seq_lens[b];
     L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
-    // tiles of 32 keys cut into s chunks, each chunk's tiles into W ranges
+  } else if (p.cu) {
+    row0 = p.cu[b];
+    L = p.cu[b + 1] - p.cu[b];
+    L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
+  } else {
+    row0 = (int64_t)b * p.L_K;
+    L = p.L_K;
+  }
+  int key_lo, key_hi;
+  if (PG || p.work) {
+    // tiles of 32 keys cut into s chunks (or the scheduled range), each
+    // chunk's tiles into W ranges
     const uint32_t T = (uint32_t)(L + kKeysPerTile - 1) / kKeysPerTile;
-    const uint32_t t0 = T * (uint32_t)split / (uint32_t)p.s;
-    const uint32_t nt = T * (uint32_t)(split + 1) / (uint32_t)p.s - t0;
+    uint32_t t0, nt;
+    if (p.work) {
+      const uint32_t f = (uint32_t)(w_first < 0 ? 0 : w_first);
+      const uint32_t e = (uint32_t)(w_end < 0 ? 0 : w_end);
+      t0 = f < T ? f : T;
+      nt = (e < T ? e : T) > t0 ? (e < T ? e : T) - t0 : 0u;
+    } else {
+      t0 = T * (uint32_t)split / (uint32_t)p.s;
+      nt = T * (uint32_t)(split + 1) / (uint32_t)p.s - t0;
+    }
     key_lo = kKeysPerTile * (int)(t0 + nt * (uint32_t)wave / W);
     key_hi = kKeysPerTile * (int)(t0 + nt * (uint32_t)(wave + 1) / W);
     key_hi = key_hi < L ? key_hi : L;
     key_lo = key_lo < key_hi ? key_lo : key_hi;
   } else {
-    if (p.cu) {
-      row0 = p.cu[b];
-      L = p.cu[b + 1] - p.cu[b];
-      L = L < 0 ? 0 : (L > p.L_K ? p.L_K : L);
-    } else {
-      row0 = (int64_t)b * p.L_K;
-      L = p.L_K;
-    }
     // L < 2^23 (one sequence's K spans < 2 GiB) and split < 64, so the
     // products fit 32 bits and the divisions stay 32-bit
     const int c0 = (int)(((uint32_t)L * (uint32_t)split) / (uint32_t)p.s);
@@ -633,8 +655,10 @@ split_partial_kernel(Params p) {
 
   const int64_t rows = (int64_t)p.B * p.H_Q;
   const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
-  const __amdgpu_buffer_rsrc_t ors =
-      make_rsrc(p.o_part + ((int64_t)split * rows + row0_tile) * D, (uint32_t)p.hpt * D * 4);
+  const bool direct = p.work ? prow < 0 : p.mode == kDirect;
+  // first chunk-state row of this workgroup's heads
+  const int64_t srow0 = direct ? 0 : (p.work ? (int64_t)prow * p.H_Q + head0 : (int64_t)split * rows + row0_tile);
+  const __amdgpu_buffer_rsrc_t ors = make_rsrc(p.o_part + srow0 * D, (uint32_t)p.hpt * D * 4);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float mk[W], wk[W];
@@ -666,7 +690,7 @@ split_partial_kernel(Params p) {
     if (h >= p.hpt) continue;
     const int64_t row = row0_tile + h;
     const float mval = Lw > 0.f ? M * kLn2 : -INFINITY;
-    if (p.mode == kDirect) {
+    if (direct) {
       const float inv = Lw > 0.f ? 1.0f / Lw : 0.f;
 #pragma unroll
       for (int bb = 0; bb < NBW; ++bb) {
@@ -684,8 +708,8 @@ split_partial_kernel(Params p) {
         __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0, 0);
       }
       if (wave == 0 && quad == 0) {
-        p.m_part[split * rows + row] = mval;
-        p.l_part[split * rows + row] = Lw;
+        p.m_part[srow0 + h] = mval;
+        p.l_part[srow0 + h] = Lw;
       }
     }
   }
@@ -699,7 +723,8 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
                                                             const float* __restrict__ m_part,
                                                             const float* __restrict__ l_part,
                                                             uint16_t* __restrict__ out, float* __restrict__ lse,
-                                                            int s, int64_t rows) {
+                                                            int s, int64_t rows,
+                                                            const int32_t* __restrict__ seqs, int H_Q) {
   __shared__ float sw[4][DA_MAX_SPLITS];
   __shared__ float sl[4][DA_MAX_SPLITS];
   __shared__ float sML[4][2];
@@ -707,15 +732,29 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
   const int w = threadIdx.x >> 6;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;  // waves are independent: no workgroup barrier below
-  const float* src = o_part + row * D + 2 * lane;
-  const int64_t stride = rows * D;
+  // Chunk i of this row sits at state row base + i * srow: uniform split
+  // counts interleave the rows; a per-sequence schedule stores sequence b's
+  // chunks from its first state row on (unsplit sequences are already done).
+  int64_t base = row, srow = rows;
+  if (seqs) {
+    const int b = (int)(row / H_Q);
+    const int h = (int)(row - (int64_t)b * H_Q);
+    const int r0 = seqs[2 * b];
+    s = seqs[2 * b + 1];
+    if (r0 < 0 || s <= 1) return;
+    s = s < DA_MAX_SPLITS ? s : DA_MAX_SPLITS;
+    base = (int64_t)r0 * H_Q + h;
+    srow = H_Q;
+  }
+  const float* src = o_part + base * D + 2 * lane;
+  const int64_t stride = srow * D;
   float2 a[kMergeBatch];
 #pragma unroll
   for (int u = 0; u < kMergeBatch; ++u)
     if (u < s) a[u] = *reinterpret_cast<const float2*>(src + u * stride);
   for (int i = lane; i < s; i += 64) {
-    sw[w][i] = m_part[i * rows + row];
-    sl[w][i] = l_part[i * rows + row];
+    sw[w][i] = m_part[base + i * srow];
+    sl[w][i] = l_part[base + i * srow];
   }
   __builtin_amdgcn_wave_barrier();
   if (lane == 0) merge_weights(sw[w], sl[w], s, sML[w]);
@@ -837,9 +876,9 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
 }
 
 int launch_combine(const float* o_part, const float* m_part, const float* l_part, uint16_t* out, float* lse,
-                   int s, int64_t rows, hipStream_t stream) {
+                   int s, int64_t rows, hipStream_t stream, const int32_t* seqs = nullptr, int H_Q = 1) {
   const int grid = (int)((rows + 3) / 4);
-  void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows};
+  void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows, &seqs, &H_Q};
   hipError_t e =
       hipLaunchKernel(reinterpret_cast<const void*>(&split_combine_kernel), dim3(grid), dim3(256), args, 0, stream);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
@@ -927,6 +966,37 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
                         static_cast<hipStream_t>(stream));
 }
 
+// Checks of the paged layout arguments (shape already checked).
+int check_paged(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+                const int32_t* seq_lens, int B, int page_size, int max_pages, int num_pages, int L_K_max) {
+  if (page_size < kKeysPerTile || page_size % kKeysPerTile != 0 || page_size > (1 << 20))
+    return da::fail(DA_ERR_UNSUPPORTED, "page_size=%d must be a multiple of %d (at most 2^20)", page_size,
+                    kKeysPerTile);
+  if (max_pages < 1 || num_pages < 0 || (int64_t)max_pages * page_size < L_K_max)
+    return da::fail(DA_ERR_SHAPE, "max_pages=%d pages of %d keys cannot hold L_K_max=%d (num_pages=%d)",
+                    max_pages, page_size, L_K_max, num_pages);
+  if ((int64_t)B * max_pages >= ((int64_t)1 << 31))
+    return da::fail(DA_ERR_SHAPE, "block table of B*max_pages=%lld entries is too large",
+                    (long long)B * max_pages);
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+    return da::fail(DA_ERR_ALIGN, "q, k_cache and v_cache must be 16-byte aligned");
+  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
+    return da::fail(DA_ERR_ALIGN, "block_table and seq_lens must be 4-byte aligned");
+  return DA_OK;
+}
+
+void set_paged(Params& p, const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+               const int32_t* seq_lens, int page_size, int max_pages, int num_pages) {
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_cache);
+  p.v = static_cast<const uint16_t*>(v_cache);
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.page_size = page_size;
+  p.max_pages = max_pages;
+  p.num_pages = num_pages;
+}
+
 }  // namespace
 
 extern "C" {
@@ -962,30 +1032,96 @@ int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache
   if ((!k_cache || !v_cache) && !(rc == DA_OK && L_K_max == 0))
     return da::fail(DA_ERR_NULL, "k_cache and v_cache must be non-NULL");
   if (rc) return rc;
-  if (page_size < kKeysPerTile || page_size % kKeysPerTile != 0 || page_size > (1 << 20))
-    return da::fail(DA_ERR_UNSUPPORTED, "page_size=%d must be a multiple of %d (at most 2^20)", page_size,
-                    kKeysPerTile);
-  if (max_pages < 1 || num_pages < 0 || (int64_t)max_pages * page_size < L_K_max)
-    return da::fail(DA_ERR_SHAPE, "max_pages=%d pages of %d keys cannot hold L_K_max=%d (num_pages=%d)",
-                    max_pages, page_size, L_K_max, num_pages);
-  if ((int64_t)B * max_pages >= ((int64_t)1 << 31))
-    return da::fail(DA_ERR_SHAPE, "block table of B*max_pages=%lld entries is too large",
-                    (long long)B * max_pages);
-  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
-    return da::fail(DA_ERR_ALIGN, "q, k_cache and v_cache must be 16-byte aligned");
-  if (!aligned(block_table, 4) || !aligned(seq_lens, 4))
-    return da::fail(DA_ERR_ALIGN, "block_table and seq_lens must be 4-byte aligned");
+  rc = check_paged(q, k_cache, v_cache, block_table, seq_lens, B, page_size, max_pages, num_pages, L_K_max);
+  if (rc) return rc;
   Params p{};
-  p.q = static_cast<const uint16_t*>(q);
-  p.k = static_cast<const uint16_t*>(k_cache);
-  p.v = static_cast<const uint16_t*>(v_cache);
-  p.block_table = block_table;
-  p.seq_lens = seq_lens;
-  p.page_size = page_size;
-  p.max_pages = max_pages;
-  p.num_pages = num_pages;
+  set_paged(p, q, k_cache, v_cache, block_table, seq_lens, page_size, max_pages, num_pages);
   return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, num_splits, pack_gqa, out, lse_out, workspace,
                     workspace_bytes, stream);
+}
+
+int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
+                             const int32_t* block_table, const int32_t* seq_lens, int page_size, int max_pages,
+                             int num_pages, void* out, float* lse_out, int d, float softmax_scale,
+                             const da_schedule* sched, const void* meta_dev, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  if (!sched) return da::fail(DA_ERR_NULL, "sched must be non-NULL");
+  const int B = sched->B, H_Q = sched->H_Q, H_KV = sched->H_KV, L_K_max = sched->L_K_max;
+  int rc = block_table ? da::check_shape(B, H_Q, H_KV, L_K_max, d)
+                       : check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  if (block_table) {
+    if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
+    if (!seq_lens) return da::fail(DA_ERR_NULL, "seq_lens must be non-NULL with a block table");
+    if ((!k || !v) && L_K_max != 0) return da::fail(DA_ERR_NULL, "k_cache and v_cache must be non-NULL");
+    rc = check_paged(q, k, v, block_table, seq_lens, B, page_size, max_pages, num_pages, L_K_max);
+    if (rc) return rc;
+  }
+  // the schedule must describe a launch of this shape
+  const int g = H_Q / H_KV;
+  const int hpt = sched->heads_per_tile;
+  if ((sched->pack_gqa != 0 && sched->pack_gqa != 1) || hpt != da::heads_per_tile(H_Q, H_KV, sched->pack_gqa) ||
+      sched->tiles != B * (H_Q / hpt) || sched->num_items < sched->tiles ||
+      (int64_t)sched->num_items > (int64_t)sched->tiles * DA_MAX_SPLITS || sched->max_splits < 1 ||
+      sched->max_splits > DA_MAX_SPLITS || sched->state_rows < 0 || sched->kv_fetch < 0 || sched->kv_fetch > 2 ||
+      (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 || (sched->max_splits > 1) != (sched->state_rows > 0))
+    return da::fail(DA_ERR_ARG, "schedule does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
+  (void)g;
+  if (!meta_dev) return da::fail(DA_ERR_NULL, "meta_dev must be non-NULL");
+  if (!aligned(meta_dev, 16)) return da::fail(DA_ERR_ALIGN, "meta_dev must be 16-byte aligned");
+  if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
+  if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
+  if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
+  const size_t need = da_schedule_workspace_bytes(sched);
+  if (need) {
+    if (!workspace || workspace_bytes < need)
+      return da::fail(DA_ERR_WORKSPACE, "schedule needs %zu workspace bytes, got %zu", need,
+                      workspace ? workspace_bytes : (size_t)0);
+    if (!aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
+  }
+  int cus = 0;
+  rc = ensure_gfx950(&cus);
+  if (rc) return rc;
+
+  Params p{};
+  if (block_table) {
+    set_paged(p, q, k, v, block_table, seq_lens, page_size, max_pages, num_pages);
+  } else {
+    p.q = static_cast<const uint16_t*>(q);
+    p.k = static_cast<const uint16_t*>(k);
+    p.v = static_cast<const uint16_t*>(v);
+    p.cu = cu_seqlens_k;
+  }
+  da_plan pl{};
+  pl.num_splits = 1;
+  pl.pack_gqa = sched->pack_gqa;
+  pl.heads_per_tile = hpt;
+  pl.tiles = sched->tiles;
+  pl.grid = sched->num_items;
+  pl.num_cus = sched->num_cus;
+  pl.group_waves = 4;
+  pl.kv_fetch = sched->kv_fetch;
+  fill_params(p, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
+  p.xcd_group = 0;  // the schedule orders its workgroups itself
+  p.work = static_cast<const int32_t*>(meta_dev);
+  p.state_rows = sched->state_rows;
+  p.mode = kPartials;
+  p.out = static_cast<uint16_t*>(out);
+  p.lse = lse_out;
+  if (need) {
+    const da::WorkspaceLayout wl = da::workspace_layout(sched->state_rows, H_Q, D, 1);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
+    p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
+    p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
+  }
+  rc = launch_partial(p, pl, static_cast<hipStream_t>(stream));
+  if (rc || !need) return rc;
+  const int32_t* seqs =
+      reinterpret_cast<const int32_t*>(static_cast<const unsigned char*>(meta_dev) + sched->seq_offset);
+  return launch_combine(p.o_part, p.m_part, p.l_part, static_cast<uint16_t*>(out), lse_out, sched->max_splits,
+                        (int64_t)B * H_Q, static_cast<hipStream_t>(stream), seqs, H_Q);
 }
 
 int da_split_partials(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, float* o_part,

@@ -6,6 +6,9 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
+#include <vector>
+
 namespace da {
 
 namespace {
@@ -179,6 +182,182 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// The uniform model with per-sequence chunking: every sequence b is cut into
+// s_b = ceil(T_b / c) chunks of at most ceil(T_b / s_b) tiles, each walked by
+// four waves.  Workgroups are issued longest first, so the compute part takes
+// rounds of the longest workgroup (the uniform model's ceil(wgs / CUs) when
+// every sequence has the same length); the streaming part counts the K/V of
+// every sequence once plus the chunk states of the split ones; the combine is
+// paid once if any sequence is split, for the largest split count.
+double schedule_time(const CostModel& m, const int64_t* tiles_of, const int32_t* lens, int B, int H_Q,
+                     int H_KV, int hpt, int64_t c, int cus) {
+  const int wide = hpt > 16 ? 1 : 0;
+  const int64_t tps = H_Q / hpt;
+  int64_t items = 0, wave_tiles = 0, max_wt = 0, keys = 0, state_rows = 0;
+  int max_s = 1;
+  for (int b = 0; b < B; ++b) {
+    const int64_t T = tiles_of[b];
+    const int s = seq_splits(T, c);
+    const int64_t wt = ((T + s - 1) / s + 3) / 4;
+    items += s;
+    wave_tiles += s * wt;
+    if (wt > max_wt) max_wt = wt;
+    keys += lens[b];
+    if (s > 1) {
+      state_rows += s;
+      if (s > max_s) max_s = s;
+    }
+  }
+  items *= tps;
+  wave_tiles *= tps;
+  const int64_t per = (int64_t)cus * max_wt;
+  const int64_t rounds = per > 0 ? (wave_tiles + per - 1) / per : 0;
+  const double tt = kv_fetch(items, cus) ? m.t_tile_staged[wide] : m.t_tile[wide];
+  const double compute = m.base[wide] + (double)rounds * (double)max_wt * tt;
+  double bytes = (double)keys * H_KV * 2.0 * kHeadDim * 2.0;
+  bytes += 2.0 * (double)state_rows * H_Q * (kHeadDim + 2) * 4.0;
+  const double stream = m.hbm0 + bytes / m.hbm_rate;
+  double t = pow(pow(compute, m.pnorm) + pow(stream, m.pnorm), 1.0 / m.pnorm);
+  if (state_rows > 0) t += m.merge0 + m.merge1[wide] * max_s;
+  return t;
+}
+
+namespace {
+struct Item {
+  int32_t tile, t0, t1, row;
+};
+}  // namespace
+
+int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
+                  int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes, da_schedule* out) {
+  if (!out) return fail(DA_ERR_NULL, "schedule output is NULL");
+  if (!seq_lens) return fail(DA_ERR_NULL, "seq_lens is NULL");
+  int rc = check_shape(B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  if (pack_gqa < -1 || pack_gqa > 1) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (num_cus <= 0) return fail(DA_ERR_ARG, "num_cus=%d must be positive here", num_cus);
+  if (cu_margin < 0 || cu_margin >= num_cus)
+    return fail(DA_ERR_ARG, "cu_margin=%d must be in [0, %d)", cu_margin, num_cus);
+  for (int b = 0; b < B; ++b)
+    if (seq_lens[b] < 0 || seq_lens[b] > L_K_max)
+      return fail(DA_ERR_SHAPE, "seq_lens[%d]=%d outside [0, L_K_max=%d]", b, seq_lens[b], L_K_max);
+  const int cus = num_cus - cu_margin;
+  const int g = H_Q / H_KV;
+  const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
+  const int hpt = heads_per_tile(H_Q, H_KV, pack);
+  const int tps = H_Q / hpt;
+
+  std::vector<int64_t> T(B);
+  int64_t t_max = 0;
+  for (int b = 0; b < B; ++b) {
+    T[b] = (seq_lens[b] + 31) / 32;
+    if (T[b] > t_max) t_max = T[b];
+  }
+  int64_t c = chunk_tiles;
+  if (c <= 0) {
+    // Candidate chunks: the longest sequence cut into 1..64 pieces.  The
+    // fastest modelled one wins; on a tie, the longer chunk.
+    const CostModel& m = mi355x_model();
+    c = t_max > 0 ? t_max : 1;
+    double best = schedule_time(m, T.data(), seq_lens, B, H_Q, H_KV, hpt, c, cus);
+    int64_t prev = c;
+    for (int s = 2; s <= kMaxSplits && t_max > 0; ++s) {
+      const int64_t cand = (t_max + s - 1) / s;
+      if (cand == prev) continue;
+      prev = cand;
+      const double ts = schedule_time(m, T.data(), seq_lens, B, H_Q, H_KV, hpt, cand, cus);
+      if (ts < best) {
+        best = ts;
+        c = cand;
+      }
+    }
+  }
+
+  // Items and per-sequence rows.
+  std::vector<int32_t> split(B), row0(B);
+  int64_t n_items = 0, rows = 0;
+  int max_s = 1;
+  for (int b = 0; b < B; ++b) {
+    split[b] = seq_splits(T[b], c);
+    row0[b] = split[b] > 1 ? (int32_t)rows : -1;
+    if (split[b] > 1) rows += split[b];
+    if (split[b] > max_s) max_s = split[b];
+    n_items += (int64_t)split[b] * tps;
+  }
+  const size_t seq_off = (size_t)n_items * 16;
+  const size_t need = seq_off + (size_t)B * 8;
+  if ((int64_t)rows * H_Q * kHeadDim * 4 >= ((int64_t)1 << 31) || need >= ((size_t)1 << 31))
+    return fail(DA_ERR_SHAPE, "schedule of %lld workgroups and %lld state rows is too large", (long long)n_items,
+                (long long)rows);
+  out->B = B;
+  out->H_Q = H_Q;
+  out->H_KV = H_KV;
+  out->L_K_max = L_K_max;
+  out->pack_gqa = pack;
+  out->heads_per_tile = hpt;
+  out->tiles = B * tps;
+  out->num_items = (int32_t)n_items;
+  out->chunk_tiles = (int32_t)c;
+  out->max_splits = max_s;
+  out->state_rows = (int32_t)rows;
+  out->num_cus = cus;
+  out->kv_fetch = kv_fetch(n_items, cus);
+  out->seq_offset = (int32_t)seq_off;
+  out->meta_bytes = (int32_t)need;
+  out->reserved = 0;
+  if (!meta) return fail(DA_ERR_NULL, "meta is NULL");
+  if (meta_bytes < need)
+    return fail(DA_ERR_WORKSPACE, "schedule needs %zu metadata bytes, got %zu", need, meta_bytes);
+
+  // G head tiles read each KV head (G = 1 when a tile holds the whole
+  // group).  Items are listed sequence, KV head, chunk, then those G tiles,
+  // so the G workgroups that read the same keys are neighbours.
+  const int G = g / hpt;
+  std::vector<Item> items;
+  items.reserve((size_t)n_items);
+  for (int b = 0; b < B; ++b) {
+    const int s = split[b];
+    for (int kv = 0; kv < H_KV; ++kv)
+      for (int i = 0; i < s; ++i)
+        for (int m = 0; m < G; ++m) {
+          Item it;
+          it.tile = b * tps + kv * G + m;
+          it.t0 = (int32_t)(T[b] * i / s);
+          it.t1 = (int32_t)(T[b] * (i + 1) / s);
+          it.row = s > 1 ? row0[b] + i : -1;
+          items.push_back(it);
+        }
+  }
+  // Longest chunks first, so that the tail of the launch holds short ones
+  // (stable: neighbours that read the same keys stay neighbours).
+  std::stable_sort(items.begin(), items.end(),
+                   [](const Item& a, const Item& b) { return a.t1 - a.t0 > b.t1 - b.t0; });
+  int32_t* w = static_cast<int32_t*>(meta);
+  const int64_t n = n_items;
+  // Workgroup i starts on XCD i % 8.  With G > 1, each block of 8G items is
+  // transposed so that the G readers of one KV head and chunk take slots
+  // j, j + 8, ..., j + 8(G-1) of the block: one XCD, one L2.  A last partial
+  // block keeps list order.
+  const int64_t blk = 8 * (int64_t)G;
+  for (int64_t pos = 0; pos < n; ++pos) {
+    int64_t bid = pos;
+    if (G > 1 && pos < n - n % blk) {
+      const int64_t base = pos - pos % blk, r = pos % blk;
+      bid = base + (r % G) * 8 + r / G;
+    }
+    w[4 * bid + 0] = items[pos].tile;
+    w[4 * bid + 1] = items[pos].t0;
+    w[4 * bid + 2] = items[pos].t1;
+    w[4 * bid + 3] = items[pos].row;
+  }
+  int32_t* sq = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(meta) + seq_off);
+  for (int b = 0; b < B; ++b) {
+    sq[2 * b] = row0[b];
+    sq[2 * b + 1] = split[b];
+  }
+  return DA_OK;
+}
+
 WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s) {
   WorkspaceLayout w{};
   const size_t rows = (size_t)B * H_Q;
@@ -211,6 +390,32 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
     if (rc) return rc;
   }
   return da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, num_cus, cu_margin, policy, out);
+}
+
+size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa) {
+  if (B <= 0 || H_Q <= 0 || H_KV <= 0 || H_Q % H_KV != 0) return 0;
+  const int g = H_Q / H_KV;
+  const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
+  const int64_t tps = H_Q / da::heads_per_tile(H_Q, H_KV, pack);
+  return (size_t)B * tps * da::kMaxSplits * 16 + (size_t)B * 8;
+}
+
+int da_make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
+                     int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes,
+                     da_schedule* out) {
+  da::clear_error();
+  if (num_cus <= 0) {
+    int is950 = 0;
+    int rc = da_device_info(&num_cus, &is950);
+    if (rc) return rc;
+  }
+  return da::make_schedule(seq_lens, B, H_Q, H_KV, L_K_max, d, pack_gqa, num_cus, cu_margin, chunk_tiles, meta,
+                           meta_bytes, out);
+}
+
+size_t da_schedule_workspace_bytes(const da_schedule* s) {
+  if (!s || s->state_rows <= 0 || s->H_Q <= 0) return 0;
+  return da::workspace_layout(s->state_rows, s->H_Q, da::kHeadDim, 1).total;
 }
 
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits) {

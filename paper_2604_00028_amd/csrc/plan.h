@@ -58,6 +58,22 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
 // Argument checks shared by the launch entry points (no HIP calls).
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d);
 
+// Per-sequence schedule (da_make_schedule).  Split count of a sequence of T
+// 32-key tiles for a target chunk of c tiles.
+inline int seq_splits(int64_t T, int64_t c) {
+  if (T <= 0) return 1;
+  const int64_t s = (T + c - 1) / c;
+  return s > kMaxSplits ? kMaxSplits : (int)s;
+}
+
+// Modelled time (us) of a schedule with target chunk c tiles; `tiles_of`
+// holds the 32-key tile count of each sequence.
+double schedule_time(const CostModel& m, const int64_t* tiles_of, const int32_t* lens, int B, int H_Q,
+                     int H_KV, int hpt, int64_t c, int cus);
+
+int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
+                  int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes, da_schedule* out);
+
 struct WorkspaceLayout {
   size_t o_off, m_off, l_off, total;
 };

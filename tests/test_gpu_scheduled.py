@@ -1,0 +1,186 @@
+"""GPU parity of the per-sequence scheduled entry point against the fp64
+oracle, for contiguous (fixed and varlen) and paged K/V.  Same bar as the
+other paths: max-abs <= 2e-2 and mean-abs <= 2e-3 on O, lse within 1e-3;
+bit-identical repeats; the same bits as the uniform launch where the chunk
+cuts coincide."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_00028_amd as da
+from oracle import decode_attention
+from workloads import config_shapes, custom_shape, make_inputs, paged_layout
+from tests.gpu_helpers import assert_parity, dev_inputs, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+LSE_TOL = 1e-3
+
+
+def check_lse(lse_t, lse):
+    lg = lse_t.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(lse)
+    assert np.array_equal(np.isfinite(lg), fin)
+    assert np.max(np.abs(lg[fin] - lse[fin]), initial=0.0) <= LSE_TOL
+
+
+def run_sched(q, k, v, lens, H_KV, L_K_max, cu=None, paged=None, chunk_tiles=0, cu_margin=0, pack=-1):
+    sched, meta = da.da_make_schedule(lens, q.shape[1], H_KV, L_K_max, pack_gqa=pack, chunk_tiles=chunk_tiles,
+                                      cu_margin=cu_margin)
+    meta_dev = meta.cuda()
+    lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device="cuda")
+    if paged is None:
+        out = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, lse_out=lse)
+    else:
+        bt, sl = paged
+        out = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, block_table=bt, seq_lens=sl, lse_out=lse)
+    torch.cuda.synchronize()
+    return out, lse, sched
+
+
+CHUNKS = [0, 1, 2, 5, 40]   # 0: chosen by the cost model
+
+
+def check_inputs(inp, what, chunks=CHUNKS, page=None, packs=(-1,)):
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    lens = [int(x) for x in inp.lengths]
+    L = max(lens + [0]) if inp.cu_seqlens_k is not None else inp.shape.L_K
+    H_KV = inp.shape.H_KV
+    if page is None:
+        q, k, v, cu = dev_inputs(inp)
+        paged = None
+    else:
+        pg = paged_layout(inp, page, seed=page + 3)
+        q = to_dev(inp.q)
+        k, v = to_dev(pg.k_cache), to_dev(pg.v_cache)
+        paged = (torch.from_numpy(pg.block_table).cuda(), torch.from_numpy(pg.seq_lens).cuda())
+        cu = None
+    for pack in packs:
+        for c in chunks:
+            say(f"scheduled {what} page={page} chunk={c} pack={pack}")
+            out, lse_t, sched = run_sched(q, k, v, lens, H_KV, L, cu=cu, paged=paged, chunk_tiles=c, pack=pack)
+            assert_parity(out, O, f"scheduled {what} chunk={c} pack={pack} ({sched.as_dict()})")
+            check_lse(lse_t, lse)
+
+
+@pytest.mark.parametrize("page", [None, 64])
+def test_varlen_gqa_scheduled(page):
+    sh = config_shapes(4)[0]
+    check_inputs(make_inputs(sh), sh.name, page=page, packs=(-1, 0))
+
+
+@pytest.mark.parametrize("shape", config_shapes(2) + config_shapes(1), ids=lambda s: s.name)
+def test_fixed_layout_scheduled(shape):
+    check_inputs(make_inputs(shape), shape.name)
+
+
+@pytest.mark.parametrize("B,H_Q,H_KV,lengths", [
+    (4, 8, 1, [0, 1, 1000, 33]),             # empty and single-key sequences
+    (4, 8, 1, [5000, 40, 40, 0]),             # one long sequence among short ones
+    (3, 128, 2, [700, 2100, 3]),              # two head tiles per KV head
+    (2, 12, 4, [300, 95]),                    # group of 3
+    (1, 8, 1, [9000]),                        # a single long sequence: up to 64 chunks
+])
+@pytest.mark.parametrize("page", [None, 32])
+def test_ragged_scheduled(B, H_Q, H_KV, lengths, page):
+    sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
+    inp = make_inputs(sh, seed=B * 10 + H_Q, lengths=lengths)
+    check_inputs(inp, f"B{B}-H{H_Q}-KV{H_KV}-{lengths}", page=page)
+
+
+def test_cu_margin_schedule():
+    sh = config_shapes(4)[0]
+    inp = make_inputs(sh)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    lens = [int(x) for x in inp.lengths]
+    for margin in (0, 64, 200, 255):
+        say(f"scheduled cu_margin={margin}")
+        out, lse_t, sched = run_sched(q, k, v, lens, sh.H_KV, sh.L_K, cu=cu, cu_margin=margin)
+        assert sched.num_cus == da.da_device_info()[0] - margin
+        assert_parity(out, O, f"cu_margin={margin}")
+        check_lse(lse_t, lse)
+
+
+@pytest.mark.parametrize("s,pack", [(1, 1), (2, 1), (4, 1), (4, 0)])
+def test_scheduled_equals_uniform_when_cuts_coincide(s, pack):
+    """Equal lengths of 512 keys cut into s chunks of 512/s keys (whole
+    tiles, whole tiles per wave): the scheduled launch computes the same
+    chunk states as the uniform one and merges them in the same order."""
+    sh = config_shapes(2)[3]
+    inp = make_inputs(sh)
+    q, k, v, _ = dev_inputs(inp)
+    say(f"scheduled vs uniform s={s} pack={pack}")
+    a = da.da_decode_attn(q, k, v, num_splits=s, pack_gqa=pack)
+    sched, meta = da.da_make_schedule([512], 64, 8, pack_gqa=pack, chunk_tiles=16 // s)
+    assert sched.max_splits == s
+    b = da.da_decode_attn_scheduled(q, k, v, sched, meta.cuda())
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("c", [0, 3])
+def test_scheduled_bit_identical_repeats(c):
+    sh = config_shapes(4)[0]
+    inp = make_inputs(sh)
+    q, k, v, cu = dev_inputs(inp)
+    lens = [int(x) for x in inp.lengths]
+    say(f"scheduled repeats chunk={c}")
+    first, lse0, _ = run_sched(q, k, v, lens, sh.H_KV, sh.L_K, cu=cu, chunk_tiles=c)
+    for _ in range(3):
+        again, lse1, _ = run_sched(q, k, v, lens, sh.H_KV, sh.L_K, cu=cu, chunk_tiles=c)
+        assert torch.equal(first.view(torch.int16), again.view(torch.int16))
+        assert torch.equal(lse0, lse1)
+
+
+@pytest.mark.parametrize("c", [0, 2])
+def test_scheduled_graph_replay_matches_eager(c):
+    sh = config_shapes(4)[0]
+    inp = make_inputs(sh)
+    q, k, v, cu = dev_inputs(inp)
+    lens = [int(x) for x in inp.lengths]
+    sched, meta = da.da_make_schedule(lens, sh.H_Q, sh.H_KV, sh.L_K, chunk_tiles=c)
+    meta_dev = meta.cuda()
+    say(f"scheduled graph replay chunk={c}")
+    eager = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu)
+    torch.cuda.synchronize()
+    out = torch.empty_like(eager)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out)
+    for r in range(4):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), f"replay {r}"
+        again = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu)
+        torch.cuda.synchronize()
+        assert torch.equal(again.view(torch.int16), eager.view(torch.int16))
+
+
+def test_ragged_highload_scheduled_sampled():
+    """A ragged high-load batch at full size (32 sequences of 1024..16384
+    keys, H_Q 64, H_KV 8; about 1.1 GB of K/V): three sequences against the
+    oracle, every output finite."""
+    rng = np.random.default_rng(2024)
+    lengths = [int(x) for x in rng.integers(1024, 16385, 32)]
+    sh = custom_shape(32, 64, 8, max(lengths), varlen=True)
+    inp = make_inputs(sh, seed=2025, lengths=lengths)
+    q, k, v, cu = dev_inputs(inp)
+    picks = [int(np.argmax(lengths)), int(np.argmin(lengths)), 7]
+    cuh = inp.cu_seqlens_k
+    for c in (0, 64):
+        say(f"ragged highload scheduled chunk={c}")
+        out, lse_t, sched = run_sched(q, k, v, lengths, 8, max(lengths), cu=cu, chunk_tiles=c)
+        for b in picks:
+            O, lse = decode_attention(inp.q[b:b + 1], inp.k[cuh[b]:cuh[b + 1]][None], inp.v[cuh[b]:cuh[b + 1]][None])
+            assert_parity(out[b:b + 1], O, f"ragged highload b={b} chunk={c}")
+            assert np.max(np.abs(lse_t[b].cpu().numpy() - lse[0])) <= LSE_TOL
+        assert torch.isfinite(out.float()).all()
