@@ -13,8 +13,9 @@ paper times with CUDA-graph replay and A/B interleaving, Section 5).
 Printed: one JSON line.  `value` is microseconds per call for the planned
 num_splits (lower is better), next to num_splits=1, a split sweep, the
 cold-cache time, the high-load shape (B=32, H_Q=64, H_KV=8, L_K=8192, 1 GiB
-of KV) against the HBM roofline, and the fp64 oracle timed on the host cores
-(a reported baseline only).
+of KV) against the HBM roofline, batches of mixed lengths under the
+per-sequence schedule against the uniform plan, and the fp64 oracle timed on
+the host cores (a reported baseline only).
 """
 
 from __future__ import annotations
@@ -59,6 +60,7 @@ def parse():
     ap.add_argument("--highload-steps", type=int, default=20)
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-long", action="store_true", help="skip the L_K = 1024/2048/8192 block")
+    ap.add_argument("--no-ragged", action="store_true", help="skip the mixed-length (per-sequence schedule) block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=("headline", "highload", "copy"), default=None,
@@ -70,6 +72,11 @@ def parse():
                          "paper's policy and fixed splits) and write the results to OUT_JSON")
     ap.add_argument("--regression-summary", metavar="IN_JSON", default=None,
                     help="summarise a --regression result into profiles/regression_160_configs.md")
+    ap.add_argument("--schedule-sweep", metavar="OUT_JSON", default=None,
+                    help="time per-sequence schedules (modelled and fixed chunk lengths) against uniform launches "
+                         "on mixed-length batches and write the results to OUT_JSON")
+    ap.add_argument("--schedule-sweep-summary", metavar="IN_JSON", default=None,
+                    help="summarise a --schedule-sweep result into profiles/schedule_mixed_length_batches.md")
     ap.add_argument("--traffic-summary", metavar="DIR", default=None,
                     help="derive per-launch HBM traffic from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE output "
                          "directories DIR/pmc_<COUNTER>_<workload> and write profiles/traffic.json")
@@ -124,6 +131,26 @@ class Variant:
         return statistics.median(self.times)
 
 
+class Timed:
+    """K calls of any launch (call(i) issues call i) captured in a HIP graph."""
+
+    def __init__(self, torch, call, steps):
+        self.steps = steps
+        for i in range(3):
+            call(i)
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            for i in range(steps):
+                call(i)
+        self.graph.replay()
+        torch.cuda.synchronize()
+        self.times = []
+
+    timed = Variant.timed
+    median = Variant.median
+
+
 def interleave(torch, variants, rounds):
     for _ in range(rounds):
         for var in variants:
@@ -148,6 +175,152 @@ def traffic_for(workload: str):
         return int(w["fetch_bytes"] + w["write_bytes"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def ragged_run(args, da, torch, np) -> dict:
+    """Per-sequence schedules against the uniform plan on batches of mixed
+    lengths: the scheduled launch (metadata made on the host, copied once),
+    the uniform plan made for the longest sequence, and fixed split counts."""
+    from workloads import algorithmic_bytes as ab, ragged_batches
+    res = {}
+    for name, lens, H_Q, H_KV in ragged_batches():
+        B, tot, L = len(lens), sum(lens), max(lens)
+        gen = torch.Generator(device="cuda").manual_seed(7)
+        q = torch.randn(B, H_Q, 128, device="cuda", generator=gen).to(torch.bfloat16)
+        kv_bytes = 2 * tot * H_KV * 256
+        copies = max(1, min(16, -(-(512 << 20) // kv_bytes)))   # keep the working set out of L2 and MALL
+        kvs = [(torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16),
+                torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16)) for _ in range(copies)]
+        cu = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
+        out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
+        steps = 10 if kv_bytes > (256 << 20) else 100
+        sched, meta = da.da_make_schedule(lens, H_Q, H_KV, L)
+        # host cost of the planner itself (C call, buffers prepared once)
+        import ctypes
+        c_lens = (ctypes.c_int32 * B)(*lens)
+        c_meta = (ctypes.c_uint8 * sched.meta_bytes)()
+        c_out = da.DaSchedule()
+        t0 = time.perf_counter()
+        for _ in range(50):
+            da.load().da_make_schedule(c_lens, B, H_Q, H_KV, L, 128, -1, 0, 0, 0, c_meta, sched.meta_bytes,
+                                       ctypes.byref(c_out))
+        plan_us = (time.perf_counter() - t0) / 50 * 1e6
+        meta_dev = meta.cuda()
+        ws_s = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+        ws_u = torch.empty(da.da_workspace_bytes(B, H_Q, 128, 64), dtype=torch.uint8, device="cuda")
+        plan = da.da_choose_splits(B, H_Q, H_KV, L)
+        log(f"timing ragged batch {name}")
+        sv = Timed(torch, lambda i: da.da_decode_attn_scheduled(q, *kvs[i % copies], sched, meta_dev, cu_seqlens_k=cu,
+                                                                out=out, workspace=ws_s), steps)
+        fixed = sorted({1, 2, 4, 8, 16, 32, plan.num_splits})
+        uv = {s: Timed(torch, lambda i, s=s: da.da_decode_attn(q, *kvs[i % copies], cu, out=out, L_K_max=L,
+                                                               num_splits=s, pack_gqa=plan.pack_gqa, workspace=ws_u),
+                       steps) for s in fixed}
+        interleave(torch, [sv] + list(uv.values()), max(3, args.rounds // 2))
+        u_us = {s: round(v.median, 2) for s, v in uv.items()}
+        best = min(u_us, key=u_us.get)
+        nbytes = ab(B, H_Q, H_KV, tot, varlen=True)
+        gbs = nbytes / (sv.median * 1e-6) / 1e9
+        res[name] = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "keys": tot, "L_K_max": L,
+                     "scheduled_us": round(sv.median, 2), "chunk_tiles": sched.chunk_tiles,
+                     "workgroups": sched.num_items, "max_splits": sched.max_splits, "plan_host_us": round(plan_us, 1),
+                     "uniform_plan_splits": plan.num_splits, "uniform_plan_us": u_us[plan.num_splits],
+                     "speedup_vs_uniform_plan": round(u_us[plan.num_splits] / sv.median, 3),
+                     "best_uniform_splits": best, "best_uniform_us": u_us[best],
+                     "vs_best_uniform": round(sv.median / u_us[best], 3), "uniform_us": u_us,
+                     "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+        del kvs, sv, uv
+    return res
+
+
+SCHED_GRID = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
+PROFILE_SCHEDULE = os.path.join(ROOT, "profiles", "schedule_mixed_length_batches.md")
+
+
+def schedule_sweep_run(args, da, torch, np) -> None:
+    """For every mixed-length batch of the fit and check sets: the modelled
+    schedule, schedules at the chunk lengths that cut the longest sequence
+    into 1..64 pieces, and the uniform launch at every split count."""
+    from workloads import schedule_batches
+    rows = []
+    for kind in ("fit", "check"):
+        for name, lens, H_Q, H_KV in schedule_batches(kind):
+            B, tot, L = len(lens), sum(lens), max(lens)
+            gen = torch.Generator(device="cuda").manual_seed(11)
+            kv_bytes = 2 * tot * H_KV * 256
+            copies = max(1, min(16, -(-(512 << 20) // kv_bytes)))
+            q = torch.randn(B, H_Q, 128, device="cuda", generator=gen).to(torch.bfloat16)
+            kvs = [(torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16),
+                    torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16))
+                   for _ in range(copies)]
+            cu = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
+            out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
+            steps = 10 if kv_bytes > (256 << 20) else (40 if kv_bytes > (32 << 20) else 200)
+            ws = torch.empty(da.da_workspace_bytes(B, H_Q, 128, 64) + 4096, dtype=torch.uint8, device="cuda")
+            log(f"schedule sweep {kind}/{name}")
+            plan = da.da_choose_splits(B, H_Q, H_KV, L)
+            uni = {s: Timed(torch, lambda i, s=s: da.da_decode_attn(q, *kvs[i % copies], cu, out=out, L_K_max=L,
+                                                                    num_splits=s, pack_gqa=plan.pack_gqa,
+                                                                    workspace=ws), steps)
+                   for s in sorted(set(SCHED_GRID) | {plan.num_splits})}
+            t_max = -(-L // 32)
+            chunks = sorted({-(-t_max // s) for s in SCHED_GRID}, reverse=True)
+            scheds = {}
+            for c in [0] + chunks:
+                sc, meta = da.da_make_schedule(lens, H_Q, H_KV, L, chunk_tiles=c)
+                md = meta.cuda()
+                scheds[c] = (sc, md, Timed(torch, lambda i, sc=sc, md=md: da.da_decode_attn_scheduled(
+                    q, *kvs[i % copies], sc, md, cu_seqlens_k=cu, out=out, workspace=ws), steps))
+            interleave(torch, list(uni.values()) + [x[2] for x in scheds.values()], 5)
+            rows.append({"set": kind, "batch": name, "B": B, "H_Q": H_Q, "H_KV": H_KV, "keys": tot, "L_K_max": L,
+                         "uniform_plan_splits": plan.num_splits,
+                         "uniform_us": {s: round(v.median, 3) for s, v in uni.items()},
+                         "auto_chunk": scheds[0][0].chunk_tiles, "auto_workgroups": scheds[0][0].num_items,
+                         "auto_us": round(scheds[0][2].median, 3),
+                         "chunk_us": {c: round(scheds[c][2].median, 3) for c in chunks}})
+            del kvs, uni, scheds
+    with open(args.schedule_sweep, "w") as f:
+        json.dump({"device_cus": da.da_device_info()[0], "rows": rows}, f)
+    log(f"wrote {args.schedule_sweep}")
+
+
+def schedule_sweep_summary(path: str) -> None:
+    d = json.load(open(path))
+    lines = ["# Per-sequence schedule on mixed-length batches (MI355X)", "",
+             "Made by `python bench.py --schedule-sweep sched.json` then "
+             "`python bench.py --schedule-sweep-summary sched.json`.", "",
+             "Per batch: the modelled schedule (`auto`), the fastest of the schedules whose chunk cuts the "
+             "longest sequence into 1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48 or 64 pieces (`grid best`), the "
+             "uniform launch planned for the longest sequence (`uniform plan`) and the fastest uniform split "
+             "count (`uniform best`).  Times in microseconds per call, HIP-graph replay, medians of 5 "
+             "interleaved replays.  `fit`: the batches the schedule model was fitted to; `check`: drawn "
+             "afterwards and never fitted.", "",
+             "| set | batch | B | H_Q/H_KV | keys | auto chunk | auto | grid best | auto/grid | uniform plan (s) "
+             "| uniform best (s) | plan/auto | best/auto |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    stats = {}
+    for r in d["rows"]:
+        cu = {int(k): v for k, v in r["chunk_us"].items()}
+        uu = {int(k): v for k, v in r["uniform_us"].items()}
+        gb = min(cu.values())
+        ub = min(uu, key=uu.get)
+        up = uu[r["uniform_plan_splits"]]
+        a = r["auto_us"]
+        stats.setdefault(r["set"], []).append((a / gb, up / a, uu[ub] / a))
+        lines.append(f"| {r['set']} | {r['batch']} | {r['B']} | {r['H_Q']}/{r['H_KV']} | {r['keys']} | "
+                     f"{r['auto_chunk']} | {a:.2f} | {gb:.2f} | {a / gb:.3f} | {up:.2f} ({r['uniform_plan_splits']}) "
+                     f"| {uu[ub]:.2f} ({ub}) | {up / a:.2f} | {uu[ub] / a:.3f} |")
+    lines.append("")
+    for k, v in stats.items():
+        g = [x[0] for x in v]
+        p = [x[1] for x in v]
+        b = [x[2] for x in v]
+        lines.append(f"- {k}: auto/grid-best mean {sum(g) / len(g):.3f}, worst {max(g):.3f}; "
+                     f"speedup over the uniform plan {min(p):.2f}x to {max(p):.2f}x; "
+                     f"best uniform / auto {min(b):.3f} to {max(b):.3f}")
+    with open(PROFILE_SCHEDULE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def cpu_baseline(inp, seconds: float):
@@ -349,6 +522,9 @@ def main():
     if args.regression_summary:
         regression_summary(args.regression_summary)
         return
+    if args.schedule_sweep_summary:
+        schedule_sweep_summary(args.schedule_sweep_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode kernel shards by "
               f"(sequence, KV head) with no exchange, so no multi-GPU figure is produced.", file=sys.stderr)
@@ -370,6 +546,9 @@ def main():
         return
     if args.regression:
         regression_run(args, da, torch)
+        return
+    if args.schedule_sweep:
+        schedule_sweep_run(args, da, torch, np)
         return
 
     # ---------------- headline: Llama-3.1-70B GQA decode, B=1, L_K=512
@@ -467,6 +646,8 @@ def main():
                              "frac": round(hgbs / HBM_PEAK_GBS, 4), "traffic": traffic_for(shh.name)}}
         del qh, kh, vh, hh, hs
 
+    ragged = None if args.no_ragged else ragged_run(args, da, torch, np)
+
     result = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -500,6 +681,7 @@ def main():
         "other_lk": other,
         "long_lk": longer,
         "high_load": high,
+        "ragged": ragged,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(sh.name)},
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(inp, args.cpu_seconds),

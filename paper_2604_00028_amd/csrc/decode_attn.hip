@@ -178,13 +178,20 @@ __device__ __forceinline__ void merge_weights(float* m, const float* l, int s, f
   ML[1] = L;
 }
 
+// Waves per SIMD each variant must fit: three for the 16-column direct-fetch
+// kernel (launches of many workgroups, several per CU), two otherwise.
+template <int NT, int FETCH>
+constexpr int kMinWaves = (NT == 1 && FETCH == 0) ? 3 : 2;
+
 // NT: 16-column head tiles per workgroup (1: up to 16 query heads, 2: up to
 // 32).  W: waves per workgroup.  FETCH: a Fetch value.  PG: paged K/V cache
 // (pages of page_size rows, page_size a multiple of 32; chunks and wave
 // ranges are then cut at 32-key tile boundaries, so every tile lies in one
-// page).
-template <int NT, int W, int FETCH, bool PG>
-__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2, 8)))
+// page).  SCH: per-sequence schedule (p.work lists every workgroup's head
+// tile, 32-key tile range and chunk-state row).  Both are template
+// parameters so that the uniform launch waits on no extra argument.
+template <int NT, int W, int FETCH, bool PG, bool SCH>
+__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(kMinWaves<NT, FETCH>, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -196,7 +203,7 @@ split_partial_kernel(Params p) {
   // ---- which tile and chunk this workgroup owns
   const int bid = blockIdx.x;
   int tile, split = 0, prow = -1, w_first = 0, w_end = 0;
-  if (p.work) {
+  if constexpr (SCH) {
     // scheduled: this workgroup's head tile, 32-key tile range and state row
     tile = p.work[4 * bid];
     w_first = p.work[4 * bid + 1];
@@ -227,12 +234,12 @@ split_partial_kernel(Params p) {
     L = p.L_K;
   }
   int key_lo, key_hi;
-  if (PG || p.work) {
+  if constexpr (PG || SCH) {
     // tiles of 32 keys cut into s chunks (or the scheduled range), each
     // chunk's tiles into W ranges
     const uint32_t T = (uint32_t)(L + kKeysPerTile - 1) / kKeysPerTile;
     uint32_t t0, nt;
-    if (p.work) {
+    if constexpr (SCH) {
       const uint32_t f = (uint32_t)(w_first < 0 ? 0 : w_first);
       const uint32_t e = (uint32_t)(w_end < 0 ? 0 : w_end);
       t0 = f < T ? f : T;
@@ -655,9 +662,9 @@ split_partial_kernel(Params p) {
 
   const int64_t rows = (int64_t)p.B * p.H_Q;
   const int64_t row0_tile = (int64_t)b * p.H_Q + head0;
-  const bool direct = p.work ? prow < 0 : p.mode == kDirect;
+  const bool direct = SCH ? prow < 0 : p.mode == kDirect;
   // first chunk-state row of this workgroup's heads
-  const int64_t srow0 = direct ? 0 : (p.work ? (int64_t)prow * p.H_Q + head0 : (int64_t)split * rows + row0_tile);
+  const int64_t srow0 = direct ? 0 : (SCH ? (int64_t)prow * p.H_Q + head0 : (int64_t)split * rows + row0_tile);
   const __amdgpu_buffer_rsrc_t ors = make_rsrc(p.o_part + srow0 * D, (uint32_t)p.hpt * D * 4);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -718,7 +725,9 @@ split_partial_kernel(Params p) {
 // Log-sum-exp combine: one wave64 per (b, h) row, 2 dims per lane.  The
 // first 16 chunk outputs are loaded before the weights are known; weights
 // and the weighted sum are taken in chunk order, so the result is
-// bit-identical across runs and producers of the same chunk states.
+// bit-identical across runs and producers of the same chunk states.  SEQ:
+// per-sequence chunk counts and state rows from `seqs`.
+template <bool SEQ>
 __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
                                                             const float* __restrict__ m_part,
                                                             const float* __restrict__ l_part,
@@ -736,7 +745,7 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
   // counts interleave the rows; a per-sequence schedule stores sequence b's
   // chunks from its first state row on (unsplit sequences are already done).
   int64_t base = row, srow = rows;
-  if (seqs) {
+  if constexpr (SEQ) {
     const int b = (int)(row / H_Q);
     const int h = (int)(row - (int64_t)b * H_Q);
     const int r0 = seqs[2 * b];
@@ -839,20 +848,20 @@ int ensure_gfx950(int* cus) {
   return DA_OK;
 }
 
-template <int NT, int W, int FETCH, bool PG>
+template <int NT, int W, int FETCH, bool PG, bool SCH>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG, SCH>);
 }
 
-template <bool PG>
+template <bool PG, bool SCH>
 const void* pick_kernel(int NT, int FETCH) {
   switch (FETCH * 2 + NT - 1) {
-    case 0: return kernel_ptr<1, 4, kFetchDirect, PG>();
-    case 1: return kernel_ptr<2, 4, kFetchDirect, PG>();
-    case 2: return kernel_ptr<1, 4, kFetchStaged, PG>();
-    case 3: return kernel_ptr<2, 4, kFetchStaged, PG>();
-    case 4: return kernel_ptr<1, 4, kFetchLds, PG>();
-    case 5: return kernel_ptr<2, 4, kFetchLds, PG>();
+    case 0: return kernel_ptr<1, 4, kFetchDirect, PG, SCH>();
+    case 1: return kernel_ptr<2, 4, kFetchDirect, PG, SCH>();
+    case 2: return kernel_ptr<1, 4, kFetchStaged, PG, SCH>();
+    case 3: return kernel_ptr<2, 4, kFetchStaged, PG, SCH>();
+    case 4: return kernel_ptr<1, 4, kFetchLds, PG, SCH>();
+    case 5: return kernel_ptr<2, 4, kFetchLds, PG, SCH>();
     default: return nullptr;
   }
 }
@@ -862,7 +871,9 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
   const int FETCH = pl.kv_fetch;
   if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
-  const void* fn = prm.block_table ? pick_kernel<true>(NT, FETCH) : pick_kernel<false>(NT, FETCH);
+  const void* fn = prm.block_table
+                       ? (prm.work ? pick_kernel<true, true>(NT, FETCH) : pick_kernel<true, false>(NT, FETCH))
+                       : (prm.work ? pick_kernel<false, true>(NT, FETCH) : pick_kernel<false, false>(NT, FETCH));
   if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
@@ -879,8 +890,9 @@ int launch_combine(const float* o_part, const float* m_part, const float* l_part
                    int s, int64_t rows, hipStream_t stream, const int32_t* seqs = nullptr, int H_Q = 1) {
   const int grid = (int)((rows + 3) / 4);
   void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows, &seqs, &H_Q};
-  hipError_t e =
-      hipLaunchKernel(reinterpret_cast<const void*>(&split_combine_kernel), dim3(grid), dim3(256), args, 0, stream);
+  const void* fn = seqs ? reinterpret_cast<const void*>(&split_combine_kernel<true>)
+                        : reinterpret_cast<const void*>(&split_combine_kernel<false>);
+  hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(256), args, 0, stream);
   if (e != hipSuccess) return da::fail(DA_ERR_HIP, "combine launch: %s", hipGetErrorString(e));
   return DA_OK;
 }

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "decode_attn.h"
 
 namespace da {
@@ -66,10 +68,33 @@ inline int seq_splits(int64_t T, int64_t c) {
   return s > kMaxSplits ? kMaxSplits : (int)s;
 }
 
+// Cost model of a per-sequence schedule (times in microseconds).  Chunks of
+// unequal length make the tail of the launch matter, so the model follows
+// the CUs one by one: each CU's share of the work, how many CUs are still
+// busy as the shares run out, and the HBM rate they divide.
+struct ScheduleModel {
+  double base[2];           // fixed part (16-column / 32-column head tiles)
+  double t_tile[2];         // one wave step (four 32-key tiles per workgroup), CU-bound
+  double t_tile_staged[2];  // ... with K and V fetched straight into LDS
+  double hbm_rate;          // bytes per microsecond the busy CUs divide
+  double pnorm;             // a step costs (t_tile^p + (busy CUs x 64 KiB / hbm_rate)^p)^(1/p)
+  double tail;              // scale of the summed steps
+  double merge0;            // combine launch, fixed part (some sequence split)
+  double merge1[2];         // ... per chunk of the most-split sequence
+};
+const ScheduleModel& mi355x_schedule_model();
+
+// Cost of one wave step while `busy` CUs stream (index busy = 1..cus), for
+// K through registers (direct) and straight into LDS (staged).
+struct StepCost {
+  std::vector<double> direct, staged;
+  StepCost(const ScheduleModel& m, int wide, int cus);
+};
+
 // Modelled time (us) of a schedule with target chunk c tiles; `tiles_of`
 // holds the 32-key tile count of each sequence.
-double schedule_time(const CostModel& m, const int64_t* tiles_of, const int32_t* lens, int B, int H_Q,
-                     int H_KV, int hpt, int64_t c, int cus);
+double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t* tiles_of, int B, int H_Q,
+                     int hpt, int64_t c, int cus);
 
 int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
                   int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes, da_schedule* out);

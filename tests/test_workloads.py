@@ -33,3 +33,13 @@ def test_paged_layout_fixed_layout_and_seed():
     assert np.array_equal(a.block_table, b.block_table) and np.array_equal(a.k_cache, b.k_cache)
     assert np.array_equal(gather(a, 1, 128, a.k_cache), inp.k[1])
     assert list(a.seq_lens) == [128, 128]
+
+
+def test_ragged_batches_are_mixed_and_seeded():
+    from workloads import ragged_batches
+    a, b = ragged_batches(), ragged_batches()
+    assert a == b
+    names = [x[0] for x in a]
+    assert len(set(names)) == len(names)
+    for name, lens, H_Q, H_KV in a:
+        assert H_Q % H_KV == 0 and len(set(lens)) > 1 and min(lens) >= 1 and max(lens) <= 65536

@@ -229,6 +229,77 @@ def all_shapes() -> List[Shape]:
     return [s for c in ALL_CONFIG_IDS for s in config_shapes(c)]
 
 
+def ragged_batches() -> List[tuple]:
+    """Batches of mixed sequence lengths for the per-sequence schedule:
+    (name, lengths, H_Q, H_KV).  Lengths are drawn from PCG64 with the
+    stated seed; K/V values for timing are drawn separately (any values)."""
+    def uniform(seed, B, lo, hi):
+        return [int(x) for x in np.random.default_rng(seed).integers(lo, hi + 1, B)]
+
+    def lognormal(seed, B, median, sigma, lo=16, hi=65536):
+        x = np.random.default_rng(seed).lognormal(np.log(median), sigma, B)
+        return [int(v) for v in np.clip(x, lo, hi)]
+
+    return [
+        ("ragged_highload_b32_h64_kv8", uniform(2024, 32, 1024, 16384), 64, 8),
+        ("bimodal_b32_h64_kv8", [16384] * 4 + [512] * 28, 64, 8),
+        ("one_long_mqa_b8_h8_kv1", [32768] + [256] * 7, 8, 1),
+        ("lognormal_mqa_b128_h8_kv1", lognormal(106, 128, 1000, 1.0), 8, 1),
+    ]
+
+
+def schedule_batches(kind: str) -> List[tuple]:
+    """Mixed-length batches for measuring the per-sequence schedule's cost
+    model: "fit" (the batches its constants were fitted to) or "check"
+    (batches drawn afterwards, never fitted).  (name, lengths, H_Q, H_KV)."""
+    def U(seed, B, lo, hi):
+        return [int(x) for x in np.random.default_rng(seed).integers(lo, hi + 1, B)]
+
+    def LN(seed, B, median, sigma, lo=16, hi=65536):
+        return [int(v) for v in np.clip(np.random.default_rng(seed).lognormal(np.log(median), sigma, B), lo, hi)]
+
+    if kind == "fit":
+        return [
+            ("ragged_b32_gqa", U(1, 32, 1024, 16384), 64, 8),
+            ("bimodal_b32_gqa", [16384] * 4 + [512] * 28, 64, 8),
+            ("ragged_b64_gqa", U(3, 64, 256, 8192), 64, 8),
+            ("ragged_b16_gqa", U(4, 16, 1024, 16384), 64, 8),
+            ("ragged_b8_gqa", U(5, 8, 512, 32768), 64, 8),
+            ("ragged_b4_gqa", U(6, 4, 256, 4096), 64, 8),
+            ("ragged_b32_mqa", U(7, 32, 128, 16384), 8, 1),
+            ("ragged_b16_mqa", U(8, 16, 128, 8192), 8, 1),
+            ("ragged_b64_mqa", U(9, 64, 1024, 32768), 8, 1),
+            ("one_long_mqa", [32768] + [256] * 7, 8, 1),
+            ("one_long_gqa", [65536] + [1024] * 15, 64, 8),
+            ("two_long_b32", [16384] * 2 + U(10, 30, 64, 1024), 32, 4),
+            ("varlen_gqa_b16", U(4000, 16, 32, 512), 32, 4),
+            ("ragged_b128_h32", U(11, 128, 32, 2048), 32, 4),
+            ("ragged_b32_g16", U(12, 32, 512, 8192), 32, 2),
+            ("ragged_b8_h128", U(13, 8, 512, 8192), 128, 2),
+            ("geometric_b32", [int(x) for x in np.minimum(32768, 64 * 2 ** np.random.default_rng(14).uniform(0, 9, 32))],
+             64, 8),
+            ("ragged_b2_mqa", U(15, 2, 1024, 65536), 8, 1),
+        ]
+    if kind == "check":
+        return [
+            ("ragged_b32_gqa", U(101, 32, 512, 16384), 64, 8),
+            ("lognorm_b64_gqa", LN(102, 64, 2000, 1.0), 64, 8),
+            ("lognorm_b16_mqa", LN(103, 16, 4000, 1.2), 8, 1),
+            ("ragged_b48_h32", U(104, 48, 64, 4096), 32, 4),
+            ("bimodal_b16", [32768] * 2 + [256] * 14, 64, 8),
+            ("one_long_b4", [50000, 300, 300, 300], 8, 1),
+            ("ragged_b24_g16", U(105, 24, 256, 12000), 32, 2),
+            ("lognorm_b128_mqa", LN(106, 128, 1000, 1.0), 8, 1),
+            ("ragged_b6_h128", U(107, 6, 1024, 16384), 128, 2),
+            ("lognorm_b32_gqa", LN(108, 32, 8000, 0.6), 64, 8),
+            ("short_b64", U(109, 64, 16, 600), 32, 4),
+            ("ragged_b12_gqa", U(110, 12, 128, 2048), 64, 8),
+            ("equal_b32_gqa", [8192] * 32, 64, 8),
+            ("equal_b1_gqa", [512], 64, 8),
+        ]
+    raise ValueError(kind)
+
+
 def algorithmic_bytes(B: int, H_Q: int, H_KV: int, total_keys: int, D: int = HEAD_DIM,
                       varlen: bool = False) -> int:
     """Bytes the method must move once: K and V once, Q read, O written (bf16),
