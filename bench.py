@@ -63,7 +63,7 @@ def parse():
     ap.add_argument("--no-ragged", action="store_true", help="skip the mixed-length (per-sequence schedule) block")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--only", choices=("headline", "highload", "copy"), default=None,
+    ap.add_argument("--only", choices=("headline", "highload", "ragged", "copy"), default=None,
                     help="time only the planned launch of one workload, or a plain 1 GiB device copy "
                          "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
@@ -372,6 +372,9 @@ def only_run(args, da, torch, np, dev):
     if args.only == "copy":
         copy_run(args, torch)
         return
+    if args.only == "ragged":
+        ragged_only(args, da, torch, np)
+        return
     sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
     inp = make_inputs(sh)
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
@@ -386,7 +389,32 @@ def only_run(args, da, torch, np, dev):
                       "frac": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
 
-TRAFFIC_WORKLOADS = {"headline": "llama70b_gqa_b1_l512", "highload": "highload_b32_h64_kv8_l8192"}
+def ragged_only(args, da, torch, np):
+    """The scheduled launch of the ragged high-load batch alone."""
+    from workloads import algorithmic_bytes as ab, ragged_batches
+    name, lens, H_Q, H_KV = ragged_batches()[0]
+    B, tot, L = len(lens), sum(lens), max(lens)
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    q = torch.randn(B, H_Q, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    k = torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    v = torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    cu = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
+    out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
+    sched, meta = da.da_make_schedule(lens, H_Q, H_KV, L)
+    meta_dev = meta.cuda()
+    ws = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+    K = args.highload_steps
+    var = Timed(torch, lambda i: da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out,
+                                                             workspace=ws), K)
+    interleave(torch, [var], args.rounds)
+    gbs = ab(B, H_Q, H_KV, tot, varlen=True) / (var.median * 1e-6) / 1e9
+    print(json.dumps({"workload": name, "us_per_call": round(var.median, 3), "chunk_tiles": sched.chunk_tiles,
+                      "workgroups": sched.num_items, "calls": K * (args.rounds + 1) + 3,
+                      "achieved_gbps": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
+
+
+TRAFFIC_WORKLOADS = {"headline": "llama70b_gqa_b1_l512", "highload": "highload_b32_h64_kv8_l8192",
+                     "ragged": "ragged_highload_b32_h64_kv8"}
 
 
 def counter_avg(path: str, kernel_prefix: str, counter: str) -> float:
