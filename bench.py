@@ -61,6 +61,8 @@ def parse():
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-long", action="store_true", help="skip the L_K = 1024/2048/8192 block")
     ap.add_argument("--no-ragged", action="store_true", help="skip the mixed-length (per-sequence schedule) block")
+    ap.add_argument("--no-cu-margin", action="store_true",
+                    help="skip the cu_margin block (decode beside a GEMM on reserved CUs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--only", choices=("headline", "highload", "ragged", "copy"), default=None,
@@ -321,6 +323,93 @@ def schedule_sweep_summary(path: str) -> None:
     with open(PROFILE_SCHEDULE, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+def cu_margin_run(args, da, torch, np) -> dict:
+    """cu_margin with a concurrent kernel.  A quarter of the CUs (8 of every
+    32 mask bits) is reserved for a bf16 GEMM on a CU-masked stream; the
+    high-load decode runs on the rest, scheduled for the whole chip
+    (cu_margin 0) or for the CUs it has (cu_margin = reserved).  Also: the
+    same pair on two unmasked streams, and each kernel alone."""
+    from paper_2604_00028_amd.streams import cu_mask_stream, destroy_stream, split_masks
+    cus = da.da_device_info()[0]
+    lens = [8192] * 32
+    B, H_Q, H_KV, tot = 32, 64, 8, sum(lens)
+    gen = torch.Generator(device="cuda").manual_seed(13)
+    q = torch.randn(B, H_Q, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    k = torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    v = torch.randn(tot, H_KV, 128, device="cuda", generator=gen).to(torch.bfloat16)
+    cu = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
+    out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
+    A = torch.randn(8192, 8192, device="cuda", generator=gen).to(torch.bfloat16)
+    Bm = torch.randn(8192, 8192, device="cuda", generator=gen).to(torch.bfloat16)
+    plain_d, plain_g = torch.cuda.Stream(), torch.cuda.Stream()
+    calls, gemms, rounds = 20, 8, max(3, args.rounds // 2)
+
+    def decode_fn(margin):
+        sched, meta = da.da_make_schedule(lens, H_Q, H_KV, 8192, cu_margin=margin)
+        md = meta.cuda()
+        ws = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+        return sched, lambda s: da.da_decode_attn_scheduled(q, k, v, sched, md, cu_seqlens_k=cu, out=out,
+                                                            workspace=ws, stream=s)
+
+    def run(dstream, dfn, gstream):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        torch.cuda.synchronize()
+        if gstream is not None:
+            ev[2].record(gstream)
+            with torch.cuda.stream(gstream):
+                for _ in range(gemms):
+                    torch.matmul(A, Bm)
+            ev[3].record(gstream)
+        if dfn is not None:
+            ev[0].record(dstream)
+            for _ in range(calls):
+                dfn(dstream)
+            ev[1].record(dstream)
+        torch.cuda.synchronize()
+        d = ev[0].elapsed_time(ev[1]) * 1000 / calls if dfn is not None else None
+        g = ev[2].elapsed_time(ev[3]) * 1000 / gemms if gstream is not None else None
+        return d, g
+
+    gs = ds = None
+    try:
+        reserve_w, decode_w = split_masks(cus, 8)
+        gs, n_res = cu_mask_stream(reserve_w)
+        ds, n_dec = cu_mask_stream(decode_w)
+        s0, f0 = decode_fn(0)
+        sm, fm = decode_fn(n_res)
+        cases = {"decode_alone_full_chip": (plain_d, f0, None),
+                 "decode_alone_masked_plan_full_chip": (ds, f0, None),
+                 "decode_alone_masked_plan_margin": (ds, fm, None),
+                 "concurrent_masked_plan_full_chip": (ds, f0, gs),
+                 "concurrent_masked_plan_margin": (ds, fm, gs),
+                 "concurrent_unmasked_plan_full_chip": (plain_d, f0, plain_g),
+                 "gemm_alone_full_chip": (None, None, plain_g),
+                 "gemm_alone_reserved": (None, None, gs)}
+        for st, fn, gst in cases.values():   # warm every path once
+            run(st, fn, gst)
+        times = {name: [] for name in cases}
+        for _ in range(rounds):
+            for name, (st, fn, gst) in cases.items():
+                times[name].append(run(st, fn, gst))
+        res = {"workload": "highload_b32_h64_kv8_l8192 + bf16 GEMM 8192^3", "reserved_cus": n_res,
+               "decode_cus": n_dec, "workgroups_plan_full_chip": s0.num_items,
+               "workgroups_plan_margin": sm.num_items}
+        for name, ts in times.items():
+            d = [x[0] for x in ts if x[0] is not None]
+            g = [x[1] for x in ts if x[1] is not None]
+            res[name] = {"decode_us": round(statistics.median(d), 2) if d else None,
+                         "gemm_us": round(statistics.median(g), 1) if g else None}
+        res["margin_speedup_concurrent"] = round(res["concurrent_masked_plan_full_chip"]["decode_us"] /
+                                                 res["concurrent_masked_plan_margin"]["decode_us"], 3)
+        return res
+    except Exception as e:  # the reservation is an optional part of the report
+        return {"error": f"{type(e).__name__}: {e}"}
+    finally:
+        for s in (gs, ds):
+            if s is not None:
+                destroy_stream(s)
 
 
 def cpu_baseline(inp, seconds: float):
@@ -675,6 +764,7 @@ def main():
         del qh, kh, vh, hh, hs
 
     ragged = None if args.no_ragged else ragged_run(args, da, torch, np)
+    margin = None if args.no_cu_margin else cu_margin_run(args, da, torch, np)
 
     result = {
         "metric": METRIC,
@@ -710,6 +800,7 @@ def main():
         "long_lk": longer,
         "high_load": high,
         "ragged": ragged,
+        "cu_margin": margin,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(sh.name)},
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(inp, args.cpu_seconds),

@@ -184,3 +184,47 @@ def test_ragged_highload_scheduled_sampled():
             assert_parity(out[b:b + 1], O, f"ragged highload b={b} chunk={c}")
             assert np.max(np.abs(lse_t[b].cpu().numpy() - lse[0])) <= LSE_TOL
         assert torch.isfinite(out.float()).all()
+
+
+def test_concurrent_kernel_on_reserved_cus():
+    """cu_margin with a concurrent kernel: a GEMM runs on a quarter of the
+    CUs (a masked stream) while the decode runs on the rest, planned with
+    that margin and without.  Every decode output is bit-identical to the
+    same schedule run alone on the whole chip, and matches the oracle."""
+    from paper_2604_00028_amd.streams import cu_mask_stream, destroy_stream, split_masks
+    cus = da.da_device_info()[0]
+    if cus % 32:
+        pytest.skip("CU count not a multiple of 32")
+    sh = config_shapes(4)[0]
+    inp = make_inputs(sh)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    lens = [int(x) for x in inp.lengths]
+    reserve_w, decode_w = split_masks(cus, 8)
+    say("creating CU-masked streams")
+    gs, n_res = cu_mask_stream(reserve_w)
+    ds, n_dec = cu_mask_stream(decode_w)
+    try:
+        assert n_res == cus // 4 and n_dec == cus - cus // 4
+        g = torch.Generator(device="cuda").manual_seed(5)
+        A = torch.randn(4096, 4096, device="cuda", generator=g).to(torch.bfloat16)
+        Bm = torch.randn(4096, 4096, device="cuda", generator=g).to(torch.bfloat16)
+        for margin in (0, n_res):
+            sched, meta = da.da_make_schedule(lens, sh.H_Q, sh.H_KV, sh.L_K, cu_margin=margin)
+            md = meta.cuda()
+            say(f"concurrent decode cu_margin={margin} ({sched.num_items} workgroups)")
+            alone = da.da_decode_attn_scheduled(q, k, v, sched, md, cu_seqlens_k=cu)
+            torch.cuda.synchronize()
+            assert_parity(alone, O, f"alone cu_margin={margin}")
+            outs = [torch.empty_like(alone) for _ in range(5)]
+            with torch.cuda.stream(gs):
+                for _ in range(4):
+                    torch.matmul(A, Bm)
+            for o in outs:
+                da.da_decode_attn_scheduled(q, k, v, sched, md, cu_seqlens_k=cu, out=o, stream=ds)
+            torch.cuda.synchronize()
+            for o in outs:
+                assert torch.equal(o.view(torch.int16), alone.view(torch.int16))
+    finally:
+        destroy_stream(gs)
+        destroy_stream(ds)

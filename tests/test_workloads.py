@@ -43,3 +43,20 @@ def test_ragged_batches_are_mixed_and_seeded():
     assert len(set(names)) == len(names)
     for name, lens, H_Q, H_KV in a:
         assert H_Q % H_KV == 0 and len(set(lens)) > 1 and min(lens) >= 1 and max(lens) <= 65536
+
+
+def test_split_masks_keep_cus_on_every_xcd():
+    """Both masks leave CUs on each of the 8 XCDs whether mask bits map to
+    XCDs in blocks of 32 or in turn."""
+    import pytest
+    from paper_2604_00028_amd.streams import split_masks
+    for per in (8, 16, 24):
+        res, dec = split_masks(256, per)
+        bits = lambda w: [i for i in range(256) if (w[i // 32] >> (i % 32)) & 1]  # noqa: E731
+        r, d = bits(res), bits(dec)
+        assert len(r) == 8 * per and len(d) == 256 - 8 * per and not set(r) & set(d)
+        for mapping in (lambda i: i // 32, lambda i: i % 8):
+            assert {mapping(i) for i in r} == set(range(8)) and {mapping(i) for i in d} == set(range(8))
+    for bad in (0, 4, 32):
+        with pytest.raises(ValueError):
+            split_masks(256, bad)
