@@ -65,7 +65,11 @@ def parse():
                     help="skip the cu_margin block (decode beside a GEMM on reserved CUs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--only", choices=("headline", "highload", "ragged", "copy"), default=None,
+    ap.add_argument("--lk", type=int, default=8192, help="with --only long: L_K of the B=1 Llama-70B GQA shape")
+    ap.add_argument("--occupancy-summary", metavar="DIR", default=None,
+                    help="summarise rocprofv3 occupancy counter runs DIR/occ_<pass>_<case> into "
+                         "profiles/occupancy_heuristic_vs_s1.md")
+    ap.add_argument("--only", choices=("headline", "highload", "long", "ragged", "copy"), default=None,
                     help="time only the planned launch of one workload, or a plain 1 GiB device copy "
                          "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
@@ -464,11 +468,15 @@ def only_run(args, da, torch, np, dev):
     if args.only == "ragged":
         ragged_only(args, da, torch, np)
         return
-    sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
-    inp = make_inputs(sh)
+    if args.only == "long":
+        sh = custom_shape(1, 64, 8, args.lk)
+        inp = make_inputs(sh, seed=3000 + args.lk)
+    else:
+        sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
+        inp = make_inputs(sh)
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
     del inp
-    K = args.steps if args.only == "headline" else args.highload_steps
+    K = args.highload_steps if args.only == "highload" else args.steps
     var = Variant(args.only, da, torch, q, k, v, sh.L_K, args.num_splits, -1, K)
     interleave(torch, [var], args.rounds)
     nbytes = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
@@ -538,6 +546,88 @@ def traffic_summary(d: str) -> None:
         json.dump(out, fh, indent=1)
         fh.write("\n")
     print(json.dumps(out))
+
+
+OCC_CASES = (  # (case, --only workload, extra flags, label)
+    ("headline_heur", "headline", "", "Llama-70B GQA B=1 L_K=512, heuristic"),
+    ("long2048_heur", "long", "--lk 2048", "Llama-70B GQA B=1 L_K=2048, heuristic"),
+    ("long2048_s1", "long", "--lk 2048 --num-splits 1", "Llama-70B GQA B=1 L_K=2048, num_splits=1"),
+    ("long8192_heur", "long", "--lk 8192", "Llama-70B GQA B=1 L_K=8192, heuristic"),
+    ("long8192_s1", "long", "--lk 8192 --num-splits 1", "Llama-70B GQA B=1 L_K=8192, num_splits=1"),
+    ("highload_heur", "highload", "", "high load B=32 L_K=8192, heuristic"),
+    ("highload_s4", "highload", "--num-splits 4", "high load B=32 L_K=8192, num_splits=4"),
+)
+OCC_PASSES = {"raw": "GRBM_GUI_ACTIVE SQ_BUSY_CU_CYCLES SQ_WAVE_CYCLES SQ_WAVES",
+              "occ": "MeanOccupancyPerActiveCU"}
+PROFILE_OCCUPANCY = os.path.join(ROOT, "profiles", "occupancy_heuristic_vs_s1.md")
+
+
+def occupancy_summary(d: str) -> None:
+    """Per case, the split kernel's dispatches: duration, GPU-active cycles,
+    busy CUs, mean occupancy of the busy CUs and occupancy in percent of 32
+    waves per CU."""
+    import csv
+    kp = "void (anonymous namespace)::split_partial_kernel"
+    lines = ["# Active CUs and occupancy: heuristic vs num_splits = 1 (MI355X, rocprofv3 counters)", "",
+             "Commands (MI355X, one GPU), for each case and pass:", "", "```",
+             "cd /tmp && export TMPDIR=/tmp && cd $REPO",
+             "rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_BUSY_CU_CYCLES SQ_WAVE_CYCLES SQ_WAVES --kernel-trace --stats \\",
+             "    --output-format csv -d gpurun_out/occ_raw_<case> -o run -- \\",
+             "    python3 bench.py --only <workload> <flags> --steps 20 --rounds 1 --highload-steps 3",
+             "rocprofv3 --pmc MeanOccupancyPerActiveCU --output-format csv -d gpurun_out/occ_occ_<case> -o run -- \\",
+             "    python3 bench.py --only <workload> <flags> --steps 20 --rounds 1 --highload-steps 3",
+             "python3 bench.py --occupancy-summary gpurun_out   # writes this file", "```", "",
+             "Per split-kernel dispatch, mean over the dispatches of the run. GRBM_GUI_ACTIVE comes summed over the "
+             "8 XCDs and is divided by 8. Busy CUs = SQ_BUSY_CU_CYCLES / GPU-active cycles (the profiler's "
+             "SIMD_UTILIZATION without the division by the CU count); over the kernel's own duration = "
+             "SQ_BUSY_CU_CYCLES / (duration x clock), the clock taken as GPU-active cycles / duration of the "
+             "longest case. For kernels of a few microseconds the GPU-active window also spans the dispatch, "
+             "so the first figure reads low. MeanOccupancyPerActiveCU is the profiler's derived metric. "
+             "Occupancy = 4 x SQ_WAVE_CYCLES / (GPU-active cycles x 256 CUs x 32 waves), the profiler's "
+             "OccupancyPercent.", "",
+             "| case | workgroups | waves | kernel us | GPU-active cycles | busy CUs (GPU-active) | busy CUs "
+             "(kernel time) | MeanOccupancyPerActiveCU | occupancy |",
+             "|---|---|---|---|---|---|---|---|---|"]
+
+    def read(case, pas):
+        path = os.path.join(d, f"occ_{pas}_{case}")
+        rows = list(csv.DictReader(open(os.path.join(path, "run_counter_collection.csv"))))
+        by, grid = {}, None
+        for r in rows:
+            if not r["Kernel_Name"].startswith(kp):
+                continue
+            by.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if grid is None and r.get("Grid_Size") and r.get("Workgroup_Size"):
+                grid = int(float(r["Grid_Size"])) // int(float(r["Workgroup_Size"]))
+        dur = None
+        stats = os.path.join(path, "run_kernel_stats.csv")
+        if os.path.exists(stats):
+            for r in csv.DictReader(open(stats)):
+                if r["Name"].startswith(kp):
+                    dur = float(r["AverageNs"]) / 1000.0
+        return {k: sum(v) / len(v) for k, v in by.items()}, grid, dur
+
+    got = []
+    for case, _, _, label in OCC_CASES:
+        try:
+            raw, grid, dur = read(case, "raw")
+            occ, _, _ = read(case, "occ")
+        except FileNotFoundError:
+            continue
+        got.append((label, raw, occ, grid, dur))
+    longest = max(got, key=lambda x: x[4] or 0.0)
+    clock = (longest[1]["GRBM_GUI_ACTIVE"] / 8.0) / longest[4]   # cycles per microsecond
+    for label, raw, occ, grid, dur in got:
+        active = raw["GRBM_GUI_ACTIVE"] / 8.0
+        busy = raw["SQ_BUSY_CU_CYCLES"]
+        occp = 100.0 * 4.0 * raw["SQ_WAVE_CYCLES"] / (active * 256 * 32)
+        lines.append(f"| {label} | {grid} | {raw['SQ_WAVES']:.0f} | {dur:.2f} | {active:,.0f} | {busy / active:.1f} | "
+                     f"{busy / (dur * clock):.1f} | {occ.get('MeanOccupancyPerActiveCU', float('nan')):.2f} | "
+                     f"{occp:.2f}% |")
+    lines += ["", f"Clock estimate: {clock:,.0f} cycles per microsecond."]
+    with open(PROFILE_OCCUPANCY, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def regression_run(args, da, torch) -> None:
@@ -638,6 +728,9 @@ def main():
         return
     if args.regression_summary:
         regression_summary(args.regression_summary)
+        return
+    if args.occupancy_summary:
+        occupancy_summary(args.occupancy_summary)
         return
     if args.schedule_sweep_summary:
         schedule_sweep_summary(args.schedule_sweep_summary)
