@@ -60,6 +60,7 @@ def parse():
     ap.add_argument("--highload-steps", type=int, default=20)
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-long", action="store_true", help="skip the L_K = 1024/2048/8192 block")
+    ap.add_argument("--no-small", action="store_true", help="skip the MQA / low-tile / varlen block")
     ap.add_argument("--no-ragged", action="store_true", help="skip the mixed-length (per-sequence schedule) block")
     ap.add_argument("--no-cu-margin", action="store_true",
                     help="skip the cu_margin block (decode beside a GEMM on reserved CUs)")
@@ -92,10 +93,10 @@ def parse():
 class Variant:
     """K calls of one launch configuration captured in a HIP graph."""
 
-    def __init__(self, name, da, torch, q, k, v, L, s, pack, steps, kv_copies=None):
+    def __init__(self, name, da, torch, q, k, v, L, s, pack, steps, kv_copies=None, cu=None):
         self.name = name
         B, H_Q, D = q.shape
-        H_KV = k.shape[2]
+        H_KV = k.shape[-2]
         self.plan = da.da_make_plan(B, H_Q, H_KV, L, D, s, pack)
         nbytes = da.da_workspace_bytes(B, H_Q, D, self.plan.num_splits)
         self.ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device="cuda") if nbytes else None
@@ -106,7 +107,8 @@ class Variant:
 
         def call(i):
             kk, vv = kvs[i % len(kvs)]
-            da.da_decode_attn(q, kk, vv, out=self.out, num_splits=s_res, pack_gqa=p_res, workspace=self.ws)
+            da.da_decode_attn(q, kk, vv, cu, out=self.out, L_K_max=L if cu is not None else None,
+                              num_splits=s_res, pack_gqa=p_res, workspace=self.ws)
 
         self.call = call
         for i in range(3):
@@ -181,6 +183,36 @@ def traffic_for(workload: str):
         return int(w["fetch_bytes"] + w["write_bytes"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def small_configs_run(args, da, torch, dev) -> dict:
+    """MQA decode (B=1, H_Q=8, H_KV=1, L_K=128), the pure-MQA low-tile sweep
+    (B in {1,2,4} x L_K in {64..512}, H_Q=32, H_KV=1) and the varlen batched
+    GQA batch: the heuristic against num_splits = 1 and fixed split counts,
+    with achieved HBM GB/s."""
+    from workloads import algorithmic_bytes as ab, config_shapes, make_inputs
+    res = {}
+    for cid, sweep in ((1, (1, 2, 4, 8)), (3, SWEEP), (4, SWEEP)):
+        for sh in config_shapes(cid):
+            inp = make_inputs(sh)
+            q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
+            cu = None if inp.cu_seqlens_k is None else torch.from_numpy(inp.cu_seqlens_k).cuda()
+            L = sh.L_K
+            log(f"timing {sh.name}")
+            hv = Variant("h", da, torch, q, k, v, L, 0, -1, args.steps, cu=cu)
+            fixed = [Variant(str(s), da, torch, q, k, v, L, s, 1, args.steps, cu=cu) for s in sweep if s <= max(L, 1)]
+            interleave(torch, [hv] + fixed, args.rounds)
+            sw = {x.plan.num_splits: round(x.median, 3) for x in fixed}
+            best = min(sw, key=sw.get)
+            nbytes = ab(sh.B, sh.H_Q, sh.H_KV, int(inp.lengths.sum()), varlen=cu is not None)
+            gbs = nbytes / (hv.median * 1e-6) / 1e9
+            res[sh.name] = {"config": cid, "B": sh.B, "H_Q": sh.H_Q, "H_KV": sh.H_KV, "L_K": L,
+                            "heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
+                            "s1_us": sw[1], "speedup_vs_s1": round(sw[1] / hv.median, 3), "best_fixed": best,
+                            "best_fixed_us": sw[best], "vs_best_fixed": round(hv.median / sw[best], 3),
+                            "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 5), "sweep_us": sw}
+            del q, k, v, hv, fixed
+    return res
 
 
 def ragged_run(args, da, torch, np) -> dict:
@@ -856,6 +888,7 @@ def main():
                              "frac": round(hgbs / HBM_PEAK_GBS, 4), "traffic": traffic_for(shh.name)}}
         del qh, kh, vh, hh, hs
 
+    small = None if args.no_small else small_configs_run(args, da, torch, dev)
     ragged = None if args.no_ragged else ragged_run(args, da, torch, np)
     margin = None if args.no_cu_margin else cu_margin_run(args, da, torch, np)
 
@@ -892,6 +925,7 @@ def main():
         "other_lk": other,
         "long_lk": longer,
         "high_load": high,
+        "mqa_and_varlen": small,
         "ragged": ragged,
         "cu_margin": margin,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
