@@ -203,7 +203,8 @@ size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa);
  *                items int32x4 [num_items]: {head tile, first tile, end
  *                  tile, state row (-1: the chunk is the whole sequence and
  *                  writes the output directly)}, with the 32-key tile range
- *                  [first, end) of that workgroup's chunk
+ *                  [first, end) of that workgroup's chunk; the last chunk of
+ *                  each sequence has end = INT32_MAX (to the sequence end)
  *                sequences int32x2 [B] at seq_offset: {first state row or
  *                  -1, split count s_b}
  *   out        filled on success
@@ -229,9 +230,12 @@ size_t da_schedule_workspace_bytes(const da_schedule* sched);
  *     da_decode_attn_paged; cu_seqlens_k ignored)
  *   sched      host struct from da_make_schedule for this B, H_Q, H_KV,
  *              L_K_max
- *   meta_dev   device copy of the metadata bytes (16-byte aligned); the
- *              kernel reads the lengths on the device, so a length that
- *              differs from the one scheduled changes only the balance
+ *   meta_dev   device copy of the metadata bytes (16-byte aligned).  The
+ *              kernel reads the lengths on the device (cu_seqlens_k or
+ *              seq_lens); where one differs from the length scheduled (up
+ *              to L_K_max) every key is still read once, since chunks are
+ *              clamped to the sequence and each sequence's last chunk runs
+ *              to its end: only the balance changes
  *   workspace  >= da_schedule_workspace_bytes(sched)
  * At most two launches (the combine only when some sequence is split), no
  * allocation, graph-capturable; results bit-identical across runs for a

@@ -2,6 +2,7 @@
 // model), the sequence partition, workspace sizing and error reporting.
 #include "plan.h"
 
+#include <limits.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -405,6 +406,12 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   // (stable: neighbours that read the same keys stay neighbours).
   std::stable_sort(items.begin(), items.end(),
                    [](const Item& a, const Item& b) { return a.t1 - a.t0 > b.t1 - b.t0; });
+  // The last chunk of a sequence runs to the end of the sequence as the
+  // device sees it, so a length that grew after scheduling is still read.
+  for (Item& it : items) {
+    const int b = it.tile / tps;
+    if (it.t1 == T[b]) it.t1 = INT32_MAX;
+  }
   int32_t* w = static_cast<int32_t*>(meta);
   const int64_t n = n_items;
   // Workgroup i starts on XCD i % 8.  With G > 1, each block of 8G items is

@@ -228,3 +228,32 @@ def test_concurrent_kernel_on_reserved_cus():
     finally:
         destroy_stream(gs)
         destroy_stream(ds)
+
+
+@pytest.mark.parametrize("page", [None, 64])
+def test_device_lengths_differ_from_scheduled(page):
+    """The schedule is made for one set of lengths, the device holds others
+    (longer and shorter, up to L_K_max): every key is still read once, so the
+    result is the oracle's for the device lengths."""
+    dev_lens = [700, 1, 333, 1500, 0, 64]
+    host_lens = [300, 40, 333, 1500, 90, 1]
+    sh = custom_shape(len(dev_lens), 16, 2, 1500, varlen=True)
+    inp = make_inputs(sh, seed=61, lengths=dev_lens)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    if page is None:
+        q, k, v, cu = dev_inputs(inp)
+        extra = dict(cu_seqlens_k=cu)
+    else:
+        pg = paged_layout(inp, page, seed=62)
+        q = to_dev(inp.q)
+        k, v = to_dev(pg.k_cache), to_dev(pg.v_cache)
+        extra = dict(block_table=torch.from_numpy(pg.block_table).cuda(),
+                     seq_lens=torch.from_numpy(pg.seq_lens).cuda())
+    for c in (0, 2, 7):
+        sched, meta = da.da_make_schedule(host_lens, sh.H_Q, sh.H_KV, 1500, chunk_tiles=c)
+        say(f"scheduled lengths differ page={page} chunk={c}")
+        lse_t = torch.empty(sh.B, sh.H_Q, dtype=torch.float32, device="cuda")
+        out = da.da_decode_attn_scheduled(q, k, v, sched, meta.cuda(), lse_out=lse_t, **extra)
+        torch.cuda.synchronize()
+        assert_parity(out, O, f"lengths differ page={page} chunk={c}")
+        check_lse(lse_t, lse)
