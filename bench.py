@@ -261,7 +261,8 @@ def ragged_run(args, da, torch, np) -> dict:
         gbs = nbytes / (sv.median * 1e-6) / 1e9
         res[name] = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "keys": tot, "L_K_max": L,
                      "scheduled_us": round(sv.median, 2), "chunk_tiles": sched.chunk_tiles,
-                     "workgroups": sched.num_items, "max_splits": sched.max_splits, "plan_host_us": round(plan_us, 1),
+                     "workgroups": sched.num_items, "max_splits": sched.max_splits, "kv_fetch": sched.kv_fetch,
+                     "plan_host_us": round(plan_us, 1),
                      "uniform_plan_splits": plan.num_splits, "uniform_plan_us": u_us[plan.num_splits],
                      "speedup_vs_uniform_plan": round(u_us[plan.num_splits] / sv.median, 3),
                      "best_uniform_splits": best, "best_uniform_us": u_us[best],

@@ -74,9 +74,10 @@ typedef struct da_plan {
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
   int32_t group_waves;    /* wave64s per workgroup (4); each takes a contiguous part of the chunk */
   int32_t kv_fetch;       /* how K/V tiles reach the matrix cores: 0 K straight into the operand
-                             layout, V through registers to LDS; 1 both row-contiguous into
-                             registers, then through LDS; 2 both row-contiguous straight into
-                             LDS, two tiles in flight per wave */
+                             layout, V through registers to LDS (chunks of one 32-key tile per
+                             wave); 1 both row-contiguous into registers, then through LDS (several
+                             workgroups per CU); 2 both row-contiguous straight into LDS, two tiles
+                             in flight per wave (at most one workgroup per CU) */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split

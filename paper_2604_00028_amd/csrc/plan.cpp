@@ -41,7 +41,9 @@ int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
 // g in {8,32} and L_K from 64 to 8192, timed with HIP-graph replay.  Over
 // that sweep the chosen split is on average 0.2% and at worst 4.3% slower
 // than the fastest measured one; fitted on half of the shapes, it chooses
-// the other half within 0.3% on average.
+// the other half within 0.3% on average.  Measured again after launches of
+// more workgroups than CUs moved to the register-staged fetch: 0.2% on
+// average, 5.1% at worst (a refit changed neither figure).
 const CostModel& mi355x_model() {
   static const CostModel m = {
       /*base=*/{2.841, 4.042},
@@ -72,7 +74,7 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
   const int64_t per_wave = (chunk + 3) / 4;
   const int64_t tiles_per_wave = (per_wave + 31) / 32;
   const int64_t per_cu = (wgs + cus - 1) / cus;
-  const double tt = kv_fetch(wgs, cus) ? m.t_tile_staged[wide] : m.t_tile[wide];
+  const double tt = kv_fetch(wgs, cus, tiles_per_wave) == kLoneFetch ? m.t_tile_staged[wide] : m.t_tile[wide];
   const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * tt;
   double bytes = (double)B * L_K * H_KV * row_bytes;
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
@@ -85,9 +87,14 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
 static int mi355x_splits(int B, int H_Q, int H_KV, int L_K, int hpt, int cus) {
   if (L_K <= 0) return 1;
   const CostModel& m = mi355x_model();
-  // Fastest modelled split count; the smallest one on an exact tie.
+  // Fastest modelled split count; the smallest one on an exact tie.  A
+  // split must be modelled at least 1% faster than one launch: closer than
+  // that the model cannot tell them apart, and a second launch that brings
+  // nothing is the one outcome the policy must avoid (never slower than one
+  // split).
+  const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, 1, cus);
   int best_s = 1;
-  double best = model_time(m, B, H_Q, H_KV, L_K, hpt, 1, cus);
+  double best = one;
   for (int s = 2; s <= kMaxSplits; ++s) {
     const double ts = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus);
     if (ts < best) {
@@ -95,7 +102,7 @@ static int mi355x_splits(int B, int H_Q, int H_KV, int L_K, int hpt, int cus) {
       best_s = s;
     }
   }
-  return best_s;
+  return best < kSplitGain * one ? best_s : 1;
 }
 
 // The paper's rule (Section 4): 128-key blocks, Batch * H_KV tiles.
@@ -120,14 +127,18 @@ int group_waves(int64_t grid, int cus) {
   return 4;
 }
 
-int kv_fetch(int64_t grid, int cus) {
-  // Fetched straight into the operand layout, neighbouring lanes read
-  // different key rows and one CU streams K at about half the rate it
-  // reaches with row-contiguous lanes.  Passing K through LDS costs LDS
-  // bandwidth and space, which pays where each workgroup has a CU to
-  // itself; when CUs hold several workgroups HBM bandwidth is the bound and
-  // the direct fetch keeps the LDS footprint small.
-  return grid <= cus ? kLoneFetch : 0;
+int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
+  // A workgroup with a CU to itself streams fastest with K and V loaded
+  // straight into LDS, two tiles in flight per wave (144 KB of LDS).  When
+  // CUs hold several workgroups, two of them per CU hide each other's
+  // latency: K and V go row-contiguous through registers into LDS (72 KB).
+  // On uniform and mixed-length launches of 128 to 2048 workgroups with at
+  // least two tiles per wave that was 1-5% faster than K fetched straight
+  // into the operand layout.  With a single tile per wave the per-workgroup
+  // overheads dominate and the smaller footprint of the operand-layout fetch
+  // (36 KB, three workgroups per CU) wins by up to 30%.
+  if (grid <= cus) return kLoneFetch;
+  return tiles_per_wave >= 2 ? 1 : 0;
 }
 
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
@@ -177,7 +188,10 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   out->grid = (int32_t)((int64_t)out->tiles * s);
   out->num_cus = cus;
   out->group_waves = group_waves(out->grid, cus);
-  out->kv_fetch = kv_fetch(out->grid, cus);
+  {
+    const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
+    out->kv_fetch = kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
+  }
   return DA_OK;
 }
 
@@ -190,7 +204,9 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // set the chosen chunk is on average 0.8% and at worst 5.6% slower than the
 // fastest measured one; fitted on half of the batches it chooses for the
 // other half within 0.7% on average (3.8% worst), and on 14 further batches
-// drawn afterwards within 0.9% of the best of 12 measured chunk lengths.
+// drawn afterwards within 0.9% of the best of 12 measured chunk lengths
+// (0.4%, 2.9% worst, measured again with the register-staged fetch for
+// launches of more workgroups than CUs).
 // The 32-column values carry the uniform model's ratios between the two
 // tile widths.
 const ScheduleModel& mi355x_schedule_model() {
@@ -275,7 +291,10 @@ double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t
   }
   // Shares run out from the smallest (CU cus-1) up; while `busy` CUs still
   // stream, a step costs tau[busy].
-  const std::vector<double>& tau = kv_fetch(items, cus) ? step.staged : step.direct;
+  int64_t max_w = 0;
+  for (int64_t w = (int64_t)count.size() - 1; w >= 1 && !max_w; --w)
+    if (count[w]) max_w = w;
+  const std::vector<double>& tau = kv_fetch(items, cus, max_w) == kLoneFetch ? step.staged : step.direct;
   double steps = 0.0;
   int64_t prev = 0;
   for (int k = 0; k < cus; ++k) {
@@ -375,7 +394,11 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   out->max_splits = max_s;
   out->state_rows = (int32_t)rows;
   out->num_cus = cus;
-  out->kv_fetch = kv_fetch(n_items, cus);
+  {
+    int64_t max_chunk = 0;  // tiles of the longest chunk
+    for (int b = 0; b < B; ++b) max_chunk = std::max<int64_t>(max_chunk, (T[b] + split[b] - 1) / split[b]);
+    out->kv_fetch = kv_fetch(n_items, cus, (max_chunk + 3) / 4);
+  }
   out->seq_offset = (int32_t)seq_off;
   out->meta_bytes = (int32_t)need;
   out->reserved = 0;

@@ -43,16 +43,22 @@ struct CostModel {
 };
 const CostModel& mi355x_model();
 
+// A split count above one is chosen only if modelled faster than one launch
+// by this factor.
+constexpr double kSplitGain = 0.99;
+
 // Modelled time (us) of one call with s splits (policy MI355X).
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus);
 
 // Waves per workgroup for a launch of `grid` workgroups on `cus` CUs.
 int group_waves(int64_t grid, int cus);
 
-// How K/V tiles reach the matrix cores for that launch (da_plan.kv_fetch);
-// kLoneFetch is the mode used when every workgroup has a CU to itself.
+// How K/V tiles reach the matrix cores for a launch of `grid` workgroups on
+// `cus` CUs whose waves walk up to `tiles_per_wave` 32-key tiles
+// (da_plan.kv_fetch); kLoneFetch is the mode used when every workgroup has a
+// CU to itself.
 constexpr int kLoneFetch = 2;
-int kv_fetch(int64_t grid, int cus);
+int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);

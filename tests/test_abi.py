@@ -205,12 +205,18 @@ def test_plan_fields_and_packing():
 
 
 def test_fetch_mode_follows_workgroups_per_cu():
-    # K passes through LDS exactly when every workgroup has a CU to itself
-    for s, staged in [(1, 1), (4, 1), (5, 0), (64, 0)]:
+    # direct-to-LDS with two tiles in flight when every workgroup has a CU to
+    # itself; K and V through registers into LDS (two workgroups per CU) otherwise
+    for s, fetch in [(1, 2), (4, 2), (5, 1), (16, 1), (64, 0)]:
         p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=1, num_cus=256)   # 64 tiles
-        assert p.grid == 64 * s and (p.kv_fetch > 0) == bool(staged) and p.group_waves == 4, (s, p.as_dict())
+        assert p.grid == 64 * s and p.kv_fetch == fetch and p.group_waves == 4, (s, p.as_dict())
     p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=1, num_cus=256, cu_margin=1)
-    assert p.kv_fetch == 0
+    assert p.kv_fetch == 1
+    # one 32-key tile per wave (chunks of at most 128 keys): the operand-layout fetch
+    p = da.da_make_plan(8, 64, 8, 512, num_splits=8, pack_gqa=1, num_cus=256)
+    assert p.grid == 512 and p.kv_fetch == 0
+    p = da.da_make_plan(8, 64, 8, 1024, num_splits=4, pack_gqa=1, num_cus=256)
+    assert p.grid == 256 and p.kv_fetch == 2
 
 
 def test_mi355x_policy_properties():
