@@ -61,6 +61,7 @@ def parse():
     ap.add_argument("--no-highload", action="store_true")
     ap.add_argument("--no-long", action="store_true", help="skip the L_K = 1024/2048/8192 block")
     ap.add_argument("--no-small", action="store_true", help="skip the MQA / low-tile / varlen block")
+    ap.add_argument("--no-streamed", action="store_true", help="skip the K/V-streamed-from-HBM block")
     ap.add_argument("--no-ragged", action="store_true", help="skip the mixed-length (per-sequence schedule) block")
     ap.add_argument("--no-cu-margin", action="store_true",
                     help="skip the cu_margin block (decode beside a GEMM on reserved CUs)")
@@ -212,6 +213,46 @@ def small_configs_run(args, da, torch, dev) -> dict:
                             "best_fixed_us": sw[best], "vs_best_fixed": round(hv.median / sw[best], 3),
                             "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 5), "sweep_us": sw}
             del q, k, v, hv, fixed
+    return res
+
+
+STREAMED_SHAPES = ((1, 64, 8, 128), (1, 64, 8, 256), (1, 64, 8, 384), (1, 64, 8, 512), (1, 64, 8, 1024),
+                   (1, 64, 8, 2048), (4, 64, 8, 512), (8, 64, 8, 1024), (1, 8, 1, 128), (1, 8, 1, 512),
+                   (1, 32, 1, 512), (4, 32, 1, 512), (16, 32, 4, 512))
+STREAMED_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
+
+
+def streamed_run(args, da, torch) -> dict:
+    """K/V streamed from HBM: every call of a timed replay reads its own copy
+    of the cache (>= 1 GiB per replay, more than L2 + MALL hold), as each
+    layer's cache is evicted by the rest of a decode step.  num_splits = 1,
+    the warm-calibrated policy, the streamed policy and fixed splits."""
+    res = {}
+    for B, H_Q, H_KV, L in STREAMED_SHAPES:
+        kvb = 2 * B * L * H_KV * 256
+        copies = max(1, min(4096, -(-(1 << 30) // kvb)))
+        gen = torch.Generator(device="cuda").manual_seed(17)
+        q = torch.randn(B, H_Q, 128, device="cuda", generator=gen).to(torch.bfloat16)
+        K = torch.empty(copies, B, L, H_KV, 128, dtype=torch.bfloat16, device="cuda").normal_(generator=gen)
+        V = torch.empty_like(K).normal_(generator=gen)
+        kvs = [(K[i], V[i]) for i in range(copies)]
+        steps = max(copies, 20)
+        warm = da.da_choose_splits(B, H_Q, H_KV, L)
+        cold = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_STREAMED)
+        splits = sorted(set(STREAMED_SWEEP) | {warm.num_splits, cold.num_splits})
+        log(f"timing streamed B={B} H_Q={H_Q} H_KV={H_KV} L_K={L} ({copies} copies)")
+        var = {s: Variant(str(s), da, torch, q, K[0], V[0], L, s, 1, steps, kv_copies=kvs) for s in splits}
+        interleave(torch, list(var.values()), max(3, args.rounds // 2))
+        us = {s: round(v.median, 3) for s, v in var.items()}
+        best = min(us, key=us.get)
+        res[f"b{B}_h{H_Q}_kv{H_KV}_l{L}"] = {
+            "B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L, "s1_us": us[1],
+            "warm_policy": warm.num_splits, "warm_policy_us": us[warm.num_splits],
+            "streamed_policy": cold.num_splits, "streamed_policy_us": us[cold.num_splits],
+            "streamed_speedup_vs_s1": round(us[1] / us[cold.num_splits], 3),
+            "best_fixed": best, "best_fixed_us": us[best],
+            "streamed_vs_best": round(us[cold.num_splits] / us[best], 3), "sweep_us": us}
+        del K, V, kvs, var
     return res
 
 
@@ -890,6 +931,7 @@ def main():
         del qh, kh, vh, hh, hs
 
     small = None if args.no_small else small_configs_run(args, da, torch, dev)
+    streamed = None if args.no_streamed else streamed_run(args, da, torch)
     ragged = None if args.no_ragged else ragged_run(args, da, torch, np)
     margin = None if args.no_cu_margin else cu_margin_run(args, da, torch, np)
 
@@ -916,7 +958,9 @@ def main():
                      for name, s_pol in (("paper", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
                                                                        policy=da.POLICY_PAPER).num_splits),
                                          ("evolved", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
-                                                                         policy=da.POLICY_EVOLVED).num_splits))},
+                                                                         policy=da.POLICY_EVOLVED).num_splits),
+                                         ("streamed", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
+                                                                          policy=da.POLICY_STREAMED).num_splits))},
         "best_fixed_splits": best_s,
         "vs_best_fixed": round(value / sweep_us[best_s], 3),
         "sweep_us": sweep_us,
@@ -927,6 +971,7 @@ def main():
         "long_lk": longer,
         "high_load": high,
         "mqa_and_varlen": small,
+        "streamed": streamed,
         "ragged": ragged,
         "cu_margin": margin,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

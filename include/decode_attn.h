@@ -57,9 +57,12 @@ typedef enum da_policy {
   DA_POLICY_PAPER = 1,  /* the paper's rule (Section 4): 128-key blocks, Batch*H_KV tiles;
                            at most 3 blocks -> 1; 4 blocks -> 1 with >= 4 tiles, else 3;
                            longer contexts fall through to the MI355X cost model */
-  DA_POLICY_EVOLVED = 2 /* the evolved single-batch setting the paper's search found (Section 3,
+  DA_POLICY_EVOLVED = 2, /* the evolved single-batch setting the paper's search found (Section 3,
                            Fig. 1): batch 1 -> 12 splits, 16 below 256 keys, GQA packing on;
                            larger batches use the MI355X cost model */
+  DA_POLICY_STREAMED = 3 /* the MI355X cost model calibrated with K/V read from HBM on every call
+                            (no cache reuse between calls, as in a decode step through all
+                            layers); it splits earlier, e.g. 4 splits at B=1, H_KV=8, L_K=512 */
 } da_policy;
 
 /* A launch plan: the scheduler metadata decided on the host before launch

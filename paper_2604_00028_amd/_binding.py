@@ -33,6 +33,7 @@ DA_ERR_ARG = -8
 POLICY_MI355X = 0
 POLICY_PAPER = 1
 POLICY_EVOLVED = 2
+POLICY_STREAMED = 3
 
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (

@@ -40,8 +40,11 @@ struct CostModel {
   double hbm_rate;         // sustained HBM bytes per microsecond, whole chip
   double hbm0;             // fixed part of the streaming bound
   double pnorm;            // the two bounds combine as (compute^p + stream^p)^(1/p)
+  double contig_tile;      // tile times scale by this when a key row holds one KV head (H_KV = 1)
 };
 const CostModel& mi355x_model();
+// The same model for K/V streamed from HBM on every call (policy STREAMED).
+const CostModel& mi355x_streamed_model();
 
 // A split count above one is chosen only if modelled faster than one launch
 // by this factor.

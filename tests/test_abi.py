@@ -248,7 +248,7 @@ def test_cu_margin_and_plan_errors():
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=7)
     with pytest.raises(da.DecodeAttnError):
-        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=3)
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=4)
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 3, 512, num_cus=256)
     with pytest.raises(da.DecodeAttnError):
@@ -260,3 +260,22 @@ def test_binding_refuses_bad_tensors():
     q = torch.zeros(1, 8, 128, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         da.da_decode_attn(q, q, q)            # CPU tensors are refused before any call
+
+
+def test_streamed_policy_splits_no_later_than_the_warm_one():
+    """With K/V read from HBM on every call a tile costs more, so the streamed
+    policy splits at least as often as the warm one on the paper's shapes,
+    and at B=1, H_KV=8, L_K=512 (4 blocks, the paper's boundary bucket) it
+    splits where the warm policy does not."""
+    for B in (1, 2, 4, 8):
+        for H_KV in (1, 2, 4, 8):
+            for L in (128, 256, 384, 512, 1024, 2048, 4096, 8192):
+                warm = da.da_choose_splits(B, 8 * H_KV, H_KV, L, num_cus=256)
+                cold = da.da_choose_splits(B, 8 * H_KV, H_KV, L, num_cus=256, policy=da.POLICY_STREAMED)
+                assert cold.num_splits >= warm.num_splits or L >= 4096, (B, H_KV, L, warm.num_splits,
+                                                                         cold.num_splits)
+                assert cold.pack_gqa == warm.pack_gqa and 1 <= cold.num_splits <= 64
+    assert da.da_choose_splits(1, 64, 8, 512, num_cus=256).num_splits == 1
+    assert da.da_choose_splits(1, 64, 8, 512, num_cus=256, policy=da.POLICY_STREAMED).num_splits > 1
+    for L in (128, 256, 384):
+        assert da.da_choose_splits(1, 64, 8, L, num_cus=256, policy=da.POLICY_STREAMED).num_splits == 1
