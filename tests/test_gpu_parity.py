@@ -119,6 +119,11 @@ def test_empty_and_short_sequences():
     (2, 64, 2, 129),     # group of 32: two head tiles
     (1, 128, 2, 70),     # group of 64: two tiles per KV head
     (5, 8, 1, 2049),     # ragged long tail
+    (2, 34, 2, 300),     # group of 17: one 17-column tile (two 16-column MFMA tiles)
+    (1, 48, 2, 200),     # group of 24
+    (1, 66, 2, 130),     # group of 33: three tiles of 11 heads
+    (1, 96, 2, 257),     # group of 48: two tiles of 24 heads
+    (3, 40, 1, 77),      # group of 40: two tiles of 20 heads
 ])
 def test_group_and_ragged_shapes(B, H_Q, H_KV, L):
     sh = custom_shape(B, H_Q, H_KV, L)

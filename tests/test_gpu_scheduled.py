@@ -81,6 +81,7 @@ def test_fixed_layout_scheduled(shape):
     (3, 128, 2, [700, 2100, 3]),              # two head tiles per KV head
     (2, 12, 4, [300, 95]),                    # group of 3
     (1, 8, 1, [9000]),                        # a single long sequence: up to 64 chunks
+    (2, 66, 2, [130, 700]),                   # group of 33: three head tiles of 11 per KV head
 ])
 @pytest.mark.parametrize("page", [None, 32])
 def test_ragged_scheduled(B, H_Q, H_KV, lengths, page):

@@ -97,7 +97,7 @@ def test_longest_chunks_first():
 
 
 @pytest.mark.parametrize("lens,H_Q,H_KV", [([4096, 4096, 2000, 64], 128, 2), ([700, 33, 5000], 64, 1),
-                                           ([300, 301], 16, 16)])
+                                           ([300, 301], 16, 16), ([130, 700, 9000], 66, 2)])
 def test_shared_kv_heads_grouped_on_one_xcd(lens, H_Q, H_KV):
     """Where G head tiles read one KV head, the G workgroups of one
     (sequence, KV head, chunk) start on one XCD (workgroup i on XCD i % 8),
