@@ -70,8 +70,13 @@ typedef enum da_policy {
  * num_splits; Section 3.1, num_splits / pack_gqa / sm_margin). */
 typedef struct da_plan {
   int32_t num_splits;     /* chunks per sequence, 1..64 */
-  int32_t pack_gqa;       /* 1: one workgroup serves all query heads of a KV head */
-  int32_t heads_per_tile; /* query heads one workgroup serves (H_Q/H_KV packed, capped at 32; 1 unpacked) */
+  int32_t pack_gqa;       /* 0: one query head per workgroup; 1: the query heads of a KV head packed
+                             into one workgroup, or for groups of more than 16 heads into tiles of at
+                             most 16 when the policy's cost model predicts that faster; 2: packed,
+                             the whole group in one workgroup (the paper's packing) */
+  int32_t heads_per_tile; /* query heads one workgroup serves: 1 unpacked; packed, the group g = H_Q/H_KV
+                             (its largest divisor <= 32 when g > 32), or with pack_gqa 1 possibly g's
+                             largest divisor <= 16 */
   int32_t tiles;          /* work tiles = B * H_Q / heads_per_tile (Section 2.1: Batch x H_KV when packed) */
   int32_t grid;           /* workgroups launched = tiles * num_splits */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
@@ -85,6 +90,8 @@ typedef struct da_plan {
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
  * policy that counts work tiles against the available compute units).
+ * Policies MI355X and STREAMED also choose the packed tile width (see
+ * da_plan); PAPER and EVOLVED keep the whole group in one tile.
  *   L_K_max  longest sequence in the batch (host-known, as with precomputed
  *            scheduler metadata, Section 5.1)
  *   num_cus  compute units to plan for; 0 = query the current device (one
@@ -96,7 +103,8 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
                      int cu_margin, int policy, da_plan* out);
 
 /* Same as da_choose_splits with num_splits and/or pack_gqa forced
- * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy).
+ * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy;
+ * pack_gqa 0, 1 or 2 as in da_plan).
  * Fills every field of `out` for the resulting launch; num_cus as for
  * da_choose_splits. */
 int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
@@ -129,7 +137,7 @@ int da_split_bounds(int L, int num_splits, int32_t* cuts);
  *                scaled scores (-inf for an empty sequence, whose O is 0)
  *   softmax_scale <= 0 selects 1/sqrt(d)
  *   num_splits   <= 0: chosen by da_choose_splits (policy MI355X); else 1..64
- *   pack_gqa     -1: chosen by the policy; 0 or 1 forced
+ *   pack_gqa     -1: chosen by the policy; 0, 1 or 2 forced (da_plan)
  *   workspace    device memory of workspace_bytes >= da_workspace_bytes(B,
  *                H_Q, d, s) for the resolved s (unused when s == 1).  Calls
  *                that share a workspace must not overlap in time.
@@ -195,7 +203,7 @@ size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa);
 
 /* Build the per-sequence schedule.
  *   seq_lens   host int32 [B]: key counts, each in [0, L_K_max]
- *   pack_gqa   -1 (chosen as by the policy) or 0/1
+ *   pack_gqa   -1 (chosen as by the policy) or 0, 1, 2 as in da_plan
  *   num_cus    0 = query the current device, > 0 = no device access
  *   cu_margin  compute units to leave to concurrent work (Section 3.1's
  *              sm_margin): the schedule is sized for num_cus - cu_margin
@@ -254,7 +262,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v,
 /* The split step alone: the partial softmax state of every chunk (the
  * per-chunk max, sum and unnormalised output the paper's final reduction
  * merges; Sections 3.1, 5.3).  Same inputs as da_decode_attn; num_splits
- * must be 1..64 and pack_gqa 0 or 1 (no policy here).
+ * must be 1..64 and pack_gqa 0, 1 or 2 (no policy here).
  *   o_part fp32 [num_splits, B, H_Q, d]: sum_j exp(s_j - m_i) v_j over chunk i
  *   m_part fp32 [num_splits, B, H_Q]:    max scaled score of chunk i (natural
  *                                        log units), -inf for an empty chunk

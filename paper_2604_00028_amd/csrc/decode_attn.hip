@@ -935,7 +935,7 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
   if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
   if (num_splits > DA_MAX_SPLITS)
     return da::fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, DA_MAX_SPLITS);
-  if (pack_gqa < -1 || pack_gqa > 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (pack_gqa < -1 || pack_gqa > 2) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
   if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
 
   // A forced split count fixes the workspace need before any device access.
@@ -1073,7 +1073,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
   // the schedule must describe a launch of this shape
   const int g = H_Q / H_KV;
   const int hpt = sched->heads_per_tile;
-  if ((sched->pack_gqa != 0 && sched->pack_gqa != 1) || hpt != da::heads_per_tile(H_Q, H_KV, sched->pack_gqa) ||
+  if (!da::heads_per_tile_valid(H_Q, H_KV, sched->pack_gqa, hpt) ||
       sched->tiles != B * (H_Q / hpt) || sched->num_items < sched->tiles ||
       (int64_t)sched->num_items > (int64_t)sched->tiles * DA_MAX_SPLITS || sched->max_splits < 1 ||
       sched->max_splits > DA_MAX_SPLITS || sched->state_rows < 0 || sched->kv_fetch < 0 || sched->kv_fetch > 2 ||
@@ -1147,7 +1147,7 @@ int da_split_partials(const void* q, const void* k, const void* v, const int32_t
     return da::fail(DA_ERR_ALIGN, "o_part must be 16-byte and m_part/l_part 4-byte aligned");
   if (num_splits < 1 || num_splits > DA_MAX_SPLITS)
     return da::fail(DA_ERR_SPLITS, "num_splits=%d not in [1, %d]", num_splits, DA_MAX_SPLITS);
-  if (pack_gqa != 0 && pack_gqa != 1) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {0,1}", pack_gqa);
+  if (pack_gqa < 0 || pack_gqa > 2) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {0,1,2}", pack_gqa);
   rc = check_state_size(B, H_Q, num_splits);
   if (rc) return rc;
   int cus = 0;

@@ -26,13 +26,19 @@ int fail(int code, const char* fmt, ...) {
 
 void clear_error() { g_last_error[0] = '\0'; }
 
-int heads_per_tile(int H_Q, int H_KV, int pack_gqa) {
+int heads_per_tile(int H_Q, int H_KV, int pack_gqa, int cap) {
   if (!pack_gqa) return 1;
   const int g = H_Q / H_KV;
-  if (g <= kMaxHeadsPerTile) return g;
-  for (int h = kMaxHeadsPerTile; h > 1; --h)
+  if (g <= cap) return g;
+  for (int h = cap; h > 1; --h)
     if (g % h == 0) return h;
   return 1;
+}
+
+bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt) {
+  if (pack < 0 || pack > 2) return false;
+  const int wide = heads_per_tile(H_Q, H_KV, pack);
+  return hpt == wide || (pack == 1 && hpt == heads_per_tile(H_Q, H_KV, pack, kNarrowHeadsPerTile));
 }
 
 // MI355X constants, fitted (log-error least squares over launches within
@@ -191,7 +197,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   int rc = check_shape(B, H_Q, H_KV, L_K_max, d);
   if (rc) return rc;
   if (num_splits > kMaxSplits) return fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, kMaxSplits);
-  if (pack_gqa < -1 || pack_gqa > 1) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (pack_gqa < -1 || pack_gqa > 2) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
   if (policy != DA_POLICY_MI355X && policy != DA_POLICY_PAPER && policy != DA_POLICY_EVOLVED &&
       policy != DA_POLICY_STREAMED)
     return fail(DA_ERR_ARG, "unknown policy %d", policy);
@@ -201,17 +207,38 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   const int cus = num_cus - cu_margin;
   const int g = H_Q / H_KV;
   const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
-  const int hpt = heads_per_tile(H_Q, H_KV, pack);
+  int hpt = heads_per_tile(H_Q, H_KV, pack);
   int s = num_splits;
-  if (s <= 0) {
-    if (policy == DA_POLICY_PAPER)
+  if (policy == DA_POLICY_PAPER || policy == DA_POLICY_EVOLVED) {
+    if (s <= 0 && policy == DA_POLICY_PAPER)
       s = paper_splits(B, H_KV, L_K_max, H_Q, hpt, cus);
-    else if (policy == DA_POLICY_EVOLVED && B == 1)
+    else if (s <= 0 && B == 1)
       s = L_K_max < 256 ? 16 : 12;  // Fig. 1: the evolved single-batch setting
-    else if (policy == DA_POLICY_STREAMED)
-      s = mi355x_splits(mi355x_streamed_model(), B, H_Q, H_KV, L_K_max, hpt, cus);
-    else
+    else if (s <= 0)
       s = mi355x_splits(mi355x_model(), B, H_Q, H_KV, L_K_max, hpt, cus);
+  } else {
+    // With pack_gqa = 1 the model also picks the width of a packed tile when
+    // the group is wider than one 16-column MFMA tile: all of it (up to 32
+    // heads) in one workgroup, or 16-head tiles whose workgroups read the
+    // same keys.  The narrow tile is cheaper per workgroup and doubles the
+    // workgroups, which pays while CUs are idle; the wide one reads each key
+    // once per group.  Narrow is taken only when modelled at least 1% faster.
+    const CostModel& m = policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model();
+    auto best = [&](int h, double* t) {
+      const int sh = s > 0 ? s : mi355x_splits(m, B, H_Q, H_KV, L_K_max, h, cus);
+      *t = model_time(m, B, H_Q, H_KV, L_K_max, h, sh, cus);
+      return sh;
+    };
+    double t_wide = 0.0, t_narrow = 0.0;
+    const int s_wide = best(hpt, &t_wide);
+    const int narrow = pack == 1 ? heads_per_tile(H_Q, H_KV, pack, kNarrowHeadsPerTile) : hpt;
+    const int s_narrow = narrow != hpt ? best(narrow, &t_narrow) : s_wide;
+    if (narrow != hpt && t_narrow < kSplitGain * t_wide) {
+      hpt = narrow;
+      s = s_narrow;
+    } else {
+      s = s_wide;
+    }
   }
   out->num_splits = s;
   out->pack_gqa = pack;
@@ -352,7 +379,7 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   if (!seq_lens) return fail(DA_ERR_NULL, "seq_lens is NULL");
   int rc = check_shape(B, H_Q, H_KV, L_K_max, d);
   if (rc) return rc;
-  if (pack_gqa < -1 || pack_gqa > 1) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1}", pack_gqa);
+  if (pack_gqa < -1 || pack_gqa > 2) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
   if (num_cus <= 0) return fail(DA_ERR_ARG, "num_cus=%d must be positive here", num_cus);
   if (cu_margin < 0 || cu_margin >= num_cus)
     return fail(DA_ERR_ARG, "cu_margin=%d must be in [0, %d)", cu_margin, num_cus);
@@ -362,8 +389,6 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   const int cus = num_cus - cu_margin;
   const int g = H_Q / H_KV;
   const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
-  const int hpt = heads_per_tile(H_Q, H_KV, pack);
-  const int tps = H_Q / hpt;
 
   std::vector<int64_t> T(B);
   int64_t t_max = 0;
@@ -371,32 +396,54 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
     T[b] = (seq_lens[b] + 31) / 32;
     if (T[b] > t_max) t_max = T[b];
   }
-  int64_t c = chunk_tiles;
   bool equal = true;
   for (int b = 1; b < B; ++b) equal = equal && seq_lens[b] == seq_lens[0];
-  if (c <= 0 && equal) {
-    // every sequence alike: the uniform plan's split count
-    const int s = t_max > 0 ? mi355x_splits(mi355x_model(), B, H_Q, H_KV, seq_lens[0], hpt, cus) : 1;
-    c = t_max > 0 ? (t_max + s - 1) / s : 1;
-  } else if (c <= 0) {
-    // Candidate chunks: the longest sequence cut into 1..64 pieces.  The
-    // fastest modelled one wins; on a tie, the longer chunk.
+  // Chunk length (in tiles) for head tiles of h heads, and its modelled
+  // time.  Equal lengths take the uniform plan's split count.  Otherwise the
+  // candidates are the longest sequence cut into 1..64 pieces; the fastest
+  // modelled one wins, on a tie the longer chunk.
+  auto choose_chunk = [&](int h, double* t) -> int64_t {
     const ScheduleModel& m = mi355x_schedule_model();
-    const StepCost step(m, hpt > 16 ? 1 : 0, cus);
-    c = t_max;
-    double best = schedule_time(m, step, T.data(), B, H_Q, hpt, c, cus);
+    const StepCost step(m, h > 16 ? 1 : 0, cus);
+    if (chunk_tiles > 0) {
+      *t = schedule_time(m, step, T.data(), B, H_Q, h, chunk_tiles, cus);
+      return chunk_tiles;
+    }
+    if (equal) {
+      const int s = t_max > 0 ? mi355x_splits(mi355x_model(), B, H_Q, H_KV, seq_lens[0], h, cus) : 1;
+      *t = model_time(mi355x_model(), B, H_Q, H_KV, seq_lens[0], h, s, cus);
+      return t_max > 0 ? (t_max + s - 1) / s : 1;
+    }
+    int64_t c = t_max;
+    double best = schedule_time(m, step, T.data(), B, H_Q, h, c, cus);
     int64_t prev = c;
     for (int s = 2; s <= kMaxSplits; ++s) {
       const int64_t cand = (t_max + s - 1) / s;
       if (cand == prev) continue;
       prev = cand;
-      const double ts = schedule_time(m, step, T.data(), B, H_Q, hpt, cand, cus);
+      const double ts = schedule_time(m, step, T.data(), B, H_Q, h, cand, cus);
       if (ts < best) {
         best = ts;
         c = cand;
       }
     }
+    *t = best;
+    return c;
+  };
+  // Packed groups wider than 16 heads: one wide tile or 16-head tiles, as in
+  // the uniform plan (narrow only when modelled at least 1% faster).
+  int hpt = heads_per_tile(H_Q, H_KV, pack);
+  double t_wide = 0.0, t_narrow = 0.0;
+  int64_t c = choose_chunk(hpt, &t_wide);
+  const int narrow = pack == 1 ? heads_per_tile(H_Q, H_KV, pack, kNarrowHeadsPerTile) : hpt;
+  if (narrow != hpt) {
+    const int64_t c_narrow = choose_chunk(narrow, &t_narrow);
+    if (t_narrow < kSplitGain * t_wide) {
+      hpt = narrow;
+      c = c_narrow;
+    }
   }
+  const int tps = H_Q / hpt;
 
   // Items and per-sequence rows.
   std::vector<int32_t> split(B), row0(B);
@@ -531,7 +578,8 @@ size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa) {
   if (B <= 0 || H_Q <= 0 || H_KV <= 0 || H_Q % H_KV != 0) return 0;
   const int g = H_Q / H_KV;
   const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
-  const int64_t tps = H_Q / da::heads_per_tile(H_Q, H_KV, pack);
+  // the narrowest head tile the scheduler may choose
+  const int64_t tps = H_Q / da::heads_per_tile(H_Q, H_KV, pack, da::kNarrowHeadsPerTile);
   return (size_t)B * tps * da::kMaxSplits * 16 + (size_t)B * 8;
 }
 

@@ -14,15 +14,21 @@ namespace da {
 constexpr int kHeadDim = DA_HEAD_DIM;
 constexpr int kMaxSplits = DA_MAX_SPLITS;
 constexpr int kMaxHeadsPerTile = 32;   // two 16-column MFMA head tiles per workgroup
+constexpr int kNarrowHeadsPerTile = 16; // one 16-column MFMA head tile per workgroup
 
 // Records a printf-style message for da_last_error() and returns `code`.
 int fail(int code, const char* fmt, ...);
 void clear_error();
 
 // Query heads one workgroup serves.  Packed: the whole GQA group of a KV head
-// when it fits in 32 columns, else the largest divisor of the group <= 32.
+// when it fits in `cap` columns, else the largest divisor of the group <= cap.
 // Unpacked: one.
-int heads_per_tile(int H_Q, int H_KV, int pack_gqa);
+int heads_per_tile(int H_Q, int H_KV, int pack_gqa, int cap = kMaxHeadsPerTile);
+
+// Whether a plan or schedule may serve `hpt` heads per workgroup in packing
+// mode `pack` (0: one head; 1: the whole group up to 32 heads, or tiles of
+// at most 16; 2: the whole group up to 32 heads).
+bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt);
 
 // First key of chunk i when L keys are cut into s balanced chunks.
 inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }

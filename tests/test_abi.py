@@ -59,7 +59,7 @@ def call_decode(lib, q=FAKE, k=FAKE, v=FAKE, cu=None, out=FAKE, lse=None, B=1, H
     (dict(L=1 << 22, H_KV=8), bnd.DA_ERR_SHAPE),
     (dict(d=64), bnd.DA_ERR_UNSUPPORTED),
     (dict(s=65), bnd.DA_ERR_SPLITS),
-    (dict(pack=2), bnd.DA_ERR_ARG),
+    (dict(pack=3), bnd.DA_ERR_ARG),
     (dict(pack=-2), bnd.DA_ERR_ARG),
     (dict(q=FAKE + 2), bnd.DA_ERR_ALIGN),
     (dict(k=FAKE + 8), bnd.DA_ERR_ALIGN),
@@ -194,10 +194,14 @@ def test_plan_fields_and_packing():
     assert p.grid == p.tiles * p.num_splits and p.num_cus == 256
     p = da.da_make_plan(1, 64, 8, 512, num_splits=4, pack_gqa=0, num_cus=256)
     assert (p.num_splits, p.pack_gqa, p.heads_per_tile, p.tiles, p.grid) == (4, 0, 1, 64, 256)
-    p = da.da_choose_splits(4, 32, 1, 256, num_cus=256)          # g = 32: one tile per KV head
-    assert p.heads_per_tile == 32 and p.tiles == 4
-    p = da.da_make_plan(2, 128, 2, 64, num_splits=1, pack_gqa=1, num_cus=256)  # g = 64 -> 2 tiles per KV head
-    assert p.heads_per_tile == 32 and p.tiles == 8
+    p = da.da_choose_splits(4, 32, 1, 256, num_cus=256)          # g = 32, 4 KV heads: two 16-head tiles each
+    assert p.heads_per_tile == 16 and p.tiles == 8
+    p = da.da_choose_splits(256, 32, 1, 2048, num_cus=256)       # g = 32 at full load: one tile per KV head
+    assert p.heads_per_tile == 32 and p.tiles == 256
+    p = da.da_make_plan(2, 128, 2, 64, num_splits=1, pack_gqa=1, num_cus=256)  # g = 64 -> 4 tiles per KV head
+    assert p.heads_per_tile == 16 and p.tiles == 16
+    p = da.da_make_plan(64, 128, 2, 8192, num_splits=1, pack_gqa=1, num_cus=256)  # -> 2 tiles per KV head
+    assert p.heads_per_tile == 32 and p.tiles == 256
     p = da.da_make_plan(1, 12, 4, 64, num_splits=1, pack_gqa=1, num_cus=256)   # g = 3
     assert p.heads_per_tile == 3 and p.tiles == 4
     p = da.da_choose_splits(1, 8, 8, 64, num_cus=256)              # MHA: nothing to pack
@@ -238,6 +242,38 @@ def test_mi355x_policy_properties():
         a = da.da_choose_splits(1, 64, 8, L, num_cus=256).num_splits
         b = da.da_choose_splits(1, 64, 8, L, num_cus=64).num_splits
         assert b <= a
+
+
+def test_head_tile_width():
+    # Packed groups wider than 16 heads: one 32-column tile, or 16-head tiles
+    # whose workgroups read the same keys; groups of at most 16 are never cut.
+    for B, H_Q, H_KV in [(1, 32, 1), (4, 32, 1), (32, 64, 2), (256, 32, 1), (2, 24, 1), (1, 128, 2), (1, 64, 8)]:
+        g = H_Q // H_KV
+        for L in (64, 512, 2048, 8192):
+            for policy in (da.POLICY_MI355X, da.POLICY_STREAMED):
+                p = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256, policy=policy)
+                assert g % p.heads_per_tile == 0 and p.heads_per_tile <= 32
+                assert p.tiles == B * H_Q // p.heads_per_tile
+                if g <= 16:
+                    assert p.heads_per_tile == g
+                else:
+                    assert p.heads_per_tile in (min(g, 32) if g % min(g, 32) == 0 else 16, 16 if g % 16 == 0 else 12)
+    # pack_gqa = 2 forces the whole group into one tile
+    p = da.da_make_plan(1, 32, 1, 512, num_splits=0, pack_gqa=2, num_cus=256)
+    assert (p.pack_gqa, p.heads_per_tile, p.tiles) == (2, 32, 1)
+    p = da.da_make_plan(1, 128, 2, 512, num_splits=2, pack_gqa=2, num_cus=256)
+    assert (p.heads_per_tile, p.tiles, p.num_splits) == (32, 4, 2)
+    # the paper's policies keep its packing: the whole group in one tile
+    assert da.da_choose_splits(1, 32, 1, 512, num_cus=256, policy=da.POLICY_PAPER).heads_per_tile == 32
+    assert da.da_choose_splits(1, 32, 1, 512, num_cus=256, policy=da.POLICY_EVOLVED).heads_per_tile == 32
+    # g = 24: a 24-head tile or two of 12
+    assert da.da_choose_splits(1, 24, 1, 512, num_cus=256).heads_per_tile == 12
+    # per-sequence schedules choose the same way, and their metadata bound covers the narrow tile
+    sched, meta = da.da_make_schedule([300, 40, 511], H_Q=32, H_KV=1, num_cus=256)
+    assert sched.heads_per_tile == 16 and sched.tiles == 6
+    assert meta.numel() <= da.da_schedule_max_bytes(3, 32, 1, 1)
+    sched, _ = da.da_make_schedule([2048] * 255 + [1024], H_Q=32, H_KV=1, num_cus=256)
+    assert sched.heads_per_tile == 32
 
 
 def test_cu_margin_and_plan_errors():

@@ -52,7 +52,7 @@ def check_paged(inp, page, variants, what, seed=0, max_pages=None):
         check_lse(lse_t, lse)
 
 
-VARIANTS = [(0, -1), (1, 1), (3, 1), (16, 1), (64, 1), (1, 0), (5, 0)]
+VARIANTS = [(0, -1), (1, 1), (3, 1), (16, 1), (64, 1), (1, 0), (5, 0), (2, 2)]
 
 
 @pytest.mark.parametrize("page", [32, 64, 96, 256])
@@ -76,7 +76,7 @@ def test_workload_shapes_paged(shape):
 def test_ragged_paged(B, H_Q, H_KV, lengths, page):
     sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
     inp = make_inputs(sh, seed=B * 100 + page, lengths=lengths)
-    check_paged(inp, page, [(1, 1), (2, 1), (7, 1), (64, 1), (3, 0), (0, -1)],
+    check_paged(inp, page, [(1, 1), (2, 1), (7, 1), (64, 1), (3, 0), (0, -1), (1, 2), (4, 2)],
                 f"B{B}-H{H_Q}-KV{H_KV}-{lengths}", seed=page + 1)
 
 

@@ -15,7 +15,7 @@ from tests.gpu_helpers import assert_parity, dev_inputs, errors, say, to_dev, to
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = [(0, -1), (1, 1), (1, 0), (2, 1), (3, 1), (4, 1), (8, 1), (16, 1), (64, 1), (4, 0), (64, 0)]
+VARIANTS = [(0, -1), (1, 1), (1, 0), (2, 1), (3, 1), (4, 1), (8, 1), (16, 1), (64, 1), (4, 0), (64, 0), (1, 2), (6, 2)]
 LSE_TOL = 1e-3
 
 
@@ -127,8 +127,25 @@ def test_empty_and_short_sequences():
 ])
 def test_group_and_ragged_shapes(B, H_Q, H_KV, L):
     sh = custom_shape(B, H_Q, H_KV, L)
-    check_case(make_inputs(sh, seed=B * 1000 + L), [(1, 1), (3, 1), (17, 1), (2, 0), (0, -1)],
+    check_case(make_inputs(sh, seed=B * 1000 + L), [(1, 1), (3, 1), (17, 1), (2, 0), (0, -1), (1, 2), (5, 2)],
                f"B{B}-H{H_Q}-KV{H_KV}-L{L}")
+
+
+@pytest.mark.parametrize("B,H_Q,H_KV,L", [(1, 32, 1, 512), (2, 64, 2, 129), (1, 128, 2, 70), (1, 48, 2, 200)])
+def test_tile_width_does_not_change_results(B, H_Q, H_KV, L):
+    """A packed group served by one wide workgroup (pack_gqa=2) or by
+    16-head workgroups (what pack_gqa=1 picks at these sizes) computes every
+    head column with the same operations in the same order."""
+    sh = custom_shape(B, H_Q, H_KV, L)
+    inp = make_inputs(sh, seed=29 + L)
+    q, k, v, cu = dev_inputs(inp)
+    for s in (1, 3):
+        assert da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=1).heads_per_tile <= 16
+        say(f"width B{B}-H{H_Q}-KV{H_KV}-L{L} s={s}")
+        a, la = run(q, k, v, cu, L, s, 1)
+        b, lb = run(q, k, v, cu, L, s, 2)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+        assert torch.equal(la, lb)
 
 
 def test_softmax_scale_argument():

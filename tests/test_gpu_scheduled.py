@@ -82,12 +82,13 @@ def test_fixed_layout_scheduled(shape):
     (2, 12, 4, [300, 95]),                    # group of 3
     (1, 8, 1, [9000]),                        # a single long sequence: up to 64 chunks
     (2, 66, 2, [130, 700]),                   # group of 33: three head tiles of 11 per KV head
+    (3, 32, 1, [300, 40, 511]),               # group of 32: 16-head tiles, or one tile with pack_gqa=2
 ])
 @pytest.mark.parametrize("page", [None, 32])
 def test_ragged_scheduled(B, H_Q, H_KV, lengths, page):
     sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
     inp = make_inputs(sh, seed=B * 10 + H_Q, lengths=lengths)
-    check_inputs(inp, f"B{B}-H{H_Q}-KV{H_KV}-{lengths}", page=page)
+    check_inputs(inp, f"B{B}-H{H_Q}-KV{H_KV}-{lengths}", page=page, packs=(-1, 2) if H_Q // H_KV > 16 else (-1,))
 
 
 def test_cu_margin_schedule():

@@ -163,13 +163,32 @@ def test_schedule_errors():
     assert call(lens, 3, 8, 1, 29, 128, -1, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_SHAPE   # a length > L_K_max
     assert call(lens, 3, 8, 3, 30, 128, -1, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_SHAPE   # H_Q % H_KV
     assert call(lens, 3, 8, 1, 30, 64, -1, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_UNSUPPORTED
-    assert call(lens, 3, 8, 1, 30, 128, 2, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_ARG
+    assert call(lens, 3, 8, 1, 30, 128, 3, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_ARG
     assert call(lens, 3, 8, 1, 30, 128, -1, CUS, CUS, 0, buf, 4096) == bnd.DA_ERR_ARG   # cu_margin
     assert call(lens, 3, 8, 1, 30, 128, -1, CUS, 0, 0, buf, 8) == bnd.DA_ERR_WORKSPACE
     assert out.meta_bytes == 3 * 16 + 3 * 8          # the size needed is reported
     assert call(lens, 3, 8, 1, 30, 128, -1, CUS, 0, 0, buf, out.meta_bytes) == bnd.DA_OK
     neg = (ctypes.c_int32 * 1)(-1)
     assert call(neg, 1, 8, 1, 30, 128, -1, CUS, 0, 0, buf, 4096) == bnd.DA_ERR_SHAPE
+
+
+def test_schedule_head_tile_width_checked():
+    # g = 32 at short lengths: 16-head tiles; the launch accepts them (it gets
+    # past the schedule check to the NULL output) and rejects widths the
+    # packing mode cannot produce
+    lib = da.load()
+    s, _ = da.da_make_schedule([300, 40, 511], 32, 1, num_cus=CUS)
+    assert (s.pack_gqa, s.heads_per_tile, s.tiles) == (1, 16, 6)
+    need = da.da_schedule_workspace_bytes(s)
+    assert scheduled(lib, s, out=None, ws=FAKE, ws_bytes=need) == bnd.DA_ERR_NULL
+    for pack, hpt in ((1, 8), (2, 16), (0, 16)):
+        bad = bnd.DaSchedule.from_buffer_copy(s)
+        bad.pack_gqa, bad.heads_per_tile = pack, hpt
+        assert scheduled(lib, bad, out=None, ws=FAKE, ws_bytes=need) == bnd.DA_ERR_ARG, (pack, hpt)
+    # pack_gqa = 2 keeps the whole group in one tile
+    w, _ = da.da_make_schedule([300, 40, 511], 32, 1, num_cus=CUS, pack_gqa=2)
+    assert (w.pack_gqa, w.heads_per_tile, w.tiles) == (2, 32, 3)
+    assert scheduled(lib, w, out=None, ws=FAKE, ws_bytes=da.da_schedule_workspace_bytes(w)) == bnd.DA_ERR_NULL
 
 
 def test_schedule_workspace_bytes():
