@@ -202,17 +202,25 @@ def small_configs_run(args, da, torch, dev) -> dict:
             log(f"timing {sh.name}")
             hv = Variant("h", da, torch, q, k, v, L, 0, -1, args.steps, cu=cu)
             fixed = [Variant(str(s), da, torch, q, k, v, L, s, 1, args.steps, cu=cu) for s in sweep if s <= max(L, 1)]
-            interleave(torch, [hv] + fixed, args.rounds)
+            # groups of more than 16 heads: one split with the whole group in one workgroup (the
+            # paper's packing), against which the planner's choice of 16-head tiles is measured
+            whole = ([Variant("w", da, torch, q, k, v, L, 1, 2, args.steps, cu=cu)]
+                     if sh.H_Q // sh.H_KV > 16 else [])
+            interleave(torch, [hv] + fixed + whole, args.rounds)
             sw = {x.plan.num_splits: round(x.median, 3) for x in fixed}
             best = min(sw, key=sw.get)
             nbytes = ab(sh.B, sh.H_Q, sh.H_KV, int(inp.lengths.sum()), varlen=cu is not None)
             gbs = nbytes / (hv.median * 1e-6) / 1e9
             res[sh.name] = {"config": cid, "B": sh.B, "H_Q": sh.H_Q, "H_KV": sh.H_KV, "L_K": L,
                             "heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
+                            "heads_per_tile": hv.plan.heads_per_tile,
                             "s1_us": sw[1], "speedup_vs_s1": round(sw[1] / hv.median, 3), "best_fixed": best,
                             "best_fixed_us": sw[best], "vs_best_fixed": round(hv.median / sw[best], 3),
                             "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 5), "sweep_us": sw}
-            del q, k, v, hv, fixed
+            if whole:
+                res[sh.name]["s1_whole_group_us"] = round(whole[0].median, 3)
+                res[sh.name]["speedup_vs_s1_whole_group"] = round(whole[0].median / hv.median, 3)
+            del q, k, v, hv, fixed, whole
     return res
 
 
