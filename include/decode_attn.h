@@ -39,6 +39,11 @@ extern "C" {
 
 #define DA_HEAD_DIM 128
 #define DA_MAX_SPLITS 64
+/* K/V bytes per call above which the planner marks K/V loads nontemporal:
+ * MI355X's 256 MiB MALL plus 8 x 4 MiB of L2.  A call reading more cannot
+ * find its K/V resident on the next call, and streaming hints then raise
+ * the sustained HBM read rate. */
+#define DA_RESIDENT_BYTES (288ull << 20)
 
 typedef enum da_status {
   DA_OK = 0,
@@ -86,6 +91,9 @@ typedef struct da_plan {
                              wave); 1 both row-contiguous into registers, then through LDS (several
                              workgroups per CU); 2 both row-contiguous straight into LDS, two tiles
                              in flight per wave (at most one workgroup per CU) */
+  int32_t kv_nontemporal; /* 1: K/V loads carry the nontemporal (streaming) cache hint, chosen when
+                             one call's K/V exceed DA_RESIDENT_BYTES and cannot stay in L2 and the
+                             MALL between calls; 0: ordinary loads */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
@@ -194,7 +202,7 @@ typedef struct da_schedule {
   int32_t kv_fetch;              /* as in da_plan */
   int32_t seq_offset;            /* byte offset of the per-sequence table in the metadata */
   int32_t meta_bytes;            /* metadata bytes written */
-  int32_t reserved;
+  int32_t kv_nontemporal;        /* as in da_plan, for the K/V of all B sequences */
 } da_schedule;
 
 /* Upper bound on the metadata bytes da_make_schedule writes for this shape

@@ -54,6 +54,7 @@ class DaPlan(ctypes.Structure):
         ("num_cus", ctypes.c_int32),
         ("group_waves", ctypes.c_int32),
         ("kv_fetch", ctypes.c_int32),
+        ("kv_nontemporal", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -63,7 +64,7 @@ class DaPlan(ctypes.Structure):
 class DaSchedule(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "B", "H_Q", "H_KV", "L_K_max", "pack_gqa", "heads_per_tile", "tiles", "num_items", "chunk_tiles",
-        "max_splits", "state_rows", "num_cus", "kv_fetch", "seq_offset", "meta_bytes", "reserved")]
+        "max_splits", "state_rows", "num_cus", "kv_fetch", "seq_offset", "meta_bytes", "kv_nontemporal")]
 
     def as_dict(self) -> dict:
         return {name: int(getattr(self, name)) for name, _ in self._fields_}

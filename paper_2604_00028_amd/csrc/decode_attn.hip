@@ -190,10 +190,13 @@ constexpr int kMinWaves = (NT == 1 && FETCH == 0) ? 3 : 2;
 // page).  SCH: per-sequence schedule (p.work lists every workgroup's head
 // tile, 32-key tile range and chunk-state row).  Both are template
 // parameters so that the uniform launch waits on no extra argument.
-template <int NT, int W, int FETCH, bool PG, bool SCH>
+template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(kMinWaves<NT, FETCH>, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  // NTL: K/V loads carry the nontemporal hint (the cache-policy field of
+  // the buffer instructions), for launches whose K/V cannot stay resident
+  constexpr int kv_aux = NTL ? 2 : 0;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -360,15 +363,15 @@ split_partial_kernel(Params p) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, voff[4 * mt + j], 0, 0);
+        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, voff[4 * mt + j], 0, kv_aux);
     } else {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, 0);
+        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, kv_aux);
     }
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, 0);
+    for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, kv_aux);
   };
 
   // S^T[16 keys x 16 heads] per (mt, nt) from the tile's 8 K operands.
@@ -556,10 +559,10 @@ split_partial_kernel(Params p) {
       unsigned char* vs = ks + kLdsTileBytes;
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0, kv_aux);
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0, kv_aux);
     };
     // Operand reads.  K operand (mt, j), lane (col, quad): key 16mt + col is
     // row col%4 of block 4mt + col/4, dims [32j + 8quad, +8) are its chunk
@@ -848,22 +851,28 @@ int ensure_gfx950(int* cus) {
   return DA_OK;
 }
 
-template <int NT, int W, int FETCH, bool PG, bool SCH>
+template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG, SCH>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG, SCH, NTL>);
 }
 
-template <bool PG, bool SCH>
+template <bool PG, bool SCH, bool NTL>
 const void* pick_kernel(int NT, int FETCH) {
   switch (FETCH * 2 + NT - 1) {
-    case 0: return kernel_ptr<1, 4, kFetchDirect, PG, SCH>();
-    case 1: return kernel_ptr<2, 4, kFetchDirect, PG, SCH>();
-    case 2: return kernel_ptr<1, 4, kFetchStaged, PG, SCH>();
-    case 3: return kernel_ptr<2, 4, kFetchStaged, PG, SCH>();
-    case 4: return kernel_ptr<1, 4, kFetchLds, PG, SCH>();
-    case 5: return kernel_ptr<2, 4, kFetchLds, PG, SCH>();
+    case 0: return kernel_ptr<1, 4, kFetchDirect, PG, SCH, NTL>();
+    case 1: return kernel_ptr<2, 4, kFetchDirect, PG, SCH, NTL>();
+    case 2: return kernel_ptr<1, 4, kFetchStaged, PG, SCH, NTL>();
+    case 3: return kernel_ptr<2, 4, kFetchStaged, PG, SCH, NTL>();
+    case 4: return kernel_ptr<1, 4, kFetchLds, PG, SCH, NTL>();
+    case 5: return kernel_ptr<2, 4, kFetchLds, PG, SCH, NTL>();
     default: return nullptr;
   }
+}
+
+template <bool NTL>
+const void* pick_kernel(bool paged, bool scheduled, int NT, int FETCH) {
+  return paged ? (scheduled ? pick_kernel<true, true, NTL>(NT, FETCH) : pick_kernel<true, false, NTL>(NT, FETCH))
+               : (scheduled ? pick_kernel<false, true, NTL>(NT, FETCH) : pick_kernel<false, false, NTL>(NT, FETCH));
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
@@ -871,9 +880,11 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
   const int FETCH = pl.kv_fetch;
   if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
-  const void* fn = prm.block_table
-                       ? (prm.work ? pick_kernel<true, true>(NT, FETCH) : pick_kernel<true, false>(NT, FETCH))
-                       : (prm.work ? pick_kernel<false, true>(NT, FETCH) : pick_kernel<false, false>(NT, FETCH));
+  if (pl.kv_nontemporal != 0 && pl.kv_nontemporal != 1)
+    return da::fail(DA_ERR_ARG, "plan asks for K/V cache hint %d", pl.kv_nontemporal);
+  const bool paged = prm.block_table != nullptr, scheduled = prm.work != nullptr;
+  const void* fn = pl.kv_nontemporal ? pick_kernel<true>(paged, scheduled, NT, FETCH)
+                                     : pick_kernel<false>(paged, scheduled, NT, FETCH);
   if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
@@ -1077,6 +1088,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
       sched->tiles != B * (H_Q / hpt) || sched->num_items < sched->tiles ||
       (int64_t)sched->num_items > (int64_t)sched->tiles * DA_MAX_SPLITS || sched->max_splits < 1 ||
       sched->max_splits > DA_MAX_SPLITS || sched->state_rows < 0 || sched->kv_fetch < 0 || sched->kv_fetch > 2 ||
+      sched->kv_nontemporal < 0 || sched->kv_nontemporal > 1 ||
       (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 || (sched->max_splits > 1) != (sched->state_rows > 0))
     return da::fail(DA_ERR_ARG, "schedule does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   (void)g;
@@ -1114,6 +1126,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
   pl.num_cus = sched->num_cus;
   pl.group_waves = 4;
   pl.kv_fetch = sched->kv_fetch;
+  pl.kv_nontemporal = sched->kv_nontemporal;
   fill_params(p, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   p.xcd_group = 0;  // the schedule orders its workgroups itself
   p.work = static_cast<const int32_t*>(meta_dev);

@@ -276,6 +276,22 @@ def test_head_tile_width():
     assert sched.heads_per_tile == 32
 
 
+def test_streaming_hint_follows_cache_capacity():
+    # K/V loads are marked nontemporal only when one call's K/V (512 bytes
+    # per key and KV head) exceed the 288 MiB of MALL and L2
+    limit = 288 << 20
+    for B, L in [(1, 512), (8, 8192), (9, 8192), (32, 8192)]:
+        for s in (0, 1, 4):
+            p = da.da_make_plan(B, 64, 8, L, num_splits=s, pack_gqa=-1, num_cus=256)
+            assert p.kv_nontemporal == int(B * L * 8 * 512 > limit), (B, L, s)
+    p = da.da_make_plan(64, 32, 1, 16384, num_splits=1, pack_gqa=2, num_cus=256)
+    assert p.kv_nontemporal == 1
+    # schedules count the keys the sequences actually hold
+    small, _ = da.da_make_schedule([8192] * 8, 64, 8, num_cus=256)
+    big, _ = da.da_make_schedule([8192] * 8 + [4096] * 4, 64, 8, num_cus=256)
+    assert (small.kv_nontemporal, big.kv_nontemporal) == (0, 1)
+
+
 def test_cu_margin_and_plan_errors():
     p = da.da_choose_splits(1, 8, 1, 4096, num_cus=256, cu_margin=200)
     assert p.num_cus == 56

@@ -55,13 +55,32 @@ def test_highload_parity_sampled_sequences():
     picks = [0, 13, 31]
     O, lse = decode_attention(inp.q[picks], inp.k[picks], inp.v[picks])
     plan = da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
-    for s, pack in [(0, -1), (1, 1), (plan.num_splits, 1), (4, 1), (16, 1)]:
+    assert plan.kv_nontemporal == 1          # 1 GiB of K/V: streaming loads
+    for s, pack in [(0, -1), (1, 1), (plan.num_splits, 1), (4, 1), (16, 1), (64, 1), (8, 0)]:
         say(f"highload s={s} pack={pack}")
         out, lse_t = run(q, k, v, cu, sh.L_K, s, pack)
         assert_parity(out[picks], O, f"highload s={s}")
         assert np.max(np.abs(lse_t.cpu().numpy()[picks] - lse)) <= LSE_TOL
         # every sequence is finite, not only the sampled ones
         assert torch.isfinite(out.float()).all()
+
+
+def test_streaming_wide_group_sampled_sequences():
+    """537 MB of K/V (streaming loads) with groups of 32 heads in one
+    workgroup (two 16-column tiles), through each K/V fetch path; the oracle
+    computes three sampled sequences."""
+    sh = custom_shape(64, 32, 1, 16384)
+    inp = make_inputs(sh, seed=41)
+    q, k, v, cu = dev_inputs(inp)
+    picks = [0, 37, 63]
+    O, lse = decode_attention(inp.q[picks], inp.k[picks], inp.v[picks])
+    for s in (1, 8, 64):
+        p = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, num_splits=s, pack_gqa=2)
+        assert p.kv_nontemporal == 1 and p.heads_per_tile == 32
+        say(f"streaming wide s={s} fetch={p.kv_fetch}")
+        out, lse_t = run(q, k, v, cu, sh.L_K, s, 2)
+        assert_parity(out[picks], O, f"streaming wide s={s}")
+        assert np.max(np.abs(lse_t.cpu().numpy()[picks] - lse)) <= LSE_TOL
 
 
 @pytest.mark.parametrize("s,pack", [(1, 1), (2, 1), (64, 1), (1, 0), (7, 0)])

@@ -122,6 +122,43 @@ def test_scheduled_equals_uniform_when_cuts_coincide(s, pack):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+@pytest.mark.parametrize("page", [None, 32])
+@pytest.mark.parametrize("B,H_Q,H_KV,lengths,c", [
+    (4, 8, 1, [0, 1, 1000, 33], 0),
+    (3, 128, 2, [700, 2100, 3], 2),
+    (2, 12, 4, [300, 95], 40),
+    (3, 32, 1, [300, 40, 511], 1),
+])
+def test_scheduled_streaming_hint_same_bits(B, H_Q, H_KV, lengths, c, page):
+    """The nontemporal K/V hint (set by the scheduler only past the cache's
+    capacity, forced on here) changes how lines are cached, never a
+    result: the same bits as without it, on every K/V fetch path the
+    schedule picks."""
+    sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
+    inp = make_inputs(sh, seed=B * 7 + H_Q, lengths=lengths)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    kw = dict(cu_seqlens_k=cu)
+    if page is not None:
+        pg = paged_layout(inp, page, seed=page)
+        k, v = to_dev(pg.k_cache), to_dev(pg.v_cache)
+        kw = dict(block_table=torch.from_numpy(pg.block_table).cuda(), seq_lens=torch.from_numpy(pg.seq_lens).cuda())
+    sched, meta = da.da_make_schedule(lengths, H_Q, H_KV, max(lengths), chunk_tiles=c)
+    assert sched.kv_nontemporal == 0
+    meta_dev = meta.cuda()
+    outs = []
+    for hint in (0, 1):
+        sched.kv_nontemporal = hint
+        say(f"scheduled hint={hint} B{B}-H{H_Q}-KV{H_KV} chunk={c} page={page} fetch={sched.kv_fetch}")
+        lse_t = torch.empty(B, H_Q, dtype=torch.float32, device="cuda")
+        outs.append((da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, lse_out=lse_t, **kw), lse_t))
+        torch.cuda.synchronize()
+    assert_parity(outs[1][0], O, "streaming hint")
+    check_lse(outs[1][1], lse)
+    assert torch.equal(outs[0][0].view(torch.int16), outs[1][0].view(torch.int16))
+    assert torch.equal(outs[0][1], outs[1][1])
+
+
 @pytest.mark.parametrize("c", [0, 3])
 def test_scheduled_bit_identical_repeats(c):
     sh = config_shapes(4)[0]

@@ -224,7 +224,8 @@ def test_scheduled_argument_errors():
     assert scheduled(lib, s, bt=FAKE, sl=FAKE, page=64, mp=2, ws=FAKE, ws_bytes=need) == bnd.DA_ERR_SHAPE
     # a schedule that does not describe this launch
     for field, val in (("tiles", 3), ("heads_per_tile", 4), ("max_splits", 65), ("num_items", 1),
-                       ("seq_offset", 0), ("state_rows", 0), ("kv_fetch", 3), ("pack_gqa", 5)):
+                       ("seq_offset", 0), ("state_rows", 0), ("kv_fetch", 3), ("pack_gqa", 5),
+                       ("kv_nontemporal", 2), ("kv_nontemporal", -1)):
         bad = bnd.DaSchedule.from_buffer_copy(s)
         setattr(bad, field, val)
         assert scheduled(lib, bad, ws=FAKE, ws_bytes=need) == bnd.DA_ERR_ARG, field
