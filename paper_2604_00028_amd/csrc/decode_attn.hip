@@ -363,12 +363,14 @@ split_partial_kernel(Params p) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, voff[4 * mt + j], 0, kv_aux);
+        for (int j = 0; j < 4; ++j)
+          kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, voff[4 * mt + j], 0, kv_aux);
     } else {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, kv_aux);
+        for (int j = 0; j < 4; ++j)
+          kreg[mt][j] = __builtin_amdgcn_raw_buffer_load_b128(kt, koff[mt] + 64u * j, 0, kv_aux);
     }
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) vreg[jj] = __builtin_amdgcn_raw_buffer_load_b128(vt, voff[jj], 0, kv_aux);
@@ -559,10 +561,12 @@ split_partial_kernel(Params p) {
       unsigned char* vs = ks + kLdsTileBytes;
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0, kv_aux);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0,
+                                                 kv_aux);
 #pragma unroll
       for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0, kv_aux);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0,
+                                                 kv_aux);
     };
     // Operand reads.  K operand (mt, j), lane (col, quad): key 16mt + col is
     // row col%4 of block 4mt + col/4, dims [32j + 8quad, +8) are its chunk
@@ -1089,7 +1093,8 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
       (int64_t)sched->num_items > (int64_t)sched->tiles * DA_MAX_SPLITS || sched->max_splits < 1 ||
       sched->max_splits > DA_MAX_SPLITS || sched->state_rows < 0 || sched->kv_fetch < 0 || sched->kv_fetch > 2 ||
       sched->kv_nontemporal < 0 || sched->kv_nontemporal > 1 ||
-      (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 || (sched->max_splits > 1) != (sched->state_rows > 0))
+      (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 ||
+      (sched->max_splits > 1) != (sched->state_rows > 0))
     return da::fail(DA_ERR_ARG, "schedule does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   (void)g;
   if (!meta_dev) return da::fail(DA_ERR_NULL, "meta_dev must be non-NULL");
