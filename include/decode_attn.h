@@ -93,7 +93,8 @@ typedef struct da_plan {
                              in flight per wave (at most one workgroup per CU) */
   int32_t kv_nontemporal; /* 1: K/V loads carry the nontemporal (streaming) cache hint, chosen when
                              one call's K/V exceed DA_RESIDENT_BYTES and cannot stay in L2 and the
-                             MALL between calls; 0: ordinary loads */
+                             MALL between calls, and one workgroup reads each key (heads_per_tile
+                             = H_Q/H_KV); 0: ordinary loads */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split

@@ -176,12 +176,14 @@ int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
   return tiles_per_wave >= 2 ? 1 : 0;
 }
 
-int kv_nontemporal(double key_rows) {
+int kv_nontemporal(double key_rows, int readers) {
   // Measured on MI355X (1 GiB of K/V at high load: 185 -> 160 us with the
   // hint; 537 MB: 103 -> 88 us).  Below the MALL's capacity the hint costs
   // what residency between calls saves (268 MB: 46 -> 48 us; 134 MB with 64
-  // workgroups: 26.2 -> 26.8 us), so it is off there.
-  return key_rows * (2.0 * kHeadDim * 2.0) > (double)DA_RESIDENT_BYTES ? 1 : 0;
+  // workgroups: 26.2 -> 26.8 us; 16-64 MB: up to 40%), so it is off there.
+  // When several workgroups read the same keys (head tiles narrower than
+  // the group), the later ones find them in L2 only without the hint.
+  return readers == 1 && key_rows * (2.0 * kHeadDim * 2.0) > (double)DA_RESIDENT_BYTES ? 1 : 0;
 }
 
 int check_shape(int B, int H_Q, int H_KV, int L_K_max, int d) {
@@ -259,7 +261,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
     out->kv_fetch = kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
   }
-  out->kv_nontemporal = kv_nontemporal((double)B * L_K_max * H_KV);
+  out->kv_nontemporal = kv_nontemporal((double)B * L_K_max * H_KV, g / hpt);
   return DA_OK;
 }
 
@@ -492,7 +494,7 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   {
     double key_rows = 0.0;
     for (int b = 0; b < B; ++b) key_rows += (double)seq_lens[b] * H_KV;
-    out->kv_nontemporal = kv_nontemporal(key_rows);
+    out->kv_nontemporal = kv_nontemporal(key_rows, g / hpt);
   }
   if (!meta) return fail(DA_ERR_NULL, "meta is NULL");
   if (meta_bytes < need)

@@ -70,9 +70,10 @@ constexpr int kLoneFetch = 2;
 int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave);
 
 // Whether a launch reading `key_rows` key rows of one KV head (K and V,
-// 512 bytes each) marks its K/V loads nontemporal (da_plan.kv_nontemporal):
-// only when they exceed DA_RESIDENT_BYTES.
-int kv_nontemporal(double key_rows);
+// 512 bytes each), each row read by `readers` workgroups (the head tiles of
+// one group), marks its K/V loads nontemporal (da_plan.kv_nontemporal): only
+// when they exceed DA_RESIDENT_BYTES and one workgroup reads each row.
+int kv_nontemporal(double key_rows, int readers);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);

@@ -286,6 +286,15 @@ def test_streaming_hint_follows_cache_capacity():
             assert p.kv_nontemporal == int(B * L * 8 * 512 > limit), (B, L, s)
     p = da.da_make_plan(64, 32, 1, 16384, num_splits=1, pack_gqa=2, num_cus=256)
     assert p.kv_nontemporal == 1
+    # several workgroups reading each key (packing off, or tiles narrower than
+    # the group): the later readers need the keys kept in L2
+    p = da.da_make_plan(32, 64, 8, 8192, num_splits=1, pack_gqa=0, num_cus=256)
+    assert p.kv_nontemporal == 0
+    for B in (64, 128, 256):
+        p = da.da_make_plan(B, 32, 1, 16384, num_splits=0, pack_gqa=1, num_cus=256)
+        assert p.kv_nontemporal == int(p.heads_per_tile == 32), p.as_dict()
+    p = da.da_make_plan(16, 128, 2, 8192, num_splits=0, pack_gqa=2, num_cus=256)   # g = 64: two 32-head tiles
+    assert p.heads_per_tile == 32 and p.kv_nontemporal == 0
     # schedules count the keys the sequences actually hold
     small, _ = da.da_make_schedule([8192] * 8, 64, 8, num_cus=256)
     big, _ = da.da_make_schedule([8192] * 8 + [4096] * 4, 64, 8, num_cus=256)
