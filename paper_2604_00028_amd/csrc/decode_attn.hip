@@ -103,6 +103,25 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 enum Mode : int { kDirect = 0, kPartials = 1 };
 
+// Division by a launch constant d >= 1 as a multiply and a shift
+// (Granlund and Montgomery, PLDI 1994, Theorem 4.2 with N = 32): with
+// l = ceil(log2 d) and m = ceil(2^(32+l) / d) - 2^32, x / d = (x +
+// mulhi(x, m)) >> l for every x < 2^32; for x < 2^31, the only numerators
+// here, the sum does not overflow.  The host computes (m, l) once per launch.
+struct Div {
+  uint32_t m, l;
+};
+
+Div make_div(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  return Div{(uint32_t)((((1ull << (32 + l)) + d - 1) / d) - (1ull << 32)), l};
+}
+
+__device__ __forceinline__ int div_by(int x, Div d) {
+  return (int)(((uint32_t)x + __umulhi((uint32_t)x, d.m)) >> d.l);
+}
+
 struct Params {
   const uint16_t* q;
   const uint16_t* k;
@@ -116,10 +135,12 @@ struct Params {
   const int32_t* block_table;  // paged layout: [B, max_pages] page ids
   const int32_t* seq_lens;     // paged layout: [B] sequence lengths
   int page_size, max_pages, num_pages;
+  Div div_page;         // page_size
   const int32_t* work;  // nullable: per-sequence schedule, int32x4 {tile, first, end, state row} per workgroup
   int state_rows;       // chunk-state rows of the schedule
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
   int xcd_group;        // 1: consecutive tiles share an XCD (packing off)
+  Div div_s, div_tps, div_g;  // s, tiles_per_seq, g
   float scale_log2;     // softmax scale * log2(e)
 };
 
@@ -216,12 +237,12 @@ split_partial_kernel(Params p) {
   } else {
     const int nwg = p.tiles * p.s;
     const int logical = (p.xcd_group && nwg % 8 == 0) ? (bid % 8) * (nwg / 8) + bid / 8 : bid;
-    tile = logical / p.s;
+    tile = div_by(logical, p.div_s);
     split = logical - tile * p.s;
   }
-  const int b = tile / p.tiles_per_seq;
+  const int b = div_by(tile, p.div_tps);
   const int head0 = (tile - b * p.tiles_per_seq) * p.hpt;
-  const int kvh = head0 / p.g;
+  const int kvh = div_by(head0, p.div_g);
 
   int64_t row0 = 0;
   int L;
@@ -248,8 +269,8 @@ split_partial_kernel(Params p) {
       t0 = f < T ? f : T;
       nt = (e < T ? e : T) > t0 ? (e < T ? e : T) - t0 : 0u;
     } else {
-      t0 = T * (uint32_t)split / (uint32_t)p.s;
-      nt = T * (uint32_t)(split + 1) / (uint32_t)p.s - t0;
+      t0 = (uint32_t)div_by((int)(T * (uint32_t)split), p.div_s);
+      nt = (uint32_t)div_by((int)(T * (uint32_t)(split + 1)), p.div_s) - t0;
     }
     key_lo = kKeysPerTile * (int)(t0 + nt * (uint32_t)wave / W);
     key_hi = kKeysPerTile * (int)(t0 + nt * (uint32_t)(wave + 1) / W);
@@ -258,8 +279,8 @@ split_partial_kernel(Params p) {
   } else {
     // L < 2^23 (one sequence's K spans < 2 GiB) and split < 64, so the
     // products fit 32 bits and the divisions stay 32-bit
-    const int c0 = (int)(((uint32_t)L * (uint32_t)split) / (uint32_t)p.s);
-    const int c1 = (int)(((uint32_t)L * (uint32_t)(split + 1)) / (uint32_t)p.s);
+    const int c0 = div_by(L * split, p.div_s);
+    const int c1 = div_by(L * (split + 1), p.div_s);
     const int n = c1 - c0;
     key_lo = c0 + (int)(((uint32_t)n * (uint32_t)wave) / W);
     key_hi = c0 + (int)(((uint32_t)n * (uint32_t)(wave + 1)) / W);
@@ -277,8 +298,8 @@ split_partial_kernel(Params p) {
   int pg_first = 0, pg_last = -1, pg_win = 0, pg_ids = 0;
   if constexpr (PG) {
     if (key_hi > key_lo) {
-      pg_first = key_lo / p.page_size;
-      pg_last = (key_hi - 1) / p.page_size;
+      pg_first = div_by(key_lo, p.div_page);
+      pg_last = div_by(key_hi - 1, p.div_page);
     }
     pg_win = pg_first;
     const int j = pg_win + lane;
@@ -290,7 +311,7 @@ split_partial_kernel(Params p) {
     const int rows = key_hi - first;
     bytes = (uint32_t)__builtin_amdgcn_readfirstlane(rows > 0 ? (uint32_t)rows * rs : 0u);
     if constexpr (PG) {
-      const int j = first / p.page_size;
+      const int j = div_by(first, p.div_page);
       if (j - pg_win >= 64 && rows > 0) {  // next window of page ids (wave-uniform)
         pg_win = j;
         const int jj = pg_win + lane;
@@ -300,7 +321,7 @@ split_partial_kernel(Params p) {
       // a page id outside the cache reads as zero keys and values
       if (page < 0 || page >= p.num_pages) bytes = 0u;
       const int64_t prow = (page < 0 || page >= p.num_pages ? 0 : (int64_t)page) * p.page_size +
-                           first % p.page_size;
+                           (first - j * p.page_size);
       elems = (prow * p.H_KV + kvh) * D;
     } else {
       elems = base_elems + (int64_t)first * p.H_KV * D;
@@ -740,7 +761,8 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
                                                             const float* __restrict__ l_part,
                                                             uint16_t* __restrict__ out, float* __restrict__ lse,
                                                             int s, int64_t rows,
-                                                            const int32_t* __restrict__ seqs, int H_Q) {
+                                                            const int32_t* __restrict__ seqs, int H_Q,
+                                                            Div div_hq) {
   __shared__ float sw[4][DA_MAX_SPLITS];
   __shared__ float sl[4][DA_MAX_SPLITS];
   __shared__ float sML[4][2];
@@ -753,8 +775,8 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
   // chunks from its first state row on (unsplit sequences are already done).
   int64_t base = row, srow = rows;
   if constexpr (SEQ) {
-    const int b = (int)(row / H_Q);
-    const int h = (int)(row - (int64_t)b * H_Q);
+    const int b = div_by((int)row, div_hq);  // rows = B * H_Q < 2^24
+    const int h = (int)row - b * H_Q;
     const int r0 = seqs[2 * b];
     s = seqs[2 * b + 1];
     if (r0 < 0 || s <= 1) return;
@@ -904,7 +926,8 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
 int launch_combine(const float* o_part, const float* m_part, const float* l_part, uint16_t* out, float* lse,
                    int s, int64_t rows, hipStream_t stream, const int32_t* seqs = nullptr, int H_Q = 1) {
   const int grid = (int)((rows + 3) / 4);
-  void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows, &seqs, &H_Q};
+  Div div_hq = make_div((uint32_t)H_Q);
+  void* args[] = {&o_part, &m_part, &l_part, &out, &lse, &s, &rows, &seqs, &H_Q, &div_hq};
   const void* fn = seqs ? reinterpret_cast<const void*>(&split_combine_kernel<true>)
                         : reinterpret_cast<const void*>(&split_combine_kernel<false>);
   hipError_t e = hipLaunchKernel(fn, dim3(grid), dim3(256), args, 0, stream);
@@ -924,6 +947,9 @@ void fill_params(Params& p, int B, int H_Q, int H_KV, int L_K_max, float scale, 
   p.tiles_per_seq = H_Q / pl.heads_per_tile;
   p.tiles = pl.tiles;
   p.s = pl.num_splits;
+  p.div_s = make_div((uint32_t)p.s);
+  p.div_tps = make_div((uint32_t)p.tiles_per_seq);
+  p.div_g = make_div((uint32_t)p.g);
   p.xcd_group = pl.heads_per_tile < p.g ? 1 : 0;  // several workgroups read each KV head
   const float sigma = scale > 0.f ? scale : 1.0f / sqrtf((float)D);
   p.scale_log2 = sigma * kLog2e;
@@ -1020,6 +1046,7 @@ void set_paged(Params& p, const void* q, const void* k_cache, const void* v_cach
   p.block_table = block_table;
   p.seq_lens = seq_lens;
   p.page_size = page_size;
+  p.div_page = make_div((uint32_t)page_size);
   p.max_pages = max_pages;
   p.num_pages = num_pages;
 }
