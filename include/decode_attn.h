@@ -67,7 +67,9 @@ typedef enum da_policy {
                            larger batches use the MI355X cost model */
   DA_POLICY_STREAMED = 3 /* the MI355X cost model calibrated with K/V read from HBM on every call
                             (no cache reuse between calls, as in a decode step through all
-                            layers); it splits earlier, e.g. 4 splits at B=1, H_KV=8, L_K=512 */
+                            layers); it splits earlier, e.g. 4 splits at B=1, H_KV=8, L_K=512,
+                            and marks K/V loads nontemporal at any size where one workgroup
+                            reads each key.  Its plans run through da_decode_attn_planned. */
 } da_policy;
 
 /* A launch plan: the scheduler metadata decided on the host before launch
@@ -159,6 +161,23 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
                    void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                    float softmax_scale, int num_splits, int pack_gqa, void* workspace,
                    size_t workspace_bytes, void* stream);
+
+/* Decode attention that runs a plan made beforehand instead of planning
+ * again (Section 5.1: scheduler metadata precomputed on the host and
+ * passed explicitly).  The plan comes from da_make_plan or da_choose_splits
+ * for this B, H_Q and H_KV, with any policy and cu_margin, and may be edited
+ * within its valid values. The launch uses exactly its split count, head
+ * tiles, K/V fetch path and cache hint.  Other arguments and the workspace
+ * need (for plan->num_splits) as in da_decode_attn.  Errors as there, plus
+ * DA_ERR_NULL (plan NULL) and DA_ERR_ARG (the plan does not describe a launch
+ * of this shape: num_splits outside 1..64, a heads_per_tile its pack_gqa
+ * cannot produce, tiles != B*H_Q/heads_per_tile, grid != tiles*num_splits,
+ * group_waves != 4, kv_fetch outside 0..2, kv_nontemporal outside 0..1,
+ * num_cus < 1), all before any device access. */
+int da_decode_attn_planned(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
+                           void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
+                           float softmax_scale, const da_plan* plan, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* Decode attention over a paged KV cache: the same computation as
  * da_decode_attn, with sequence b's keys held in fixed-size pages (the

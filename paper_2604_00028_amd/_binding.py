@@ -38,7 +38,7 @@ POLICY_STREAMED = 3
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (
     "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
-    "da_decode_attn_paged", "da_schedule_max_bytes", "da_make_schedule", "da_schedule_workspace_bytes",
+    "da_decode_attn_planned", "da_decode_attn_paged", "da_schedule_max_bytes", "da_make_schedule", "da_schedule_workspace_bytes",
     "da_decode_attn_scheduled", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror",
     "da_last_error",
 )
@@ -118,6 +118,9 @@ def load() -> ctypes.CDLL:
     lib.da_split_bounds.restype = _I
     lib.da_decode_attn.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _I, _P, _Z, _P]
     lib.da_decode_attn.restype = _I
+    lib.da_decode_attn_planned.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, ctypes.POINTER(DaPlan),
+                                           _P, _Z, _P]
+    lib.da_decode_attn_planned.restype = _I
     lib.da_decode_attn_paged.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
                                          _P, _Z, _P]
     lib.da_decode_attn_paged.restype = _I
@@ -263,6 +266,30 @@ def da_decode_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu_seqlens
     _check(load().da_decode_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),
                                  B, H_Q, H_KV, L, d, float(softmax_scale), int(num_splits), int(pack_gqa),
                                  ws_ptr, ws_bytes, s_handle))
+    return out
+
+
+def da_decode_attn_planned(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, plan: DaPlan,
+                           cu_seqlens_k: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           lse_out: Optional[torch.Tensor] = None, *, L_K_max: Optional[int] = None,
+                           softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None,
+                           stream=None) -> torch.Tensor:
+    """da_decode_attn with a plan made beforehand (da_make_plan /
+    da_choose_splits, any policy or cu_margin), run exactly as it is."""
+    B, H_Q, H_KV, L, d = _shapes(q, k, v, cu_seqlens_k, L_K_max)
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
+    s_handle = _stream(dev, stream)
+    if workspace is None:
+        nbytes = da_workspace_bytes(B, H_Q, d, plan.num_splits)
+        if nbytes:
+            workspace = workspace_for(dev, s_handle, nbytes)
+    ws_ptr = _ptr(workspace)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().da_decode_attn_planned(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),
+                                         B, H_Q, H_KV, L, d, float(softmax_scale), ctypes.byref(plan),
+                                         ws_ptr, ws_bytes, s_handle))
     return out
 
 

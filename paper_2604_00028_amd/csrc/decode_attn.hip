@@ -969,8 +969,23 @@ Params make_params(const void* q, const void* k, const void* v, const int32_t* c
 // What the decode entry points share once their inputs are checked: the
 // plan, the workspace check, then one launch (s == 1) or the chunk states
 // followed by the log-sum-exp combine.  `p` carries the K/V layout.
+// A plan made beforehand must describe a launch of this shape.
+int check_plan(const da_plan* pl, int B, int H_Q, int H_KV) {
+  if (!pl) return da::fail(DA_ERR_NULL, "plan is NULL");
+  const int hpt = pl->heads_per_tile;
+  if (pl->num_splits < 1 || pl->num_splits > DA_MAX_SPLITS || !da::heads_per_tile_valid(H_Q, H_KV, pl->pack_gqa, hpt) ||
+      (int64_t)pl->tiles != (int64_t)B * (H_Q / hpt) || (int64_t)pl->grid != (int64_t)pl->tiles * pl->num_splits ||
+      pl->group_waves != 4 || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
+      pl->kv_nontemporal > 1 || pl->num_cus < 1)
+    return da::fail(DA_ERR_ARG, "plan does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
+  return DA_OK;
+}
+
+// `given`: a plan made beforehand (checked), run as it is; NULL: plan here
+// from (num_splits, pack_gqa) with the MI355X policy.
 int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale, int num_splits,
-               int pack_gqa, void* out, float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+               int pack_gqa, void* out, float* lse_out, void* workspace, size_t workspace_bytes, void* stream,
+               const da_plan* given = nullptr) {
   if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
   if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
   if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
@@ -988,13 +1003,16 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
                       workspace ? workspace_bytes : (size_t)0);
     return check_state_size(B, H_Q, s);
   };
-  int rc = check_workspace(num_splits);
+  int rc = check_workspace(given ? given->num_splits : num_splits);
   if (rc) return rc;
   int cus = 0;
   rc = ensure_gfx950(&cus);
   if (rc) return rc;
   da_plan pl;
-  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+  if (given)
+    pl = *given;
+  else
+    rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   const int s = pl.num_splits;
   rc = check_workspace(s);
@@ -1073,6 +1091,23 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
   p.cu = cu_seqlens_k;
   return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, num_splits, pack_gqa, out, lse_out, workspace,
                     workspace_bytes, stream);
+}
+
+int da_decode_attn_planned(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, void* out,
+                           float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
+                           const da_plan* plan, void* workspace, size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  rc = check_plan(plan, B, H_Q, H_KV);
+  if (rc) return rc;
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.cu = cu_seqlens_k;
+  return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, plan->num_splits, plan->pack_gqa, out, lse_out,
+                    workspace, workspace_bytes, stream, plan);
 }
 
 int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,

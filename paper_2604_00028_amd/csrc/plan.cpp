@@ -261,7 +261,9 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
     out->kv_fetch = kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
   }
-  out->kv_nontemporal = kv_nontemporal((double)B * L_K_max * H_KV, g / hpt);
+  // STREAMED plans for K/V that are not resident whatever their size
+  out->kv_nontemporal = policy == DA_POLICY_STREAMED ? (g / hpt == 1 ? 1 : 0)
+                                                     : kv_nontemporal((double)B * L_K_max * H_KV, g / hpt);
   return DA_OK;
 }
 

@@ -3,6 +3,7 @@ its host-side logic (argument checks, planner, partition, workspace sizing)
 behaves as documented.  No kernel runs here; every call below returns before
 any HIP call."""
 
+import ctypes
 import json
 import os
 import re
@@ -299,6 +300,39 @@ def test_streaming_hint_follows_cache_capacity():
     small, _ = da.da_make_schedule([8192] * 8, 64, 8, num_cus=256)
     big, _ = da.da_make_schedule([8192] * 8 + [4096] * 4, 64, 8, num_cus=256)
     assert (small.kv_nontemporal, big.kv_nontemporal) == (0, 1)
+
+
+def test_planned_entry_checks_the_plan():
+    lib = da.load()
+    FAKE = 1 << 20
+    P = ctypes.c_void_p
+    def call(plan, B=2, H_Q=64, H_KV=8, L=512, ws=FAKE, ws_bytes=1 << 30):
+        return lib.da_decode_attn_planned(P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), None, B, H_Q, H_KV, L, 128, 0.0,
+                                          ctypes.byref(plan) if plan is not None else None, P(ws), ws_bytes, None)
+    assert lib.da_decode_attn_planned(P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), None, 2, 64, 8, 512, 128, 0.0,
+                                      None, P(FAKE), 1 << 30, None) == bnd.DA_ERR_NULL
+    good = da.da_make_plan(2, 64, 8, 512, num_splits=4, pack_gqa=1, num_cus=256)
+    for field, val in (("num_splits", 0), ("num_splits", 65), ("heads_per_tile", 4), ("heads_per_tile", 0),
+                       ("tiles", 15), ("grid", 63), ("group_waves", 8), ("kv_fetch", 3), ("kv_nontemporal", 2),
+                       ("num_cus", 0), ("pack_gqa", 3)):
+        bad = bnd.DaPlan.from_buffer_copy(good)
+        setattr(bad, field, val)
+        assert call(bad) == bnd.DA_ERR_ARG, field
+    # a plan for another shape
+    assert call(good, B=3) == bnd.DA_ERR_ARG
+    assert call(good, H_Q=32, H_KV=4) == bnd.DA_ERR_ARG
+    # the workspace its split count needs
+    assert call(good, ws=0, ws_bytes=0) == bnd.DA_ERR_WORKSPACE
+
+
+def test_streamed_policy_marks_loads_nontemporal():
+    # the streamed policy plans for K/V that are never resident
+    p = da.da_choose_splits(1, 64, 8, 512, num_cus=256, policy=da.POLICY_STREAMED)
+    assert p.kv_nontemporal == 1
+    assert da.da_choose_splits(1, 64, 8, 512, num_cus=256).kv_nontemporal == 0
+    # unless several workgroups read each key
+    p = da.da_make_plan(1, 64, 8, 512, num_splits=1, pack_gqa=0, num_cus=256, policy=da.POLICY_STREAMED)
+    assert p.kv_nontemporal == 0
 
 
 def test_cu_margin_and_plan_errors():

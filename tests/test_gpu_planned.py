@@ -1,0 +1,81 @@
+"""GPU parity of the planned entry point (a plan made beforehand, run as it
+is) against the fp64 oracle, and its bits against the planning entry point:
+the plan decides how the work is spread and cached, never the result."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_00028_amd as da
+from oracle import decode_attention
+from workloads import config_shapes, custom_shape, make_inputs
+from tests.gpu_helpers import assert_parity, dev_inputs, say
+
+pytestmark = pytest.mark.gpu
+
+LSE_TOL = 1e-3
+
+
+def planned(q, k, v, cu, L, plan):
+    lse = torch.empty(q.shape[0], q.shape[1], dtype=torch.float32, device="cuda")
+    out = da.da_decode_attn_planned(q, k, v, plan, cu, lse_out=lse, L_K_max=L)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def same_bits(a, b):
+    return torch.equal(a[0].view(torch.int16), b[0].view(torch.int16)) and torch.equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("B,H_Q,H_KV,L,varlen", [
+    (1, 64, 8, 512, False),     # Llama-70B shape
+    (1, 8, 1, 128, False),      # MQA
+    (3, 32, 1, 777, False),     # a group of 32: two tile widths
+    (2, 128, 2, 300, False),    # a group of 64
+    (4, 32, 4, 200, True),      # varlen GQA
+    (5, 8, 1, 2049, False),     # ragged tail
+])
+def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
+    """Plans from each policy, with and without a CU margin and with every
+    K/V fetch path and cache hint edited in: oracle parity, and the same bits
+    for the same split count and head tiles."""
+    sh = custom_shape(B, H_Q, H_KV, L, varlen=varlen)
+    inp = make_inputs(sh, seed=B * 31 + L)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    plans = [da.da_choose_splits(B, H_Q, H_KV, L, policy=pol)
+             for pol in (da.POLICY_MI355X, da.POLICY_STREAMED, da.POLICY_PAPER, da.POLICY_EVOLVED)]
+    plans.append(da.da_choose_splits(B, H_Q, H_KV, L, cu_margin=200))
+    plans += [da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pk) for s in (1, 3) for pk in (0, 1, 2)]
+    first = {}
+    for plan in plans:
+        for fetch in (0, 1, 2):
+            for hint in (0, 1):
+                p = da.DaPlan.from_buffer_copy(plan)
+                p.kv_fetch, p.kv_nontemporal = fetch, hint
+                say(f"planned B{B}-H{H_Q}-KV{H_KV}-L{L} {p.as_dict()}")
+                got = planned(q, k, v, cu, L, p)
+                assert_parity(got[0], O, f"planned {p.as_dict()}")
+                lg = got[1].cpu().numpy().astype(np.float64)
+                fin = np.isfinite(lse)
+                assert np.max(np.abs(lg[fin] - lse[fin]), initial=0.0) <= LSE_TOL
+                key = (p.num_splits, p.heads_per_tile)
+                if key in first:
+                    assert same_bits(got, first[key]), (key, p.as_dict())
+                else:
+                    first[key] = got
+
+
+@pytest.mark.parametrize("shape", config_shapes(2) + config_shapes(1), ids=lambda s: s.name)
+def test_planned_equals_planning_entry(shape):
+    """The plan da_decode_attn makes for itself, passed explicitly, gives the
+    same bits."""
+    inp = make_inputs(shape)
+    q, k, v, cu = dev_inputs(inp)
+    for s, pack in ((0, -1), (1, 1), (4, 1), (2, 0)):
+        plan = da.da_make_plan(shape.B, shape.H_Q, shape.H_KV, shape.L_K, num_splits=s, pack_gqa=pack)
+        say(f"planned vs planning {shape.name} s={s} pack={pack}")
+        lse = torch.empty(shape.B, shape.H_Q, dtype=torch.float32, device="cuda")
+        a = da.da_decode_attn(q, k, v, lse_out=lse, num_splits=s, pack_gqa=pack)
+        torch.cuda.synchronize()
+        assert same_bits((a, lse), planned(q, k, v, cu, shape.L_K, plan))
