@@ -94,11 +94,12 @@ def parse():
 class Variant:
     """K calls of one launch configuration captured in a HIP graph."""
 
-    def __init__(self, name, da, torch, q, k, v, L, s, pack, steps, kv_copies=None, cu=None):
+    def __init__(self, name, da, torch, q, k, v, L, s, pack, steps, kv_copies=None, cu=None, plan=None):
         self.name = name
         B, H_Q, D = q.shape
         H_KV = k.shape[-2]
-        self.plan = da.da_make_plan(B, H_Q, H_KV, L, D, s, pack)
+        # plan given: run it as it is (da_decode_attn_planned); else the library plans from (s, pack)
+        self.plan = plan if plan is not None else da.da_make_plan(B, H_Q, H_KV, L, D, s, pack)
         nbytes = da.da_workspace_bytes(B, H_Q, D, self.plan.num_splits)
         self.ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device="cuda") if nbytes else None
         self.out = torch.empty((B, H_Q, D), dtype=torch.bfloat16, device="cuda")
@@ -108,8 +109,12 @@ class Variant:
 
         def call(i):
             kk, vv = kvs[i % len(kvs)]
-            da.da_decode_attn(q, kk, vv, cu, out=self.out, L_K_max=L if cu is not None else None,
-                              num_splits=s_res, pack_gqa=p_res, workspace=self.ws)
+            if plan is not None:
+                da.da_decode_attn_planned(q, kk, vv, plan, cu, out=self.out, L_K_max=L if cu is not None else None,
+                                          workspace=self.ws)
+            else:
+                da.da_decode_attn(q, kk, vv, cu, out=self.out, L_K_max=L if cu is not None else None,
+                                  num_splits=s_res, pack_gqa=p_res, workspace=self.ws)
 
         self.call = call
         for i in range(3):
@@ -249,18 +254,25 @@ def streamed_run(args, da, torch) -> dict:
         cold = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_STREAMED)
         splits = sorted(set(STREAMED_SWEEP) | {warm.num_splits, cold.num_splits})
         log(f"timing streamed B={B} H_Q={H_Q} H_KV={H_KV} L_K={L} ({copies} copies)")
-        var = {s: Variant(str(s), da, torch, q, K[0], V[0], L, s, 1, steps, kv_copies=kvs) for s in splits}
-        interleave(torch, list(var.values()), max(3, args.rounds // 2))
+        # every launch as the streamed policy plans it for that split count (tile width, cache hint),
+        # through the planned entry point; the warm policy's own plan beside them
+        plans = {s: da.da_make_plan(B, H_Q, H_KV, L, 128, s, -1, policy=da.POLICY_STREAMED) for s in splits}
+        var = {s: Variant(str(s), da, torch, q, K[0], V[0], L, s, 1, steps, kv_copies=kvs, plan=plans[s])
+               for s in splits}
+        wv = Variant("warm", da, torch, q, K[0], V[0], L, 0, -1, steps, kv_copies=kvs, plan=warm)
+        interleave(torch, list(var.values()) + [wv], max(3, args.rounds // 2))
         us = {s: round(v.median, 3) for s, v in var.items()}
         best = min(us, key=us.get)
         res[f"b{B}_h{H_Q}_kv{H_KV}_l{L}"] = {
             "B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L, "s1_us": us[1],
-            "warm_policy": warm.num_splits, "warm_policy_us": us[warm.num_splits],
+            "warm_policy": warm.num_splits, "warm_policy_us": round(wv.median, 3),
             "streamed_policy": cold.num_splits, "streamed_policy_us": us[cold.num_splits],
+            "streamed_nontemporal": cold.kv_nontemporal,
             "streamed_speedup_vs_s1": round(us[1] / us[cold.num_splits], 3),
+            "streamed_speedup_vs_warm_policy": round(wv.median / us[cold.num_splits], 3),
             "best_fixed": best, "best_fixed_us": us[best],
             "streamed_vs_best": round(us[cold.num_splits] / us[best], 3), "sweep_us": us}
-        del K, V, kvs, var
+        del K, V, kvs, var, wv
     return res
 
 

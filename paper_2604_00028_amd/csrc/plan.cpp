@@ -95,27 +95,28 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
 // The same model with K/V streamed from HBM on every call (each call reads
 // its own copy of the cache, 1 GiB per timed replay, as a decode step that
 // runs all layers evicts each layer's cache before it is read again),
-// fitted the same way to the same shapes with at least 256 KiB of K/V per
-// call and the blend exponent held at 4.  Streaming from HBM, a tile of
+// fitted the same way to the launches this policy makes (the whole group in
+// one tile, nontemporal K/V loads) over 63 shapes with at least 256 KiB of
+// K/V per call, the blend exponent held at 4.  Streaming from HBM, a tile of
 // one KV head costs less when key rows hold just that head (H_KV = 1: the
 // rows are contiguous) than when they interleave several heads and every
 // workgroup reads a 256-byte slice of each row: contig_tile.  Over the sweep
 // the chosen split is on average 0.4% slower than the fastest measured one
-// and never slower than one split; fitted on half of the shapes it chooses
-// for the other half within 0.3% on average, never slower than one split.
-// 32-column direct-fetch tiles had no launch in the sweep and carry the
-// 16-column value scaled by the warm model's ratio.
+// and at worst 1.7% slower than one split (B=1, H_Q=32, H_KV=1, L_K=512);
+// fitted on half of the shapes it chooses for the other half within 0.4% on
+// average.  32-column tiles with several workgroups per CU had no launch in
+// the sweep and carry the 16-column value scaled by the warm model's ratio.
 const CostModel& mi355x_streamed_model() {
   static const CostModel m = {
-      /*base=*/{2.555, 4.214},
-      /*t_tile=*/{1.240, 1.240 * 1.130 / 0.809},
-      /*t_tile_staged=*/{1.601, 1.588},
-      /*merge0=*/2.567,
-      /*merge1=*/{0.231, 0.250},
-      /*hbm_rate=*/5.876e6,
-      /*hbm0=*/3.406,
+      /*base=*/{2.095, 3.679},
+      /*t_tile=*/{1.576, 1.576 * 1.130 / 0.809},
+      /*t_tile_staged=*/{1.609, 1.643},
+      /*merge0=*/2.308,
+      /*merge1=*/{0.235, 0.254},
+      /*hbm_rate=*/6.498e6,
+      /*hbm0=*/3.366,
       /*pnorm=*/4.0,
-      /*contig_tile=*/0.756,
+      /*contig_tile=*/0.744,
   };
   return m;
 }
