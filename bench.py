@@ -739,26 +739,34 @@ def regression_run(args, da, torch) -> None:
                 v = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
                 est_us = 5.0 + 2.0 * B * L * H_KV * 256 / 5e6
                 K = int(max(10, min(100, 2000.0 / est_us)))
-                # each distinct launch (split count, packing on) is timed once; the heuristic and the
-                # paper's policy reuse the sweep's timing when they pick a split it already covers
-                paper_s = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER).num_splits
-                evolved_s = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_EVOLVED).num_splits
-                heur_s = da.da_choose_splits(B, H_Q, H_KV, L).num_splits
-                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s, paper_s, evolved_s})
+                # fixed split counts as the library plans them (packing on, V slices where they pay);
+                # the heuristic reuses the sweep's timing when it picks a split the sweep covers; the
+                # paper's and the evolved policy run their own plans (one workgroup per chunk), and so does
+                # one split with the paper's launch shape (pack_gqa = 2)
+                paper = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER)
+                evolved = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_EVOLVED)
+                heur = da.da_choose_splits(B, H_Q, H_KV, L)
+                heur_s = heur.num_splits
+                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s})
                 variants = {s: Variant(str(s), da, torch, q, k, v, L, s, 1, K) for s in splits}
-                interleave(torch, list(variants.values()), args.rounds)
+                own = {"paper": Variant("paper", da, torch, q, k, v, L, 0, -1, K, plan=paper),
+                       "evolved": Variant("evolved", da, torch, q, k, v, L, 0, -1, K, plan=evolved),
+                       "s1_one_wg": Variant("s1_one_wg", da, torch, q, k, v, L, 1, 2, K)}
+                interleave(torch, list(variants.values()) + list(own.values()), args.rounds)
                 sw = {s: round(x.median, 3) for s, x in variants.items() if s in REG_SWEEP}
                 best = min(sw, key=sw.get)
                 row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L,
-                       "heuristic_splits": heur_s, "heuristic_us": round(variants[heur_s].median, 3),
-                       "paper_splits": paper_s, "paper_us": round(variants[paper_s].median, 3),
-                       "evolved_splits": evolved_s, "evolved_us": round(variants[evolved_s].median, 3),
+                       "heuristic_splits": heur_s, "heuristic_v_slices": heur.v_slices,
+                       "heuristic_us": round(variants[heur_s].median, 3),
+                       "paper_splits": paper.num_splits, "paper_us": round(own["paper"].median, 3),
+                       "evolved_splits": evolved.num_splits, "evolved_us": round(own["evolved"].median, 3),
+                       "s1_one_workgroup_per_chunk_us": round(own["s1_one_wg"].median, 3),
                        "s1_us": sw[1], "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
                 results.append(row)
                 log(f"B={B} H_KV={H_KV} L_K={L}: heuristic s={row['heuristic_splits']} {row['heuristic_us']} us, "
                     f"s=1 {row['s1_us']}, paper s={row['paper_splits']} {row['paper_us']}, "
                     f"best s={best} {sw[best]}")
-                del q, k, v, variants
+                del q, k, v, variants, own
     json.dump({"configs": results}, open(args.regression, "w"), indent=1)
     worst_s1 = max(r["heuristic_us"] / r["s1_us"] for r in results)
     worst_best = max(r["heuristic_us"] / r["best_fixed_us"] for r in results)
@@ -773,6 +781,7 @@ def regression_summary(path: str) -> None:
     r_best = [r["heuristic_us"] / r["best_fixed_us"] for r in rows]
     r_paper = [r["heuristic_us"] / r["paper_us"] for r in rows]
     r_evo = [r["heuristic_us"] / r["evolved_us"] for r in rows if r["B"] == 1]
+    r_one = [r["heuristic_us"] / r["s1_one_workgroup_per_chunk_us"] for r in rows if "s1_one_workgroup_per_chunk_us" in r]
     faster = sum(x < 0.99 for x in r_s1)
     slower = [r for r, x in zip(rows, r_s1) if x > 1 / 0.99]
     over5 = [r for r, x in zip(rows, r_best) if x > 1.05]
@@ -782,9 +791,11 @@ def regression_summary(path: str) -> None:
         "Batch in {1, 2, 4, 8} x L_K in {128, 256, 384, 512, 1024, 2048, 4096, 8192} x H_KV in {1, 2, 4, 8, 32},",
         "H_Q = 8 * H_KV, D = 128, bf16, synthetic inputs. Each shape times the MI355X heuristic, num_splits = 1,",
         "the paper's policy (policy PAPER), the evolved single-batch setting of its Fig. 1 (policy EVOLVED) and",
-        "fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8),",
-        "as graph-replayed calls interleaved over rounds (median). Each distinct launch is timed once: a policy",
-        "that picks a split of the sweep shares that split's timing.",
+        "fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8), as graph-replayed calls interleaved",
+        "over rounds (median). Fixed splits are planned by the library (GQA packing on, V slices where they pay);",
+        "the heuristic shares the sweep's timing when it picks a split the sweep covers. The paper's and the evolved",
+        "policy run their own plans (one workgroup per KV head and chunk), and so does one split with the paper's",
+        "launch shape (`pack_gqa = 2`: one workgroup per KV head, no V slices).",
         "",
         "Command (MI355X, one GPU):",
         "",
@@ -798,19 +809,23 @@ def regression_summary(path: str) -> None:
         f"{max(r_s1):.3f}x the time of s = 1; faster by more than 1% in {faster}.",
         f"* Heuristic vs the best fixed split: within 5% in {n - len(over5)} of {n}; worst {max(r_best):.3f}x, "
         f"mean {statistics.mean(r_best):.3f}x.",
+        (f"* Heuristic vs one split with one workgroup per KV head (the paper's launch): mean "
+         f"{statistics.mean(r_one):.3f}x its time, best {min(r_one):.3f}x, worst {max(r_one):.3f}x; faster by more "
+         f"than 1% in {sum(x < 0.99 for x in r_one)} of {len(r_one)}.") if r_one else "",
         f"* Heuristic vs the paper's policy: mean {statistics.mean(r_paper):.3f}x its time, "
         f"best {min(r_paper):.3f}x, worst {max(r_paper):.3f}x.",
         f"* Heuristic vs the evolved single-batch setting (Fig. 1; batch 1 only, {len(r_evo)} shapes): mean "
         f"{statistics.mean(r_evo):.3f}x its time, best {min(r_evo):.3f}x, worst {max(r_evo):.3f}x.",
         "",
-        "| B | H_KV | L_K | heuristic s | us | s = 1 us | vs s = 1 | paper s | paper us | evolved s | evolved us "
-        "| best s | best us | vs best |",
-        "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
+        "| B | H_KV | L_K | heuristic s (V slices) | us | s = 1 us | vs s = 1 | s = 1, one WG per KV head us | "
+        "paper s | paper us | evolved s | evolved us | best s | best us | vs best |",
+        "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
     ]
     for r, a, c in zip(rows, r_s1, r_best):
-        lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_splits']} | {r['heuristic_us']} | "
-                     f"{r['s1_us']} | {1 / a:.2f}x | {r['paper_splits']} | {r['paper_us']} | {r['evolved_splits']} | "
-                     f"{r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
+        lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_splits']} "
+                     f"({r.get('heuristic_v_slices', 1)}) | {r['heuristic_us']} | {r['s1_us']} | {1 / a:.2f}x | "
+                     f"{r.get('s1_one_workgroup_per_chunk_us', '')} | {r['paper_splits']} | {r['paper_us']} | "
+                     f"{r['evolved_splits']} | {r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
     open(PROFILE_REGRESSION, "w").write("\n".join(lines) + "\n")
     print(f"wrote {PROFILE_REGRESSION}")
 
@@ -867,6 +882,13 @@ def main():
     torch.cuda.synchronize()
     heur = Variant("heuristic", da, torch, q, k, v, sh.L_K, 0, -1, K)
     base = Variant("s1", da, torch, q, k, v, sh.L_K, 1, 1, K)
+    # one split with one workgroup per (sequence, KV head): the paper's launch (pack_gqa = 2, no V slices)
+    paper_s1 = Variant("s1_one_wg", da, torch, q, k, v, sh.L_K, 1, 2, K)
+    # each policy's own plan, run as it is
+    pol = {name: Variant(name, da, torch, q, k, v, sh.L_K, 0, -1, K,
+                         plan=da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K, policy=code))
+           for name, code in (("paper", da.POLICY_PAPER), ("evolved", da.POLICY_EVOLVED),
+                              ("streamed", da.POLICY_STREAMED))}
     sweep = [Variant(f"s{s}", da, torch, q, k, v, sh.L_K, s, 1, K) for s in SWEEP if s != 1]
     unpacked = [Variant("s1_unpacked", da, torch, q, k, v, sh.L_K, 1, 0, K),
                 Variant("heur_unpacked", da, torch, q, k, v, sh.L_K, heur.plan.num_splits, 0, K)]
@@ -876,8 +898,10 @@ def main():
                torch.randn_like(v, dtype=torch.float32).to(torch.bfloat16)) for _ in range(ncopy)]
     cold_h = Variant("cold_heuristic", da, torch, q, k, v, sh.L_K, 0, -1, K, kv_copies=copies)
     cold_1 = Variant("cold_s1", da, torch, q, k, v, sh.L_K, 1, 1, K, kv_copies=copies)
+    cold_p = Variant("cold_s1_one_wg", da, torch, q, k, v, sh.L_K, 1, 2, K, kv_copies=copies)
     log("timing headline variants")
-    interleave(torch, [heur, base] + sweep + unpacked + [cold_h, cold_1], args.rounds)
+    interleave(torch, [heur, base, paper_s1] + list(pol.values()) + sweep + unpacked + [cold_h, cold_1, cold_p],
+               args.rounds)
     value = heur.median
     s1 = base.median
     sweep_us = {1: round(s1, 3)}
@@ -888,8 +912,10 @@ def main():
     achieved = bytes_call / (value * 1e-6) / 1e9
     q25, q75 = np.percentile(heur.times, [25, 75])
     cold = {"heuristic": round(cold_h.median, 3), "s1": round(cold_1.median, 3),
-            "speedup_vs_s1": round(cold_1.median / cold_h.median, 3)}
-    del copies, cold_h, cold_1
+            "speedup_vs_s1": round(cold_1.median / cold_h.median, 3),
+            "s1_one_workgroup_per_chunk": round(cold_p.median, 3),
+            "speedup_vs_s1_one_workgroup_per_chunk": round(cold_p.median / cold_h.median, 3)}
+    del copies, cold_h, cold_1, cold_p
 
     # other config-2 lengths: heuristic vs s=1 and a few fixed splits
     other = {}
@@ -900,11 +926,15 @@ def main():
         log(f"timing L_K={L}")
         hv = Variant("h", da, torch, qL, kL, vL, L, 0, -1, K)
         bv = Variant("1", da, torch, qL, kL, vL, L, 1, 1, K)
+        pv = Variant("1_one_wg", da, torch, qL, kL, vL, L, 1, 2, K)
         sv = [Variant(str(x), da, torch, qL, kL, vL, L, x, 1, K) for x in (2, 4, 8, 16)]
-        interleave(torch, [hv, bv] + sv, args.rounds)
+        interleave(torch, [hv, bv, pv] + sv, args.rounds)
         sw = {1: round(bv.median, 3), **{x.plan.num_splits: round(x.median, 3) for x in sv}}
         other[L] = {"heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
+                    "v_slices": hv.plan.v_slices,
                     "s1_us": round(bv.median, 3), "speedup_vs_s1": round(bv.median / hv.median, 3),
+                    "s1_one_workgroup_per_chunk_us": round(pv.median, 3),
+                    "speedup_vs_s1_one_workgroup_per_chunk": round(pv.median / hv.median, 3),
                     "best_fixed": min(sw, key=sw.get), "best_fixed_us": min(sw.values())}
 
     # longer Llama GQA contexts at B=1, where splitting pays on MI355X
@@ -970,17 +1000,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": sh.name, "B": sh.B, "H_Q": sh.H_Q, "H_KV": sh.H_KV, "head_dim": sh.D,
                    "L_K": sh.L_K, "num_splits": heur.plan.num_splits, "pack_gqa": heur.plan.pack_gqa,
-                   "grid_workgroups": heur.plan.grid, "num_cus": cus},
+                   "v_slices": heur.plan.v_slices, "grid_workgroups": heur.plan.grid, "num_cus": cus},
         "s1_us": round(s1, 3),
         "speedup_vs_s1": round(s1 / value, 3),
+        "s1_one_workgroup_per_chunk_us": round(paper_s1.median, 3),
+        "speedup_vs_s1_one_workgroup_per_chunk": round(paper_s1.median / value, 3),
         "iqr_us": [round(q25, 3), round(q75, 3)],
-        "policies": {name: {"num_splits": s_pol, "us": sweep_us.get(s_pol)}
-                     for name, s_pol in (("paper", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
-                                                                       policy=da.POLICY_PAPER).num_splits),
-                                         ("evolved", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
-                                                                         policy=da.POLICY_EVOLVED).num_splits),
-                                         ("streamed", da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K,
-                                                                          policy=da.POLICY_STREAMED).num_splits))},
+        "policies": {name: {"num_splits": var.plan.num_splits, "v_slices": var.plan.v_slices,
+                            "us": round(var.median, 3)} for name, var in pol.items()},
         "best_fixed_splits": best_s,
         "vs_best_fixed": round(value / sweep_us[best_s], 3),
         "sweep_us": sweep_us,

@@ -85,7 +85,9 @@ typedef struct da_plan {
                              (its largest divisor <= 32 when g > 32), or with pack_gqa 1 possibly g's
                              largest divisor <= 16 */
   int32_t tiles;          /* work tiles = B * H_Q / heads_per_tile (Section 2.1: Batch x H_KV when packed) */
-  int32_t grid;           /* workgroups launched = tiles * num_splits */
+  int32_t grid;           /* workgroups launched: tiles * num_splits, or with V slices
+                             v_slices * 8 * ceil(tiles * num_splits / 8) (a chunk's slices share an
+                             XCD; the workgroups past the last chunk return at once) */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
   int32_t group_waves;    /* wave64s per workgroup (4); each takes a contiguous part of the chunk */
   int32_t kv_fetch;       /* how K/V tiles reach the matrix cores: 0 K straight into the operand
@@ -96,7 +98,13 @@ typedef struct da_plan {
   int32_t kv_nontemporal; /* 1: K/V loads carry the nontemporal (streaming) cache hint, chosen when
                              one call's K/V exceed DA_RESIDENT_BYTES and cannot stay in L2 and the
                              MALL between calls, and one workgroup reads each key (heads_per_tile
-                             = H_Q/H_KV); 0: ordinary loads */
+                             = H_Q/H_KV, v_slices = 1); 0: ordinary loads */
+  int32_t v_slices;       /* workgroups that share each chunk: each computes the chunk's scores and
+                             128/v_slices of the output dims (1, 2 or 4; more than 1 only with
+                             kv_fetch 2, heads_per_tile = H_Q/H_KV and pack_gqa != 2).  The
+                             policies MI355X and STREAMED choose it where a launch keeps one
+                             workgroup per CU and its K/V fit in L2; results are the same bits
+                             for every value. */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split

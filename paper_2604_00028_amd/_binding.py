@@ -55,6 +55,7 @@ class DaPlan(ctypes.Structure):
         ("group_waves", ctypes.c_int32),
         ("kv_fetch", ctypes.c_int32),
         ("kv_nontemporal", ctypes.c_int32),
+        ("v_slices", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

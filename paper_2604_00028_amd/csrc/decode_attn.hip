@@ -80,7 +80,7 @@ constexpr int kLdsStageBytes = 2 * kLdsTileBytes;                // K and V of o
 // LDS of one workgroup of W waves with NT head tiles: the per-wave stages,
 // reused after the tile loop for the wave-state merge (W slots, one wave
 // state of NT x kStateVals x 64 floats each).
-constexpr int merge_slot_bytes(int NT) { return NT * kStateVals * 64 * 4; }
+constexpr int merge_slot_bytes(int NT) { return NT * kStateVals * 64 * 4; }  // V slices use less
 constexpr int stage_bytes(int FETCH) {
   return FETCH == kFetchLds ? 2 * kLdsStageBytes
                             : kKeysPerTile * (kVPitch + (FETCH == kFetchStaged ? kKPitch : 0));
@@ -211,21 +211,36 @@ constexpr int kMinWaves = (NT == 1 && FETCH == 0) ? 3 : 2;
 // page).  SCH: per-sequence schedule (p.work lists every workgroup's head
 // tile, 32-key tile range and chunk-state row).  Both are template
 // parameters so that the uniform launch waits on no extra argument.
-template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL>
+template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL, int VS>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(kMinWaves<NT, FETCH>, 8)))
 split_partial_kernel(Params p) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   // NTL: K/V loads carry the nontemporal hint (the cache-policy field of
   // the buffer instructions), for launches whose K/V cannot stay resident
   constexpr int kv_aux = NTL ? 2 : 0;
+  // VS: the workgroup computes 128/VS of the output dims (its V slice); the
+  // VS workgroups of a tile's chunk share its scores.  NB 16-dim blocks.
+  static_assert(VS == 1 || (FETCH == kFetchLds && !SCH), "V slices only with direct-to-LDS fetch");
+  constexpr int NB = 8 / VS;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15;   // MFMA column: head within a 16-head tile
   const int quad = lane >> 4;  // MFMA row group
 
-  // ---- which tile and chunk this workgroup owns
-  const int bid = blockIdx.x;
+  // ---- which tile and chunk this workgroup owns (and which V slice)
+  int bid = blockIdx.x;
+  int nb0 = 0;  // first 16-dim output block of this workgroup
+  if constexpr (VS > 1) {
+    // Launched as VS x 8 x ceil(chunks / 8) workgroups: block ids 8i + x
+    // hold slice i mod VS of chunk 8 (i / VS) + x, so the slices of a chunk
+    // share an XCD and its L2 serves their repeated K reads.  Ids past the
+    // last chunk have nothing to do (the whole workgroup leaves at once).
+    const int vslice = (bid >> 3) % VS;
+    bid = (bid & 7) + 8 * ((bid >> 3) / VS);
+    if (bid >= p.tiles * p.s) return;
+    nb0 = vslice * NB;
+  }
   int tile, split = 0, prow = -1, w_first = 0, w_end = 0;
   if constexpr (SCH) {
     // scheduled: this workgroup's head tile, 32-key tile range and state row
@@ -346,13 +361,13 @@ split_partial_kernel(Params p) {
   }
 
   float m_run[NT], l_run[NT];
-  f32x4 acc_o[NT][8];
+  f32x4 acc_o[NT][NB];  // output blocks nb0 .. nb0 + NB - 1
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     m_run[nt] = -INFINITY;
     l_run[nt] = 0.f;
 #pragma unroll
-    for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nn = 0; nn < NB; ++nn) acc_o[nt][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
   constexpr bool KS = FETCH == kFetchStaged;
@@ -443,7 +458,7 @@ split_partial_kernel(Params p) {
       // multiply by one (a wave-uniform branch)
       if (__any(alpha != 1.0f)) {
 #pragma unroll
-        for (int nn = 0; nn < 8; ++nn) acc_o[nt][nn] *= alpha;
+        for (int nn = 0; nn < NB; ++nn) acc_o[nt][nn] *= alpha;
       }
       u32x4 pk;
       pk.x = pack_bf16x2(x[0], x[1]);
@@ -470,32 +485,41 @@ split_partial_kernel(Params p) {
   // explicit wait: the compiler cannot tell that they touch the other stage
   // and would otherwise drain every outstanding load before them.
   auto pv = [&](const bf16x8 (&pb)[NT], auto vaddr, auto opaque) {
-    s16x4 vlo[8], vhi[8];
+    s16x4 vlo[NB], vhi[NB];
     if constexpr (decltype(opaque)::value) {
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn) {
+      for (int nn = 0; nn < NB; ++nn) {
         asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(vlo[nn]) : "v"((uint32_t)vaddr(0, nn)) : "memory");
         asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(vhi[nn]) : "v"((uint32_t)vaddr(1, nn)) : "memory");
       }
       // The wait names every result as an operand it updates, so nothing
       // that reads them can be scheduled before it.
-      asm volatile("s_waitcnt lgkmcnt(0)"
-                   : "+v"(vlo[0]), "+v"(vlo[1]), "+v"(vlo[2]), "+v"(vlo[3]), "+v"(vlo[4]), "+v"(vlo[5]),
-                     "+v"(vlo[6]), "+v"(vlo[7]), "+v"(vhi[0]), "+v"(vhi[1]), "+v"(vhi[2]), "+v"(vhi[3]),
-                     "+v"(vhi[4]), "+v"(vhi[5]), "+v"(vhi[6]), "+v"(vhi[7])
-                   :
-                   : "memory");
+      if constexpr (NB == 8)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(vlo[0]), "+v"(vlo[1]), "+v"(vlo[2]), "+v"(vlo[3]), "+v"(vlo[4]), "+v"(vlo[5]),
+                       "+v"(vlo[6]), "+v"(vlo[7]), "+v"(vhi[0]), "+v"(vhi[1]), "+v"(vhi[2]), "+v"(vhi[3]),
+                       "+v"(vhi[4]), "+v"(vhi[5]), "+v"(vhi[6]), "+v"(vhi[7])
+                     :
+                     : "memory");
+      else if constexpr (NB == 4)
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(vlo[0]), "+v"(vlo[1]), "+v"(vlo[2]), "+v"(vlo[3]), "+v"(vhi[0]), "+v"(vhi[1]),
+                       "+v"(vhi[2]), "+v"(vhi[3])
+                     :
+                     : "memory");
+      else
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(vlo[0]), "+v"(vlo[1]), "+v"(vhi[0]), "+v"(vhi[1]) : : "memory");
     } else {
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn) {
+      for (int nn = 0; nn < NB; ++nn) {
         vlo[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)vaddr(0, nn));
         vhi[nn] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)vaddr(1, nn));
       }
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);      // the 16 DS reads first
-    __builtin_amdgcn_sched_group_barrier(0x008, 8 * NT, 0);  // then the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * NB, 0);   // the DS reads first
+    __builtin_amdgcn_sched_group_barrier(0x008, NB * NT, 0);  // then the MFMAs
 #pragma unroll
-    for (int nn = 0; nn < 8; ++nn) {
+    for (int nn = 0; nn < NB; ++nn) {
       const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vlo[nn], vhi[nn], 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
@@ -572,6 +596,10 @@ split_partial_kernel(Params p) {
     for (int blk = 0; blk < 8; ++blk)
       dmaoff[blk] = (uint32_t)(4 * blk + rr) * rs + 16u * (uint32_t)((cp - 2 * rr) & 15);
     unsigned char* const sbase = smem + wave * stage_bytes(FETCH);
+    // with V slices a lane loads its V chunk only if the chunk (8 dims) is
+    // in this workgroup's slice: dims [16 nb0, 16 (nb0 + NB))
+    const int vblock = ((cp - 2 * rr) & 15) >> 1;
+    const bool vload = VS == 1 || (vblock >= nb0 && vblock < nb0 + NB);
     auto dma_tile = [&](int stage, int t) {
       int64_t elems;
       uint32_t left;
@@ -584,17 +612,19 @@ split_partial_kernel(Params p) {
       for (int blk = 0; blk < 8; ++blk)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(kt, (lds_void*)(ks + blk * kBlockStride), 16, dmaoff[blk], 0, 0,
                                                  kv_aux);
+      if (vload) {
 #pragma unroll
-      for (int blk = 0; blk < 8; ++blk)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0,
-                                                 kv_aux);
+        for (int blk = 0; blk < 8; ++blk)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(vt, (lds_void*)(vs + blk * kBlockStride), 16, dmaoff[blk], 0, 0,
+                                                   kv_aux);
+      }
     };
     // Operand reads.  K operand (mt, j), lane (col, quad): key 16mt + col is
     // row col%4 of block 4mt + col/4, dims [32j + 8quad, +8) are its chunk
     // 4j + quad.  V (see pv): key 16mt + 4quad + k is row k of block
     // 4mt + quad, dims [16nn + 4m, +4) sit in chunk 2nn + m/2.  The rotated
     // offsets differ per lane and per operand, so they are computed once.
-    uint32_t kro[2][4], vro[2][8];
+    uint32_t kro[2][4], vro[2][NB];
     {
       const int kr = col & 3;
       const int vk = col >> 2;
@@ -606,9 +636,10 @@ split_partial_kernel(Params p) {
           kro[mt][j] = lds_offset(sbase) + (uint32_t)((4 * mt + (col >> 2)) * kBlockStride + kr * 256 +
                                                       16 * ((4 * j + quad + 2 * kr) & 15));
 #pragma unroll
-        for (int nn = 0; nn < 8; ++nn)
-          vro[mt][nn] = lds_offset(sbase) + (uint32_t)(kLdsTileBytes + (4 * mt + quad) * kBlockStride + vk * 256 +
-                                                       16 * ((2 * nn + (vm >> 1) + 2 * vk) & 15) + 8 * (vm & 1));
+        for (int nn = 0; nn < NB; ++nn)
+          vro[mt][nn] = lds_offset(sbase) +
+                        (uint32_t)(kLdsTileBytes + (4 * mt + quad) * kBlockStride + vk * 256 +
+                                   16 * ((2 * (nb0 + nn) + (vm >> 1) + 2 * vk) & 15) + 8 * (vm & 1));
       }
     }
     // `stage` is a compile-time constant, so its offset folds into the LDS
@@ -666,22 +697,26 @@ split_partial_kernel(Params p) {
   //      the W states for its 8/W blocks of 16 output dims -- maximum,
   //      weights, then sums taken in wave order, so the result is the same
   //      on every run -- and writes that slice of the output.
-  static_assert(8 % W == 0, "each wave merges a whole number of 16-dim blocks");
-  constexpr int NBW = 8 / W;
+  // With fewer blocks than waves (V slices) waves 0 .. NB - 1 merge one
+  // block each and the others only take part in the exchange.
+  static_assert(NB % W == 0 || W % NB == 0, "blocks must divide among the waves");
+  constexpr int NBW = NB >= W ? NB / W : 1;
+  constexpr int SV = 2 + 4 * NB;  // state values per lane and head tile: m, l, NB x 4 outputs
+  const bool merges = NB >= W || wave < NB;
   float lsum[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) lsum[nt] = sum_rows(l_run[nt]);
-  auto slot = [&](int w) { return reinterpret_cast<float*>(smem) + (size_t)w * (merge_slot_bytes(NT) / 4); };
+  auto slot = [&](int w) { return reinterpret_cast<float*>(smem) + (size_t)w * (NT * SV * 64); };
   __syncthreads();  // every wave is done with its stages
   {
     float* v0 = slot(wave) + lane;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      float* v = v0 + nt * kStateVals * 64;
+      float* v = v0 + nt * SV * 64;
       v[0] = m_run[nt];
       v[64] = lsum[nt];
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn)
+      for (int nn = 0; nn < NB; ++nn)
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[(2 + nn * 4 + i) * 64] = acc_o[nt][nn][i];
     }
@@ -700,49 +735,50 @@ split_partial_kernel(Params p) {
     float M = -INFINITY;
 #pragma unroll
     for (int k = 0; k < W; ++k) {
-      mk[k] = slot(k)[nt * kStateVals * 64 + lane];
+      mk[k] = slot(k)[nt * SV * 64 + lane];
       M = fmaxf(M, mk[k]);
     }
     float Lw = 0.f;
 #pragma unroll
     for (int k = 0; k < W; ++k) {
       wk[k] = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mk[k] - M);  // all empty: stays empty
-      Lw = fmaf(wk[k], slot(k)[(nt * kStateVals + 1) * 64 + lane], Lw);
+      Lw = fmaf(wk[k], slot(k)[(nt * SV + 1) * 64 + lane], Lw);
     }
-    // lane (col, quad) owns dims 16nn + 4quad + [0, 4) of head 16nt + col
+    // lane (col, quad) owns dims 16(nb0 + nn) + 4quad + [0, 4) of head
+    // 16nt + col, nn = wave * NBW + bb
     f32x4 o[NBW];
 #pragma unroll
     for (int bb = 0; bb < NBW; ++bb) {
-      const int nn = wave * NBW + bb;
+      const int nn = merges ? wave * NBW + bb : 0;
       o[bb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int k = 0; k < W; ++k)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          o[bb][i] = fmaf(wk[k], slot(k)[(nt * kStateVals + 2 + nn * 4 + i) * 64 + lane], o[bb][i]);
+          o[bb][i] = fmaf(wk[k], slot(k)[(nt * SV + 2 + nn * 4 + i) * 64 + lane], o[bb][i]);
     }
     const int h = nt * 16 + col;
-    if (h >= p.hpt) continue;
+    if (h >= p.hpt || !merges) continue;
     const int64_t row = row0_tile + h;
     const float mval = Lw > 0.f ? M * kLn2 : -INFINITY;
     if (direct) {
       const float inv = Lw > 0.f ? 1.0f / Lw : 0.f;
 #pragma unroll
       for (int bb = 0; bb < NBW; ++bb) {
-        const int nn = wave * NBW + bb;
+        const int nn = nb0 + wave * NBW + bb;
         *reinterpret_cast<uint2*>(p.out + row * D + 16 * nn + 4 * quad) =
             make_uint2(pack_bf16x2(o[bb][0] * inv, o[bb][1] * inv), pack_bf16x2(o[bb][2] * inv, o[bb][3] * inv));
       }
-      if (p.lse && wave == 0 && quad == 0) p.lse[row] = Lw > 0.f ? mval + logf(Lw) : -INFINITY;
+      if (p.lse && wave == 0 && quad == 0 && nb0 == 0) p.lse[row] = Lw > 0.f ? mval + logf(Lw) : -INFINITY;
     } else {
 #pragma unroll
       for (int bb = 0; bb < NBW; ++bb) {
-        const int nn = wave * NBW + bb;
+        const int nn = nb0 + wave * NBW + bb;
         const u32x4 bits = {__float_as_uint(o[bb][0]), __float_as_uint(o[bb][1]), __float_as_uint(o[bb][2]),
                             __float_as_uint(o[bb][3])};
         __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0, 0);
       }
-      if (wave == 0 && quad == 0) {
+      if (wave == 0 && quad == 0 && nb0 == 0) {
         p.m_part[srow0 + h] = mval;
         p.l_part[srow0 + h] = Lw;
       }
@@ -877,13 +913,28 @@ int ensure_gfx950(int* cus) {
   return DA_OK;
 }
 
-template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL>
+template <int NT, int W, int FETCH, bool PG, bool SCH, bool NTL, int VS = 1>
 const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG, SCH, NTL>);
+  return reinterpret_cast<const void*>(&split_partial_kernel<NT, W, FETCH, PG, SCH, NTL, VS>);
 }
 
 template <bool PG, bool SCH, bool NTL>
-const void* pick_kernel(int NT, int FETCH) {
+const void* pick_kernel(int NT, int FETCH, int VS) {
+  if (VS != 1) {
+    // V slices: direct-to-LDS fetch of uniform launches only
+    if constexpr (SCH) {
+      return nullptr;
+    } else {
+      if (FETCH != kFetchLds) return nullptr;
+      if (VS == 2)
+        return NT == 1 ? kernel_ptr<1, 4, kFetchLds, PG, SCH, NTL, 2>()
+                       : kernel_ptr<2, 4, kFetchLds, PG, SCH, NTL, 2>();
+      if (VS == 4)
+        return NT == 1 ? kernel_ptr<1, 4, kFetchLds, PG, SCH, NTL, 4>()
+                       : kernel_ptr<2, 4, kFetchLds, PG, SCH, NTL, 4>();
+      return nullptr;
+    }
+  }
   switch (FETCH * 2 + NT - 1) {
     case 0: return kernel_ptr<1, 4, kFetchDirect, PG, SCH, NTL>();
     case 1: return kernel_ptr<2, 4, kFetchDirect, PG, SCH, NTL>();
@@ -896,9 +947,10 @@ const void* pick_kernel(int NT, int FETCH) {
 }
 
 template <bool NTL>
-const void* pick_kernel(bool paged, bool scheduled, int NT, int FETCH) {
-  return paged ? (scheduled ? pick_kernel<true, true, NTL>(NT, FETCH) : pick_kernel<true, false, NTL>(NT, FETCH))
-               : (scheduled ? pick_kernel<false, true, NTL>(NT, FETCH) : pick_kernel<false, false, NTL>(NT, FETCH));
+const void* pick_kernel(bool paged, bool scheduled, int NT, int FETCH, int VS) {
+  if (paged)
+    return scheduled ? pick_kernel<true, true, NTL>(NT, FETCH, VS) : pick_kernel<true, false, NTL>(NT, FETCH, VS);
+  return scheduled ? pick_kernel<false, true, NTL>(NT, FETCH, VS) : pick_kernel<false, false, NTL>(NT, FETCH, VS);
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
@@ -909,9 +961,9 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   if (pl.kv_nontemporal != 0 && pl.kv_nontemporal != 1)
     return da::fail(DA_ERR_ARG, "plan asks for K/V cache hint %d", pl.kv_nontemporal);
   const bool paged = prm.block_table != nullptr, scheduled = prm.work != nullptr;
-  const void* fn = pl.kv_nontemporal ? pick_kernel<true>(paged, scheduled, NT, FETCH)
-                                     : pick_kernel<false>(paged, scheduled, NT, FETCH);
-  if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d", FETCH);
+  const void* fn = pl.kv_nontemporal ? pick_kernel<true>(paged, scheduled, NT, FETCH, pl.v_slices)
+                                     : pick_kernel<false>(paged, scheduled, NT, FETCH, pl.v_slices);
+  if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d with %d V slices", FETCH, pl.v_slices);
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
   if (rc) return rc;
@@ -974,9 +1026,10 @@ int check_plan(const da_plan* pl, int B, int H_Q, int H_KV) {
   if (!pl) return da::fail(DA_ERR_NULL, "plan is NULL");
   const int hpt = pl->heads_per_tile;
   if (pl->num_splits < 1 || pl->num_splits > DA_MAX_SPLITS || !da::heads_per_tile_valid(H_Q, H_KV, pl->pack_gqa, hpt) ||
-      (int64_t)pl->tiles != (int64_t)B * (H_Q / hpt) || (int64_t)pl->grid != (int64_t)pl->tiles * pl->num_splits ||
+      (int64_t)pl->tiles != (int64_t)B * (H_Q / hpt) ||
+      (int64_t)pl->grid != da::launch_grid((int64_t)pl->tiles * pl->num_splits, pl->v_slices) ||
       pl->group_waves != 4 || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
-      pl->kv_nontemporal > 1 || pl->num_cus < 1)
+      pl->kv_nontemporal > 1 || pl->num_cus < 1 || !da::v_slices_valid(H_Q, H_KV, *pl))
     return da::fail(DA_ERR_ARG, "plan does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   return DA_OK;
 }
@@ -1194,6 +1247,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
   pl.group_waves = 4;
   pl.kv_fetch = sched->kv_fetch;
   pl.kv_nontemporal = sched->kv_nontemporal;
+  pl.v_slices = 1;
   fill_params(p, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   p.xcd_group = 0;  // the schedule orders its workgroups itself
   p.work = static_cast<const int32_t*>(meta_dev);

@@ -49,7 +49,10 @@ bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt) {
 // than the fastest measured one; fitted on half of the shapes, it chooses
 // the other half within 0.3% on average.  Measured again after launches of
 // more workgroups than CUs moved to the register-staged fetch: 0.2% on
-// average, 5.1% at worst (a refit changed neither figure).
+// average, 5.1% at worst (a refit changed neither figure).  The V-slice
+// factors were fitted afterwards, the other constants held, to 16 shapes x
+// up to 8 split counts x 1, 2, 4 slices (warm: every choice within 2.9% of
+// the fastest measured launch, 0.2% on average; streamed: 5.3%, 1.1%).
 const CostModel& mi355x_model() {
   static const CostModel m = {
       /*base=*/{2.841, 4.042},
@@ -61,28 +64,30 @@ const CostModel& mi355x_model() {
       /*hbm0=*/0.006,
       /*pnorm=*/2.389,
       /*contig_tile=*/1.0,
+      /*vs_tile=*/{1.0, 0.812, 0.714},
   };
   return m;
 }
 
-// Time of one call with s chunks per sequence:
-//   compute = base + (workgroups per CU) x (32-key tiles per wave) x t_tile
+// Time of one call with s chunks per sequence, each shared by vs workgroups
+// (V slices):
+//   compute = base + (workgroups per CU) x (32-key tiles per wave) x t_tile x vs_tile[vs]
 //   stream  = hbm0 + (K/V bytes + chunk-state traffic) / hbm_rate
 //   T = (compute^p + stream^p)^(1/p) + [s > 1] (merge0 + merge1 s)
 // Every workgroup has four waves, one per SIMD, and walks a quarter of its
 // chunk each; workgroups that share a CU share its SIMDs.  The soft maximum
 // reflects that a CU's tile loop slows as the chip nears its HBM rate.
-double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus) {
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs) {
   const int wide = hpt > 16 ? 1 : 0;
   const double row_bytes = 2.0 * kHeadDim * 2.0;  // K and V row of one KV head
   const int64_t tiles = (int64_t)B * H_Q / hpt;
-  const int64_t wgs = tiles * s;
+  const int64_t wgs = launch_grid(tiles * s, vs);
   const int64_t chunk = ((int64_t)L_K + s - 1) / s;
   const int64_t per_wave = (chunk + 3) / 4;
   const int64_t tiles_per_wave = (per_wave + 31) / 32;
   const int64_t per_cu = (wgs + cus - 1) / cus;
   const double tt = (kv_fetch(wgs, cus, tiles_per_wave) == kLoneFetch ? m.t_tile_staged[wide] : m.t_tile[wide]) *
-                    (H_KV == 1 ? m.contig_tile : 1.0);
+                    (H_KV == 1 ? m.contig_tile : 1.0) * m.vs_tile[vs == 4 ? 2 : vs - 1];
   const double compute = m.base[wide] + (double)per_cu * (double)tiles_per_wave * tt;
   double bytes = (double)B * L_K * H_KV * row_bytes;
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
@@ -117,22 +122,49 @@ const CostModel& mi355x_streamed_model() {
       /*hbm0=*/3.366,
       /*pnorm=*/4.0,
       /*contig_tile=*/0.744,
+      /*vs_tile=*/{1.0, 0.943, 0.856},
   };
   return m;
 }
 
-static int mi355x_splits(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int cus) {
+// V slices for s chunks per sequence when `slices` allows them: 2 or 4
+// where the launch keeps one workgroup per CU, the call's K/V fit in L2 (so
+// that the slices' repeated K reads stay there; the slice factors were
+// measured on such calls) and the model puts them at least 1% ahead of one
+// slice; *t gets the modelled time.
+static int best_vslices(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, bool slices,
+                        double* t) {
+  const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, 1);
+  int best_vs = 1;
+  double best = one;
+  const int64_t tiles = (int64_t)B * H_Q / hpt;
+  slices = slices && (double)B * L_K * H_KV * (2.0 * kHeadDim * 2.0) <= (double)kL2Bytes;
+  for (int vs = 2; slices && vs <= 4 && launch_grid(tiles * s, vs) <= cus; vs *= 2) {
+    const double tv = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, vs);
+    if (tv < best && tv < kSplitGain * one) {
+      best = tv;
+      best_vs = vs;
+    }
+  }
+  *t = best;
+  return best_vs;
+}
+
+static int mi355x_splits(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int cus,
+                         bool slices = false) {
   if (L_K <= 0) return 1;
-  // Fastest modelled split count; the smallest one on an exact tie.  A
-  // split must be modelled at least 1% faster than one launch: closer than
-  // that the model cannot tell them apart, and a second launch that brings
-  // nothing is the one outcome the policy must avoid (never slower than one
-  // split).
-  const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, 1, cus);
+  // Fastest modelled split count (each with its best V slices); the
+  // smallest one on an exact tie.  A split must be modelled at least 1%
+  // faster than one launch: closer than that the model cannot tell them
+  // apart, and a second launch that brings nothing is the one outcome the
+  // policy must avoid (never slower than one split).
+  double one = 0.0;
+  best_vslices(m, B, H_Q, H_KV, L_K, hpt, 1, cus, slices, &one);
   int best_s = 1;
   double best = one;
   for (int s = 2; s <= kMaxSplits; ++s) {
-    const double ts = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus);
+    double ts = 0.0;
+    best_vslices(m, B, H_Q, H_KV, L_K, hpt, s, cus, slices, &ts);
     if (ts < best) {
       best = ts;
       best_s = s;
@@ -175,6 +207,12 @@ int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
   // (36 KB, three workgroups per CU) wins by up to 30%.
   if (grid <= cus) return kLoneFetch;
   return tiles_per_wave >= 2 ? 1 : 0;
+}
+
+bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl) {
+  if (pl.v_slices == 1) return true;
+  return (pl.v_slices == 2 || pl.v_slices == 4) && pl.kv_fetch == kLoneFetch && pl.pack_gqa != 2 &&
+         pl.heads_per_tile == H_Q / H_KV;
 }
 
 int kv_nontemporal(double key_rows, int readers) {
@@ -234,10 +272,14 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     // same keys.  The narrow tile is cheaper per workgroup and doubles the
     // workgroups, which pays while CUs are idle; the wide one reads each key
     // once per group.  Narrow is taken only when modelled at least 1% faster.
+    // V slices (the output dims of a chunk split over 2 or 4 workgroups that
+    // share its scores) are considered where one tile serves the group and
+    // not with the paper's packing (pack_gqa 2).
     const CostModel& m = policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model();
     auto best = [&](int h, double* t) {
-      const int sh = s > 0 ? s : mi355x_splits(m, B, H_Q, H_KV, L_K_max, h, cus);
-      *t = model_time(m, B, H_Q, H_KV, L_K_max, h, sh, cus);
+      const bool slices = pack != 2 && h == g;
+      const int sh = s > 0 ? s : mi355x_splits(m, B, H_Q, H_KV, L_K_max, h, cus, slices);
+      best_vslices(m, B, H_Q, H_KV, L_K_max, h, sh, cus, slices, t);
       return sh;
     };
     double t_wide = 0.0, t_narrow = 0.0;
@@ -251,20 +293,29 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
       s = s_wide;
     }
   }
+  int vs = 1;
+  if (policy == DA_POLICY_MI355X || policy == DA_POLICY_STREAMED) {
+    double t = 0.0;
+    vs = best_vslices(policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model(), B, H_Q, H_KV,
+                      L_K_max, hpt, s, cus, pack != 2 && hpt == g, &t);
+  }
   out->num_splits = s;
   out->pack_gqa = pack;
   out->heads_per_tile = hpt;
   out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
-  out->grid = (int32_t)((int64_t)out->tiles * s);
+  out->v_slices = vs;
+  out->grid = (int32_t)launch_grid((int64_t)out->tiles * s, vs);
   out->num_cus = cus;
   out->group_waves = group_waves(out->grid, cus);
   {
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
     out->kv_fetch = kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
   }
-  // STREAMED plans for K/V that are not resident whatever their size
-  out->kv_nontemporal = policy == DA_POLICY_STREAMED ? (g / hpt == 1 ? 1 : 0)
-                                                     : kv_nontemporal((double)B * L_K_max * H_KV, g / hpt);
+  // STREAMED plans for K/V that are not resident whatever their size.  The
+  // V slices of a chunk all read its keys, as the head tiles of a group do.
+  const int readers = (g / hpt) * vs;
+  out->kv_nontemporal = policy == DA_POLICY_STREAMED ? (readers == 1 ? 1 : 0)
+                                                     : kv_nontemporal((double)B * L_K_max * H_KV, readers);
   return DA_OK;
 }
 

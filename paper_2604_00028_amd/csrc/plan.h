@@ -15,6 +15,7 @@ constexpr int kHeadDim = DA_HEAD_DIM;
 constexpr int kMaxSplits = DA_MAX_SPLITS;
 constexpr int kMaxHeadsPerTile = 32;   // two 16-column MFMA head tiles per workgroup
 constexpr int kNarrowHeadsPerTile = 16; // one 16-column MFMA head tile per workgroup
+constexpr int64_t kL2Bytes = 8ll << 22;  // MI355X: 4 MiB of L2 on each of 8 XCDs
 
 // Records a printf-style message for da_last_error() and returns `code`.
 int fail(int code, const char* fmt, ...);
@@ -47,6 +48,7 @@ struct CostModel {
   double hbm0;             // fixed part of the streaming bound
   double pnorm;            // the two bounds combine as (compute^p + stream^p)^(1/p)
   double contig_tile;      // tile times scale by this when a key row holds one KV head (H_KV = 1)
+  double vs_tile[3];       // tile times scale by this with 1, 2 or 4 V slices per chunk
 };
 const CostModel& mi355x_model();
 // The same model for K/V streamed from HBM on every call (policy STREAMED).
@@ -57,7 +59,19 @@ const CostModel& mi355x_streamed_model();
 constexpr double kSplitGain = 0.99;
 
 // Modelled time (us) of one call with s splits (policy MI355X).
-double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus);
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs = 1);
+
+// Whether `pl` may serve each chunk with pl.v_slices workgroups (1, 2 or 4):
+// more than one only with K/V straight into LDS, one tile per group and
+// not the paper's packing (pack_gqa 2).
+bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl);
+
+// Workgroups launched for `chunks` (tile, chunk) pairs with vs V slices:
+// with slices, whole groups of 8 chunks, so that a chunk's slices share an
+// XCD (the padding workgroups return at once).
+inline int64_t launch_grid(int64_t chunks, int vs) {
+  return vs == 1 ? chunks : (int64_t)vs * 8 * ((chunks + 7) / 8);
+}
 
 // Waves per workgroup for a launch of `grid` workgroups on `cus` CUs.
 int group_waves(int64_t grid, int cus);

@@ -16,6 +16,12 @@ from paper_2604_00028_amd import _binding as bnd
 from oracle import even_bounds, evolved_split_policy, paper_split_policy
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def launch_grid(chunks, vs):
+    """Workgroups of a launch of `chunks` (tile, chunk) pairs with vs V slices
+    (with slices, whole groups of 8 chunks)."""
+    return chunks if vs == 1 else vs * 8 * -(-chunks // 8)
 HEADER = os.path.join(ROOT, "include", "decode_attn.h")
 GOLDEN = os.path.join(ROOT, "tests", "golden", "paper_policy.json")
 
@@ -158,8 +164,11 @@ def test_paper_policy_reproduces_the_paper_table():
         if c["s"] is not None:
             assert plan.num_splits == c["s"], c
         else:
-            mi = da.da_choose_splits(c["B"], H_Q, c["H_KV"], c["L_K"], num_cus=256, policy=da.POLICY_MI355X)
-            assert plan.num_splits == mi.num_splits, c
+            # past its rule the paper defers to the stack's own choice: the MI355X cost model for the
+            # paper's launch shape (one workgroup per KV head and chunk, no V slices)
+            mi = da.da_make_plan(c["B"], H_Q, c["H_KV"], c["L_K"], num_splits=0, pack_gqa=2, num_cus=256,
+                                 policy=da.POLICY_MI355X)
+            assert plan.num_splits == mi.num_splits and plan.v_slices == mi.v_slices == 1, c
 
 
 def test_evolved_policy_reproduces_the_paper_figure():
@@ -192,7 +201,7 @@ def test_paper_policy_matches_the_oracle_rule_on_a_grid():
 def test_plan_fields_and_packing():
     p = da.da_choose_splits(1, 64, 8, 512, num_cus=256)
     assert p.pack_gqa == 1 and p.heads_per_tile == 8 and p.tiles == 8
-    assert p.grid == p.tiles * p.num_splits and p.num_cus == 256
+    assert p.grid == launch_grid(p.tiles * p.num_splits, p.v_slices) and p.num_cus == 256
     p = da.da_make_plan(1, 64, 8, 512, num_splits=4, pack_gqa=0, num_cus=256)
     assert (p.num_splits, p.pack_gqa, p.heads_per_tile, p.tiles, p.grid) == (4, 0, 1, 64, 256)
     p = da.da_choose_splits(4, 32, 1, 256, num_cus=256)          # g = 32, 4 KV heads: two 16-head tiles each
@@ -210,17 +219,18 @@ def test_plan_fields_and_packing():
 
 
 def test_fetch_mode_follows_workgroups_per_cu():
+    # (the paper's packing, pack_gqa = 2, so that no V slices multiply the grid)
     # direct-to-LDS with two tiles in flight when every workgroup has a CU to
     # itself; K and V through registers into LDS (two workgroups per CU) otherwise
     for s, fetch in [(1, 2), (4, 2), (5, 1), (16, 1), (64, 0)]:
-        p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=1, num_cus=256)   # 64 tiles
+        p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=2, num_cus=256)   # 64 tiles
         assert p.grid == 64 * s and p.kv_fetch == fetch and p.group_waves == 4, (s, p.as_dict())
-    p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=1, num_cus=256, cu_margin=1)
+    p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=2, num_cus=256, cu_margin=1)
     assert p.kv_fetch == 1
     # one 32-key tile per wave (chunks of at most 128 keys): the operand-layout fetch
-    p = da.da_make_plan(8, 64, 8, 512, num_splits=8, pack_gqa=1, num_cus=256)
+    p = da.da_make_plan(8, 64, 8, 512, num_splits=8, pack_gqa=2, num_cus=256)
     assert p.grid == 512 and p.kv_fetch == 0
-    p = da.da_make_plan(8, 64, 8, 1024, num_splits=4, pack_gqa=1, num_cus=256)
+    p = da.da_make_plan(8, 64, 8, 1024, num_splits=4, pack_gqa=2, num_cus=256)
     assert p.grid == 256 and p.kv_fetch == 2
 
 
@@ -314,7 +324,7 @@ def test_planned_entry_checks_the_plan():
     good = da.da_make_plan(2, 64, 8, 512, num_splits=4, pack_gqa=1, num_cus=256)
     for field, val in (("num_splits", 0), ("num_splits", 65), ("heads_per_tile", 4), ("heads_per_tile", 0),
                        ("tiles", 15), ("grid", 63), ("group_waves", 8), ("kv_fetch", 3), ("kv_nontemporal", 2),
-                       ("num_cus", 0), ("pack_gqa", 3)):
+                       ("num_cus", 0), ("pack_gqa", 3), ("v_slices", 3), ("v_slices", 0)):
         bad = bnd.DaPlan.from_buffer_copy(good)
         setattr(bad, field, val)
         assert call(bad) == bnd.DA_ERR_ARG, field
@@ -326,13 +336,44 @@ def test_planned_entry_checks_the_plan():
 
 
 def test_streamed_policy_marks_loads_nontemporal():
-    # the streamed policy plans for K/V that are never resident
-    p = da.da_choose_splits(1, 64, 8, 512, num_cus=256, policy=da.POLICY_STREAMED)
-    assert p.kv_nontemporal == 1
-    assert da.da_choose_splits(1, 64, 8, 512, num_cus=256).kv_nontemporal == 0
-    # unless several workgroups read each key
+    # the streamed policy plans for K/V that are never resident: nontemporal
+    # loads wherever one workgroup reads each key (one tile per group, one V slice)
+    p = da.da_make_plan(1, 64, 8, 512, num_splits=0, pack_gqa=2, num_cus=256, policy=da.POLICY_STREAMED)
+    assert p.kv_nontemporal == 1 and p.v_slices == 1
+    assert da.da_make_plan(1, 64, 8, 512, num_splits=0, pack_gqa=2, num_cus=256).kv_nontemporal == 0
+    for B, H_Q, H_KV, L in [(1, 64, 8, 512), (1, 8, 1, 4096), (32, 64, 8, 8192), (4, 32, 1, 256)]:
+        p = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256, policy=da.POLICY_STREAMED)
+        assert p.kv_nontemporal == int(p.v_slices == 1 and p.heads_per_tile == H_Q // H_KV), p.as_dict()
+    # packing off: several workgroups read each key
     p = da.da_make_plan(1, 64, 8, 512, num_splits=1, pack_gqa=0, num_cus=256, policy=da.POLICY_STREAMED)
     assert p.kv_nontemporal == 0
+
+
+def test_v_slices():
+    # chunks shared by 2 or 4 workgroups (each its part of the output dims)
+    # where a launch keeps one workgroup per CU and one tile serves the group
+    for B, H_Q, H_KV, L in [(1, 64, 8, 512), (1, 64, 8, 128), (4, 64, 8, 512), (1, 8, 1, 512), (16, 32, 4, 512),
+                            (32, 64, 8, 8192), (1, 32, 1, 512), (8, 64, 8, 4096)]:
+        for policy in (da.POLICY_MI355X, da.POLICY_STREAMED):
+            p = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256, policy=policy)
+            assert p.v_slices in (1, 2, 4) and p.grid == launch_grid(p.tiles * p.num_splits, p.v_slices)
+            if p.v_slices > 1:
+                assert p.grid <= 256 and p.kv_fetch == 2 and p.heads_per_tile == H_Q // H_KV
+    assert da.da_choose_splits(1, 64, 8, 512, num_cus=256).v_slices == 4
+    assert da.da_choose_splits(32, 64, 8, 8192, num_cus=256).v_slices == 1       # the grid fills the chip
+    assert da.da_choose_splits(1, 32, 1, 512, num_cus=256).v_slices == 1         # two 16-head tiles per group
+    # the paper's packing and policies keep one workgroup per chunk
+    assert da.da_make_plan(1, 64, 8, 512, num_splits=0, pack_gqa=2, num_cus=256).v_slices == 1
+    for policy in (da.POLICY_PAPER, da.POLICY_EVOLVED):
+        assert da.da_choose_splits(1, 64, 8, 512, num_cus=256, policy=policy).v_slices == 1
+    # a forced split count still takes its best slices
+    p = da.da_make_plan(1, 64, 8, 512, num_splits=1, pack_gqa=1, num_cus=256)
+    assert (p.num_splits, p.v_slices, p.grid) == (1, 4, 32)
+    # the slices of a chunk share an XCD: whole groups of 8 chunks, the rest idle
+    p = da.da_make_plan(1, 8, 1, 512, num_splits=1, pack_gqa=1, num_cus=256)
+    assert (p.tiles, p.v_slices, p.grid) == (1, 4, 32)
+    # calls whose K/V exceed L2 keep one workgroup per chunk
+    assert da.da_choose_splits(4, 256, 32, 2048, num_cus=256).v_slices == 1
 
 
 def test_cu_margin_and_plan_errors():

@@ -37,8 +37,8 @@ def same_bits(a, b):
 ])
 def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
     """Plans from each policy, with and without a CU margin and with every
-    K/V fetch path and cache hint edited in: oracle parity, and the same bits
-    for the same split count and head tiles."""
+    K/V fetch path, V slice count and cache hint edited in: oracle parity,
+    and the same bits for the same split count and head tiles."""
     sh = custom_shape(B, H_Q, H_KV, L, varlen=varlen)
     inp = make_inputs(sh, seed=B * 31 + L)
     O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
@@ -48,11 +48,16 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
     plans.append(da.da_choose_splits(B, H_Q, H_KV, L, cu_margin=200))
     plans += [da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pk) for s in (1, 3) for pk in (0, 1, 2)]
     first = {}
+    g = H_Q // H_KV
     for plan in plans:
-        for fetch in (0, 1, 2):
+        # V slices only with K/V straight into LDS, one tile per group and not the paper's packing
+        vss = (1, 2, 4) if plan.heads_per_tile == g and plan.pack_gqa != 2 else (1,)
+        for fetch, vs in [(0, 1), (1, 1)] + [(2, v) for v in vss]:
             for hint in (0, 1):
                 p = da.DaPlan.from_buffer_copy(plan)
-                p.kv_fetch, p.kv_nontemporal = fetch, hint
+                p.kv_fetch, p.kv_nontemporal, p.v_slices = fetch, hint, vs
+                chunks = p.tiles * p.num_splits
+                p.grid = chunks if vs == 1 else vs * 8 * -(-chunks // 8)
                 say(f"planned B{B}-H{H_Q}-KV{H_KV}-L{L} {p.as_dict()}")
                 got = planned(q, k, v, cu, L, p)
                 assert_parity(got[0], O, f"planned {p.as_dict()}")
