@@ -75,6 +75,8 @@ def parse():
                     help="time only the planned launch of one workload, or a plain 1 GiB device copy "
                          "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
+    ap.add_argument("--pack-gqa", type=int, default=-1,
+                    help="with --only: force pack_gqa (2: one workgroup per KV head and chunk, the paper's launch)")
     ap.add_argument("--regression", metavar="OUT_JSON", default=None,
                     help="time the paper's 160-configuration regression matrix (heuristic, num_splits=1, the "
                          "paper's policy and fixed splits) and write the results to OUT_JSON")
@@ -571,7 +573,7 @@ def only_run(args, da, torch, np, dev):
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
     del inp
     K = args.highload_steps if args.only == "highload" else args.steps
-    var = Variant(args.only, da, torch, q, k, v, sh.L_K, args.num_splits, -1, K)
+    var = Variant(args.only, da, torch, q, k, v, sh.L_K, args.num_splits, args.pack_gqa, K)
     interleave(torch, [var], args.rounds)
     nbytes = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
     gbs = nbytes / (var.median * 1e-6) / 1e9
@@ -642,12 +644,16 @@ def traffic_summary(d: str) -> None:
     print(json.dumps(out))
 
 
-OCC_CASES = (  # (case, --only workload, extra flags, label)
-    ("headline_heur", "headline", "", "Llama-70B GQA B=1 L_K=512, heuristic"),
+OCC_CASES = (  # (case, --only workload, extra flags, label); s = 1 as the paper launches it
+    ("headline_heur", "headline", "", "Llama-70B GQA B=1 L_K=512, heuristic (s=1, 4 V slices)"),
+    ("headline_s1", "headline", "--num-splits 1 --pack-gqa 2",
+     "Llama-70B GQA B=1 L_K=512, num_splits=1, one workgroup per KV head"),
     ("long2048_heur", "long", "--lk 2048", "Llama-70B GQA B=1 L_K=2048, heuristic"),
-    ("long2048_s1", "long", "--lk 2048 --num-splits 1", "Llama-70B GQA B=1 L_K=2048, num_splits=1"),
+    ("long2048_s1", "long", "--lk 2048 --num-splits 1 --pack-gqa 2",
+     "Llama-70B GQA B=1 L_K=2048, num_splits=1, one workgroup per KV head"),
     ("long8192_heur", "long", "--lk 8192", "Llama-70B GQA B=1 L_K=8192, heuristic"),
-    ("long8192_s1", "long", "--lk 8192 --num-splits 1", "Llama-70B GQA B=1 L_K=8192, num_splits=1"),
+    ("long8192_s1", "long", "--lk 8192 --num-splits 1 --pack-gqa 2",
+     "Llama-70B GQA B=1 L_K=8192, num_splits=1, one workgroup per KV head"),
     ("highload_heur", "highload", "", "high load B=32 L_K=8192, heuristic"),
     ("highload_s4", "highload", "--num-splits 4", "high load B=32 L_K=8192, num_splits=4"),
 )
