@@ -179,9 +179,12 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
  * need (for plan->num_splits) as in da_decode_attn.  Errors as there, plus
  * DA_ERR_NULL (plan NULL) and DA_ERR_ARG (the plan does not describe a launch
  * of this shape: num_splits outside 1..64, a heads_per_tile its pack_gqa
- * cannot produce, tiles != B*H_Q/heads_per_tile, grid != tiles*num_splits,
+ * cannot produce, tiles != B*H_Q/heads_per_tile, a grid other than the one
+ * the da_plan.grid comment gives for its tiles, num_splits and v_slices,
  * group_waves != 4, kv_fetch outside 0..2, kv_nontemporal outside 0..1,
- * num_cus < 1), all before any device access. */
+ * num_cus < 1, v_slices other than 1, 2 or 4, or v_slices > 1 with a
+ * kv_fetch other than 2, pack_gqa 2 or heads_per_tile below the group),
+ * all before any device access. */
 int da_decode_attn_planned(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                            void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                            float softmax_scale, const da_plan* plan, void* workspace,
@@ -210,6 +213,19 @@ int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache
                          float* lse_out, int B, int H_Q, int H_KV, int page_size, int max_pages,
                          int num_pages, int L_K_max, int d, float softmax_scale, int num_splits,
                          int pack_gqa, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Paged decode attention that runs a plan made beforehand, as
+ * da_decode_attn_planned does for contiguous K/V (Section 5.1: scheduler
+ * metadata precomputed on the host).  Paged arguments as for
+ * da_decode_attn_paged; plan, workspace and errors as for
+ * da_decode_attn_planned.  This is how a STREAMED plan or one made with a
+ * cu_margin reaches a paged cache with one split count for the batch. */
+int da_decode_attn_paged_planned(const void* q, const void* k_cache, const void* v_cache,
+                                 const int32_t* block_table, const int32_t* seq_lens, void* out,
+                                 float* lse_out, int B, int H_Q, int H_KV, int page_size,
+                                 int max_pages, int num_pages, int L_K_max, int d,
+                                 float softmax_scale, const da_plan* plan, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* Per-sequence scheduler metadata: the precomputed scheduling of Section 5.1
  * carried down to one split count per sequence, so that in a batch of mixed

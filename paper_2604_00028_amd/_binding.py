@@ -38,7 +38,8 @@ POLICY_STREAMED = 3
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (
     "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
-    "da_decode_attn_planned", "da_decode_attn_paged", "da_schedule_max_bytes", "da_make_schedule", "da_schedule_workspace_bytes",
+    "da_decode_attn_planned", "da_decode_attn_paged", "da_decode_attn_paged_planned", "da_schedule_max_bytes",
+    "da_make_schedule", "da_schedule_workspace_bytes",
     "da_decode_attn_scheduled", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror",
     "da_last_error",
 )
@@ -125,6 +126,9 @@ def load() -> ctypes.CDLL:
     lib.da_decode_attn_paged.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
                                          _P, _Z, _P]
     lib.da_decode_attn_paged.restype = _I
+    lib.da_decode_attn_paged_planned.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F,
+                                                 ctypes.POINTER(DaPlan), _P, _Z, _P]
+    lib.da_decode_attn_paged_planned.restype = _I
     lib.da_schedule_max_bytes.argtypes = [_I, _I, _I, _I]
     lib.da_schedule_max_bytes.restype = _Z
     lib.da_make_schedule.argtypes = [_P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _P, _Z, ctypes.POINTER(DaSchedule)]
@@ -294,13 +298,8 @@ def da_decode_attn_planned(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pl
     return out
 
 
-def da_decode_attn_paged(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
-                         seq_lens: torch.Tensor, L_K_max: int, out: Optional[torch.Tensor] = None,
-                         lse_out: Optional[torch.Tensor] = None, *, softmax_scale: float = 0.0, num_splits: int = 0,
-                         pack_gqa: int = -1, workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """Decode attention over a paged KV cache; returns `out`.
-    k_cache, v_cache: [num_pages, page_size, H_KV, d] bf16; block_table: [B, max_pages] int32;
-    seq_lens: [B] int32; L_K_max: host-known longest sequence."""
+def _paged_args(q, k_cache, v_cache, block_table, seq_lens):
+    """Check a paged call's tensors; (B, H_Q, H_KV, d, page_size, max_pages, num_pages)."""
     for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache)):
         if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
             raise ValueError(f"{name} must be a contiguous bfloat16 CUDA tensor")
@@ -313,7 +312,17 @@ def da_decode_attn_paged(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
     num_pages, page_size, H_KV, dk = k_cache.shape
     if dk != d or block_table.dim() != 2 or block_table.shape[0] != B or seq_lens.numel() != B:
         raise ValueError("block_table must be [B, max_pages], seq_lens [B], and the head dims must agree")
-    max_pages = block_table.shape[1]
+    return B, H_Q, H_KV, d, page_size, block_table.shape[1], num_pages
+
+
+def da_decode_attn_paged(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
+                         seq_lens: torch.Tensor, L_K_max: int, out: Optional[torch.Tensor] = None,
+                         lse_out: Optional[torch.Tensor] = None, *, softmax_scale: float = 0.0, num_splits: int = 0,
+                         pack_gqa: int = -1, workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Decode attention over a paged KV cache; returns `out`.
+    k_cache, v_cache: [num_pages, page_size, H_KV, d] bf16; block_table: [B, max_pages] int32;
+    seq_lens: [B] int32; L_K_max: host-known longest sequence."""
+    B, H_Q, H_KV, d, page_size, max_pages, num_pages = _paged_args(q, k_cache, v_cache, block_table, seq_lens)
     dev = q.device
     if out is None:
         out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
@@ -328,6 +337,29 @@ def da_decode_attn_paged(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.
                                        _ptr(out), _ptr(lse_out), B, H_Q, H_KV, page_size, max_pages, num_pages,
                                        int(L_K_max), d, float(softmax_scale), int(num_splits), int(pack_gqa),
                                        _ptr(workspace), ws_bytes, s_handle))
+    return out
+
+
+def da_decode_attn_paged_planned(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                                 block_table: torch.Tensor, seq_lens: torch.Tensor, L_K_max: int, plan: DaPlan,
+                                 out: Optional[torch.Tensor] = None, lse_out: Optional[torch.Tensor] = None, *,
+                                 softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None,
+                                 stream=None) -> torch.Tensor:
+    """da_decode_attn_paged with a plan made beforehand, run exactly as it is."""
+    B, H_Q, H_KV, d, page_size, max_pages, num_pages = _paged_args(q, k_cache, v_cache, block_table, seq_lens)
+    dev = q.device
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=dev)
+    s_handle = _stream(dev, stream)
+    if workspace is None:
+        nbytes = da_workspace_bytes(B, H_Q, d, plan.num_splits)
+        if nbytes:
+            workspace = workspace_for(dev, s_handle, nbytes)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().da_decode_attn_paged_planned(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(block_table),
+                                               _ptr(seq_lens), _ptr(out), _ptr(lse_out), B, H_Q, H_KV, page_size,
+                                               max_pages, num_pages, int(L_K_max), d, float(softmax_scale),
+                                               ctypes.byref(plan), _ptr(workspace), ws_bytes, s_handle))
     return out
 
 

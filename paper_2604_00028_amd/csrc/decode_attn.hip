@@ -1109,6 +1109,20 @@ int check_paged(const void* q, const void* k_cache, const void* v_cache, const i
   return DA_OK;
 }
 
+// Shape, pointer and layout checks of the paged entry points.
+int check_paged_inputs(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+                       const int32_t* seq_lens, int B, int H_Q, int H_KV, int page_size, int max_pages,
+                       int num_pages, int L_K_max, int d) {
+  int rc = da::check_shape(B, H_Q, H_KV, L_K_max, d);
+  if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
+  if (!block_table || !seq_lens) return da::fail(DA_ERR_NULL, "block_table and seq_lens must be non-NULL");
+  // With L_K_max == 0 no key is ever read, so empty pools may be NULL.
+  if ((!k_cache || !v_cache) && !(rc == DA_OK && L_K_max == 0))
+    return da::fail(DA_ERR_NULL, "k_cache and v_cache must be non-NULL");
+  if (rc) return rc;
+  return check_paged(q, k_cache, v_cache, block_table, seq_lens, B, page_size, max_pages, num_pages, L_K_max);
+}
+
 void set_paged(Params& p, const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
                const int32_t* seq_lens, int page_size, int max_pages, int num_pages) {
   p.q = static_cast<const uint16_t*>(q);
@@ -1168,18 +1182,30 @@ int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache
                          int page_size, int max_pages, int num_pages, int L_K_max, int d, float softmax_scale,
                          int num_splits, int pack_gqa, void* workspace, size_t workspace_bytes, void* stream) {
   da::clear_error();
-  int rc = da::check_shape(B, H_Q, H_KV, L_K_max, d);
-  if (!q) return da::fail(DA_ERR_NULL, "q must be non-NULL");
-  if (!block_table || !seq_lens) return da::fail(DA_ERR_NULL, "block_table and seq_lens must be non-NULL");
-  if ((!k_cache || !v_cache) && !(rc == DA_OK && L_K_max == 0))
-    return da::fail(DA_ERR_NULL, "k_cache and v_cache must be non-NULL");
-  if (rc) return rc;
-  rc = check_paged(q, k_cache, v_cache, block_table, seq_lens, B, page_size, max_pages, num_pages, L_K_max);
+  int rc = check_paged_inputs(q, k_cache, v_cache, block_table, seq_lens, B, H_Q, H_KV, page_size, max_pages,
+                              num_pages, L_K_max, d);
   if (rc) return rc;
   Params p{};
   set_paged(p, q, k_cache, v_cache, block_table, seq_lens, page_size, max_pages, num_pages);
   return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, num_splits, pack_gqa, out, lse_out, workspace,
                     workspace_bytes, stream);
+}
+
+int da_decode_attn_paged_planned(const void* q, const void* k_cache, const void* v_cache,
+                                 const int32_t* block_table, const int32_t* seq_lens, void* out, float* lse_out,
+                                 int B, int H_Q, int H_KV, int page_size, int max_pages, int num_pages, int L_K_max,
+                                 int d, float softmax_scale, const da_plan* plan, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  da::clear_error();
+  int rc = check_paged_inputs(q, k_cache, v_cache, block_table, seq_lens, B, H_Q, H_KV, page_size, max_pages,
+                              num_pages, L_K_max, d);
+  if (rc) return rc;
+  rc = check_plan(plan, B, H_Q, H_KV);
+  if (rc) return rc;
+  Params p{};
+  set_paged(p, q, k_cache, v_cache, block_table, seq_lens, page_size, max_pages, num_pages);
+  return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, plan->num_splits, plan->pack_gqa, out, lse_out,
+                    workspace, workspace_bytes, stream, plan);
 }
 
 int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
@@ -1201,7 +1227,6 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
     if (rc) return rc;
   }
   // the schedule must describe a launch of this shape
-  const int g = H_Q / H_KV;
   const int hpt = sched->heads_per_tile;
   if (!da::heads_per_tile_valid(H_Q, H_KV, sched->pack_gqa, hpt) ||
       sched->tiles != B * (H_Q / hpt) || sched->num_items < sched->tiles ||
@@ -1211,7 +1236,6 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
       (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 ||
       (sched->max_splits > 1) != (sched->state_rows > 0))
     return da::fail(DA_ERR_ARG, "schedule does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
-  (void)g;
   if (!meta_dev) return da::fail(DA_ERR_NULL, "meta_dev must be non-NULL");
   if (!aligned(meta_dev, 16)) return da::fail(DA_ERR_ALIGN, "meta_dev must be 16-byte aligned");
   if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");

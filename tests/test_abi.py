@@ -335,6 +335,29 @@ def test_planned_entry_checks_the_plan():
     assert call(good, ws=0, ws_bytes=0) == bnd.DA_ERR_WORKSPACE
 
 
+def test_paged_planned_entry_checks_arguments():
+    lib = da.load()
+    FAKE = 1 << 20
+    P = ctypes.c_void_p
+    good = da.da_make_plan(2, 64, 8, 512, num_splits=4, pack_gqa=1, num_cus=256)
+
+    def call(plan, B=2, H_Q=64, H_KV=8, L=512, page=64, max_pages=8, bt=FAKE, ws=FAKE, ws_bytes=1 << 30):
+        return lib.da_decode_attn_paged_planned(P(FAKE), P(FAKE), P(FAKE), P(bt) if bt else None, P(FAKE), P(FAKE),
+                                                None, B, H_Q, H_KV, page, max_pages, 64, L, 128, 0.0,
+                                                ctypes.byref(plan) if plan is not None else None, P(ws), ws_bytes,
+                                                None)
+    assert call(None) == bnd.DA_ERR_NULL
+    assert call(good, bt=0) == bnd.DA_ERR_NULL
+    assert call(good, page=48) == bnd.DA_ERR_UNSUPPORTED          # not a multiple of 32 keys
+    assert call(good, max_pages=7) == bnd.DA_ERR_SHAPE            # 7 pages of 64 < 512 keys
+    for field, val in (("num_splits", 0), ("grid", 63), ("kv_fetch", 3), ("v_slices", 3)):
+        bad = bnd.DaPlan.from_buffer_copy(good)
+        setattr(bad, field, val)
+        assert call(bad) == bnd.DA_ERR_ARG, field
+    assert call(good, B=3, max_pages=8) == bnd.DA_ERR_ARG         # a plan for another shape
+    assert call(good, ws=0, ws_bytes=0) == bnd.DA_ERR_WORKSPACE
+
+
 def test_streamed_policy_marks_loads_nontemporal():
     # the streamed policy plans for K/V that are never resident: nontemporal
     # loads wherever one workgroup reads each key (one tile per group, one V slice)

@@ -219,3 +219,45 @@ def test_highload_paged_full_size():
         a = da.da_decode_attn(q, k, v, L_K_max=sh.L_K, num_splits=s, pack_gqa=1)
         b, _ = run_paged(q, kc, vc, bt, sl, sh.L_K, s, 1)
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("B,H_Q,H_KV,lengths,page", [
+    (1, 64, 8, [512], 64),                # Llama-70B shape, one sequence
+    (3, 32, 1, [777, 40, 300], 32),       # a group of 32: two tile widths
+    (4, 12, 4, [31, 32, 33, 95], 96),     # group of 3, lengths around a tile
+])
+def test_paged_planned_plans_of_every_kind(B, H_Q, H_KV, lengths, page):
+    """Plans made beforehand (each policy, a CU margin, forced splits and
+    packings, every fetch path, V slice count and cache hint edited in) run
+    on a paged cache: oracle parity, and the bits of the planning paged entry
+    point for the same split count and packing."""
+    sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
+    inp = make_inputs(sh, seed=B * 7 + page, lengths=lengths)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    pg = paged_layout(inp, page, seed=page + 3)
+    q = to_dev(inp.q)
+    kc, vc, bt, sl = dev_paged(pg)
+    L = max(lengths)
+    plans = [da.da_choose_splits(B, H_Q, H_KV, L, policy=pol)
+             for pol in (da.POLICY_MI355X, da.POLICY_STREAMED, da.POLICY_PAPER)]
+    plans.append(da.da_choose_splits(B, H_Q, H_KV, L, cu_margin=200))
+    plans += [da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pk) for s in (1, 4) for pk in (0, 1, 2)]
+    g = H_Q // H_KV
+    for plan in plans:
+        ref = run_paged(q, kc, vc, bt, sl, L, plan.num_splits, plan.pack_gqa)
+        vss = (1, 2, 4) if plan.heads_per_tile == g and plan.pack_gqa != 2 else (1,)
+        for fetch, vs in [(0, 1), (1, 1)] + [(2, v) for v in vss]:
+            for hint in (0, 1):
+                p = da.DaPlan.from_buffer_copy(plan)
+                p.kv_fetch, p.kv_nontemporal, p.v_slices = fetch, hint, vs
+                chunks = p.tiles * p.num_splits
+                p.grid = chunks if vs == 1 else vs * 8 * -(-chunks // 8)
+                say(f"paged planned B{B}-H{H_Q}-KV{H_KV}-{lengths} page={page} {p.as_dict()}")
+                lse_t = torch.empty(B, H_Q, dtype=torch.float32, device="cuda")
+                out = da.da_decode_attn_paged_planned(q, kc, vc, bt, sl, L, p, lse_out=lse_t)
+                torch.cuda.synchronize()
+                assert_parity(out, O, f"paged planned {p.as_dict()}")
+                check_lse(lse_t, lse)
+                # neither the tile width, the fetch path, V slices nor the hint change the bits
+                assert torch.equal(out.view(torch.int16), ref[0].view(torch.int16)), p.as_dict()
+                assert torch.equal(lse_t, ref[1]), p.as_dict()
