@@ -101,7 +101,7 @@ typedef struct da_plan {
                              = H_Q/H_KV, v_slices = 1); 0: ordinary loads */
   int32_t v_slices;       /* workgroups that share each chunk: each computes the chunk's scores and
                              128/v_slices of the output dims (1, 2 or 4; more than 1 only with
-                             kv_fetch 2, heads_per_tile = H_Q/H_KV and pack_gqa != 2).  The
+                             kv_fetch 2 and pack_gqa 1, or pack_gqa 0 when H_Q = H_KV).  The
                              policies MI355X and STREAMED choose it where a launch keeps one
                              workgroup per CU and its K/V fit in L2; results are the same bits
                              for every value. */
@@ -183,7 +183,7 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
  * the da_plan.grid comment gives for its tiles, num_splits and v_slices,
  * group_waves != 4, kv_fetch outside 0..2, kv_nontemporal outside 0..1,
  * num_cus < 1, v_slices other than 1, 2 or 4, or v_slices > 1 with a
- * kv_fetch other than 2, pack_gqa 2 or heads_per_tile below the group),
+ * kv_fetch other than 2, with pack_gqa 2, or unpacked with H_Q != H_KV),
  * all before any device access. */
 int da_decode_attn_planned(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                            void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,

@@ -53,6 +53,10 @@ bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt) {
 // factors were fitted afterwards, the other constants held, to 16 shapes x
 // up to 8 split counts x 1, 2, 4 slices (warm: every choice within 2.9% of
 // the fastest measured launch, 0.2% on average; streamed: 5.3%, 1.1%).
+// Held unchanged for 16-head tiles of wider groups, they pick the fastest
+// of 2 widths x 4 split counts x 1, 2, 4 slices on all 15 shapes of a
+// second sweep (groups of 32 to 64 heads, L_K 64 to 2048; streamed: 1.9%
+// from the fastest on average, 14% at worst).
 const CostModel& mi355x_model() {
   static const CostModel m = {
       /*base=*/{2.841, 4.042},
@@ -211,8 +215,10 @@ int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
 
 bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl) {
   if (pl.v_slices == 1) return true;
-  return (pl.v_slices == 2 || pl.v_slices == 4) && pl.kv_fetch == kLoneFetch && pl.pack_gqa != 2 &&
-         pl.heads_per_tile == H_Q / H_KV;
+  // direct-to-LDS launches only; not the paper's packing, and unpacked only
+  // where one head is the whole group
+  return (pl.v_slices == 2 || pl.v_slices == 4) && pl.kv_fetch == kLoneFetch &&
+         (pl.pack_gqa == 1 || (pl.pack_gqa == 0 && H_Q == H_KV));
 }
 
 int kv_nontemporal(double key_rows, int readers) {
@@ -273,11 +279,12 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     // workgroups, which pays while CUs are idle; the wide one reads each key
     // once per group.  Narrow is taken only when modelled at least 1% faster.
     // V slices (the output dims of a chunk split over 2 or 4 workgroups that
-    // share its scores) are considered where one tile serves the group and
-    // not with the paper's packing (pack_gqa 2).
+    // share its scores) are considered for packed tiles of either width, not
+    // with the paper's packing (pack_gqa 2), and unpacked only where one head
+    // is the group.
     const CostModel& m = policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model();
     auto best = [&](int h, double* t) {
-      const bool slices = pack != 2 && h == g;
+      const bool slices = pack == 1 || (pack == 0 && h == g);
       const int sh = s > 0 ? s : mi355x_splits(m, B, H_Q, H_KV, L_K_max, h, cus, slices);
       best_vslices(m, B, H_Q, H_KV, L_K_max, h, sh, cus, slices, t);
       return sh;
@@ -297,7 +304,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   if (policy == DA_POLICY_MI355X || policy == DA_POLICY_STREAMED) {
     double t = 0.0;
     vs = best_vslices(policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model(), B, H_Q, H_KV,
-                      L_K_max, hpt, s, cus, pack != 2 && hpt == g, &t);
+                      L_K_max, hpt, s, cus, pack == 1 || (pack == 0 && hpt == g), &t);
   }
   out->num_splits = s;
   out->pack_gqa = pack;

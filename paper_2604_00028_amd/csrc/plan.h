@@ -62,8 +62,9 @@ constexpr double kSplitGain = 0.99;
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs = 1);
 
 // Whether `pl` may serve each chunk with pl.v_slices workgroups (1, 2 or 4):
-// more than one only with K/V straight into LDS, one tile per group and
-// not the paper's packing (pack_gqa 2).
+// more than one only with K/V straight into LDS, packed tiles of either
+// width (pack_gqa 1; not the paper's packing) or unpacked where one head is
+// the group.
 bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl);
 
 // Workgroups launched for `chunks` (tile, chunk) pairs with vs V slices:

@@ -374,17 +374,23 @@ def test_streamed_policy_marks_loads_nontemporal():
 
 def test_v_slices():
     # chunks shared by 2 or 4 workgroups (each its part of the output dims)
-    # where a launch keeps one workgroup per CU and one tile serves the group
+    # where a launch keeps one workgroup per CU, with any packed tile width
     for B, H_Q, H_KV, L in [(1, 64, 8, 512), (1, 64, 8, 128), (4, 64, 8, 512), (1, 8, 1, 512), (16, 32, 4, 512),
                             (32, 64, 8, 8192), (1, 32, 1, 512), (8, 64, 8, 4096)]:
         for policy in (da.POLICY_MI355X, da.POLICY_STREAMED):
             p = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256, policy=policy)
             assert p.v_slices in (1, 2, 4) and p.grid == launch_grid(p.tiles * p.num_splits, p.v_slices)
             if p.v_slices > 1:
-                assert p.grid <= 256 and p.kv_fetch == 2 and p.heads_per_tile == H_Q // H_KV
+                assert p.grid <= 256 and p.kv_fetch == 2 and p.pack_gqa == 1
     assert da.da_choose_splits(1, 64, 8, 512, num_cus=256).v_slices == 4
     assert da.da_choose_splits(32, 64, 8, 8192, num_cus=256).v_slices == 1       # the grid fills the chip
-    assert da.da_choose_splits(1, 32, 1, 512, num_cus=256).v_slices == 1         # two 16-head tiles per group
+    # a group of 32 in 16-head tiles: two tiles per KV head, each in four slices
+    p = da.da_choose_splits(1, 32, 1, 512, num_cus=256)
+    assert (p.heads_per_tile, p.num_splits, p.v_slices, p.grid) == (16, 1, 4, 32)
+    # the hint stays off with several readers of each key
+    assert da.da_choose_splits(1, 32, 1, 512, num_cus=256, policy=da.POLICY_STREAMED).kv_nontemporal == 0
+    # unpacked, slices only where one head is the group
+    assert da.da_make_plan(1, 8, 1, 512, num_splits=1, pack_gqa=0, num_cus=256).v_slices == 1
     # the paper's packing and policies keep one workgroup per chunk
     assert da.da_make_plan(1, 64, 8, 512, num_splits=0, pack_gqa=2, num_cus=256).v_slices == 1
     for policy in (da.POLICY_PAPER, da.POLICY_EVOLVED):

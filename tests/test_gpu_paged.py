@@ -245,7 +245,7 @@ def test_paged_planned_plans_of_every_kind(B, H_Q, H_KV, lengths, page):
     g = H_Q // H_KV
     for plan in plans:
         ref = run_paged(q, kc, vc, bt, sl, L, plan.num_splits, plan.pack_gqa)
-        vss = (1, 2, 4) if plan.heads_per_tile == g and plan.pack_gqa != 2 else (1,)
+        vss = (1, 2, 4) if plan.pack_gqa == 1 or (plan.pack_gqa == 0 and g == 1) else (1,)
         for fetch, vs in [(0, 1), (1, 1)] + [(2, v) for v in vss]:
             for hint in (0, 1):
                 p = da.DaPlan.from_buffer_copy(plan)

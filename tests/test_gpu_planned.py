@@ -50,11 +50,14 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
     first = {}
     g = H_Q // H_KV
     for plan in plans:
-        # V slices only with K/V straight into LDS, one tile per group and not the paper's packing
-        vss = (1, 2, 4) if plan.heads_per_tile == g and plan.pack_gqa != 2 else (1,)
-        for fetch, vs in [(0, 1), (1, 1)] + [(2, v) for v in vss]:
+        # V slices only with K/V straight into LDS, packed (not the paper's packing) or one head per group
+        vss = (1, 2, 4) if plan.pack_gqa == 1 or (plan.pack_gqa == 0 and g == 1) else (1,)
+        # packed groups of more than 16 heads: both tile widths
+        widths = {plan.heads_per_tile} | ({16, 32} if plan.pack_gqa == 1 and g > 16 else set())
+        for w, fetch, vs in [(w, f, v) for w in sorted(widths) for f, v in [(0, 1), (1, 1)] + [(2, v) for v in vss]]:
             for hint in (0, 1):
                 p = da.DaPlan.from_buffer_copy(plan)
+                p.heads_per_tile, p.tiles = w, B * H_Q // w
                 p.kv_fetch, p.kv_nontemporal, p.v_slices = fetch, hint, vs
                 chunks = p.tiles * p.num_splits
                 p.grid = chunks if vs == 1 else vs * 8 * -(-chunks // 8)

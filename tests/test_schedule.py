@@ -122,13 +122,17 @@ def test_equal_lengths_match_the_uniform_plan():
     launch: the same split count as the MI355X plan for L a multiple of 128
     (its key-granular waves then hold whole tiles).  Schedules do not share
     chunks among V slices, so the comparison is with the plan without them
-    (the whole group in one tile gives it where a group is one tile)."""
+    (the whole group in one tile gives it where a group is one tile; for
+    wider groups only the uniform shape of the schedule is checked)."""
     for B, H_Q, H_KV in ((1, 64, 8), (1, 8, 1), (4, 32, 1), (32, 64, 8), (8, 16, 2)):
         for L in (128, 512, 2048, 8192):
             plan = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=CUS)
+            sched, _, seqs = check_schedule([L] * B, H_Q, H_KV)
+            if plan.v_slices > 1 and H_Q // H_KV > 16:
+                assert len(set(seqs[:, 1])) == 1 and sched.num_items == sched.tiles * seqs[0, 1]
+                continue
             if plan.v_slices > 1:
                 plan = da.da_make_plan(B, H_Q, H_KV, L, num_splits=0, pack_gqa=2, num_cus=CUS)
-            sched, _, seqs = check_schedule([L] * B, H_Q, H_KV)
             assert set(seqs[:, 1]) == {plan.num_splits}, (B, H_Q, H_KV, L)
             assert sched.num_items == plan.grid and sched.kv_fetch == plan.kv_fetch
 
