@@ -214,8 +214,8 @@ def traffic_for(workload: str):
 def small_configs_run(args, da, torch, dev) -> dict:
     """MQA decode (B=1, H_Q=8, H_KV=1, L_K=128), the pure-MQA low-tile sweep
     (B in {1,2,4} x L_K in {64..512}, H_Q=32, H_KV=1) and the varlen batched
-    GQA batch: the heuristic against num_splits = 1 and fixed split counts,
-    with achieved HBM GB/s."""
+    GQA batch: the heuristic against num_splits = 1, fixed split counts and
+    the paper's one-split launch, with achieved HBM GB/s."""
     from workloads import algorithmic_bytes as ab, config_shapes, make_inputs
     res = {}
     for cid, sweep in ((1, (1, 2, 4, 8)), (3, SWEEP), (4, SWEEP)):
@@ -237,7 +237,7 @@ def small_configs_run(args, da, torch, dev) -> dict:
             gbs = nbytes / (hv.median * 1e-6) / 1e9
             res[sh.name] = {"config": cid, "B": sh.B, "H_Q": sh.H_Q, "H_KV": sh.H_KV, "L_K": L,
                             "heuristic_us": round(hv.median, 3), "num_splits": hv.plan.num_splits,
-                            "heads_per_tile": hv.plan.heads_per_tile,
+                            "heads_per_tile": hv.plan.heads_per_tile, "v_slices": hv.plan.v_slices,
                             "s1_us": sw[1], "speedup_vs_s1": round(sw[1] / hv.median, 3), "best_fixed": best,
                             "best_fixed_us": sw[best], "vs_best_fixed": round(hv.median / sw[best], 3),
                             "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 5), "sweep_us": sw}
