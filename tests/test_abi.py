@@ -405,6 +405,34 @@ def test_v_slices():
     assert da.da_choose_splits(4, 256, 32, 2048, num_cus=256).v_slices == 1
 
 
+def test_planned_entry_accepts_slices_of_either_tile_width():
+    """V slices pass the plan check for packed tiles of both widths and for
+    unpacked launches where one head is the group; unpacked launches of
+    wider groups and the paper's packing are refused.  Two splits and no
+    workspace: an accepted plan stops at the workspace check, so nothing
+    reaches a device."""
+    lib = da.load()
+    FAKE = 1 << 20
+    P = ctypes.c_void_p
+
+    def call(plan, B, H_Q, H_KV, L):
+        return lib.da_decode_attn_planned(P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), None, B, H_Q, H_KV, L, 128, 0.0,
+                                          ctypes.byref(plan), None, 0, None)
+
+    def edited(B, H_Q, H_KV, L, pack, hpt, vs):
+        p = da.da_make_plan(B, H_Q, H_KV, L, num_splits=2, pack_gqa=pack, num_cus=256)
+        p = bnd.DaPlan.from_buffer_copy(p)
+        p.heads_per_tile, p.tiles, p.v_slices, p.kv_fetch = hpt, B * H_Q // hpt, vs, 2
+        p.grid = launch_grid(p.tiles * 2, vs)
+        return p
+    for vs in (2, 4):
+        for hpt in (16, 32):    # a group of 32 in one tile or two
+            assert call(edited(1, 32, 1, 512, 1, hpt, vs), 1, 32, 1, 512) == bnd.DA_ERR_WORKSPACE
+        assert call(edited(1, 8, 8, 512, 0, 1, vs), 1, 8, 8, 512) == bnd.DA_ERR_WORKSPACE  # one head per group
+        assert call(edited(1, 8, 1, 512, 0, 1, vs), 1, 8, 1, 512) == bnd.DA_ERR_ARG     # unpacked group of 8
+        assert call(edited(1, 8, 1, 512, 2, 8, vs), 1, 8, 1, 512) == bnd.DA_ERR_ARG     # the paper's packing
+
+
 def test_cu_margin_and_plan_errors():
     p = da.da_choose_splits(1, 8, 1, 4096, num_cus=256, cu_margin=200)
     assert p.num_cus == 56
