@@ -3,8 +3,8 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 
-One step is one call of the whole path -- plan (host), split-partial kernel
-with the in-kernel chunk merge -- over the Llama-3.1-70B-shaped GQA decode
+One step is one call of the whole path -- plan (host), split-partial kernel,
+and the log-sum-exp combine when the plan splits -- over the Llama-3.1-70B-shaped GQA decode
 batch (B=1, H_Q=64, H_KV=8, D=128, L_K=512, bf16, synthetic N(0,1) inputs
 already resident in HBM).  K steps are captured in one HIP graph and
 replayed; HIP events on the replay stream bracket the timed replays (the
@@ -35,7 +35,7 @@ if ROOT not in sys.path:
 METRIC = "decode-attention µs/call + achieved HBM GB/s (% of peak), heuristic vs num_splits=1"
 HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2604_00028_amd", "csrc", "decode_attn.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_00028_amd", "csrc", f) for f in ("decode_attn.hip", "plan.cpp")]
 SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
 LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
@@ -196,14 +196,22 @@ def algorithmic_bytes(B, H_Q, H_KV, L, D=128):
     return ab(B, H_Q, H_KV, B * L, D)
 
 
+def kernel_source_sha() -> str:
+    """Hash of the sources that decide which kernel runs and what it reads:
+    the kernels and the planner that picks the variant."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
 def traffic_for(workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
     it was taken on the current kernel source; else None."""
     try:
         with open(PROFILE_TRAFFIC) as f:
             t = json.load(f)
-        sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-        if t.get("kernel_source_sha256") != sha:
+        if t.get("kernel_source_sha256") != kernel_source_sha():
             return None
         w = t["workloads"][workload]
         return int(w["fetch_bytes"] + w["write_bytes"])
@@ -531,13 +539,8 @@ def cu_margin_run(args, da, torch, np) -> dict:
 def cpu_baseline(inp, seconds: float):
     """The fp64 oracle as it stands, on the host cores, on repeated calls of
     the same problem for about `seconds`."""
-    import numpy as np
     from oracle import decode_attention
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+    cores, blas, model = host_cores()
     decode_attention(inp.q, inp.k, inp.v)
     n = 0
     t0 = time.perf_counter()
@@ -545,8 +548,29 @@ def cpu_baseline(inp, seconds: float):
         decode_attention(inp.q, inp.k, inp.v)
         n += 1
     dt = time.perf_counter() - t0
-    return {"value": round(dt / n * 1e6, 2), "unit": "us/call", "cores": int(threads), "kind": "oracle",
+    return {"value": round(dt / n * 1e6, 2), "unit": "us/call", "cores": cores, "blas_threads": blas,
+            "cpu_model": model, "kind": "oracle",
             "sample": f"{n} full calls of the benchmarked shape (fp64 NumPy, {seconds:.0f} s budget)"}
+
+
+def host_cores():
+    """(cores this process may run on, BLAS threads NumPy uses, CPU model)."""
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        blas = None
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, blas, model
 
 
 def copy_run(args, torch):
@@ -644,7 +668,7 @@ def traffic_summary(d: str) -> None:
     copy_kib = float(1 << 20)
     fetch_scale = copy_kib / counter_avg(f("FETCH_SIZE", "copy"), "__amd_rocclr_copyBuffer", "FETCH_SIZE")
     write_scale = copy_kib / counter_avg(f("WRITE_SIZE", "copy"), "__amd_rocclr_copyBuffer", "WRITE_SIZE")
-    out = {"kernel_source_sha256": hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest(),
+    out = {"kernel_source_sha256": kernel_source_sha(),
            "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4),
            "command": "rocprofv3 --pmc <FETCH_SIZE|WRITE_SIZE> --output-format csv -d DIR/pmc_<counter>_<w> -o run "
                       "-- python3 bench.py --only <w> --steps 20 --rounds 1 --highload-steps 3",

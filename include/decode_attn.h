@@ -129,8 +129,9 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
 int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
                  int num_cus, int cu_margin, int policy, da_plan* out);
 
-/* Bytes of workspace da_decode_attn needs for num_splits chunks: 0 when
- * num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
+/* Bytes of workspace da_decode_attn needs for num_splits chunks: the chunk
+ * states (per-chunk max, sum and unnormalised output) that the paper's final
+ * reduction merges (Sections 3.1 and 5.3).  0 when num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
  * [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q].  No initialisation is
  * needed; every call overwrites what it reads. */
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
@@ -338,13 +339,17 @@ int da_combine_splits(const float* o_part, const float* m_part, const float* l_p
                       float* lse_out, int num_splits, int B, int H_Q, int d, void* stream);
 
 /* Compute units of the current device (hipDeviceAttributeMultiprocessorCount,
- * cached per device) and whether it is gfx950. */
+ * cached per device) and whether it is gfx950: the CU count the split policy
+ * counts work tiles against (Section 4).  Errors: DA_ERR_NULL, DA_ERR_HIP. */
 int da_device_info(int* num_cus, int* is_gfx950);
 
-/* Static text for a da_status code. */
+/* Static text for a da_status code.  No passage of the paper: library
+ * infrastructure.  Never NULL; "unknown error" for a code not in da_status. */
 const char* da_strerror(int code);
 
-/* Message describing the calling thread's most recent failure ("" if none). */
+/* Message describing the calling thread's most recent failure ("" if none).
+ * No passage of the paper: library infrastructure.  The text is owned by the
+ * library and valid until the thread's next call into it. */
 const char* da_last_error(void);
 
 #ifdef __cplusplus

@@ -237,16 +237,27 @@ def _shapes(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, cu: Optional[torc
 
 
 _workspaces: Dict[Tuple[int, int], torch.Tensor] = {}
+# Workspaces replaced by a larger one.  They are never freed: a HIP graph
+# captured earlier keeps their addresses, and kernels queued on a stream
+# other than torch's current one may still be using them, so returning them
+# to the caching allocator could hand live memory to another tensor.
+_retired: List[torch.Tensor] = []
 
 
 def workspace_for(dev: torch.device, stream_handle: int, nbytes: int) -> torch.Tensor:
     """A workspace of at least nbytes, cached per (device, stream).  Calls on
-    one stream run in order, so they can share it; the library overwrites
-    whatever it reads, so it needs no initialisation."""
-    key = (dev.index if dev.index is not None else torch.cuda.current_device(), stream_handle)
+    one stream run in order, so they can share it.  It is zero-filled when
+    allocated: the chunk-state regions need no initialisation (every call
+    writes what it reads), and the arrival counters of single-launch plans
+    start at zero and are left at zero by every call.  A cache that has to
+    grow keeps its old buffer alive for the life of the process."""
+    index = dev.index if dev.index is not None else (torch.cuda.current_device() if dev.type == "cuda" else -1)
+    key = (index, stream_handle)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
-        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        if ws is not None:
+            _retired.append(ws)
+        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=dev)
         _workspaces[key] = ws
     return ws
 

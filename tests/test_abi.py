@@ -472,3 +472,27 @@ def test_streamed_policy_splits_no_later_than_the_warm_one():
     assert da.da_choose_splits(1, 64, 8, 512, num_cus=256, policy=da.POLICY_STREAMED).num_splits > 1
     for L in (128, 256, 384):
         assert da.da_choose_splits(1, 64, 8, L, num_cus=256, policy=da.POLICY_STREAMED).num_splits == 1
+
+
+def test_workspace_cache_keeps_replaced_buffers_alive():
+    """A cached workspace that has to grow is replaced but never freed: a
+    graph captured with the old buffer, or kernels still queued on another
+    stream, keep using its address.  Checked with CPU tensors (the cache only
+    allocates), watching the old storage with a weak reference."""
+    import gc
+    import weakref
+
+    import torch
+    dev = torch.device("cpu")
+    key_stream = 0x5EED
+    small = bnd.workspace_for(dev, key_stream, 1000)
+    assert small.numel() >= 1000 and int(small.sum()) == 0       # zero-filled
+    ptr = small.data_ptr()
+    alive = weakref.ref(small)
+    del small
+    big = bnd.workspace_for(dev, key_stream, 50_000)
+    assert big.numel() >= 50_000 and big.data_ptr() != ptr
+    gc.collect()
+    assert alive() is not None and alive().data_ptr() == ptr      # the old buffer is still held
+    assert bnd.workspace_for(dev, key_stream, 2000) is big        # smaller requests reuse the cache
+    bnd._workspaces.pop((-1, key_stream), None)

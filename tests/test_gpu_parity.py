@@ -309,3 +309,37 @@ def test_workspace_reused_across_split_counts():
         if s in outs:
             assert torch.equal(out.view(torch.int16), outs[s].view(torch.int16))
         outs[s] = out
+
+
+def test_graph_keeps_its_workspace_after_the_cache_grows():
+    """A graph captured at s=2 holds the cached workspace's address; an eager
+    call at s=64 on the same stream makes the cache grow.  The replaced
+    buffer must stay allocated, so later replays still give the captured
+    call's bits."""
+    sh = config_shapes(2)[3]
+    inp = make_inputs(sh)
+    O, _ = decode_attention(inp.q, inp.k, inp.v)
+    q, k, v, cu = dev_inputs(inp)
+    say("graph workspace after cache growth: capture s=2, eager s=64")
+    ref2, _ = run(q, k, v, cu, sh.L_K, 2, 1)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    out = torch.empty_like(ref2)
+    with torch.cuda.stream(stream):
+        da.da_decode_attn(q, k, v, out=out, num_splits=2, pack_gqa=1)    # cache a workspace for this stream
+    stream.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        da.da_decode_attn(q, k, v, out=out, num_splits=2, pack_gqa=1)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        big = da.da_decode_attn(q, k, v, num_splits=64, pack_gqa=1)       # grows the cache
+        junk = torch.full((1 << 22,), 7, dtype=torch.uint8, device="cuda")  # new allocations on the stream
+    stream.synchronize()
+    assert_parity(big, O, "eager s=64 after capture")
+    for r in range(3):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref2.view(torch.int16)), f"replay {r}"
+    del junk

@@ -200,6 +200,62 @@ def test_softmax_shift_invariance_large_scores():
     np.testing.assert_allclose(O[0, 0], w @ bf16_bits_to_f64(v)[0, :, 0], rtol=1e-12, atol=1e-14)
 
 
+# ------------------------------------------------------------- the partition
+
+def balanced_partition_ok(cuts, L, s):
+    """Whether `cuts` is a balanced partition of L keys into s chunks, as the
+    split step defines it (chunks of floor(L/s) or ceil(L/s) keys, in order,
+    covering every key once): checked from the definition, not the formula."""
+    if len(cuts) != s + 1 or cuts[0] != 0 or cuts[-1] != L:
+        return False
+    sizes = [cuts[i + 1] - cuts[i] for i in range(s)]
+    if min(sizes) < 0 or max(sizes) - min(sizes) > 1:
+        return False
+    # empty chunks only when there are more chunks than keys
+    return L >= s or sizes.count(0) == s - L
+
+
+def test_even_bounds_worked_examples():
+    # chunk i is [floor(iL/s), floor((i+1)L/s)): worked out by hand
+    assert even_bounds(10, 3) == [0, 3, 6, 10]
+    assert even_bounds(5, 8) == [0, 0, 1, 1, 2, 3, 3, 4, 5]
+    assert even_bounds(0, 4) == [0, 0, 0, 0, 0]
+    assert even_bounds(7, 1) == [0, 7]
+    assert even_bounds(64, 64) == list(range(65))
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 5, 31, 32, 45, 127, 512, 1000, 8192])
+def test_even_bounds_is_balanced(L):
+    for s in range(1, 65):
+        cuts = even_bounds(L, s)
+        assert balanced_partition_ok(cuts, L, s), (L, s, cuts)
+        # exactly L mod s chunks hold one key more than the others
+        sizes = np.diff(cuts)
+        assert int((sizes == L // s + 1).sum()) == L % s
+
+
+def test_even_bounds_brute_force_tiny():
+    """For tiny L and s, enumerate every non-decreasing cut vector and keep
+    the balanced ones; the floor cuts must be among them, and for s <= L
+    (no empty chunk) the chunk sizes are the unique multiset {q, q+1}."""
+    import itertools
+    for L in range(0, 7):
+        for s in range(1, 6):
+            balanced = [c for c in itertools.combinations_with_replacement(range(L + 1), s - 1)
+                        if balanced_partition_ok([0, *c, L], L, s)]
+            assert tuple(even_bounds(L, s)[1:-1]) in balanced
+            q, r = divmod(L, s)
+            assert sorted(np.diff(even_bounds(L, s)).tolist()) == [q] * (s - r) + [q + 1] * r
+
+
+def test_partition_check_rejects_an_unbalanced_split():
+    # a plausible mistake: every key in the last chunk, or cuts off by one
+    assert not balanced_partition_ok([0, 0, 0, 10], 10, 3)
+    assert not balanced_partition_ok([0, 4, 8, 10], 10, 3)
+    assert not balanced_partition_ok([0, 3, 6, 9], 10, 3)
+    assert not balanced_partition_ok([0, 0, 2, 2, 5], 5, 4)
+
+
 # ------------------------------------------------------------- invariants
 
 def test_convex_hull():
