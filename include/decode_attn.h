@@ -44,6 +44,13 @@ extern "C" {
  * find its K/V resident on the next call, and streaming hints then raise
  * the sustained HBM read rate. */
 #define DA_RESIDENT_BYTES (288ull << 20)
+/* Bytes at the end of a workspace that hold the arrival counters of
+ * single-launch merges (da_plan.combine == 1): one uint32 per tile, 256 bytes
+ * apart (atomics on one cache line are serialised, so counters of different
+ * tiles must not share one), so such a plan has at most DA_ARRIVAL_BYTES /
+ * 256 = 4096 tiles. */
+#define DA_ARRIVAL_BYTES (1 << 20)
+#define DA_ARRIVAL_STRIDE 256
 
 typedef enum da_status {
   DA_OK = 0,
@@ -105,6 +112,13 @@ typedef struct da_plan {
                              policies MI355X and STREAMED choose it where a launch keeps one
                              workgroup per CU and its K/V fit in L2; results are the same bits
                              for every value. */
+  int32_t combine;        /* how num_splits > 1 chunk states are merged (the final reduction of
+                             Sections 3.1 and 5.3): 0 a second kernel launch; 1 inside the split
+                             launch, by the last workgroup of each tile to finish (an arrival
+                             counter per tile in the workspace; no workgroup waits for another;
+                             at most DA_ARRIVAL_BYTES / DA_ARRIVAL_STRIDE tiles).  Both give the same bits.  0 when
+                             num_splits == 1.  The policies pick the merge their cost model
+                             prices lower. */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
@@ -131,9 +145,19 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
 
 /* Bytes of workspace da_decode_attn needs for num_splits chunks: the chunk
  * states (per-chunk max, sum and unnormalised output) that the paper's final
- * reduction merges (Sections 3.1 and 5.3).  0 when num_splits == 1.  Layout (each region 256-byte aligned): Otilde fp32
- * [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q].  No initialisation is
- * needed; every call overwrites what it reads. */
+ * reduction merges (Sections 3.1 and 5.3), and the arrival counters of a
+ * single-launch merge.  0 when num_splits == 1.  Layout: from offset 0,
+ * Otilde fp32 [s,B,H_Q,D] | m fp32 [s,B,H_Q] | l fp32 [s,B,H_Q] (each
+ * region 256-byte aligned); the arrival counters, one uint32 per tile every
+ * DA_ARRIVAL_STRIDE bytes, start at (workspace_bytes - DA_ARRIVAL_BYTES)
+ * rounded down to 256 bytes, i.e. in
+ * the last DA_ARRIVAL_BYTES of the buffer the caller passes, whatever its
+ * size.  Chunk states need no initialisation (every call writes what it
+ * reads) and never reach the counter region.  The counters must be zero
+ * before the first call whose plan has combine == 1 (zero the buffer once
+ * when it is allocated); every such call leaves them zero, so one buffer
+ * serves calls of any shape in turn.  A plan with combine == 0 does not
+ * touch the counters and needs only the chunk-state bytes. */
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
 
 /* Cut points of sequence chunking: chunk i of a sequence of L keys is
@@ -162,10 +186,13 @@ int da_split_bounds(int L, int num_splits, int32_t* cuts);
  *                H_Q, d, s) for the resolved s (unused when s == 1).  Calls
  *                that share a workspace must not overlap in time.
  * s == 1: one kernel launch.  s > 1: the split kernel writes the chunk
- * states to the workspace and the combine kernel merges them in chunk order
- * (exactly da_split_partials followed by da_combine_splits), so results are
- * bit-identical across runs on one device for a fixed (num_splits,
- * pack_gqa). */
+ * states to the workspace, and they are merged in chunk order either by the
+ * combine kernel (exactly da_split_partials followed by da_combine_splits)
+ * or, when the plan's combine is 1, inside the same launch by the last
+ * workgroup of each tile (the workspace's arrival counters must then be
+ * zero, see da_workspace_bytes).  Both merges give the same bits, and
+ * results are bit-identical across runs on one device for a fixed
+ * (num_splits, pack_gqa). */
 int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                    void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                    float softmax_scale, int num_splits, int pack_gqa, void* workspace,

@@ -57,6 +57,7 @@ class DaPlan(ctypes.Structure):
         ("kv_fetch", ctypes.c_int32),
         ("kv_nontemporal", ctypes.c_int32),
         ("v_slices", ctypes.c_int32),
+        ("combine", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

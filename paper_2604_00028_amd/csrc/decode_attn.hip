@@ -57,7 +57,7 @@ constexpr int D = DA_HEAD_DIM;
 constexpr int kKeysPerTile = 32;
 constexpr int kVPitch = 288;                 // bytes per staged V row (256 + 32 pad)
 constexpr int kKPitch = 288;                 // bytes per staged K row (256 + 32 pad)
-constexpr int kMergeBatch = 16;              // chunk states loaded at once in a merge
+constexpr int kDeviceScope = 16;             // cache-policy field: sc1, device-scope coherent access
 constexpr int kStateVals = 2 + 32;           // one wave's state per lane: m, l, 8 x 4 outputs
 
 // How a tile's K and V reach the matrix cores.
@@ -89,6 +89,8 @@ constexpr int smem_bytes(int W, int NT, int FETCH) {
   return W * stage_bytes(FETCH) > W * merge_slot_bytes(NT) ? W * stage_bytes(FETCH) : W * merge_slot_bytes(NT);
 }
 static_assert(smem_bytes(4, 2, kFetchLds) <= 160 * 1024, "a workgroup must fit the LDS of one CU");
+static_assert(smem_bytes(4, 1, kFetchDirect) >= (2 * (DA_MAX_SPLITS + 16) * 32 + 8 * 32) * 4,
+              "the single-launch merge stages chunk maxima and sums in LDS");
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -101,7 +103,11 @@ typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-enum Mode : int { kDirect = 0, kPartials = 1 };
+// kDirect: one chunk per sequence, the normalised output is written.
+// kPartials: chunk states go to the workspace for a separate combine launch.
+// kFused: chunk states go to the workspace with device-scope stores, and
+// the last workgroup of a tile to finish merges them (single launch).
+enum Mode : int { kDirect = 0, kPartials = 1, kFused = 2 };
 
 // Division by a launch constant d >= 1 as a multiply and a shift
 // (Granlund and Montgomery, PLDI 1994, Theorem 4.2 with N = 32): with
@@ -132,6 +138,7 @@ struct Params {
   float* o_part;        // [s, B, H_Q, D]          (kPartials)
   float* m_part;        // [s, B, H_Q]
   float* l_part;        // [s, B, H_Q]
+  uint32_t* arrivals;   // kFused: one arrival counter per tile, zero between calls
   const int32_t* block_table;  // paged layout: [B, max_pages] page ids
   const int32_t* seq_lens;     // paged layout: [B] sequence lengths
   int page_size, max_pages, num_pages;
@@ -181,22 +188,226 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// Chunk weights of one (sequence, head) row from its s chunk states:
-// M = max m_i over non-empty chunks (l_i > 0), w_i = exp(m_i - M) (0 for an
-// empty chunk), L = sum_i w_i l_i accumulated in chunk order.  m holds the
-// maxima on entry and the weights on return; ML receives (M, L).
-__device__ __forceinline__ void merge_weights(float* m, const float* l, int s, float* ML) {
-  float M = -INFINITY;
-  for (int i = 0; i < s; ++i)
-    if (l[i] > 0.f) M = fmaxf(M, m[i]);
-  float L = 0.f;
-  for (int i = 0; i < s; ++i) {
-    const float w = l[i] > 0.f ? __builtin_amdgcn_exp2f((m[i] - M) * kLog2e) : 0.f;
-    m[i] = w;
-    L = fmaf(w, l[i], L);
+// Maximum over the 64 lanes of a wave (exact: the order does not matter).
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+__device__ __forceinline__ float lane_value(float x, int i) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), i));
+}
+
+// The log-sum-exp merge of s <= 64 chunk states (the paper's final
+// reduction, Sections 3.1 and 5.3) for up to NR rows, by one wave: the lane
+// holds output dims 2*lane and 2*lane + 1 of each row, and lane i holds the
+// max and sum of chunk i.  Chunk i of row r is state row base[r] + i * srow
+// (Otilde at o_part[row * D], m and l at m_part[row], l_part[row]).  Per
+// row: M = max m_i over chunks with l_i > 0, w_i = exp(m_i - M) (0 for an
+// empty chunk), then L = sum_i w_i l_i and O = sum_i w_i Otilde_i, both
+// accumulated in chunk order i = 0..s-1, O / L rounded to bf16 and lse = M +
+// ln L.  Every output element takes the same operations in the same order
+// whichever kernel runs this, so the separate combine launch and the
+// single-launch merge give the same bits.  COH: the states were written in
+// this launch by other workgroups with device-scope stores and are read with
+// device-scope loads.  State offsets are below 2 GiB (checked on the host).
+template <int NR, bool COH>
+__device__ __forceinline__ void merge_rows(const float* o_part, const float* m_part, const float* l_part,
+                                           const int64_t (&base)[NR], const int64_t (&orow)[NR], int nr,
+                                           int64_t srow, int s, uint16_t* out, float* lse, int lane) {
+  constexpr int aux = COH ? kDeviceScope : 0;
+  constexpr int CB = NR == 1 ? 16 : (32 / NR > 0 ? 32 / NR : 1);  // chunks loaded at once per row
+  const __amdgpu_buffer_rsrc_t ors = make_rsrc(o_part, 0x7fffffff);
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(m_part, 0x7fffffff);
+  const __amdgpu_buffer_rsrc_t lrs = make_rsrc(l_part, 0x7fffffff);
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  float mi[NR], li[NR];
+  f32x2 a[NR][CB];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    mi[r] = -INFINITY;
+    li[r] = 0.f;
+    if (r < nr && lane < s) {
+      const uint32_t off = (uint32_t)(base[r] + (int64_t)lane * srow) * 4u;
+      mi[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, off, 0, aux));
+      li[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(lrs, off, 0, aux));
+    }
+#pragma unroll
+    for (int u = 0; u < CB; ++u)
+      if (r < nr && u < s)
+        a[r][u] = __builtin_bit_cast(
+            f32x2, __builtin_amdgcn_raw_buffer_load_b64(
+                       ors, (uint32_t)((base[r] + (int64_t)u * srow) * D + 2 * lane) * 4u, 0, aux));
   }
-  ML[0] = M;
-  ML[1] = L;
+  float wi[NR], M[NR], L[NR], o0[NR], o1[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const bool live = li[r] > 0.f;
+    M[r] = wave_max(live ? mi[r] : -INFINITY);
+    wi[r] = live ? __builtin_amdgcn_exp2f((mi[r] - M[r]) * kLog2e) : 0.f;
+    L[r] = 0.f;
+    for (int i = 0; i < s; ++i) L[r] = fmaf(lane_value(wi[r], i), lane_value(li[r], i), L[r]);
+    o0[r] = 0.f;
+    o1[r] = 0.f;
+  }
+  for (int i0 = 0; i0 < s; i0 += CB) {
+    if (i0 > 0) {
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int u = 0; u < CB; ++u)
+          if (r < nr && i0 + u < s)
+            a[r][u] = __builtin_bit_cast(
+                f32x2, __builtin_amdgcn_raw_buffer_load_b64(
+                           ors, (uint32_t)((base[r] + (int64_t)(i0 + u) * srow) * D + 2 * lane) * 4u, 0, aux));
+    }
+#pragma unroll
+    for (int u = 0; u < CB; ++u)
+      if (i0 + u < s) {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+          const float w = lane_value(wi[r], i0 + u);
+          const bool live = lane_value(li[r], i0 + u) > 0.f;
+          o0[r] = fmaf(w, live ? a[r][u].x : 0.f, o0[r]);
+          o1[r] = fmaf(w, live ? a[r][u].y : 0.f, o1[r]);
+        }
+      }
+  }
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    if (r >= nr) continue;
+    const float inv = L[r] > 0.f ? 1.0f / L[r] : 0.f;
+    *reinterpret_cast<uint32_t*>(out + orow[r] * D + 2 * lane) = pack_bf16x2(o0[r] * inv, o1[r] * inv);
+    if (lse && lane == 0) lse[orow[r]] = L[r] > 0.f ? M[r] + logf(L[r]) : -INFINITY;
+  }
+}
+
+// The single-launch merge: the last workgroup of a tile merges the tile's
+// s chunk states for its hpt <= 32 rows (query heads), with every thread
+// holding float4 output columns.  The states were written in this launch by
+// other workgroups with device-scope stores and are read with device-scope
+// loads.  Per output element the operations and their order are those of
+// merge_rows (maximum over non-empty chunks, then the weights, L and O
+// accumulated in chunk order), so both merges give the same bits.  The
+// code is kept short and rolled: it runs once per tile, on cold
+// instruction caches.  `lds` holds at least 3 x 64 x 32 floats.
+template <int NT, int W>
+__device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t row0_tile, int tid) {
+  constexpr int T = 64 * W;              // threads
+  constexpr int R = T / 32;              // thread t stages row t % 32 of chunks t / 32 + R u
+  constexpr int IPT = NT * 16 * 32 / T;  // float4 columns per thread (hpt * 32 items over T threads)
+  constexpr int CB = 16 / IPT;           // chunks of columns loaded at once
+  constexpr uint32_t kOut = 0xfffffff0u; // an offset past every buffer: reads zero, touches nothing
+  const int hpt = p.hpt, s = p.s;
+  // 32-bit offsets: the chunk states of a call stay below 2 GiB (checked on the host), and the
+  // buffer ranges end with them, so out-of-range rows and chunks read as zeros
+  const uint32_t rows = (uint32_t)p.B * (uint32_t)p.H_Q;
+  const uint32_t r0 = (uint32_t)row0_tile;
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(p.m_part, (uint32_t)s * rows * 4u);
+  const __amdgpu_buffer_rsrc_t lrs = make_rsrc(p.l_part, (uint32_t)s * rows * 4u);
+  const __amdgpu_buffer_rsrc_t ors = make_rsrc(p.o_part, (uint32_t)s * rows * (uint32_t)D * 4u);
+  // chunk rows are padded to 64 + CB so that a batch reads them unconditionally
+  float* lm = lds;                               // [64 + CB chunks][32 rows] maxima
+  float* ll = lds + (DA_MAX_SPLITS + CB) * 32;   // [64 + CB][32] sums
+  float* lp = ll + (DA_MAX_SPLITS + CB) * 32;    // [R][32] maxima over each thread's live chunks
+  // column items of this thread: item tid + T j is row item / 32, float4 column item % 32
+  uint32_t ooff[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const uint32_t item = (uint32_t)(tid + T * j), h = item >> 5, c = item & 31u;
+    ooff[j] = h < (uint32_t)hpt ? ((r0 + h) * D + 4u * c) * 4u : kOut;
+  }
+  const uint32_t ostride = rows * (uint32_t)D * 4u;  // bytes between two chunks of one row
+  f32x4 a[IPT][CB];
+  const int items = hpt * 32;  // column items of the tile; item groups j with T j >= items are skipped
+  auto load_cols = [&](int i0) {
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+#pragma unroll
+      for (int u = 0; u < CB; ++u)
+        if (T * j < items && i0 + u < s)  // uniform
+        a[j][u] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       ors, ooff[j] != kOut ? ooff[j] + (uint32_t)(i0 + u) * ostride : kOut, 0, kDeviceScope));
+  };
+  {
+    const uint32_t h = (uint32_t)tid & 31u;
+    const int i0 = tid >> 5;
+    const uint32_t moff = h < (uint32_t)hpt ? (r0 + h) * 4u : kOut;
+    float mv[DA_MAX_SPLITS / R], lv[DA_MAX_SPLITS / R];
+#pragma unroll
+    for (int u = 0; u < DA_MAX_SPLITS / R; ++u) {
+      if (R * u >= s) break;  // uniform
+      const int i = i0 + R * u;
+      const uint32_t off = moff != kOut && i < s ? moff + (uint32_t)i * rows * 4u : kOut;
+      mv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, off, 0, kDeviceScope));
+      lv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(lrs, off, 0, kDeviceScope));
+    }
+    load_cols(0);  // in flight while the maxima are staged
+    float pm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < DA_MAX_SPLITS / R; ++u) {
+      if (R * u >= s) break;
+      const int i = i0 + R * u;  // < 64; rows and chunks out of range read as l = 0, never live
+      lm[i * 32 + h] = mv[u];
+      ll[i * 32 + h] = lv[u];
+      pm = lv[u] > 0.f ? fmaxf(pm, mv[u]) : pm;
+    }
+    lp[i0 * 32 + h] = pm;
+  }
+  __syncthreads();
+  float M[IPT], L[IPT];
+  f32x4 o[IPT];
+  int hh[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    hh[j] = ((tid + T * j) >> 5) & 31;
+    M[j] = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < R; ++r) M[j] = fmaxf(M[j], lp[r * 32 + hh[j]]);
+    L[j] = 0.f;
+    o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int i0 = 0; i0 < s; i0 += CB) {
+    if (i0 > 0) load_cols(i0);
+    // the batch's maxima and sums, read at once (rows past s are read, never used)
+    float bm[IPT][CB], bl[IPT][CB];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j)
+#pragma unroll
+      for (int u = 0; u < CB; ++u) {
+        bm[j][u] = lm[(i0 + u) * 32 + hh[j]];
+        bl[j][u] = ll[(i0 + u) * 32 + hh[j]];
+      }
+#pragma unroll
+    for (int u = 0; u < CB; ++u) {
+      if (i0 + u < s) {
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) {
+          if (T * j >= items) break;  // uniform
+          const float mi = bm[j][u], li = bl[j][u];
+          const bool live = li > 0.f;
+          const float w = live ? __builtin_amdgcn_exp2f((mi - M[j]) * kLog2e) : 0.f;
+          L[j] = fmaf(w, li, L[j]);
+          // an empty chunk's output is exactly zero here (w = 0 and O~ = 0 add nothing), as the
+          // combine's guard on empty chunks makes it
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[j][e] = fmaf(w, a[j][u][e], o[j][e]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int item = tid + T * j, h = item >> 5, c = item & 31;
+    if (h >= hpt) continue;
+    const int64_t row = row0_tile + h;
+    const float inv = L[j] > 0.f ? 1.0f / L[j] : 0.f;
+    *reinterpret_cast<uint2*>(p.out + row * D + 4 * c) =
+        make_uint2(pack_bf16x2(o[j][0] * inv, o[j][1] * inv), pack_bf16x2(o[j][2] * inv, o[j][3] * inv));
+    if (p.lse && c == 0) p.lse[row] = L[j] > 0.f ? M[j] + logf(L[j]) : -INFINITY;
+  }
 }
 
 // Waves per SIMD each variant must fit: three for the 16-column direct-fetch
@@ -770,7 +981,7 @@ split_partial_kernel(Params p) {
             make_uint2(pack_bf16x2(o[bb][0] * inv, o[bb][1] * inv), pack_bf16x2(o[bb][2] * inv, o[bb][3] * inv));
       }
       if (p.lse && wave == 0 && quad == 0 && nb0 == 0) p.lse[row] = Lw > 0.f ? mval + logf(Lw) : -INFINITY;
-    } else {
+    } else if (SCH || p.mode == kPartials) {
 #pragma unroll
       for (int bb = 0; bb < NBW; ++bb) {
         const int nn = nb0 + wave * NBW + bb;
@@ -782,15 +993,60 @@ split_partial_kernel(Params p) {
         p.m_part[srow0 + h] = mval;
         p.l_part[srow0 + h] = Lw;
       }
+    } else {
+      // kFused: device-scope stores write the chunk state through L2, so
+      // it is visible to every XCD once the stores have completed
+#pragma unroll
+      for (int bb = 0; bb < NBW; ++bb) {
+        const int nn = nb0 + wave * NBW + bb;
+        const u32x4 bits = {__float_as_uint(o[bb][0]), __float_as_uint(o[bb][1]), __float_as_uint(o[bb][2]),
+                            __float_as_uint(o[bb][3])};
+        __builtin_amdgcn_raw_buffer_store_b128(bits, ors, (uint32_t)(h * D + 16 * nn + 4 * quad) * 4u, 0,
+                                               kDeviceScope);
+      }
+      if (wave == 0 && quad == 0 && nb0 == 0) {
+        __hip_atomic_store(p.m_part + srow0 + h, mval, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(p.l_part + srow0 + h, Lw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+
+  if constexpr (!SCH) {
+    if (p.mode == kFused) {
+      // Single-launch merge.  Hand-off: every wave waits until its chunk
+      // state stores have completed (they are device-scope, written through
+      // L2), then thread 0 takes an arrival ticket for the tile.  The
+      // workgroup that takes the last of the tile's s x VS tickets has seen
+      // every other workgroup's ticket, each taken after that workgroup's
+      // stores completed, so device-scope loads now return all the states.
+      // This is the agent-scope release/acquire sequence of the AMDGPU memory
+      // model without its L2 write-back and invalidate, which only non-atomic
+      // data needs; the chunk states are written and read with device-scope
+      // (sc1) accesses only.  No workgroup waits for another.  The last one
+      // sets the counter back to zero for the next call.
+      __shared__ int s_last;
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0) {
+        const uint32_t n = (uint32_t)p.s * VS;
+        // counters sit a cache line apart: atomics on one line are serialised
+        uint32_t* counter = p.arrivals + (size_t)tile * da::kArrivalStride;
+        const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool last = prev + 1u == n;
+        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = last ? 1 : 0;
+      }
+      __syncthreads();
+      if (!s_last) return;
+      merge_tile<NT, W>(p, reinterpret_cast<float*>(smem), row0_tile, tid);
     }
   }
 }
 
-// Log-sum-exp combine: one wave64 per (b, h) row, 2 dims per lane.  The
-// first 16 chunk outputs are loaded before the weights are known; weights
-// and the weighted sum are taken in chunk order, so the result is
-// bit-identical across runs and producers of the same chunk states.  SEQ:
-// per-sequence chunk counts and state rows from `seqs`.
+// Log-sum-exp combine launch: one wave64 per (b, h) row, 2 dims per lane
+// (merge_rows), so the result is bit-identical across runs, producers of the
+// same chunk states, and the single-launch merge.  SEQ: per-sequence chunk
+// counts and state rows from `seqs`.
 template <bool SEQ>
 __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restrict__ o_part,
                                                             const float* __restrict__ m_part,
@@ -799,9 +1055,6 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
                                                             int s, int64_t rows,
                                                             const int32_t* __restrict__ seqs, int H_Q,
                                                             Div div_hq) {
-  __shared__ float sw[4][DA_MAX_SPLITS];
-  __shared__ float sl[4][DA_MAX_SPLITS];
-  __shared__ float sML[4][2];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
@@ -820,40 +1073,9 @@ __global__ void __launch_bounds__(256) split_combine_kernel(const float* __restr
     base = (int64_t)r0 * H_Q + h;
     srow = H_Q;
   }
-  const float* src = o_part + base * D + 2 * lane;
-  const int64_t stride = srow * D;
-  float2 a[kMergeBatch];
-#pragma unroll
-  for (int u = 0; u < kMergeBatch; ++u)
-    if (u < s) a[u] = *reinterpret_cast<const float2*>(src + u * stride);
-  for (int i = lane; i < s; i += 64) {
-    sw[w][i] = m_part[base + i * srow];
-    sl[w][i] = l_part[base + i * srow];
-  }
-  __builtin_amdgcn_wave_barrier();
-  if (lane == 0) merge_weights(sw[w], sl[w], s, sML[w]);
-  __builtin_amdgcn_wave_barrier();
-  float o0 = 0.f, o1 = 0.f;
-  for (int i0 = 0; i0 < s; i0 += kMergeBatch) {
-    if (i0 > 0) {
-#pragma unroll
-      for (int u = 0; u < kMergeBatch; ++u)
-        if (i0 + u < s) a[u] = *reinterpret_cast<const float2*>(src + (i0 + u) * stride);
-    }
-#pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u)
-      if (i0 + u < s) {
-        const float wi = sw[w][i0 + u];
-        const bool live = sl[w][i0 + u] > 0.f;
-        o0 = fmaf(wi, live ? a[u].x : 0.f, o0);
-        o1 = fmaf(wi, live ? a[u].y : 0.f, o1);
-      }
-  }
-  const float M = sML[w][0];
-  const float Lsum = sML[w][1];
-  const float inv = Lsum > 0.f ? 1.0f / Lsum : 0.f;
-  *reinterpret_cast<uint32_t*>(out + row * D + 2 * lane) = pack_bf16x2(o0 * inv, o1 * inv);
-  if (lse && lane == 0) lse[row] = Lsum > 0.f ? M + logf(Lsum) : -INFINITY;
+  const int64_t bases[1] = {base};
+  const int64_t orows[1] = {row};
+  merge_rows<1, false>(o_part, m_part, l_part, bases, orows, 1, srow, s, out, lse, lane);
 }
 
 // ---------------------------------------------------------------- host side
@@ -1029,7 +1251,8 @@ int check_plan(const da_plan* pl, int B, int H_Q, int H_KV) {
       (int64_t)pl->tiles != (int64_t)B * (H_Q / hpt) ||
       (int64_t)pl->grid != da::launch_grid((int64_t)pl->tiles * pl->num_splits, pl->v_slices) ||
       pl->group_waves != 4 || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
-      pl->kv_nontemporal > 1 || pl->num_cus < 1 || !da::v_slices_valid(H_Q, H_KV, *pl))
+      pl->kv_nontemporal > 1 || pl->num_cus < 1 || !da::v_slices_valid(H_Q, H_KV, *pl) || pl->combine < 0 ||
+      pl->combine > 1 || (pl->combine == 1 && (pl->num_splits < 2 || pl->tiles > da::kMaxArrivalTiles)))
     return da::fail(DA_ERR_ARG, "plan does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   return DA_OK;
 }
@@ -1047,16 +1270,18 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
   if (pack_gqa < -1 || pack_gqa > 2) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
   if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
 
-  // A forced split count fixes the workspace need before any device access.
-  auto check_workspace = [&](int s) {
+  // A forced split count fixes the workspace need before any device access
+  // (the arrival counters only for a single-launch merge).
+  auto check_workspace = [&](int s, bool fused) {
     if (s <= 1) return (int)DA_OK;
-    const size_t need = da::workspace_layout(B, H_Q, d, s).total;
+    const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
+    const size_t need = fused ? wl.total : wl.states;
     if (!workspace || workspace_bytes < need)
       return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, need,
                       workspace ? workspace_bytes : (size_t)0);
     return check_state_size(B, H_Q, s);
   };
-  int rc = check_workspace(given ? given->num_splits : num_splits);
+  int rc = check_workspace(given ? given->num_splits : num_splits, given && given->combine == 1);
   if (rc) return rc;
   int cus = 0;
   rc = ensure_gfx950(&cus);
@@ -1068,7 +1293,8 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
     rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
   const int s = pl.num_splits;
-  rc = check_workspace(s);
+  const bool fused = s > 1 && pl.combine == 1;
+  rc = check_workspace(s, fused);
   if (rc) return rc;
   const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
 
@@ -1080,10 +1306,17 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
     return launch_partial(p, pl, static_cast<hipStream_t>(stream));
   }
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  p.mode = kPartials;
+  p.mode = fused ? kFused : kPartials;
   p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
   p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
   p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
+  if (fused) {
+    // one launch: the last workgroup of each tile merges its chunk states
+    p.arrivals = reinterpret_cast<uint32_t*>(ws + da::arrival_offset(workspace_bytes));
+    p.out = static_cast<uint16_t*>(out);
+    p.lse = lse_out;
+    return launch_partial(p, pl, static_cast<hipStream_t>(stream));
+  }
   rc = launch_partial(p, pl, static_cast<hipStream_t>(stream));
   if (rc) return rc;
   return launch_combine(p.o_part, p.m_part, p.l_part, static_cast<uint16_t*>(out), lse_out, s, (int64_t)B * H_Q,
@@ -1272,6 +1505,7 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
   pl.kv_fetch = sched->kv_fetch;
   pl.kv_nontemporal = sched->kv_nontemporal;
   pl.v_slices = 1;
+  pl.combine = 0;
   fill_params(p, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   p.xcd_group = 0;  // the schedule orders its workgroups itself
   p.work = static_cast<const int32_t*>(meta_dev);
@@ -1334,8 +1568,10 @@ int da_combine_splits(const float* o_part, const float* m_part, const float* l_p
   if (!aligned(o_part, 8) || !aligned(m_part, 4) || !aligned(l_part, 4) || !aligned(out, 4) ||
       (lse_out && !aligned(lse_out, 4)))
     return da::fail(DA_ERR_ALIGN, "misaligned combine operand");
+  int rc = check_state_size(B, H_Q, num_splits);
+  if (rc) return rc;
   int cus = 0;
-  int rc = ensure_gfx950(&cus);
+  rc = ensure_gfx950(&cus);
   if (rc) return rc;
   return launch_combine(o_part, m_part, l_part, static_cast<uint16_t*>(out), lse_out, num_splits, (int64_t)B * H_Q,
                         static_cast<hipStream_t>(stream));

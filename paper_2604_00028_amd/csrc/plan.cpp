@@ -64,6 +64,8 @@ const CostModel& mi355x_model() {
       /*t_tile_staged=*/{0.671, 0.854},
       /*merge0=*/2.458,
       /*merge1=*/{0.218, 0.253},
+      /*fused0=*/2.458,
+      /*fused1=*/{0.218, 0.253},
       /*hbm_rate=*/6.319e6,
       /*hbm0=*/0.006,
       /*pnorm=*/2.389,
@@ -81,7 +83,8 @@ const CostModel& mi355x_model() {
 // Every workgroup has four waves, one per SIMD, and walks a quarter of its
 // chunk each; workgroups that share a CU share its SIMDs.  The soft maximum
 // reflects that a CU's tile loop slows as the chip nears its HBM rate.
-double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs) {
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs,
+                  bool fused) {
   const int wide = hpt > 16 ? 1 : 0;
   const double row_bytes = 2.0 * kHeadDim * 2.0;  // K and V row of one KV head
   const int64_t tiles = (int64_t)B * H_Q / hpt;
@@ -97,7 +100,7 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
   const double stream = m.hbm0 + bytes / m.hbm_rate;
   double t = pow(pow(compute, m.pnorm) + pow(stream, m.pnorm), 1.0 / m.pnorm);
-  if (s > 1) t += m.merge0 + m.merge1[wide] * s;
+  if (s > 1) t += fused ? m.fused0 + m.fused1[wide] * s : m.merge0 + m.merge1[wide] * s;
   return t;
 }
 
@@ -122,6 +125,8 @@ const CostModel& mi355x_streamed_model() {
       /*t_tile_staged=*/{1.609, 1.643},
       /*merge0=*/2.308,
       /*merge1=*/{0.235, 0.254},
+      /*fused0=*/2.308,
+      /*fused1=*/{0.235, 0.254},
       /*hbm_rate=*/6.498e6,
       /*hbm0=*/3.366,
       /*pnorm=*/4.0,
@@ -131,6 +136,14 @@ const CostModel& mi355x_streamed_model() {
   return m;
 }
 
+// Whether s > 1 chunk states are merged inside the split launch by the last
+// workgroup of each tile (da_plan.combine 1) rather than by a second launch:
+// whichever merge the model prices lower.
+bool fused_merge(const CostModel& m, int hpt, int s, int64_t tiles) {
+  const int wide = hpt > 16 ? 1 : 0;
+  return s > 1 && tiles <= kMaxArrivalTiles && m.fused0 + m.fused1[wide] * s < m.merge0 + m.merge1[wide] * s;
+}
+
 // V slices for s chunks per sequence when `slices` allows them: 2 or 4
 // where the launch keeps one workgroup per CU, the call's K/V fit in L2 (so
 // that the slices' repeated K reads stay there; the slice factors were
@@ -138,13 +151,14 @@ const CostModel& mi355x_streamed_model() {
 // slice; *t gets the modelled time.
 static int best_vslices(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, bool slices,
                         double* t) {
-  const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, 1);
+  const int64_t tiles = (int64_t)B * H_Q / hpt;
+  const bool fused = fused_merge(m, hpt, s, tiles);
+  const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, 1, fused);
   int best_vs = 1;
   double best = one;
-  const int64_t tiles = (int64_t)B * H_Q / hpt;
   slices = slices && (double)B * L_K * H_KV * (2.0 * kHeadDim * 2.0) <= (double)kL2Bytes;
   for (int vs = 2; slices && vs <= 4 && launch_grid(tiles * s, vs) <= cus; vs *= 2) {
-    const double tv = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, vs);
+    const double tv = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, vs, fused);
     if (tv < best && tv < kSplitGain * one) {
       best = tv;
       best_vs = vs;
@@ -307,6 +321,10 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
                       L_K_max, hpt, s, cus, pack == 1 || (pack == 0 && hpt == g), &t);
   }
   out->num_splits = s;
+  out->combine = fused_merge(policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model(), hpt, s,
+                             (int64_t)B * H_Q / hpt)
+                     ? 1
+                     : 0;
   out->pack_gqa = pack;
   out->heads_per_tile = hpt;
   out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
@@ -622,7 +640,8 @@ WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s) {
   w.o_off = 0;
   w.m_off = align256(w.o_off + (size_t)s * rows * d * sizeof(float));
   w.l_off = align256(w.m_off + (size_t)s * rows * sizeof(float));
-  w.total = align256(w.l_off + (size_t)s * rows * sizeof(float));
+  w.states = align256(w.l_off + (size_t)s * rows * sizeof(float));
+  w.total = w.states + DA_ARRIVAL_BYTES;
   return w;
 }
 
@@ -674,7 +693,7 @@ int da_make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_
 
 size_t da_schedule_workspace_bytes(const da_schedule* s) {
   if (!s || s->state_rows <= 0 || s->H_Q <= 0) return 0;
-  return da::workspace_layout(s->state_rows, s->H_Q, da::kHeadDim, 1).total;
+  return da::workspace_layout(s->state_rows, s->H_Q, da::kHeadDim, 1).states;
 }
 
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits) {

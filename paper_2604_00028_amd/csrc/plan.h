@@ -44,6 +44,8 @@ struct CostModel {
   double t_tile_staged[2]; // ... K and V fetched straight into LDS (at most one workgroup per CU)
   double merge0;           // second launch that combines the chunk states, fixed part (s > 1)
   double merge1[2];        // ... per chunk
+  double fused0;           // single-launch merge by the last workgroup of a tile, fixed part (s > 1)
+  double fused1[2];        // ... per chunk
   double hbm_rate;         // sustained HBM bytes per microsecond, whole chip
   double hbm0;             // fixed part of the streaming bound
   double pnorm;            // the two bounds combine as (compute^p + stream^p)^(1/p)
@@ -58,8 +60,15 @@ const CostModel& mi355x_streamed_model();
 // by this factor.
 constexpr double kSplitGain = 0.99;
 
-// Modelled time (us) of one call with s splits (policy MI355X).
-double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs = 1);
+// Modelled time (us) of one call with s splits (policy MI355X); `fused`:
+// the chunk states are merged inside the split launch (da_plan.combine 1)
+// rather than by a second launch.
+double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs = 1,
+                  bool fused = false);
+
+// Whether a plan of s chunks per sequence over `tiles` tiles of `hpt` heads
+// merges the chunk states inside the split launch (da_plan.combine).
+bool fused_merge(const CostModel& m, int hpt, int s, int64_t tiles);
 
 // Whether `pl` may serve each chunk with pl.v_slices workgroups (1, 2 or 4):
 // more than one only with K/V straight into LDS, packed tiles of either
@@ -135,9 +144,19 @@ double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t
 int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
                   int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes, da_schedule* out);
 
+// Workspace regions (256-byte aligned): chunk states Otilde | m | l from
+// offset 0 (`states` ends them), and the arrival counters of single-launch
+// merges in the last DA_ARRIVAL_BYTES of the caller's buffer, wherever its
+// end is.  Chunk states of any shape stop before that region, so calls of
+// different shapes can share one buffer without writing into the counters.
 struct WorkspaceLayout {
-  size_t o_off, m_off, l_off, total;
+  size_t o_off, m_off, l_off, states, total;
 };
 WorkspaceLayout workspace_layout(int B, int H_Q, int d, int s);
+constexpr int kArrivalStride = DA_ARRIVAL_STRIDE / 4;  // uint32 words between two tiles' counters
+constexpr int64_t kMaxArrivalTiles = DA_ARRIVAL_BYTES / DA_ARRIVAL_STRIDE;  // tiles a single-launch merge can count
+
+// Offset of the arrival counters in a workspace of `bytes` bytes.
+inline size_t arrival_offset(size_t bytes) { return (bytes - DA_ARRIVAL_BYTES) & ~(size_t)255; }
 
 }  // namespace da

@@ -150,7 +150,8 @@ def test_workspace_bytes():
     assert da.da_workspace_bytes(1, 64, 128, 1) == 0
     for B, H, s in [(1, 8, 2), (32, 64, 8), (16, 32, 64)]:
         n = da.da_workspace_bytes(B, H, 128, s)
-        need = s * B * H * 128 * 4 + 2 * s * B * H * 4
+        # chunk states (Otilde, m, l), then the fixed arrival-counter region at the end
+        need = s * B * H * 128 * 4 + 2 * s * B * H * 4 + (1 << 20)
         assert need <= n <= need + 3 * 256 and n % 256 == 0
 
 
@@ -333,6 +334,24 @@ def test_planned_entry_checks_the_plan():
     assert call(good, H_Q=32, H_KV=4) == bnd.DA_ERR_ARG
     # the workspace its split count needs
     assert call(good, ws=0, ws_bytes=0) == bnd.DA_ERR_WORKSPACE
+    # the merge: 0 or 1, the single-launch merge only with a split and at most 4096 tiles
+    for val in (-1, 2):
+        bad = bnd.DaPlan.from_buffer_copy(good)
+        bad.combine = val
+        assert call(bad) == bnd.DA_ERR_ARG, val
+    one = da.da_make_plan(2, 64, 8, 512, num_splits=1, pack_gqa=1, num_cus=256)
+    one.combine = 1
+    assert call(one) == bnd.DA_ERR_ARG
+    many = da.da_make_plan(4097, 8, 8, 64, num_splits=2, pack_gqa=0, num_cus=256)
+    many.combine = 1
+    assert many.tiles > 4096 and call(many, B=4097, H_Q=8, H_KV=8, L=64) == bnd.DA_ERR_ARG
+    # a single-launch merge needs the counter region too: states alone are not enough
+    fused = bnd.DaPlan.from_buffer_copy(good)
+    fused.combine = 1
+    states = da.da_workspace_bytes(2, 64, 128, 4) - (1 << 20)
+    assert call(fused, ws_bytes=states) == bnd.DA_ERR_WORKSPACE
+    good.combine = 0
+    assert call(good, ws_bytes=states - 256) == bnd.DA_ERR_WORKSPACE
 
 
 def test_paged_planned_entry_checks_arguments():

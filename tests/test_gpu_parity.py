@@ -303,6 +303,8 @@ def test_workspace_reused_across_split_counts():
     outs = {}
     for s in (64, 8, 2, 5, 8, 64, 3):
         say(f"shared workspace s={s}")
+        ws[:-(1 << 20)].fill_(255)      # chunk states need no initialisation
+        ws[-(1 << 20):].zero_()         # arrival counters of a single-launch merge start at zero
         out = da.da_decode_attn(q, k, v, num_splits=s, pack_gqa=1, workspace=ws)
         torch.cuda.synchronize()
         assert_parity(out, O, f"shared workspace s={s}")

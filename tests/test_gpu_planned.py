@@ -72,6 +72,11 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
                     assert same_bits(got, first[key]), (key, p.as_dict())
                 else:
                     first[key] = got
+                if p.num_splits > 1:
+                    # the other merge (a second launch, or inside the split launch): the same bits
+                    p.combine = 1 - p.combine
+                    say(f"planned, other merge {p.as_dict()}")
+                    assert same_bits(planned(q, k, v, cu, L, p), got), p.as_dict()
 
 
 @pytest.mark.parametrize("shape", config_shapes(2) + config_shapes(1), ids=lambda s: s.name)
