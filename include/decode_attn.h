@@ -157,7 +157,9 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
  * before the first call whose plan has combine == 1 (zero the buffer once
  * when it is allocated); every such call leaves them zero, so one buffer
  * serves calls of any shape in turn.  A plan with combine == 0 does not
- * touch the counters and needs only the chunk-state bytes. */
+ * touch the counters, but every call with num_splits > 1 needs the full
+ * da_workspace_bytes, so that no call's chunk states reach the counter
+ * region of a buffer shared with single-launch calls. */
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits);
 
 /* Cut points of sequence chunking: chunk i of a sequence of L keys is

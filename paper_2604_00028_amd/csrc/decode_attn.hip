@@ -1270,18 +1270,18 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
   if (pack_gqa < -1 || pack_gqa > 2) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
   if (workspace && !aligned(workspace, 16)) return da::fail(DA_ERR_ALIGN, "workspace must be 16-byte aligned");
 
-  // A forced split count fixes the workspace need before any device access
-  // (the arrival counters only for a single-launch merge).
-  auto check_workspace = [&](int s, bool fused) {
+  // A forced split count fixes the workspace need before any device access.
+  // Every split call needs the counter region too, so that no call's chunk
+  // states reach the counters another call on the same buffer relies on.
+  auto check_workspace = [&](int s) {
     if (s <= 1) return (int)DA_OK;
-    const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
-    const size_t need = fused ? wl.total : wl.states;
+    const size_t need = da::workspace_layout(B, H_Q, d, s).total;
     if (!workspace || workspace_bytes < need)
       return da::fail(DA_ERR_WORKSPACE, "num_splits=%d needs %zu workspace bytes, got %zu", s, need,
                       workspace ? workspace_bytes : (size_t)0);
     return check_state_size(B, H_Q, s);
   };
-  int rc = check_workspace(given ? given->num_splits : num_splits, given && given->combine == 1);
+  int rc = check_workspace(given ? given->num_splits : num_splits);
   if (rc) return rc;
   int cus = 0;
   rc = ensure_gfx950(&cus);
@@ -1294,7 +1294,7 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
   if (rc) return rc;
   const int s = pl.num_splits;
   const bool fused = s > 1 && pl.combine == 1;
-  rc = check_workspace(s, fused);
+  rc = check_workspace(s);
   if (rc) return rc;
   const da::WorkspaceLayout wl = da::workspace_layout(B, H_Q, d, s);
 

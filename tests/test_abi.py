@@ -345,13 +345,12 @@ def test_planned_entry_checks_the_plan():
     many = da.da_make_plan(4097, 8, 8, 64, num_splits=2, pack_gqa=0, num_cus=256)
     many.combine = 1
     assert many.tiles > 4096 and call(many, B=4097, H_Q=8, H_KV=8, L=64) == bnd.DA_ERR_ARG
-    # a single-launch merge needs the counter region too: states alone are not enough
-    fused = bnd.DaPlan.from_buffer_copy(good)
-    fused.combine = 1
+    # every split plan needs the counter region too: chunk states alone are not enough
     states = da.da_workspace_bytes(2, 64, 128, 4) - (1 << 20)
-    assert call(fused, ws_bytes=states) == bnd.DA_ERR_WORKSPACE
-    good.combine = 0
-    assert call(good, ws_bytes=states - 256) == bnd.DA_ERR_WORKSPACE
+    for comb in (0, 1):
+        plan = bnd.DaPlan.from_buffer_copy(good)
+        plan.combine = comb
+        assert call(plan, ws_bytes=states) == bnd.DA_ERR_WORKSPACE, comb
 
 
 def test_paged_planned_entry_checks_arguments():
@@ -515,3 +514,4 @@ def test_workspace_cache_keeps_replaced_buffers_alive():
     assert alive() is not None and alive().data_ptr() == ptr      # the old buffer is still held
     assert bnd.workspace_for(dev, key_stream, 2000) is big        # smaller requests reuse the cache
     bnd._workspaces.pop((-1, key_stream), None)
+
