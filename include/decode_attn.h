@@ -51,6 +51,9 @@ extern "C" {
  * 256 = 4096 tiles. */
 #define DA_ARRIVAL_BYTES (1 << 20)
 #define DA_ARRIVAL_STRIDE 256
+/* Chunk-state bytes the scratch of da_decode_attn_noalloc holds (per device,
+ * for the life of the process, with DA_ARRIVAL_BYTES of counters after it). */
+#define DA_NOALLOC_STATE_BYTES (32 << 20)
 
 typedef enum da_status {
   DA_OK = 0,
@@ -219,6 +222,25 @@ int da_decode_attn_planned(const void* q, const void* k, const void* v, const in
                            void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                            float softmax_scale, const da_plan* plan, void* workspace,
                            size_t workspace_bytes, void* stream);
+
+/* da_decode_attn for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * The same arguments without the workspace, the same plan (policy MI355X)
+ * and the same bits as da_decode_attn for that plan.  The chunk states and
+ * arrival counters of a split plan live in a fixed scratch array of
+ * DA_NOALLOC_STATE_BYTES + DA_ARRIVAL_BYTES bytes that every device holds
+ * from the library's load until the process ends; no call allocates or
+ * frees anything.  The first call on a device looks up the array's address
+ * and clears its counters with a kernel on `stream`.  Every call on a device
+ * shares that array and leaves the previous call's chunk states in it:
+ * calls that overlap in time on one device (other streams, other host
+ * threads) race and must not be made.  Errors as for da_decode_attn, and
+ * DA_ERR_WORKSPACE when the plan's chunk states exceed
+ * DA_NOALLOC_STATE_BYTES (for a forced num_splits before any device
+ * access), e.g. num_splits = 64 at B = 32, H_Q = 64. */
+int da_decode_attn_noalloc(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
+                           void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
+                           float softmax_scale, int num_splits, int pack_gqa, void* stream);
 
 /* Decode attention over a paged KV cache: the same computation as
  * da_decode_attn, with sequence b's keys held in fixed-size pages (the

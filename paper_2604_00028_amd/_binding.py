@@ -38,7 +38,7 @@ POLICY_STREAMED = 3
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (
     "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
-    "da_decode_attn_planned", "da_decode_attn_paged", "da_decode_attn_paged_planned", "da_schedule_max_bytes",
+    "da_decode_attn_planned", "da_decode_attn_noalloc", "da_decode_attn_paged", "da_decode_attn_paged_planned", "da_schedule_max_bytes",
     "da_make_schedule", "da_schedule_workspace_bytes",
     "da_decode_attn_scheduled", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror",
     "da_last_error",
@@ -124,6 +124,8 @@ def load() -> ctypes.CDLL:
     lib.da_decode_attn_planned.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, ctypes.POINTER(DaPlan),
                                            _P, _Z, _P]
     lib.da_decode_attn_planned.restype = _I
+    lib.da_decode_attn_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _F, _I, _I, _P]
+    lib.da_decode_attn_noalloc.restype = _I
     lib.da_decode_attn_paged.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _F, _I, _I,
                                          _P, _Z, _P]
     lib.da_decode_attn_paged.restype = _I
@@ -307,6 +309,23 @@ def da_decode_attn_planned(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pl
     _check(load().da_decode_attn_planned(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),
                                          B, H_Q, H_KV, L, d, float(softmax_scale), ctypes.byref(plan),
                                          ws_ptr, ws_bytes, s_handle))
+    return out
+
+
+def da_decode_attn_noalloc(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                           cu_seqlens_k: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                           lse_out: Optional[torch.Tensor] = None, *, L_K_max: Optional[int] = None,
+                           softmax_scale: float = 0.0, num_splits: int = 0, pack_gqa: int = -1,
+                           stream=None) -> torch.Tensor:
+    """da_decode_attn with no workspace: the library's fixed per-device
+    scratch holds the chunk states.  Pass `out` to make the call allocate
+    nothing at all."""
+    B, H_Q, H_KV, L, d = _shapes(q, k, v, cu_seqlens_k, L_K_max)
+    if out is None:
+        out = torch.empty((B, H_Q, d), dtype=torch.bfloat16, device=q.device)
+    _check(load().da_decode_attn_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(cu_seqlens_k), _ptr(out), _ptr(lse_out),
+                                         B, H_Q, H_KV, L, d, float(softmax_scale), int(num_splits), int(pack_gqa),
+                                         _stream(q.device, stream)))
     return out
 
 

@@ -46,6 +46,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "decode_attn.h"
@@ -1369,6 +1370,60 @@ void set_paged(Params& p, const void* q, const void* k_cache, const void* v_cach
   p.num_pages = num_pages;
 }
 
+// ---------------------------------------------------------------- no-allocation scratch
+
+// Device memory for da_decode_attn_noalloc: one call's chunk states (up to
+// DA_NOALLOC_STATE_BYTES) followed by the arrival-counter region, a file-scope
+// array that each device holds from module load until the process ends.  In
+// host code its name only stands in for the symbol: the device address comes
+// from hipGetSymbolAddress, once per device, and only that address is used.
+constexpr size_t kScratchBytes = (size_t)DA_NOALLOC_STATE_BYTES + DA_ARRIVAL_BYTES;
+
+__global__ void __launch_bounds__(256) zero_words(uint32_t* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+std::atomic<unsigned char*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// The current device's address of `scratch`.  The first call on a device
+// takes it with hipGetSymbolAddress and clears the arrival counters (they
+// must start at zero) with a kernel on `stream`, not a memset, so that the
+// first call may be captured in a graph.
+int scratch_address(hipStream_t stream, unsigned char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return da::fail(DA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return da::fail(DA_ERR_UNSUPPORTED, "device index %d", dev);
+  unsigned char* ptr = g_scratch[dev].load(std::memory_order_acquire);
+  if (!ptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ptr = g_scratch[dev].load(std::memory_order_acquire);
+    if (!ptr) {
+      void* addr = nullptr;
+      e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !addr)
+        return da::fail(DA_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      uint32_t* counters = reinterpret_cast<uint32_t*>(static_cast<unsigned char*>(addr) +
+                                                       da::arrival_offset(kScratchBytes));
+      int words = DA_ARRIVAL_BYTES / 4;
+      void* args[] = {&counters, &words};
+      e = hipLaunchKernel(reinterpret_cast<const void*>(&zero_words), dim3(64), dim3(256), args, 0, stream);
+      if (e != hipSuccess) return da::fail(DA_ERR_HIP, "scratch counter clear: %s", hipGetErrorString(e));
+      ptr = static_cast<unsigned char*>(addr);
+      g_scratch[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return DA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1408,6 +1463,51 @@ int da_decode_attn_planned(const void* q, const void* k, const void* v, const in
   p.cu = cu_seqlens_k;
   return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, plan->num_splits, plan->pack_gqa, out, lse_out,
                     workspace, workspace_bytes, stream, plan);
+}
+
+int da_decode_attn_noalloc(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k, void* out,
+                           float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d, float softmax_scale,
+                           int num_splits, int pack_gqa, void* stream) {
+  da::clear_error();
+  int rc = check_inputs(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, d);
+  if (rc) return rc;
+  if (!out) return da::fail(DA_ERR_NULL, "out must be non-NULL");
+  if (!aligned(out, 16)) return da::fail(DA_ERR_ALIGN, "out must be 16-byte aligned");
+  if (lse_out && !aligned(lse_out, 4)) return da::fail(DA_ERR_ALIGN, "lse_out must be 4-byte aligned");
+  if (num_splits > DA_MAX_SPLITS)
+    return da::fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, DA_MAX_SPLITS);
+  if (pack_gqa < -1 || pack_gqa > 2) return da::fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
+  auto fits = [&](int s) {
+    const size_t need = s > 1 ? da::workspace_layout(B, H_Q, d, s).total : 0;
+    if (need > kScratchBytes)
+      return da::fail(DA_ERR_WORKSPACE,
+                      "num_splits=%d needs %zu bytes of chunk state and counters; the no-allocation scratch "
+                      "holds %zu",
+                      s, need, kScratchBytes);
+    return (int)DA_OK;
+  };
+  rc = fits(num_splits);  // a forced split count is known before any device access
+  if (rc) return rc;
+  int cus = 0;
+  rc = ensure_gfx950(&cus);
+  if (rc) return rc;
+  da_plan pl;
+  rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+  if (rc) return rc;
+  rc = fits(pl.num_splits);
+  if (rc) return rc;
+  unsigned char* ws = nullptr;
+  if (pl.num_splits > 1) {
+    rc = scratch_address(static_cast<hipStream_t>(stream), &ws);
+    if (rc) return rc;
+  }
+  Params p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.cu = cu_seqlens_k;
+  return run_decode(p, B, H_Q, H_KV, L_K_max, d, softmax_scale, pl.num_splits, pl.pack_gqa, out, lse_out, ws,
+                    ws ? kScratchBytes : 0, stream, &pl);
 }
 
 int da_decode_attn_paged(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,

@@ -515,3 +515,25 @@ def test_workspace_cache_keeps_replaced_buffers_alive():
     assert bnd.workspace_for(dev, key_stream, 2000) is big        # smaller requests reuse the cache
     bnd._workspaces.pop((-1, key_stream), None)
 
+
+def test_noalloc_entry_checks_arguments_before_device_access(lib):
+    """The no-allocation entry point validates everything, and refuses a
+    forced split count whose chunk states exceed its fixed scratch, before
+    any HIP call (so here, with no GPU, no device error can come first)."""
+    P = ctypes.c_void_p
+
+    def call(q=FAKE, k=FAKE, v=FAKE, out=FAKE, lse=None, B=1, H_Q=8, H_KV=1, L=128, d=128, s=1, pack=1):
+        return lib.da_decode_attn_noalloc(P(q) if q else None, P(k) if k else None, P(v) if v else None, None,
+                                          P(out) if out else None, P(lse) if lse else None, B, H_Q, H_KV, L, d,
+                                          0.0, s, pack, None)
+    assert call(q=0) == bnd.DA_ERR_NULL
+    assert call(out=0) == bnd.DA_ERR_NULL
+    assert call(out=FAKE + 4) == bnd.DA_ERR_ALIGN
+    assert call(lse=FAKE + 1) == bnd.DA_ERR_ALIGN
+    assert call(d=64) == bnd.DA_ERR_UNSUPPORTED
+    assert call(s=65) == bnd.DA_ERR_SPLITS
+    assert call(pack=3) == bnd.DA_ERR_ARG
+    assert call(H_KV=3) == bnd.DA_ERR_SHAPE
+    # 64 chunks of B=32, H_Q=64: 68 MB of chunk state > the 32 MiB scratch
+    assert call(B=32, H_Q=64, H_KV=8, L=8192, s=64) == bnd.DA_ERR_WORKSPACE
+    assert "scratch" in da.da_last_error()
