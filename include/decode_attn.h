@@ -138,6 +138,19 @@ typedef struct da_plan {
 int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
                      int cu_margin, int policy, da_plan* out);
 
+/* The split policy's modelled time of one call, in microseconds: the cost
+ * model that replaces the paper's H100 rule on MI355X (Section 4 counts work
+ * tiles against the compute units; here the count of workgroups per CU, the
+ * 32-key tiles each wave walks, the HBM rate and the merge of the chunk
+ * states are priced with measured constants).  policy DA_POLICY_STREAMED
+ * uses the constants for K/V read from HBM on every call, any other value
+ * those of DA_POLICY_MI355X.  heads_per_tile, v_slices and combine as in
+ * da_plan; num_cus > 0.  Host only.  Returns -1 for arguments that describe
+ * no launch (heads_per_tile not dividing H_Q, num_splits outside 1..64,
+ * v_slices not 1, 2 or 4, combine not 0 or 1, non-positive sizes). */
+double da_model_time(int policy, int B, int H_Q, int H_KV, int L_K, int heads_per_tile, int num_splits,
+                     int v_slices, int combine, int num_cus);
+
 /* Same as da_choose_splits with num_splits and/or pack_gqa forced
  * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy;
  * pack_gqa 0, 1 or 2 as in da_plan).

@@ -37,7 +37,7 @@ POLICY_STREAMED = 3
 
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (
-    "da_choose_splits", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
+    "da_choose_splits", "da_model_time", "da_make_plan", "da_workspace_bytes", "da_split_bounds", "da_decode_attn",
     "da_decode_attn_planned", "da_decode_attn_noalloc", "da_decode_attn_paged", "da_decode_attn_paged_planned", "da_schedule_max_bytes",
     "da_make_schedule", "da_schedule_workspace_bytes",
     "da_decode_attn_scheduled", "da_split_partials", "da_combine_splits", "da_device_info", "da_strerror",
@@ -113,6 +113,8 @@ def load() -> ctypes.CDLL:
         raise RuntimeError(f"two HIP runtimes are loaded ({runtimes}); torch must be imported first")
     lib.da_choose_splits.argtypes = [_I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(DaPlan)]
     lib.da_choose_splits.restype = _I
+    lib.da_model_time.argtypes = [_I] * 10
+    lib.da_model_time.restype = ctypes.c_double
     lib.da_make_plan.argtypes = [_I, _I, _I, _I, _I, _I, _I, _I, _I, _I, ctypes.POINTER(DaPlan)]
     lib.da_make_plan.restype = _I
     lib.da_workspace_bytes.argtypes = [_I, _I, _I, _I]
@@ -181,6 +183,13 @@ def da_choose_splits(B: int, H_Q: int, H_KV: int, L_K_max: int, d: int = HEAD_DI
     plan = DaPlan()
     _check(load().da_choose_splits(B, H_Q, H_KV, L_K_max, d, num_cus, cu_margin, policy, ctypes.byref(plan)))
     return plan
+
+
+def da_model_time(policy: int, B: int, H_Q: int, H_KV: int, L_K: int, heads_per_tile: int, num_splits: int,
+                  v_slices: int = 1, combine: int = 0, num_cus: int = 256) -> float:
+    """The planner's modelled microseconds per call (-1 for no launch)."""
+    return float(load().da_model_time(policy, B, H_Q, H_KV, L_K, heads_per_tile, num_splits, v_slices, combine,
+                                      num_cus))
 
 
 def da_make_plan(B: int, H_Q: int, H_KV: int, L_K_max: int, d: int = HEAD_DIM, num_splits: int = 0,

@@ -1,0 +1,299 @@
+"""Calibration of the planner's cost models from measured sweeps.
+
+    python -m paper_2604_00028_amd.calibrate            # fit and print
+    python -m paper_2604_00028_amd.calibrate --write    # also regenerate csrc/cost_model.inc
+
+The split policy (paper Section 4) replaces the paper's H100 rule with a cost
+model over num_splits in [1, 64]; its constants are measured on MI355X.  The
+measurements are committed sweep summaries under profiles/ (written by
+`bench.py --calibrate OUT.json --calibrate-set warm|streamed`): for each shape
+(B, H_Q, H_KV, L_K), the microseconds per call of every launch the planner can
+choose -- split count, packed tile width, V slices, and the merge of the chunk
+states (a second launch, or inside the split launch).  This module fits the
+constants to them and writes them to csrc/cost_model.inc, which plan.cpp
+includes.  A CPU test refits the committed sweeps and checks that they give
+the committed constants.
+
+The model (the same arithmetic as model_time in csrc/plan.cpp, for a launch
+of `wgs` workgroups of four waves over chunks of ceil(L_K / s) keys):
+
+    compute = base + ceil(wgs / CUs) * (32-key tiles per wave) * t_tile * contig^[H_KV = 1] * vs_tile
+    stream  = hbm0 + (K/V bytes + chunk-state bytes) / hbm_rate
+    T = (compute^p + stream^p)^(1/p) + [s > 1] (merge0 + merge1 s   |  fused0 + fused1 s)
+
+t_tile is t_tile_staged when every workgroup has a CU to itself.  Each term
+has a 16-column and a 32-column (more than 16 heads per workgroup) value.
+
+Fit: least squares of log(model) - log(measured) over every launch within
+1.6x of its shape's fastest (the launches a planner might pick), in the logs
+of the parameters, from fixed starting values: deterministic for a given
+sweep.  Policy MI355X (K/V resident, as in graph replays of one call) fits
+every constant but contig (1) and hbm0 (0); policy STREAMED (every call
+reads its cache from HBM) holds p at 4 and fits contig.  Both tie the 32-column tile time of
+launches with several workgroups per CU to the 16-column one (TIED).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+from typing import Dict, List
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+HEADER = os.path.join(HERE, "csrc", "cost_model.inc")
+SWEEPS = {"warm": os.path.join(ROOT, "profiles", "calibration_warm.json"),
+          "streamed": os.path.join(ROOT, "profiles", "calibration_streamed.json")}
+
+CUS = 256
+HEAD_DIM = 128
+ROW_BYTES = 2.0 * HEAD_DIM * 2.0          # K and V row of one KV head per key
+STATE_BYTES = (HEAD_DIM + 2) * 4.0        # Otilde, m, l of one head and chunk
+WINDOW = 1.6
+SLICE_KV_BYTES = 16 << 20   # K/V bytes up to which the planner considers V slices (half the L2)
+
+# name, 16-column / 32-column pair index (None: one value)
+NAMES = ["base0", "base1", "tt0", "tt1", "ts0", "ts1", "merge0", "merge1_0", "merge1_1", "fused0", "fused1_0",
+         "fused1_1", "hbm_rate", "hbm0", "pnorm", "contig", "vs2", "vs4"]
+HELD = {"warm": {"contig": 1.0, "hbm0": 0.0}, "streamed": {"pnorm": 4.0}}
+# 32-column tiles with several workgroups per CU are rare among the fastest
+# launches, so their tile time is tied to the 16-column one by the ratio the
+# two widths show with K/V straight into LDS: tt1 = tt0 * ts1 / ts0.
+TIED = ("tt1",)
+START = {   # starting values of the fit
+    "warm": dict(base0=2.841, base1=4.042, tt0=0.809, tt1=1.130, ts0=0.671, ts1=0.854, merge0=2.458, merge1_0=0.218,
+                 merge1_1=0.253, fused0=1.5, fused1_0=0.1, fused1_1=0.12, hbm_rate=6.319e6, hbm0=0.05, pnorm=2.389,
+                 contig=1.0, vs2=0.812, vs4=0.714),
+    "streamed": dict(base0=2.095, base1=3.679, tt0=1.576, tt1=2.2, ts0=1.609, ts1=1.643, merge0=2.308,
+                     merge1_0=0.235, merge1_1=0.254, fused0=1.5, fused1_0=0.1, fused1_1=0.12, hbm_rate=6.498e6,
+                     hbm0=3.366, pnorm=4.0, contig=0.744, vs2=0.943, vs4=0.856),
+}
+
+
+def launch_grid(chunks, vs):
+    return np.where(vs == 1, chunks, vs * 8 * ((chunks + 7) // 8))
+
+
+def kv_fetch(grid, tiles_per_wave, cus=CUS):
+    """2: K/V straight into LDS (one workgroup per CU); 1: through registers
+    (several per CU, at least two tiles per wave); 0: K into the operand
+    layout (one tile per wave)."""
+    return np.where(grid <= cus, 2, np.where(tiles_per_wave >= 2, 1, 0))
+
+
+def model_time(c: Dict[str, float], B, H_Q, H_KV, L, hpt, s, vs, fused, cus=CUS):
+    """Modelled microseconds per call (arrays broadcast)."""
+    B, H_Q, H_KV, L, hpt, s, vs, fused = (np.asarray(x, dtype=np.int64) for x in (B, H_Q, H_KV, L, hpt, s, vs, fused))
+    wide = hpt > 16
+    tiles = B * H_Q // hpt
+    wgs = launch_grid(tiles * s, vs)
+    chunk = (L + s - 1) // s
+    per_wave = (chunk + 3) // 4
+    tpw = (per_wave + 31) // 32
+    per_cu = (wgs + cus - 1) // cus
+    staged = kv_fetch(wgs, tpw, cus) == 2
+    tt = np.where(staged, np.where(wide, c["ts1"], c["ts0"]), np.where(wide, c["tt1"], c["tt0"]))
+    tt = tt * np.where(H_KV == 1, c["contig"], 1.0) * np.where(vs == 4, c["vs4"], np.where(vs == 2, c["vs2"], 1.0))
+    compute = np.where(wide, c["base1"], c["base0"]) + per_cu * tpw * tt
+    nbytes = B * L * H_KV * ROW_BYTES + np.where(s > 1, 2.0 * s * B * H_Q * STATE_BYTES, 0.0)
+    stream = c["hbm0"] + nbytes / c["hbm_rate"]
+    p = c["pnorm"]
+    t = (compute ** p + stream ** p) ** (1.0 / p)
+    merge = np.where(fused == 1, c["fused0"] + np.where(wide, c["fused1_1"], c["fused1_0"]) * s,
+                     c["merge0"] + np.where(wide, c["merge1_1"], c["merge1_0"]) * s)
+    return t + np.where(s > 1, merge, 0.0)
+
+
+def choosable(sh: dict) -> list:
+    """A shape's timed launches that the planner can choose: V slices only
+    up to SLICE_KV_BYTES of K/V."""
+    kv = sh["B"] * sh["L"] * sh["H_KV"] * ROW_BYTES
+    return [t for t in sh["launches"] if t[2] == 1 or kv <= SLICE_KV_BYTES]
+
+
+def launches(sweep: dict) -> Dict[str, np.ndarray]:
+    """The sweep's choosable launches as arrays, with each shape's fastest time."""
+    cols = {k: [] for k in ("B", "H_Q", "H_KV", "L", "hpt", "s", "vs", "fused", "us", "best", "shape")}
+    for i, sh in enumerate(sweep["shapes"]):
+        best = min(t[4] for t in choosable(sh))
+        for hpt, s, vs, fused, us in choosable(sh):
+            for k, v in (("B", sh["B"]), ("H_Q", sh["H_Q"]), ("H_KV", sh["H_KV"]), ("L", sh["L"]), ("hpt", hpt),
+                         ("s", s), ("vs", vs), ("fused", fused), ("us", us), ("best", best), ("shape", i)):
+                cols[k].append(v)
+    return {k: np.asarray(v, dtype=np.float64 if k in ("us", "best") else np.int64) for k, v in cols.items()}
+
+
+def fit(sweep: dict, which: str) -> Dict[str, float]:
+    """Constants of policy `which` ("warm" or "streamed") fitted to a sweep."""
+    from scipy.optimize import least_squares
+    d = launches(sweep)
+    keep = d["us"] <= WINDOW * d["best"]
+    d = {k: v[keep] for k, v in d.items()}
+    free = [n for n in NAMES if n not in HELD[which] and n not in TIED]
+    start = START[which]
+    x0 = np.log([start[n] for n in free])
+
+    def consts(x):
+        c = dict(HELD[which])
+        c.update({n: float(math.exp(v)) for n, v in zip(free, x)})
+        c["tt1"] = c["tt0"] * c["ts1"] / c["ts0"]
+        return c
+
+    def resid(x):
+        t = model_time(consts(x), d["B"], d["H_Q"], d["H_KV"], d["L"], d["hpt"], d["s"], d["vs"], d["fused"])
+        return np.log(t) - np.log(d["us"])
+
+    res = least_squares(resid, x0, method="trf", x_scale=1.0, xtol=1e-12, ftol=1e-12, gtol=1e-12, max_nfev=4000)
+    return {n: float(f"{v:.6g}") for n, v in consts(res.x).items()}
+
+
+def fit_error(sweep: dict, c: Dict[str, float]) -> Dict[str, float]:
+    """RMS and worst relative error of the model over the fitted window."""
+    d = launches(sweep)
+    keep = d["us"] <= WINDOW * d["best"]
+    t = model_time(c, *(d[k][keep] for k in ("B", "H_Q", "H_KV", "L", "hpt", "s", "vs", "fused")))
+    r = np.log(t) - np.log(d["us"][keep])
+    return {"launches": int(keep.sum()), "rms_log_error": float(np.sqrt(np.mean(r * r))),
+            "worst_ratio": float(np.exp(np.max(np.abs(r))))}
+
+
+def heads_per_tile(H_Q: int, H_KV: int, cap: int) -> int:
+    g = H_Q // H_KV
+    return g if g <= cap else max(h for h in range(1, cap + 1) if g % h == 0)
+
+
+def plan_mi355x(c: Dict[str, float], B: int, H_Q: int, H_KV: int, L: int, cus: int = CUS, gain: float = 0.99,
+                l2_bytes: float = SLICE_KV_BYTES, max_arrival_tiles: int = 4096, split_gain: float = None):
+    """The choice the planner makes with constants `c` for num_splits and
+    pack_gqa left to it (the steps of plan() in csrc/plan.cpp): per packed
+    tile width the split count with its best V slices, a split, V slices or
+    the narrow width only when modelled `gain` faster.  (hpt, s, vs, combine)."""
+    g = H_Q // H_KV
+    kv_bytes = B * L * H_KV * ROW_BYTES
+
+    def fused(h, s):
+        w = h > 16
+        return s > 1 and B * H_Q // h <= max_arrival_tiles and \
+            c["fused0"] + c["fused1_1" if w else "fused1_0"] * s < c["merge0"] + c["merge1_1" if w else "merge1_0"] * s
+
+    def t(h, s, vs):
+        return float(model_time(c, B, H_Q, H_KV, L, h, s, vs, 1 if fused(h, s) else 0, cus))
+
+    def best_vs(h, s, slices):
+        one = t(h, s, 1)
+        bv, bt = 1, one
+        tiles = B * H_Q // h
+        slices = slices and kv_bytes <= l2_bytes
+        vs = 2
+        while slices and vs <= 4 and (tiles * s if vs == 1 else vs * 8 * -(-(tiles * s) // 8)) <= cus:
+            tv = t(h, s, vs)
+            if tv < bt and tv < gain * one:
+                bv, bt = vs, tv
+            vs *= 2
+        return bv, bt
+
+    def splits(h, slices):
+        if L <= 0:
+            return 1
+        _, one = best_vs(h, 1, slices)
+        bs, bt = 1, one
+        for s in range(2, 65):
+            _, ts = best_vs(h, s, slices)
+            if ts < bt:
+                bs, bt = s, ts
+        return bs if bt < (gain if split_gain is None else split_gain) * one else 1
+
+    pack = 1 if g > 1 else 0
+    wide = heads_per_tile(H_Q, H_KV, 32) if pack else 1
+    narrow = heads_per_tile(H_Q, H_KV, 16) if pack else 1
+    slices = lambda h: pack == 1 or h == g
+    s_w = splits(wide, slices(wide))
+    _, t_w = best_vs(wide, s_w, slices(wide))
+    hpt, s = wide, s_w
+    if narrow != wide:
+        s_n = splits(narrow, slices(narrow))
+        _, t_n = best_vs(narrow, s_n, slices(narrow))
+        if t_n < gain * t_w:
+            hpt, s = narrow, s_n
+    vs, _ = best_vs(hpt, s, slices(hpt))
+    return hpt, s, vs, 1 if fused(hpt, s) else 0
+
+
+def regret(sweep: dict, plan) -> Dict[str, object]:
+    """How the launch the planner picks fares on a sweep: plan(B, H_Q, H_KV,
+    L_K) gives (heads per tile, s, V slices, combine); its measured time (a
+    split count the sweep did not time takes the nearest timed one below)
+    over the shape's fastest, and over one split as the paper launches it
+    (the whole group in one workgroup, no V slices)."""
+    rows = []
+    for sh in sweep["shapes"]:
+        t = {(h, s, v, c): us for h, s, v, c, us in choosable(sh)}
+        hpt, s, vs, comb = plan(sh["B"], sh["H_Q"], sh["H_KV"], sh["L"])
+        timed = [k for k in t if k[0] == hpt and k[2] == vs and k[3] == comb and k[1] <= s]
+        key = max(timed, key=lambda k: k[1]) if timed else min(t, key=t.get)
+        wide = max(k[0] for k in t)
+        rows.append({"B": sh["B"], "H_Q": sh["H_Q"], "H_KV": sh["H_KV"], "L": sh["L"], "plan": [hpt, s, vs, comb],
+                     "us": t[key], "best": min(t.values()), "best_launch": list(min(t, key=t.get)),
+                     "s1_paper": t[(wide, 1, 1, 0)]})
+    r = [x["us"] / x["best"] for x in rows]
+    p = [x["s1_paper"] / x["us"] for x in rows]
+    return {"shapes": len(rows), "mean_vs_best": float(np.mean(r)), "worst_vs_best": float(np.max(r)),
+            "within_5pct": int(sum(x <= 1.05 for x in r)), "worst_speedup_vs_s1_paper": float(np.min(p)),
+            "rows": rows}
+
+
+def model_literal(c: Dict[str, float]) -> str:
+    f = lambda n: repr(float(c[n]))
+    return ("{{{b0}, {b1}}}, {{{tt0}, {tt1}}}, {{{ts0}, {ts1}}}, {m0}, {{{m10}, {m11}}}, {f0}, {{{f10}, {f11}}}, "
+            "{rate}, {hbm0}, {p}, {contig}, {{1.0, {vs2}, {vs4}}}").format(
+        b0=f("base0"), b1=f("base1"), tt0=f("tt0"), tt1=f("tt1"), ts0=f("ts0"), ts1=f("ts1"), m0=f("merge0"),
+        m10=f("merge1_0"), m11=f("merge1_1"), f0=f("fused0"), f10=f("fused1_0"), f11=f("fused1_1"),
+        rate=f("hbm_rate"), hbm0=f("hbm0"), p=f("pnorm"), contig=f("contig"), vs2=f("vs2"), vs4=f("vs4"))
+
+
+def header_text(models: Dict[str, Dict[str, float]]) -> str:
+    lines = ["// Cost-model constants of the split policies, in the order of the CostModel",
+             "// fields: base, t_tile, t_tile_staged, merge0, merge1, fused0, fused1, hbm_rate,",
+             "// hbm0, pnorm, contig_tile, vs_tile.  Generated by",
+             "// `python -m paper_2604_00028_amd.calibrate --write` from the sweeps",
+             "// profiles/calibration_warm.json and profiles/calibration_streamed.json;",
+             "// do not edit by hand.",
+             f"#define DA_COST_MODEL_WARM {{{model_literal(models['warm'])}}}",
+             f"#define DA_COST_MODEL_STREAMED {{{model_literal(models['streamed'])}}}", ""]
+    return "\n".join(lines)
+
+
+def parse_header(text: str) -> Dict[str, List[float]]:
+    """The numbers of each model in a generated header, in field order."""
+    import re
+    out = {}
+    for which, macro in (("warm", "DA_COST_MODEL_WARM"), ("streamed", "DA_COST_MODEL_STREAMED")):
+        m = re.search(rf"#define {macro} (.*)", text)
+        out[which] = [float(x) for x in re.findall(r"[-+0-9.e]+", m.group(1))]
+    return out
+
+
+def fit_all() -> Dict[str, Dict[str, float]]:
+    return {which: fit(json.load(open(path)), which) for which, path in SWEEPS.items()}
+
+
+def main() -> None:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--write", action="store_true", help="regenerate csrc/cost_model.inc")
+    args = ap.parse_args()
+    models = fit_all()
+    for which, c in models.items():
+        err = fit_error(json.load(open(SWEEPS[which])), c)
+        print(which, json.dumps(c), json.dumps(err))
+    if args.write:
+        with open(HEADER, "w") as f:
+            f.write(header_text(models))
+        print(f"wrote {HEADER}")
+
+
+if __name__ == "__main__":
+    main()

@@ -41,37 +41,15 @@ bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt) {
   return hpt == wide || (pack == 1 && hpt == heads_per_tile(H_Q, H_KV, pack, kNarrowHeadsPerTile));
 }
 
-// MI355X constants, fitted (log-error least squares over launches within
-// 1.6x of each shape's best) to a sweep of num_splits in
-// {1,2,3,4,6,8,12,16,24,32,48,64} over B in {1,2,4,8,16,32}, H_KV in {1,4,8},
-// g in {8,32} and L_K from 64 to 8192, timed with HIP-graph replay.  Over
-// that sweep the chosen split is on average 0.2% and at worst 4.3% slower
-// than the fastest measured one; fitted on half of the shapes, it chooses
-// the other half within 0.3% on average.  Measured again after launches of
-// more workgroups than CUs moved to the register-staged fetch: 0.2% on
-// average, 5.1% at worst (a refit changed neither figure).  The V-slice
-// factors were fitted afterwards, the other constants held, to 16 shapes x
-// up to 8 split counts x 1, 2, 4 slices (warm: every choice within 2.9% of
-// the fastest measured launch, 0.2% on average; streamed: 5.3%, 1.1%).
-// Held unchanged for 16-head tiles of wider groups, they pick the fastest
-// of 2 widths x 4 split counts x 1, 2, 4 slices on all 15 shapes of a
-// second sweep (groups of 32 to 64 heads, L_K 64 to 2048; streamed: 1.9%
-// from the fastest on average, 14% at worst).
+// The constants of both policies are fitted by paper_2604_00028_amd/calibrate.py
+// (log-error least squares over the launches within 1.6x of each shape's
+// fastest) to measured sweeps of every launch the planner can choose, and
+// generated into cost_model.inc.
+#include "cost_model.inc"
+
+// Policy MI355X: K/V resident between calls, as in graph replays of one call.
 const CostModel& mi355x_model() {
-  static const CostModel m = {
-      /*base=*/{2.841, 4.042},
-      /*t_tile=*/{0.809, 1.130},
-      /*t_tile_staged=*/{0.671, 0.854},
-      /*merge0=*/2.458,
-      /*merge1=*/{0.218, 0.253},
-      /*fused0=*/2.458,
-      /*fused1=*/{0.218, 0.253},
-      /*hbm_rate=*/6.319e6,
-      /*hbm0=*/0.006,
-      /*pnorm=*/2.389,
-      /*contig_tile=*/1.0,
-      /*vs_tile=*/{1.0, 0.812, 0.714},
-  };
+  static const CostModel m = DA_COST_MODEL_WARM;
   return m;
 }
 
@@ -105,34 +83,15 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
 }
 
 // The same model with K/V streamed from HBM on every call (each call reads
-// its own copy of the cache, 1 GiB per timed replay, as a decode step that
-// runs all layers evicts each layer's cache before it is read again),
-// fitted the same way to the launches this policy makes (the whole group in
-// one tile, nontemporal K/V loads) over 63 shapes with at least 256 KiB of
-// K/V per call, the blend exponent held at 4.  Streaming from HBM, a tile of
-// one KV head costs less when key rows hold just that head (H_KV = 1: the
-// rows are contiguous) than when they interleave several heads and every
-// workgroup reads a 256-byte slice of each row: contig_tile.  Over the sweep
-// the chosen split is on average 0.4% slower than the fastest measured one
-// and at worst 1.7% slower than one split (B=1, H_Q=32, H_KV=1, L_K=512);
-// fitted on half of the shapes it chooses for the other half within 0.4% on
-// average.  32-column tiles with several workgroups per CU had no launch in
-// the sweep and carry the 16-column value scaled by the warm model's ratio.
+// its own copy of the cache, as a decode step that runs every layer evicts
+// each layer's cache before it is read again), fitted to launches that read
+// their own copy of the cache on every call (at least 1 GiB per timed
+// replay).  Streaming from HBM, a tile of one KV head costs less when key
+// rows hold just that head (H_KV = 1: contiguous rows) than when they
+// interleave several heads and every workgroup reads a 256-byte slice of
+// each row: contig_tile.
 const CostModel& mi355x_streamed_model() {
-  static const CostModel m = {
-      /*base=*/{2.095, 3.679},
-      /*t_tile=*/{1.576, 1.576 * 1.130 / 0.809},
-      /*t_tile_staged=*/{1.609, 1.643},
-      /*merge0=*/2.308,
-      /*merge1=*/{0.235, 0.254},
-      /*fused0=*/2.308,
-      /*fused1=*/{0.235, 0.254},
-      /*hbm_rate=*/6.498e6,
-      /*hbm0=*/3.366,
-      /*pnorm=*/4.0,
-      /*contig_tile=*/0.744,
-      /*vs_tile=*/{1.0, 0.943, 0.856},
-  };
+  static const CostModel m = DA_COST_MODEL_STREAMED;
   return m;
 }
 
@@ -156,7 +115,7 @@ static int best_vslices(const CostModel& m, int B, int H_Q, int H_KV, int L_K, i
   const double one = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, 1, fused);
   int best_vs = 1;
   double best = one;
-  slices = slices && (double)B * L_K * H_KV * (2.0 * kHeadDim * 2.0) <= (double)kL2Bytes;
+  slices = slices && (double)B * L_K * H_KV * (2.0 * kHeadDim * 2.0) <= (double)kSliceKvBytes;
   for (int vs = 2; slices && vs <= 4 && launch_grid(tiles * s, vs) <= cus; vs *= 2) {
     const double tv = model_time(m, B, H_Q, H_KV, L_K, hpt, s, cus, vs, fused);
     if (tv < best && tv < kSplitGain * one) {
@@ -667,6 +626,16 @@ int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, i
     if (rc) return rc;
   }
   return da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, num_cus, cu_margin, policy, out);
+}
+
+double da_model_time(int policy, int B, int H_Q, int H_KV, int L_K, int heads_per_tile, int num_splits,
+                     int v_slices, int combine, int num_cus) {
+  if (B <= 0 || H_Q <= 0 || H_KV <= 0 || H_Q % H_KV != 0 || L_K < 0 || heads_per_tile <= 0 ||
+      H_Q % heads_per_tile != 0 || num_splits < 1 || num_splits > da::kMaxSplits ||
+      (v_slices != 1 && v_slices != 2 && v_slices != 4) || combine < 0 || combine > 1 || num_cus <= 0)
+    return -1.0;
+  const da::CostModel& m = policy == DA_POLICY_STREAMED ? da::mi355x_streamed_model() : da::mi355x_model();
+  return da::model_time(m, B, H_Q, H_KV, L_K, heads_per_tile, num_splits, num_cus, v_slices, combine == 1);
 }
 
 size_t da_schedule_max_bytes(int B, int H_Q, int H_KV, int pack_gqa) {

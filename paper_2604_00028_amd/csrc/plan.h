@@ -16,6 +16,11 @@ constexpr int kMaxSplits = DA_MAX_SPLITS;
 constexpr int kMaxHeadsPerTile = 32;   // two 16-column MFMA head tiles per workgroup
 constexpr int kNarrowHeadsPerTile = 16; // one 16-column MFMA head tile per workgroup
 constexpr int64_t kL2Bytes = 8ll << 22;  // MI355X: 4 MiB of L2 on each of 8 XCDs
+// K/V bytes of a call up to which V slices are considered: half the L2.  The
+// slices of a chunk re-read its keys from their XCD's L2, which holds only
+// that XCD's share of the chunks; at 32 MiB (B=16, H_KV=4, L_K=1024) four
+// slices measured 19% slower than the best split.
+constexpr int64_t kSliceKvBytes = kL2Bytes / 2;
 
 // Records a printf-style message for da_last_error() and returns `code`.
 int fail(int code, const char* fmt, ...);

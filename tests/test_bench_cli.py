@@ -23,10 +23,50 @@ def test_more_than_one_gpu_is_refused(n):
 
 
 def test_cpu_baseline_record():
+    """The oracle's baseline on a sample of a high-load-shaped call (here a
+    small stand-in), scaled to one call, with the host's core count and CPU
+    model."""
     sys.path.insert(0, ROOT)
     import bench
-    from workloads import config_shapes, make_inputs
-    rec = bench.cpu_baseline(make_inputs(config_shapes(1)[0]), 0.2)
+    from workloads import custom_shape, make_inputs
+    rec = bench.cpu_baseline_highload(make_inputs(custom_shape(32, 16, 2, 64), seed=1), 0.2)
     assert rec["kind"] == "oracle" and rec["unit"] == "us/call"
-    assert rec["value"] > 0 and rec["cores"] >= 1
-    assert "full calls" in rec["sample"]
+    assert rec["value"] > 0 and rec["cores"] == len(os.sched_getaffinity(0))
+    assert isinstance(rec["cpu_model"], str)
+    assert "8 of the 32 sequences" in rec["sample"] and "scaled to one call" in rec["sample"]
+
+
+def test_validation_rejects_a_wrong_output():
+    """Every timed launch is checked against the oracle before it is timed
+    (the paper's harness rejects invalid candidates, Section 3.2): an output
+    off by a little more than the bar, or not finite, is recorded as
+    invalid; the oracle's own output rounded to bf16 passes."""
+    sys.path.insert(0, ROOT)
+    import numpy as np
+    import torch
+    import bench
+    from oracle import decode_attention
+    from workloads import custom_shape, f32_to_bf16_bits, make_inputs
+    inp = make_inputs(custom_shape(3, 16, 2, 77), seed=4)
+    O, _ = decode_attention(inp.q, inp.k, inp.v)
+    as_bf16 = lambda x: torch.from_numpy(f32_to_bf16_bits(x.astype(np.float32)).view(np.int16)).view(torch.bfloat16)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    full = bench.OracleFull(np, inp)
+    rows = bench.OracleRows(np, torch, t(inp.q), t(inp.k), t(inp.v), [0, 2])
+
+    class Fake:
+        def __init__(self, out, name):
+            self.out, self.name = out, name
+
+        def sample(self, torch):
+            return self.out
+
+    good = as_bf16(O)
+    off = as_bf16(O + 0.03)
+    nan = good.clone()
+    nan[1, 3, 5] = float("nan")
+    bench.VALIDATION.update(validated=0, invalid=[])
+    bench.validate(torch, full, [Fake(good, "good"), Fake(off, "off"), Fake(nan, "nan")], "planted")
+    bench.validate(torch, rows, [Fake(good, "good rows"), Fake(off, "off rows")], "planted")
+    assert bench.VALIDATION["validated"] == 5
+    assert sorted(x["launch"] for x in bench.VALIDATION["invalid"]) == ["nan", "off", "off rows"]
