@@ -41,10 +41,10 @@ HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
 LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
 # The paper's regression matrix (Section 5.3): Batch x L_K x H_KV, here with H_Q = 8 * H_KV.
 REG_B = (1, 2, 4, 8)
-REG_L = (128, 256, 384, 512, 1024, 2048, 4096, 8192)
+REG_L = (128, 256, 384, 512, 576, 640, 768, 1024, 2048, 4096, 8192)
 REG_HKV = (1, 2, 4, 8, 32)
 REG_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)
-PROFILE_REGRESSION = os.path.join(ROOT, "profiles", "regression_160_configs.md")
+PROFILE_REGRESSION = os.path.join(ROOT, "profiles", "regression_matrix.md")
 
 
 def log(msg: str) -> None:
@@ -75,6 +75,9 @@ def parse():
                     help="time only the planned launch of one workload, or a plain 1 GiB device copy "
                          "(the reference for HBM traffic counters), for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
+    ap.add_argument("--combine", type=int, default=-1,
+                    help="with --only and a forced num_splits > 1: merge the chunk states in a second launch (0) or "
+                         "inside the split launch (1); -1 leaves it to the planner")
     ap.add_argument("--pack-gqa", type=int, default=-1,
                     help="with --only: force pack_gqa (2: one workgroup per KV head and chunk, the paper's launch)")
     ap.add_argument("--regression", metavar="OUT_JSON", default=None,
@@ -193,9 +196,12 @@ def interleave(torch, variants, rounds):
     would choose anyway, say) are one configuration: they pool their
     timings, so that run-to-run noise is not reported as a difference
     between them."""
-    for _ in range(rounds):
-        for var in variants:
-            var.timed(torch)
+    n = len(variants)
+    for r in range(rounds):
+        # each round starts at another variant, so that no launch is always timed in the same place
+        # (a fixed order biased equal launches by a few percent at a few microseconds)
+        for j in range(n):
+            variants[(r + j) % n].timed(torch)
     groups = {}
     for var in variants:
         key = getattr(var, "key", None)
@@ -449,7 +455,7 @@ def schedule_sweep_run(args, da, torch, np) -> None:
             plan = da.da_choose_splits(B, H_Q, H_KV, L)
             uni = {s: Timed(torch, lambda i, s=s: da.da_decode_attn(q, *kvs[i % copies], cu, out=out, L_K_max=L,
                                                                     num_splits=s, pack_gqa=plan.pack_gqa,
-                                                                    workspace=ws), steps)
+                                                                    workspace=ws), steps, out, f"uniform s{s}")
                    for s in sorted(set(SCHED_GRID) | {plan.num_splits})}
             t_max = -(-L // 32)
             chunks = sorted({-(-t_max // s) for s in SCHED_GRID}, reverse=True)
@@ -458,17 +464,23 @@ def schedule_sweep_run(args, da, torch, np) -> None:
                 sc, meta = da.da_make_schedule(lens, H_Q, H_KV, L, chunk_tiles=c)
                 md = meta.cuda()
                 scheds[c] = (sc, md, Timed(torch, lambda i, sc=sc, md=md: da.da_decode_attn_scheduled(
-                    q, *kvs[i % copies], sc, md, cu_seqlens_k=cu, out=out, workspace=ws), steps))
+                    q, *kvs[i % copies], sc, md, cu_seqlens_k=cu, out=out, workspace=ws), steps, out,
+                    f"chunk {c}"))
+            longest = max(range(B), key=lambda b: lens[b])
+            validate(torch, OracleVarlen(np, torch, q, kvs[0][0], kvs[0][1], lens, sorted({0, longest})),
+                     list(uni.values()) + [x[2] for x in scheds.values()], f"schedule sweep {name}")
             interleave(torch, list(uni.values()) + [x[2] for x in scheds.values()], 5)
             rows.append({"set": kind, "batch": name, "B": B, "H_Q": H_Q, "H_KV": H_KV, "keys": tot, "L_K_max": L,
                          "uniform_plan_splits": plan.num_splits,
                          "uniform_us": {s: round(v.median, 3) for s, v in uni.items()},
                          "auto_chunk": scheds[0][0].chunk_tiles, "auto_workgroups": scheds[0][0].num_items,
-                         "auto_us": round(scheds[0][2].median, 3),
-                         "chunk_us": {c: round(scheds[c][2].median, 3) for c in chunks}})
+                         "auto_us": round(scheds[0][2].median, 3), "auto_hpt": scheds[0][0].heads_per_tile,
+                         "chunk_us": {c: round(scheds[c][2].median, 3) for c in chunks},
+                         "chunk_hpt": {c: scheds[c][0].heads_per_tile for c in chunks}})
             del kvs, uni, scheds
     with open(args.schedule_sweep, "w") as f:
-        json.dump({"device_cus": da.da_device_info()[0], "rows": rows}, f)
+        json.dump({"device_cus": da.da_device_info()[0], "kernel_source_sha256": kernel_source_sha(),
+                   "validated": VALIDATION["validated"], "invalid": VALIDATION["invalid"], "rows": rows}, f)
     log(f"wrote {args.schedule_sweep}")
 
 
@@ -665,11 +677,14 @@ def only_run(args, da, torch, np, dev):
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
     del inp
     K = args.highload_steps if args.only == "highload" else args.steps
-    var = Variant(args.only, da, torch, q, k, v, sh.L_K, args.num_splits, args.pack_gqa, K)
+    plan = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, 128, args.num_splits, args.pack_gqa)
+    if args.combine >= 0:
+        plan = with_combine(da, plan, args.combine)
+    var = Variant(args.only, da, torch, q, k, v, sh.L_K, 0, -1, K, plan=plan)
     interleave(torch, [var], args.rounds)
     nbytes = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
     gbs = nbytes / (var.median * 1e-6) / 1e9
-    print(json.dumps({"workload": sh.name, "us_per_call": round(var.median, 3), "num_splits": var.plan.num_splits,
+    print(json.dumps({"workload": sh.name, "us_per_call": round(var.median, 3), "plan": plan_brief(var.plan),
                       "calls": K * (args.rounds + 1) + 3, "achieved_gbps": round(gbs, 1),
                       "frac": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
@@ -823,8 +838,15 @@ def occupancy_summary(d: str) -> None:
 
 
 def regression_run(args, da, torch) -> None:
-    """Every configuration of the matrix: the MI355X heuristic, num_splits = 1, the paper's policy and a
-    fixed-split sweep, each as graph-replayed calls interleaved over rounds (synthetic inputs)."""
+    """Every configuration of the matrix (the paper's Batch x L_K x H_KV
+    sweep, Section 5.3, plus the L_K = 576/640/768 boundary of Section 4.1):
+    the MI355X heuristic, one split launched as the paper launches it (the
+    whole group in one workgroup, no V slices), one split as the planner
+    makes it, the paper's and the evolved policy's own plans, and fixed
+    split counts, each checked against the oracle (sampled sequences) and
+    then timed as graph-replayed calls interleaved over rounds (median and
+    IQR per launch, no pooling of equal launches)."""
+    import numpy as np
     results = []
     gen = torch.Generator(device="cuda")
     for B in REG_B:
@@ -837,63 +859,79 @@ def regression_run(args, da, torch) -> None:
                 v = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
                 est_us = 5.0 + 2.0 * B * L * H_KV * 256 / 5e6
                 K = int(max(10, min(100, 2000.0 / est_us)))
-                # fixed split counts as the library plans them (packing on, V slices where they pay);
-                # the heuristic reuses the sweep's timing when it picks a split the sweep covers; the
-                # paper's and the evolved policy run their own plans (one workgroup per chunk), and so does
-                # one split with the paper's launch shape (pack_gqa = 2)
                 paper = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER)
                 evolved = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_EVOLVED)
                 heur = da.da_choose_splits(B, H_Q, H_KV, L)
-                heur_s = heur.num_splits
-                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L} | {heur_s})
-                variants = {s: Variant(str(s), da, torch, q, k, v, L, s, 1, K) for s in splits}
-                own = {"paper": Variant("paper", da, torch, q, k, v, L, 0, -1, K, plan=paper),
+                splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L})
+                variants = {s: Variant(f"s{s}", da, torch, q, k, v, L, s, 1, K) for s in splits}
+                own = {"heuristic": Variant("heuristic", da, torch, q, k, v, L, 0, -1, K, plan=heur),
+                       "paper": Variant("paper", da, torch, q, k, v, L, 0, -1, K, plan=paper),
                        "evolved": Variant("evolved", da, torch, q, k, v, L, 0, -1, K, plan=evolved),
-                       "s1_one_wg": Variant("s1_one_wg", da, torch, q, k, v, L, 1, 2, K)}
-                interleave(torch, list(variants.values()) + list(own.values()), args.rounds)
-                sw = {s: round(x.median, 3) for s, x in variants.items() if s in REG_SWEEP}
+                       "s1_paper_launch": Variant("s1_paper_launch", da, torch, q, k, v, L, 1, 2, K)}
+                allv = list(variants.values()) + list(own.values())
+                validate(torch, OracleRows(np, torch, q, k, v, [0] if B == 1 else [0, B - 1]), allv,
+                         f"regression B={B} H_KV={H_KV} L_K={L}")
+                for r in range(args.rounds):     # interleaved and rotated, no pooling: every launch keeps its times
+                    for j in range(len(allv)):
+                        allv[(r + j) % len(allv)].timed(torch)
+                sw = {s: round(x.median, 3) for s, x in variants.items()}
                 best = min(sw, key=sw.get)
+                iqr = lambda x: [round(t, 3) for t in np.percentile(x.times, [25, 75])]
                 row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L,
-                       "heuristic_splits": heur_s, "heuristic_v_slices": heur.v_slices,
-                       "heuristic_us": round(variants[heur_s].median, 3),
+                       "heuristic_plan": plan_brief(heur), "heuristic_splits": heur.num_splits,
+                       "heuristic_us": round(own["heuristic"].median, 3), "heuristic_iqr": iqr(own["heuristic"]),
+                       "s1_paper_launch_us": round(own["s1_paper_launch"].median, 3),
+                       "s1_paper_launch_iqr": iqr(own["s1_paper_launch"]),
+                       "s1_us": sw[1], "s1_iqr": iqr(variants[1]),
                        "paper_splits": paper.num_splits, "paper_us": round(own["paper"].median, 3),
                        "evolved_splits": evolved.num_splits, "evolved_us": round(own["evolved"].median, 3),
-                       "s1_one_workgroup_per_chunk_us": round(own["s1_one_wg"].median, 3),
-                       "s1_us": sw[1], "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
+                       "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
                 results.append(row)
-                log(f"B={B} H_KV={H_KV} L_K={L}: heuristic s={row['heuristic_splits']} {row['heuristic_us']} us, "
-                    f"s=1 {row['s1_us']}, paper s={row['paper_splits']} {row['paper_us']}, "
-                    f"best s={best} {sw[best]}")
-                del q, k, v, variants, own
-    json.dump({"configs": results}, open(args.regression, "w"), indent=1)
-    worst_s1 = max(r["heuristic_us"] / r["s1_us"] for r in results)
+                log(f"B={B} H_KV={H_KV} L_K={L}: heuristic {row['heuristic_plan']} {row['heuristic_us']} us, "
+                    f"s=1 paper launch {row['s1_paper_launch_us']}, best s={best} {sw[best]}")
+                del q, k, v, variants, own, allv
+    json.dump({"configs": results, "validated": VALIDATION["validated"], "invalid": VALIDATION["invalid"],
+               "kernel_source_sha256": kernel_source_sha()}, open(args.regression, "w"), indent=1)
+    worst_s1 = max(r["heuristic_us"] / r["s1_paper_launch_us"] for r in results)
     worst_best = max(r["heuristic_us"] / r["best_fixed_us"] for r in results)
-    print(json.dumps({"regression_configs": len(results), "worst_heuristic_over_s1": round(worst_s1, 3),
+    print(json.dumps({"regression_configs": len(results), "validated": VALIDATION["validated"],
+                      "invalid": len(VALIDATION["invalid"]),
+                      "worst_heuristic_over_s1_paper_launch": round(worst_s1, 3),
                       "worst_heuristic_over_best_fixed": round(worst_best, 3)}), flush=True)
+    if VALIDATION["invalid"]:
+        sys.exit(3)
 
 
 def regression_summary(path: str) -> None:
-    rows = json.load(open(path))["configs"]
+    d = json.load(open(path))
+    rows = d["configs"]
     n = len(rows)
+    r_p1 = [r["heuristic_us"] / r["s1_paper_launch_us"] for r in rows]
     r_s1 = [r["heuristic_us"] / r["s1_us"] for r in rows]
     r_best = [r["heuristic_us"] / r["best_fixed_us"] for r in rows]
     r_paper = [r["heuristic_us"] / r["paper_us"] for r in rows]
     r_evo = [r["heuristic_us"] / r["evolved_us"] for r in rows if r["B"] == 1]
-    r_one = [r["heuristic_us"] / r["s1_one_workgroup_per_chunk_us"] for r in rows if "s1_one_workgroup_per_chunk_us" in r]
-    faster = sum(x < 0.99 for x in r_s1)
-    slower = [r for r, x in zip(rows, r_s1) if x > 1 / 0.99]
-    over5 = [r for r, x in zip(rows, r_best) if x > 1.05]
+    # slower than one split beyond noise: the ratio under 0.99x its speed and the heuristic's
+    # interquartile range above the one-split launch's
+    beyond = lambda r, key: r["heuristic_us"] > r[key + "_us"] / 0.99 and r["heuristic_iqr"][0] > r[key + "_iqr"][1]
+    slower_p1 = [r for r in rows if beyond(r, "s1_paper_launch")]
+    slower_s1 = [r for r in rows if beyond(r, "s1")]
+    under99_p1 = sum(x > 1 / 0.99 for x in r_p1)
+    over5 = sum(x > 1.05 for x in r_best)
+    bnd = [r for r in rows if r["L_K"] in (576, 640, 768)]
     lines = [
-        "# Regression matrix: 160 decode shapes (the paper's Section 5.3 sweep) on MI355X",
+        f"# Regression matrix: {n} decode shapes (the paper's Section 5.3 sweep and its L_K >= 640 boundary) "
+        "on MI355X",
         "",
-        "Batch in {1, 2, 4, 8} x L_K in {128, 256, 384, 512, 1024, 2048, 4096, 8192} x H_KV in {1, 2, 4, 8, 32},",
-        "H_Q = 8 * H_KV, D = 128, bf16, synthetic inputs. Each shape times the MI355X heuristic, num_splits = 1,",
-        "the paper's policy (policy PAPER), the evolved single-batch setting of its Fig. 1 (policy EVOLVED) and",
-        "fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8), as graph-replayed calls interleaved",
-        "over rounds (median). Fixed splits are planned by the library (GQA packing on, V slices where they pay);",
-        "the heuristic shares the sweep's timing when it picks a split the sweep covers. The paper's and the evolved",
-        "policy run their own plans (one workgroup per KV head and chunk), and so does one split with the paper's",
-        "launch shape (`pack_gqa = 2`: one workgroup per KV head, no V slices).",
+        "Batch in {1, 2, 4, 8} x L_K in {128, 256, 384, 512, 576, 640, 768, 1024, 2048, 4096, 8192} x H_KV in",
+        "{1, 2, 4, 8, 32}, H_Q = 8 * H_KV, D = 128, bf16, synthetic inputs. Each shape times, as graph-replayed",
+        "calls interleaved over rounds (median; each launch keeps its own times, equal launches are not pooled):",
+        "the MI355X heuristic; one split launched as the paper launches it (`pack_gqa = 2`: one workgroup per",
+        "KV head with the whole group, no V slices); one split as the planner makes it (its tile width and V",
+        "slices); the paper's policy (policy PAPER); the evolved single-batch setting of its Fig. 1 (policy",
+        "EVOLVED); and fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8) as the library plans",
+        "them. Every launch was checked against the fp64 oracle (sampled sequences) before it was timed:",
+        f"{d.get('validated', 0)} launches, {len(d.get('invalid', []))} invalid.",
         "",
         "Command (MI355X, one GPU):",
         "",
@@ -903,27 +941,36 @@ def regression_summary(path: str) -> None:
         "```",
         "",
         f"* Shapes: {n}.",
-        f"* Heuristic vs num_splits = 1: at least 0.99x its speed in {n - len(slower)} of {n} shapes; worst "
-        f"{max(r_s1):.3f}x the time of s = 1; faster by more than 1% in {faster}.",
-        f"* Heuristic vs the best fixed split: within 5% in {n - len(over5)} of {n}; worst {max(r_best):.3f}x, "
+        f"* Heuristic vs one split as the paper launches it: at least 0.99x its speed in {n - under99_p1} of {n} "
+        f"shapes (worst {max(r_p1):.3f}x its time); slower beyond both interquartile ranges in {len(slower_p1)}; "
+        f"faster by more than 1% in {sum(x < 0.99 for x in r_p1)}; mean {statistics.mean(r_p1):.3f}x its time, "
+        f"best {min(r_p1):.3f}x.",
+        f"* Heuristic vs one split as the planner makes it: worst {max(r_s1):.3f}x its time; slower beyond both "
+        f"interquartile ranges in {len(slower_s1)}; faster by more than 1% in {sum(x < 0.99 for x in r_s1)}.",
+        f"* Heuristic vs the best fixed split: within 5% in {n - over5} of {n}; worst {max(r_best):.3f}x, "
         f"mean {statistics.mean(r_best):.3f}x.",
-        (f"* Heuristic vs one split with one workgroup per KV head (the paper's launch): mean "
-         f"{statistics.mean(r_one):.3f}x its time, best {min(r_one):.3f}x, worst {max(r_one):.3f}x; faster by more "
-         f"than 1% in {sum(x < 0.99 for x in r_one)} of {len(r_one)}.") if r_one else "",
         f"* Heuristic vs the paper's policy: mean {statistics.mean(r_paper):.3f}x its time, "
         f"best {min(r_paper):.3f}x, worst {max(r_paper):.3f}x.",
         f"* Heuristic vs the evolved single-batch setting (Fig. 1; batch 1 only, {len(r_evo)} shapes): mean "
         f"{statistics.mean(r_evo):.3f}x its time, best {min(r_evo):.3f}x, worst {max(r_evo):.3f}x.",
+        f"* The L_K = 576, 640, 768 boundary ({len(bnd)} shapes): heuristic vs the paper's one-split launch "
+        f"{min(r['heuristic_us'] / r['s1_paper_launch_us'] for r in bnd):.3f}x to "
+        f"{max(r['heuristic_us'] / r['s1_paper_launch_us'] for r in bnd):.3f}x its time; vs the paper's policy "
+        f"{min(r['heuristic_us'] / r['paper_us'] for r in bnd):.3f}x to "
+        f"{max(r['heuristic_us'] / r['paper_us'] for r in bnd):.3f}x." if bnd else "",
         "",
-        "| B | H_KV | L_K | heuristic s (V slices) | us | s = 1 us | vs s = 1 | s = 1, one WG per KV head us | "
+        "IQR columns: 25th-75th percentile of the per-replay microseconds.",
+        "",
+        "| B | H_KV | L_K | heuristic plan | us (IQR) | s = 1 paper launch us (IQR) | vs it | s = 1 planned us | "
         "paper s | paper us | evolved s | evolved us | best s | best us | vs best |",
         "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
     ]
-    for r, a, c in zip(rows, r_s1, r_best):
-        lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_splits']} "
-                     f"({r.get('heuristic_v_slices', 1)}) | {r['heuristic_us']} | {r['s1_us']} | {1 / a:.2f}x | "
-                     f"{r.get('s1_one_workgroup_per_chunk_us', '')} | {r['paper_splits']} | {r['paper_us']} | "
-                     f"{r['evolved_splits']} | {r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
+    for r, a, c in zip(rows, r_p1, r_best):
+        hi, pi = r["heuristic_iqr"], r["s1_paper_launch_iqr"]
+        lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_plan']} | {r['heuristic_us']} "
+                     f"({hi[0]}-{hi[1]}) | {r['s1_paper_launch_us']} ({pi[0]}-{pi[1]}) | {1 / a:.2f}x | "
+                     f"{r['s1_us']} | {r['paper_splits']} | {r['paper_us']} | {r['evolved_splits']} | "
+                     f"{r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
     open(PROFILE_REGRESSION, "w").write("\n".join(lines) + "\n")
     print(f"wrote {PROFILE_REGRESSION}")
 
@@ -988,7 +1035,7 @@ def validate(torch, oracle, variants, what):
 
 CAL_HEADS = ((1, 8, 1), (1, 64, 8), (1, 32, 1), (2, 32, 1), (4, 32, 1), (16, 32, 4), (4, 64, 8), (8, 64, 8),
              (32, 64, 8), (2, 128, 2), (1, 256, 32), (4, 256, 32))
-CAL_L = (64, 128, 256, 512, 1024, 2048, 4096, 8192)
+CAL_L = (64, 128, 256, 384, 512, 640, 768, 1024, 2048, 4096, 8192)
 CAL_SPLITS = {"warm": (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64), "streamed": (1, 2, 3, 4, 6, 8, 12, 16, 24, 32)}
 L2_BYTES = 8 << 22
 RESIDENT_BYTES = 288 << 20

@@ -48,6 +48,7 @@ ROOT = os.path.dirname(HERE)
 HEADER = os.path.join(HERE, "csrc", "cost_model.inc")
 SWEEPS = {"warm": os.path.join(ROOT, "profiles", "calibration_warm.json"),
           "streamed": os.path.join(ROOT, "profiles", "calibration_streamed.json")}
+SCHEDULE_SWEEP = os.path.join(ROOT, "profiles", "calibration_schedule.json")
 
 CUS = 256
 HEAD_DIM = 128
@@ -246,6 +247,184 @@ def regret(sweep: dict, plan) -> Dict[str, object]:
             "rows": rows}
 
 
+# ---------------------------------------------------------------- per-sequence schedule model
+#
+# The chunk length of a per-sequence schedule (da_make_schedule) comes from
+# its own model (schedule_time in csrc/plan.cpp): sequences cut into
+# ceil(T_b / c) chunks of 32-key tiles, workgroups dealt longest first to the
+# CUs, and a wave step costing tau(A) = (t_tile^p + (A x 64 KiB / R)^p)^(1/p)
+# while A CUs are still busy.  Its 16-column constants are fitted to a sweep
+# of timed schedules (bench.py --schedule-sweep); the 32-column ones carry the
+# warm uniform model's ratios between the two tile widths.
+
+SCHED_NAMES = ["base", "t_tile", "t_staged", "hbm_rate", "pnorm", "tail", "merge0", "merge1"]
+# tail scales the summed steps, which t_tile and hbm_rate already scale: it
+# is held at 1 (a free tail leaves the fit one degree of freedom with no
+# information, along which it drifts).
+SCHED_HELD = {"tail": 1.0}
+SCHED_START = dict(base=3.19, t_tile=0.9375, t_staged=0.8113, hbm_rate=11.144e6, pnorm=1.194, tail=1.289,
+                   merge0=2.703, merge1=0.2368)
+MAX_SPLITS = 64
+
+
+def seq_splits(T: int, c: int) -> int:
+    return 1 if T <= 0 else min(MAX_SPLITS, -(-T // c))
+
+
+def schedule_time(sc: Dict[str, float], warm: Dict[str, float], tiles_of, H_Q: int, hpt: int, c: int,
+                  cus: int = CUS) -> float:
+    """Modelled microseconds of a schedule with target chunk c tiles (the
+    arithmetic of schedule_time in csrc/plan.cpp)."""
+    wide = hpt > 16
+    ratio = lambda k0, k1: warm[k1] / warm[k0] if wide else 1.0
+    base = sc["base"] * ratio("base0", "base1")
+    t_tile = sc["t_tile"] * ratio("tt0", "tt1")
+    t_staged = sc["t_staged"] * ratio("ts0", "ts1")
+    merge1 = sc["merge1"] * ratio("merge1_0", "merge1_1")
+    tps = H_Q // hpt
+    t_max = max(tiles_of) if len(tiles_of) else 0
+    q_max = max(c, -(-t_max // MAX_SPLITS))
+    count = [0] * ((q_max + 1 + 3) // 4 + 1)
+    items = state_rows = 0
+    max_s = 1
+    for T in tiles_of:
+        s = seq_splits(T, c)
+        q, big = T // s, T % s
+        count[(q + 1 + 3) // 4] += big * tps
+        count[(q + 3) // 4] += (s - big) * tps
+        items += s * tps
+        if s > 1:
+            state_rows += s
+            max_s = max(max_s, s)
+    share = [0] * (cus + 1)
+    every = nxt = 0
+    for w in range(len(count) - 1, 0, -1):
+        n = count[w]
+        if not n:
+            continue
+        rem = n % cus
+        every += (n // cus) * w
+        if rem:
+            share[nxt] += w
+            if nxt + rem <= cus:
+                share[nxt + rem] -= w
+            else:
+                share[cus] -= w
+                share[0] += w
+                share[nxt + rem - cus] -= w
+        nxt = (nxt + n) % cus
+    run = every
+    for j in range(cus):
+        run += share[j]
+        share[j] = run
+    max_w = next((w for w in range(len(count) - 1, 0, -1) if count[w]), 0)
+    staged = items <= cus
+    t1 = t_staged if staged else t_tile
+    p = sc["pnorm"]
+    step_bytes = 4.0 * 32 * 2 * HEAD_DIM * 2
+    steps = 0.0
+    prev = 0
+    for k in range(cus):
+        sh = share[cus - 1 - k]
+        if sh <= prev:
+            continue
+        a = cus - k
+        tau = (t1 ** p + (a * step_bytes / sc["hbm_rate"]) ** p) ** (1.0 / p)
+        steps += (sh - prev) * tau
+        prev = sh
+    t = base + sc["tail"] * steps + 2.0 * state_rows * H_Q * STATE_BYTES / sc["hbm_rate"]
+    if state_rows > 0:
+        t += sc["merge0"] + merge1 * max_s
+    return t
+
+
+def schedule_batches_by_name():
+    """(set, name) -> (lengths, H_Q, H_KV) of the batches the schedule sweep times."""
+    import sys
+    if ROOT not in sys.path:
+        sys.path.insert(0, ROOT)
+    from workloads import schedule_batches
+    return {(kind, name): (lens, H_Q, H_KV) for kind in ("fit", "check")
+            for name, lens, H_Q, H_KV in schedule_batches(kind)}
+
+
+def schedule_points(sweep: dict, kinds=("fit",)):
+    """(tiles_of, H_Q, hpt, c, us, batch best) for every timed chunk length of
+    the sweep's batches of the given sets."""
+    batches = schedule_batches_by_name()
+    pts = []
+    for r in sweep["rows"]:
+        if r["set"] not in kinds:
+            continue
+        lens, H_Q, _ = batches[(r["set"], r["batch"])]
+        tiles_of = [-(-L // 32) for L in lens]
+        best = min(r["chunk_us"].values())
+        for c, us in r["chunk_us"].items():
+            pts.append((tiles_of, H_Q, int(r["chunk_hpt"][c]), int(c), float(us), best))
+    return pts
+
+
+def fit_schedule(sweep: dict, warm: Dict[str, float]) -> Dict[str, float]:
+    """Schedule-model constants fitted to the sweep's "fit" batches (log-error
+    least squares over chunk lengths within 1.6x of each batch's fastest)."""
+    from scipy.optimize import least_squares
+    pts = [p for p in schedule_points(sweep) if p[4] <= WINDOW * p[5]]
+    free = [n for n in SCHED_NAMES if n not in SCHED_HELD]
+
+    def consts(x):
+        sc = dict(SCHED_HELD)
+        sc.update({n: float(math.exp(v)) for n, v in zip(free, x)})
+        return sc
+
+    def resid(x):
+        sc = consts(x)
+        return np.array([math.log(schedule_time(sc, warm, t, H_Q, hpt, c)) - math.log(us)
+                         for t, H_Q, hpt, c, us, _ in pts])
+
+    x0 = np.log([SCHED_START[n] for n in free])
+    res = least_squares(resid, x0, method="trf", xtol=1e-10, ftol=1e-10, gtol=1e-10, max_nfev=2000)
+    return {n: float(f"{v:.6g}") for n, v in consts(res.x).items()}
+
+
+def choose_chunk(sc: Dict[str, float], warm: Dict[str, float], lens, H_Q: int, hpt: int, cus: int = CUS) -> int:
+    """The chunk length da_make_schedule picks for unequal lengths at head
+    tile width hpt: the fastest modelled of the longest sequence cut into
+    1..64 pieces, the longer chunk on a tie."""
+    tiles_of = [-(-L // 32) for L in lens]
+    t_max = max(tiles_of)
+    c, best, prev = t_max, schedule_time(sc, warm, tiles_of, H_Q, hpt, t_max, cus), t_max
+    for s in range(2, MAX_SPLITS + 1):
+        cand = -(-t_max // s)
+        if cand == prev:
+            continue
+        prev = cand
+        t = schedule_time(sc, warm, tiles_of, H_Q, hpt, cand, cus)
+        if t < best:
+            best, c = t, cand
+    return c
+
+
+def schedule_regret(sweep: dict, sc: Dict[str, float], warm: Dict[str, float]) -> Dict[str, object]:
+    """The modelled chunk against the fastest timed one, per batch (both
+    sets), at the tile width the sweep timed."""
+    batches = schedule_batches_by_name()
+    out = {}
+    for kind in ("fit", "check"):
+        r_all = []
+        for r in sweep["rows"]:
+            if r["set"] != kind:
+                continue
+            lens, H_Q, _ = batches[(kind, r["batch"])]
+            cu = {int(c): us for c, us in r["chunk_us"].items()}
+            hpt = int(r["auto_hpt"])
+            c = choose_chunk(sc, warm, lens, H_Q, hpt)
+            timed = [x for x in cu if x >= c]
+            got = cu[min(timed)] if timed else cu[max(cu)]
+            r_all.append(got / min(cu.values()))
+        out[kind] = {"batches": len(r_all), "mean": float(np.mean(r_all)), "worst": float(np.max(r_all))}
+    return out
+
+
 def model_literal(c: Dict[str, float]) -> str:
     f = lambda n: repr(float(c[n]))
     return ("{{{b0}, {b1}}}, {{{tt0}, {tt1}}}, {{{ts0}, {ts1}}}, {m0}, {{{m10}, {m11}}}, {f0}, {{{f10}, {f11}}}, "
@@ -255,30 +434,48 @@ def model_literal(c: Dict[str, float]) -> str:
         rate=f("hbm_rate"), hbm0=f("hbm0"), p=f("pnorm"), contig=f("contig"), vs2=f("vs2"), vs4=f("vs4"))
 
 
-def header_text(models: Dict[str, Dict[str, float]]) -> str:
+def schedule_literal(sc: Dict[str, float], warm: Dict[str, float]) -> str:
+    r = lambda k0, k1: warm[k1] / warm[k0]
+    f = lambda x: repr(float(f"{x:.6g}"))
+    return "{{{b0}, {b1}}}, {{{t0}, {t1}}}, {{{s0}, {s1}}}, {rate}, {p}, {tail}, {m0}, {{{m10}, {m11}}}".format(
+        b0=f(sc["base"]), b1=f(sc["base"] * r("base0", "base1")), t0=f(sc["t_tile"]),
+        t1=f(sc["t_tile"] * r("tt0", "tt1")), s0=f(sc["t_staged"]), s1=f(sc["t_staged"] * r("ts0", "ts1")),
+        rate=f(sc["hbm_rate"]), p=f(sc["pnorm"]), tail=f(sc["tail"]), m0=f(sc["merge0"]), m10=f(sc["merge1"]),
+        m11=f(sc["merge1"] * r("merge1_0", "merge1_1")))
+
+
+def header_text(models: Dict[str, Dict[str, float]], schedule: Dict[str, float] = None) -> str:
     lines = ["// Cost-model constants of the split policies, in the order of the CostModel",
              "// fields: base, t_tile, t_tile_staged, merge0, merge1, fused0, fused1, hbm_rate,",
-             "// hbm0, pnorm, contig_tile, vs_tile.  Generated by",
+             "// hbm0, pnorm, contig_tile, vs_tile; and of the per-sequence schedule, in the",
+             "// order of the ScheduleModel fields.  Generated by",
              "// `python -m paper_2604_00028_amd.calibrate --write` from the sweeps",
-             "// profiles/calibration_warm.json and profiles/calibration_streamed.json;",
-             "// do not edit by hand.",
+             "// profiles/calibration_{warm,streamed,schedule}.json; do not edit by hand.",
              f"#define DA_COST_MODEL_WARM {{{model_literal(models['warm'])}}}",
-             f"#define DA_COST_MODEL_STREAMED {{{model_literal(models['streamed'])}}}", ""]
-    return "\n".join(lines)
+             f"#define DA_COST_MODEL_STREAMED {{{model_literal(models['streamed'])}}}"]
+    if schedule is not None:
+        lines.append(f"#define DA_SCHEDULE_MODEL {{{schedule_literal(schedule, models['warm'])}}}")
+    return "\n".join(lines + [""])
 
 
 def parse_header(text: str) -> Dict[str, List[float]]:
     """The numbers of each model in a generated header, in field order."""
     import re
     out = {}
-    for which, macro in (("warm", "DA_COST_MODEL_WARM"), ("streamed", "DA_COST_MODEL_STREAMED")):
+    for which, macro in (("warm", "DA_COST_MODEL_WARM"), ("streamed", "DA_COST_MODEL_STREAMED"),
+                         ("schedule", "DA_SCHEDULE_MODEL")):
         m = re.search(rf"#define {macro} (.*)", text)
-        out[which] = [float(x) for x in re.findall(r"[-+0-9.e]+", m.group(1))]
+        if m:
+            out[which] = [float(x) for x in re.findall(r"[-+0-9.e]+", m.group(1))]
     return out
 
 
 def fit_all() -> Dict[str, Dict[str, float]]:
     return {which: fit(json.load(open(path)), which) for which, path in SWEEPS.items()}
+
+
+def fit_schedule_all(models: Dict[str, Dict[str, float]]) -> Dict[str, float]:
+    return fit_schedule(json.load(open(SCHEDULE_SWEEP)), models["warm"])
 
 
 def main() -> None:
@@ -287,11 +484,17 @@ def main() -> None:
     args = ap.parse_args()
     models = fit_all()
     for which, c in models.items():
-        err = fit_error(json.load(open(SWEEPS[which])), c)
-        print(which, json.dumps(c), json.dumps(err))
+        sweep = json.load(open(SWEEPS[which]))
+        err = fit_error(sweep, c)
+        plan = (lambda c: lambda B, H, K, L: plan_mi355x(c, B, H, K, L))(c)
+        r = regret(sweep, plan)
+        print(which, json.dumps(c), json.dumps(err), json.dumps({k: v for k, v in r.items() if k != "rows"}))
+    sched = fit_schedule_all(models)
+    print("schedule", json.dumps(sched),
+          json.dumps(schedule_regret(json.load(open(SCHEDULE_SWEEP)), sched, models["warm"])))
     if args.write:
         with open(HEADER, "w") as f:
-            f.write(header_text(models))
+            f.write(header_text(models, sched))
         print(f"wrote {HEADER}")
 
 

@@ -332,6 +332,52 @@ __device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t 
             f32x4, __builtin_amdgcn_raw_buffer_load_b128(
                        ors, ooff[j] != kOut ? ooff[j] + (uint32_t)(i0 + u) * ostride : kOut, 0, kDeviceScope));
   };
+  auto store_item = [&](int j, float M, float L, const f32x4& o) {
+    const int item = tid + T * j, h = item >> 5, c = item & 31;
+    if (h >= hpt) return;
+    const int64_t row = row0_tile + h;
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+    *reinterpret_cast<uint2*>(p.out + row * D + 4 * c) =
+        make_uint2(pack_bf16x2(o[0] * inv, o[1] * inv), pack_bf16x2(o[2] * inv, o[3] * inv));
+    if (p.lse && c == 0) p.lse[row] = L > 0.f ? M + logf(L) : -INFINITY;
+  };
+  if (s <= CB) {
+    // one batch: every thread loads the maxima and sums of its own rows'
+    // chunks with its columns and merges in registers (no LDS, no barrier)
+    load_cols(0);
+    float bm[IPT][CB], bl[IPT][CB];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+      const uint32_t h = (uint32_t)(tid + T * j) >> 5;
+      const uint32_t moff = h < (uint32_t)hpt ? (r0 + h) * 4u : kOut;
+#pragma unroll
+      for (int u = 0; u < CB; ++u) {  // chunks past s read as l = 0, never live
+        const uint32_t off = moff != kOut && u < s ? moff + (uint32_t)u * rows * 4u : kOut;
+        bm[j][u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(mrs, off, 0, kDeviceScope));
+        bl[j][u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(lrs, off, 0, kDeviceScope));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) {
+      if (T * j >= items) break;  // uniform
+      float M = -INFINITY, L = 0.f;
+      f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < CB; ++u) M = bl[j][u] > 0.f ? fmaxf(M, bm[j][u]) : M;
+#pragma unroll
+      for (int u = 0; u < CB; ++u) {
+        if (u < s) {
+          const bool live = bl[j][u] > 0.f;
+          const float w = live ? __builtin_amdgcn_exp2f((bm[j][u] - M) * kLog2e) : 0.f;
+          L = fmaf(w, bl[j][u], L);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e] = fmaf(w, a[j][u][e], o[e]);
+        }
+      }
+      store_item(j, M, L, o);
+    }
+    return;
+  }
   {
     const uint32_t h = (uint32_t)tid & 31u;
     const int i0 = tid >> 5;
@@ -400,15 +446,7 @@ __device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t 
     }
   }
 #pragma unroll
-  for (int j = 0; j < IPT; ++j) {
-    const int item = tid + T * j, h = item >> 5, c = item & 31;
-    if (h >= hpt) continue;
-    const int64_t row = row0_tile + h;
-    const float inv = L[j] > 0.f ? 1.0f / L[j] : 0.f;
-    *reinterpret_cast<uint2*>(p.out + row * D + 4 * c) =
-        make_uint2(pack_bf16x2(o[j][0] * inv, o[j][1] * inv), pack_bf16x2(o[j][2] * inv, o[j][3] * inv));
-    if (p.lse && c == 0) p.lse[row] = L[j] > 0.f ? M[j] + logf(L[j]) : -INFINITY;
-  }
+  for (int j = 0; j < IPT; ++j) store_item(j, M[j], L[j], o[j]);
 }
 
 // Waves per SIMD each variant must fit: three for the 16-column direct-fetch

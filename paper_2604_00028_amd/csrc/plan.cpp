@@ -305,29 +305,15 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Constants fitted (log-error least squares over launches within 1.6x of
-// each batch's best) to 216 measured schedules: 18 batches of mixed lengths
-// (2 to 128 sequences of 32 to 65536 keys; H_Q/H_KV in 8/1, 32/4, 32/2,
-// 64/8, 128/2) x 12 chunk lengths, timed with HIP-graph replay.  Over that
-// set the chosen chunk is on average 0.8% and at worst 5.6% slower than the
-// fastest measured one; fitted on half of the batches it chooses for the
-// other half within 0.7% on average (3.8% worst), and on 14 further batches
-// drawn afterwards within 0.9% of the best of 12 measured chunk lengths
-// (0.4%, 2.9% worst, measured again with the register-staged fetch for
-// launches of more workgroups than CUs).
-// The 32-column values carry the uniform model's ratios between the two
-// tile widths.
+// Constants fitted by paper_2604_00028_amd/calibrate.py (log-error least
+// squares over chunk lengths within 1.6x of each batch's fastest) to timed
+// schedules of mixed-length batches (bench.py --schedule-sweep: 18 batches of
+// 2 to 128 sequences of 32 to 65536 keys at 12 chunk lengths each), and
+// generated into cost_model.inc.  tail is held at 1 (t_tile and hbm_rate
+// already scale the summed steps).  The 32-column values carry the uniform
+// model's ratios between the two tile widths.
 const ScheduleModel& mi355x_schedule_model() {
-  static const ScheduleModel m = {
-      /*base=*/{3.190, 3.190 * 4.042 / 2.841},
-      /*t_tile=*/{0.9375, 0.9375 * 1.130 / 0.809},
-      /*t_tile_staged=*/{0.8113, 0.8113 * 0.854 / 0.671},
-      /*hbm_rate=*/11.144e6,
-      /*pnorm=*/1.194,
-      /*tail=*/1.289,
-      /*merge0=*/2.703,
-      /*merge1=*/{0.2368, 0.2368 * 0.253 / 0.218},
-  };
+  static const ScheduleModel m = DA_SCHEDULE_MODEL;
   return m;
 }
 
