@@ -478,9 +478,53 @@ def fit_schedule_all(models: Dict[str, Dict[str, float]]) -> Dict[str, float]:
     return fit_schedule(json.load(open(SCHEDULE_SWEEP)), models["warm"])
 
 
+SUMMARY = os.path.join(ROOT, "profiles", "calibration_summary.md")
+
+
+def write_summary(models, sched) -> None:
+    """profiles/calibration_summary.md: the fitted constants, how well the model
+    fits each sweep, and how the planner's choice fares on it."""
+    lines = ["# Cost-model calibration on MI355X", "",
+             "Made by `python -m paper_2604_00028_amd.calibrate --write --summary` from the committed sweeps",
+             "(`python3 bench.py --calibrate profiles/calibration_{warm,streamed}.json --calibrate-set "
+             "{warm,streamed} --rounds 5`,",
+             "`python3 bench.py --schedule-sweep profiles/calibration_schedule.json`), each launch checked against "
+             "the oracle before it was timed.", ""]
+    for which, c in models.items():
+        sweep = json.load(open(SWEEPS[which]))
+        err = fit_error(sweep, c)
+        r = regret(sweep, (lambda c: lambda B, H, K, L: plan_mi355x(c, B, H, K, L))(c))
+        lines += [f"## Policy {'MI355X (K/V resident between calls)' if which == 'warm' else 'STREAMED (K/V read from HBM on every call)'}", "",
+                  f"* Sweep: {len(sweep['shapes'])} shapes, {sweep['validated']} launches timed and validated, "
+                  f"{len(sweep['invalid'])} invalid.",
+                  f"* Fit: {err['launches']} launches within {WINDOW}x of their shape's fastest; RMS log error "
+                  f"{err['rms_log_error']:.3f}, worst {err['worst_ratio']:.3f}x.",
+                  f"* The planner's choice (a split count the sweep did not time is read at the nearest timed one "
+                  f"below): {r['mean_vs_best']:.4f}x the fastest timed launch on average, {r['worst_vs_best']:.3f}x "
+                  f"at worst, within 5% on {r['within_5pct']} of {r['shapes']} shapes; against one split as the "
+                  f"paper launches it, never below {r['worst_speedup_vs_s1_paper']:.3f}x its speed.",
+                  "", "| constant | value |", "|---|---|"]
+        lines += [f"| {n} | {v:.6g} |" for n, v in sorted(c.items())]
+        lines.append("")
+    sw = json.load(open(SCHEDULE_SWEEP))
+    reg = schedule_regret(sw, sched, models["warm"])
+    lines += ["## Per-sequence schedule", "",
+              f"* Sweep: {len(sw['rows'])} mixed-length batches, {sw.get('validated', 0)} launches validated, "
+              f"{len(sw.get('invalid', []))} invalid.",
+              f"* The modelled chunk against the fastest of 12 timed chunk lengths (a chunk the sweep did not time is "
+              f"read at the next longer timed one): fitted batches {reg['fit']['mean']:.4f}x on average, "
+              f"{reg['fit']['worst']:.3f}x at worst; batches never fitted {reg['check']['mean']:.4f}x, "
+              f"{reg['check']['worst']:.3f}x at worst.", "", "| constant | value |", "|---|---|"]
+    lines += [f"| {n} | {v:.6g} |" for n, v in sorted(sched.items())]
+    with open(SUMMARY, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {SUMMARY}")
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--write", action="store_true", help="regenerate csrc/cost_model.inc")
+    ap.add_argument("--summary", action="store_true", help="write profiles/calibration_summary.md")
     args = ap.parse_args()
     models = fit_all()
     for which, c in models.items():
@@ -496,6 +540,8 @@ def main() -> None:
         with open(HEADER, "w") as f:
             f.write(header_text(models, sched))
         print(f"wrote {HEADER}")
+    if args.summary:
+        write_summary(models, sched)
 
 
 if __name__ == "__main__":
