@@ -4,18 +4,27 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 
 One step is one call of the whole path -- plan (host), split-partial kernel,
-and the log-sum-exp combine when the plan splits -- over the Llama-3.1-70B-shaped GQA decode
-batch (B=1, H_Q=64, H_KV=8, D=128, L_K=512, bf16, synthetic N(0,1) inputs
-already resident in HBM).  K steps are captured in one HIP graph and
-replayed; HIP events on the replay stream bracket the timed replays (the
-paper times with CUDA-graph replay and A/B interleaving, Section 5).
+and the log-sum-exp merge of the chunk states when the plan splits (inside
+the split launch or in a second launch, as the plan says) -- over synthetic
+N(0,1) bf16 inputs already resident in HBM.  Calls are captured in HIP
+graphs and replayed; HIP events on the replay stream bracket the timed
+replays, and the variants of a workload are interleaved round by round with
+the order rotated (the paper times with CUDA-graph replay and A/B
+interleaving, Section 5).  Every timed launch is first checked against the
+fp64 oracle (sampled sequences on 1 GiB shapes); a launch that disagrees is
+reported and the run exits with status 3.
 
-Printed: one JSON line.  `value` is microseconds per call for the planned
-num_splits (lower is better), next to num_splits=1, a split sweep, the
-cold-cache time, the high-load shape (B=32, H_Q=64, H_KV=8, L_K=8192, 1 GiB
-of KV) against the HBM roofline, batches of mixed lengths under the
-per-sequence schedule against the uniform plan, and the fp64 oracle timed on
-the host cores (a reported baseline only).
+Printed: one JSON line.  `value` is microseconds per call of the planned
+launch on the high-load shape (B=32, H_Q=64, H_KV=8, D=128, L_K=8192, 1 GiB of
+K/V), with its HBM roofline and counter traffic, its split sweep and one
+split as the paper launches it.  Beside it: the Llama-3.1-70B GQA decode
+shape (B=1, L_K=512) against one split, a split sweep, both merges and a cold
+cache; B=1 contexts of 1024-8192 keys; the low-head workloads (MQA, pure MQA,
+varlen GQA) against the paper's one-split launch; the same shapes with every
+call reading its cache from HBM; batches of mixed lengths under the
+per-sequence schedule; the high-load call beside a GEMM on reserved CUs; a
+plain 1 GiB read kernel (the HBM read ceiling); and the fp64 oracle timed on
+the host cores (a reported baseline only).  Compact summaries come last.
 """
 
 from __future__ import annotations
@@ -71,9 +80,9 @@ def parse():
     ap.add_argument("--occupancy-summary", metavar="DIR", default=None,
                     help="summarise rocprofv3 occupancy counter runs DIR/occ_<pass>_<case> into "
                          "profiles/occupancy_heuristic_vs_s1.md")
-    ap.add_argument("--only", choices=("headline", "highload", "long", "ragged", "copy"), default=None,
-                    help="time only the planned launch of one workload, or a plain 1 GiB device copy "
-                         "(the reference for HBM traffic counters), for profiler runs")
+    ap.add_argument("--only", choices=("headline", "highload", "long", "ragged", "copy", "readprobe"), default=None,
+                    help="time only the planned launch of one workload, a plain 1 GiB device copy (the reference "
+                         "for HBM traffic counters) or the 1 GiB read probe, for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
     ap.add_argument("--combine", type=int, default=-1,
                     help="with --only and a forced num_splits > 1: merge the chunk states in a second launch (0) or "
@@ -658,12 +667,61 @@ def copy_run(args, torch):
                       "us_per_copy": round(us, 2), "gbps": round(2 * n / (us * 1e-6) / 1e9, 1)}), flush=True)
 
 
+PROBE_GRID = (256, 512, 1024, 2048, 4096)
+
+
+def read_probe_run(torch, steps: int = 20) -> dict:
+    """The HBM read ceiling: a kernel that only reads 1 GiB with 16-byte
+    loads (libhbm_probe.so, csrc/hbm_probe.hip), at 1-16 workgroups per CU,
+    with and without the nontemporal hint; microseconds per launch from HIP
+    events around `steps` launches on the current stream, after two warm-up
+    launches.  The fastest configuration's rate is the practical ceiling the
+    decode kernel's achieved bandwidth is set against."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2604_00028_amd", "libhbm_probe.so"))
+    lib.hbm_read_probe.restype = ctypes.c_int
+    lib.hbm_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                                   ctypes.c_int, ctypes.c_void_p]
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(3)
+    sink = torch.empty(max(PROBE_GRID) * 256, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    grid = {}
+    for wgs in PROBE_GRID:
+        for nt in (0, 1):
+            def launch():
+                rc = lib.hbm_read_probe(src.data_ptr(), n, sink.data_ptr(), sink.numel() * 4, wgs, nt,
+                                        stream.cuda_stream)
+                if rc != 0:
+                    raise RuntimeError(f"hbm_read_probe failed ({rc})")
+            launch()
+            launch()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(steps):
+                launch()
+            b.record(stream)
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1000.0 / steps
+            grid[f"wg{wgs}_{'nt' if nt else 'plain'}"] = round(n / (us * 1e-6) / 1e9, 1)
+    best = max(grid, key=grid.get)
+    del src, sink
+    return {"bytes": n, "best_gbps": grid[best], "best": best, "frac_of_peak": round(grid[best] / HBM_PEAK_GBS, 4),
+            "gbps": grid}
+
+
 def only_run(args, da, torch, np, dev):
     """Planned (or forced) launch of one workload, nothing else: the command
     the rocprofv3 summaries are taken from."""
     from workloads import config_shapes, custom_shape, make_inputs
     if args.only == "copy":
         copy_run(args, torch)
+        return
+    if args.only == "readprobe":
+        print(json.dumps({"workload": "read_probe_1GiB", **read_probe_run(torch, max(1, args.highload_steps))}),
+              flush=True)
         return
     if args.only == "ragged":
         ragged_only(args, da, torch, np)
@@ -1289,6 +1347,8 @@ def main():
     streamed = None if args.no_streamed else streamed_run(args, da, torch)
     ragged = None if args.no_ragged else ragged_run(args, da, torch, np)
     margin = None if args.no_cu_margin else cu_margin_run(args, da, torch, np)
+    log("timing the HBM read probe")
+    probe = read_probe_run(torch)
 
     result = {
         "metric": METRIC,
@@ -1320,6 +1380,7 @@ def main():
         "streamed": streamed,
         "ragged": ragged,
         "cu_margin": margin,
+        "hbm_read_probe": probe,
     }
     # compact summaries last, where a tail of the output shows them
     if low:
@@ -1333,7 +1394,9 @@ def main():
     result["high_load_summary"] = {"us": high["us_per_call"], "gbs": round(achieved, 1),
                                    "frac": round(achieved / HBM_PEAK_GBS, 4), "plan": high["plan"],
                                    "s1_paper_launch_us": high["s1_paper_launch_us"],
-                                   "best_fixed_us": high["best_fixed_us"], "validated": VALIDATION["validated"]}
+                                   "best_fixed_us": high["best_fixed_us"], "validated": VALIDATION["validated"],
+                                   "read_probe_gbps": probe["best_gbps"],
+                                   "frac_of_read_probe": round(achieved / probe["best_gbps"], 4)}
     print(json.dumps(result), flush=True)
     if VALIDATION["invalid"]:
         log(f"{len(VALIDATION['invalid'])} timed launches disagree with the oracle")

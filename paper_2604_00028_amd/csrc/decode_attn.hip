@@ -299,6 +299,7 @@ __device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t 
   constexpr int R = T / 32;              // thread t stages row t % 32 of chunks t / 32 + R u
   constexpr int IPT = NT * 16 * 32 / T;  // float4 columns per thread (hpt * 32 items over T threads)
   constexpr int CB = 16 / IPT;           // chunks of columns loaded at once
+  static_assert(CB == da::kFusedBatch[NT - 1], "the planner prices the merge in batches of CB chunks");
   constexpr uint32_t kOut = 0xfffffff0u; // an offset past every buffer: reads zero, touches nothing
   const int hpt = p.hpt, s = p.s;
   // 32-bit offsets: the chunk states of a call stay below 2 GiB (checked on the host), and the

@@ -57,7 +57,7 @@ const CostModel& mi355x_model() {
 // (V slices):
 //   compute = base + (workgroups per CU) x (32-key tiles per wave) x t_tile x vs_tile[vs]
 //   stream  = hbm0 + (K/V bytes + chunk-state traffic) / hbm_rate
-//   T = (compute^p + stream^p)^(1/p) + [s > 1] (merge0 + merge1 s)
+//   T = (compute^p + stream^p)^(1/p) + merge_time
 // Every workgroup has four waves, one per SIMD, and walks a quarter of its
 // chunk each; workgroups that share a CU share its SIMDs.  The soft maximum
 // reflects that a CU's tile loop slows as the chip nears its HBM rate.
@@ -78,8 +78,19 @@ double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt
   if (s > 1) bytes += 2.0 * s * (double)B * H_Q * (kHeadDim + 2) * 4.0;
   const double stream = m.hbm0 + bytes / m.hbm_rate;
   double t = pow(pow(compute, m.pnorm) + pow(stream, m.pnorm), 1.0 / m.pnorm);
-  if (s > 1) t += fused ? m.fused0 + m.fused1[wide] * s : m.merge0 + m.merge1[wide] * s;
-  return t;
+  return t + merge_time(m, hpt, s, fused);
+}
+
+// The merge of s > 1 chunk states: a second launch, merge0 + merge1 s; or
+// inside the split launch, where one workgroup per tile loads the s x hpt
+// chunk states in batches of kFusedBatch chunks: fused0 + fused1 s hpt / 8 +
+// fused2 (batches - 1).
+double merge_time(const CostModel& m, int hpt, int s, bool fused) {
+  if (s <= 1) return 0.0;
+  const int wide = hpt > 16 ? 1 : 0;
+  if (!fused) return m.merge0 + m.merge1[wide] * s;
+  const int n = kFusedBatch[wide];
+  return m.fused0 + m.fused1[wide] * s * (hpt / 8.0) + m.fused2 * ((s + n - 1) / n - 1);
 }
 
 // The same model with K/V streamed from HBM on every call (each call reads
@@ -99,8 +110,7 @@ const CostModel& mi355x_streamed_model() {
 // workgroup of each tile (da_plan.combine 1) rather than by a second launch:
 // whichever merge the model prices lower.
 bool fused_merge(const CostModel& m, int hpt, int s, int64_t tiles) {
-  const int wide = hpt > 16 ? 1 : 0;
-  return s > 1 && tiles <= kMaxArrivalTiles && m.fused0 + m.fused1[wide] * s < m.merge0 + m.merge1[wide] * s;
+  return s > 1 && tiles <= kMaxArrivalTiles && merge_time(m, hpt, s, true) < merge_time(m, hpt, s, false);
 }
 
 // V slices for s chunks per sequence when `slices` allows them: 2 or 4

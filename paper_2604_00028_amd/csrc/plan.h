@@ -50,7 +50,8 @@ struct CostModel {
   double merge0;           // second launch that combines the chunk states, fixed part (s > 1)
   double merge1[2];        // ... per chunk
   double fused0;           // single-launch merge by the last workgroup of a tile, fixed part (s > 1)
-  double fused1[2];        // ... per chunk
+  double fused1[2];        // ... per chunk and 8 heads of the tile (the state bytes that workgroup loads)
+  double fused2;           // ... per batch of chunks after the first (kFusedBatch chunks per batch)
   double hbm_rate;         // sustained HBM bytes per microsecond, whole chip
   double hbm0;             // fixed part of the streaming bound
   double pnorm;            // the two bounds combine as (compute^p + stream^p)^(1/p)
@@ -70,6 +71,15 @@ constexpr double kSplitGain = 0.99;
 // rather than by a second launch.
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs = 1,
                   bool fused = false);
+
+// Chunk states the merging workgroup of a single-launch merge loads at once
+// (16-column / 32-column head tiles): one batch is merged in registers, more
+// are staged through LDS batch by batch.
+constexpr int kFusedBatch[2] = {8, 4};
+
+// Modelled time (us) the merge of s chunk states of tiles of `hpt` heads adds
+// to a call: a second launch, or inside the split launch (`fused`).
+double merge_time(const CostModel& m, int hpt, int s, bool fused);
 
 // Whether a plan of s chunks per sequence over `tiles` tiles of `hpt` heads
 // merges the chunk states inside the split launch (da_plan.combine).

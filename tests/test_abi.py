@@ -172,6 +172,10 @@ def test_paper_policy_reproduces_the_paper_table():
             assert plan.num_splits == mi.num_splits and plan.v_slices == mi.v_slices == 1, c
 
 
+FIELDS_OF_MODEL = ["base0", "base1", "tt0", "tt1", "ts0", "ts1", "merge0", "merge1_0", "merge1_1", "fused0",
+                   "fused1_0", "fused1_1", "fused2", "hbm_rate", "hbm0", "pnorm", "contig", "vs1", "vs2", "vs4"]
+
+
 def test_evolved_policy_reproduces_the_paper_figure():
     table = json.load(open(os.path.join(ROOT, "tests", "golden", "evolved_policy.json")))
     for c in table["cases"]:
@@ -179,8 +183,14 @@ def test_evolved_policy_reproduces_the_paper_figure():
         if c["s"] is not None:
             assert plan.num_splits == c["s"] and plan.pack_gqa == 1, c
         else:
-            mi = da.da_choose_splits(c["B"], 64, 8, c["L_K"], num_cus=256, policy=da.POLICY_MI355X)
-            assert plan.num_splits == mi.num_splits, c
+            # beyond batch 1: the MI355X cost model's split count for launches of one
+            # workgroup per chunk (the paper's policies take no V slices)
+            from paper_2604_00028_amd import calibrate as cal
+            warm = dict(zip(FIELDS_OF_MODEL, cal.parse_header(open(cal.HEADER).read())["warm"]))
+            warm["vs1"] = 1.0
+            want = cal.plan_mi355x(warm, c["B"], 64, 8, c["L_K"], l2_bytes=0)
+            assert want[0] == 8 and want[2] == 1 and plan.num_splits == want[1], (c, want)
+            assert plan.v_slices == 1
     for B in (1, 2, 4):
         for L in (1, 100, 255, 256, 511, 4096):
             want = evolved_split_policy(L, B)

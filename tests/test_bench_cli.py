@@ -70,3 +70,25 @@ def test_validation_rejects_a_wrong_output():
     bench.validate(torch, rows, [Fake(good, "good rows"), Fake(off, "off rows")], "planted")
     assert bench.VALIDATION["validated"] == 5
     assert sorted(x["launch"] for x in bench.VALIDATION["invalid"]) == ["nan", "off", "off rows"]
+
+
+def test_read_probe_library_checks_its_arguments():
+    """The HBM read probe the benchmark sets the decode kernel against is
+    built beside the decode library and rejects invalid arguments before any
+    device access (no GPU here)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2604_00028_amd", "libhbm_probe.so")
+    if not os.path.exists(path):
+        pytest.skip("libhbm_probe.so is not built")
+    lib = ctypes.CDLL(path)
+    f = lib.hbm_read_probe
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                  ctypes.c_void_p]
+    p = ctypes.c_void_p(0x1000)
+    assert f(None, 1 << 20, p, 1 << 20, 256, 0, None) == 1                 # no source
+    assert f(p, 1 << 20, None, 1 << 20, 256, 0, None) == 1                 # no sink
+    assert f(p, (1 << 20) + 8, p, 1 << 20, 256, 0, None) == 1              # not whole 16-byte vectors
+    assert f(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 0, None) == 1          # sink too small for the grid
+    assert f(p, 1 << 20, p, 1 << 20, 0, 0, None) == 1                      # no workgroups
+    assert f(p, 1 << 20, p, 1 << 20, 256, 2, None) == 1                    # hint not 0 or 1
