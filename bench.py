@@ -152,7 +152,11 @@ class Variant:
         self.times = []
 
     def sample(self, torch):
-        """The output of one eager call on the first K/V copy."""
+        """The output of one eager call on the first K/V copy, written over
+        NaNs: a launch that leaves any output unwritten (shared `out`
+        buffers would otherwise hold another launch's result) fails the
+        check."""
+        self.out.fill_(float("nan"))
         self.call(0)
         torch.cuda.synchronize()
         return self.out.clone()
@@ -405,8 +409,9 @@ def ragged_run(args, da, torch, np) -> dict:
                                        ctypes.byref(c_out))
         plan_us = (time.perf_counter() - t0) / 50 * 1e6
         meta_dev = meta.cuda()
-        ws_s = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
-        ws_u = torch.empty(da.da_workspace_bytes(B, H_Q, 128, 64), dtype=torch.uint8, device="cuda")
+        # zero-filled: the arrival counters of merges inside the split launch start at zero
+        ws_s = torch.zeros(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+        ws_u = torch.zeros(da.da_workspace_bytes(B, H_Q, 128, 64), dtype=torch.uint8, device="cuda")
         plan = da.da_choose_splits(B, H_Q, H_KV, L)
         log(f"timing ragged batch {name}")
         sv = Timed(torch, lambda i: da.da_decode_attn_scheduled(q, *kvs[i % copies], sched, meta_dev, cu_seqlens_k=cu,
@@ -459,7 +464,7 @@ def schedule_sweep_run(args, da, torch, np) -> None:
             cu = torch.from_numpy(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)).cuda()
             out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
             steps = 10 if kv_bytes > (256 << 20) else (40 if kv_bytes > (32 << 20) else 200)
-            ws = torch.empty(da.da_workspace_bytes(B, H_Q, 128, 64) + 4096, dtype=torch.uint8, device="cuda")
+            ws = torch.zeros(da.da_workspace_bytes(B, H_Q, 128, 64) + 4096, dtype=torch.uint8, device="cuda")
             log(f"schedule sweep {kind}/{name}")
             plan = da.da_choose_splits(B, H_Q, H_KV, L)
             uni = {s: Timed(torch, lambda i, s=s: da.da_decode_attn(q, *kvs[i % copies], cu, out=out, L_K_max=L,
@@ -468,13 +473,21 @@ def schedule_sweep_run(args, da, torch, np) -> None:
                    for s in sorted(set(SCHED_GRID) | {plan.num_splits})}
             t_max = -(-L // 32)
             chunks = sorted({-(-t_max // s) for s in SCHED_GRID}, reverse=True)
-            scheds = {}
+            scheds = {}   # (chunk, merge) -> (schedule, metadata, timed launch); chunk 0: as modelled
             for c in [0] + chunks:
                 sc, meta = da.da_make_schedule(lens, H_Q, H_KV, L, chunk_tiles=c)
                 md = meta.cuda()
-                scheds[c] = (sc, md, Timed(torch, lambda i, sc=sc, md=md: da.da_decode_attn_scheduled(
-                    q, *kvs[i % copies], sc, md, cu_seqlens_k=cu, out=out, workspace=ws), steps, out,
-                    f"chunk {c}"))
+                # either merge of the split sequences (the second launch, or inside the split launch
+                # where the tiles have arrival counters); the modelled schedule as it comes
+                combs = [sc.combine] if c == 0 or sc.state_rows == 0 else \
+                    [0, 1] if sc.tiles <= MAX_ARRIVAL_TILES else [0]
+                for k in combs:
+                    sk = da.DaSchedule.from_buffer_copy(sc)
+                    sk.combine = k
+                    scheds[(c, k)] = (sk, md, Timed(torch, lambda i, sk=sk, md=md: da.da_decode_attn_scheduled(
+                        q, *kvs[i % copies], sk, md, cu_seqlens_k=cu, out=out, workspace=ws), steps, out,
+                        f"chunk {c} merge {k}"))
+            auto = next(v for key, v in scheds.items() if key[0] == 0)
             longest = max(range(B), key=lambda b: lens[b])
             validate(torch, OracleVarlen(np, torch, q, kvs[0][0], kvs[0][1], lens, sorted({0, longest})),
                      list(uni.values()) + [x[2] for x in scheds.values()], f"schedule sweep {name}")
@@ -482,10 +495,13 @@ def schedule_sweep_run(args, da, torch, np) -> None:
             rows.append({"set": kind, "batch": name, "B": B, "H_Q": H_Q, "H_KV": H_KV, "keys": tot, "L_K_max": L,
                          "uniform_plan_splits": plan.num_splits,
                          "uniform_us": {s: round(v.median, 3) for s, v in uni.items()},
-                         "auto_chunk": scheds[0][0].chunk_tiles, "auto_workgroups": scheds[0][0].num_items,
-                         "auto_us": round(scheds[0][2].median, 3), "auto_hpt": scheds[0][0].heads_per_tile,
-                         "chunk_us": {c: round(scheds[c][2].median, 3) for c in chunks},
-                         "chunk_hpt": {c: scheds[c][0].heads_per_tile for c in chunks}})
+                         "auto_chunk": auto[0].chunk_tiles, "auto_workgroups": auto[0].num_items,
+                         "auto_us": round(auto[2].median, 3), "auto_hpt": auto[0].heads_per_tile,
+                         "auto_combine": auto[0].combine,
+                         "chunk_us_by_combine": {c: {k: round(v[2].median, 3) for (cc, k), v in scheds.items()
+                                                     if cc == c} for c in chunks},
+                         "chunk_hpt": {c: next(v[0].heads_per_tile for (cc, _), v in scheds.items() if cc == c)
+                                       for c in chunks}})
             del kvs, uni, scheds
     with open(args.schedule_sweep, "w") as f:
         json.dump({"device_cus": da.da_device_info()[0], "kernel_source_sha256": kernel_source_sha(),
@@ -498,8 +514,10 @@ def schedule_sweep_summary(path: str) -> None:
     lines = ["# Per-sequence schedule on mixed-length batches (MI355X)", "",
              "Made by `python bench.py --schedule-sweep sched.json` then "
              "`python bench.py --schedule-sweep-summary sched.json`.", "",
-             "Per batch: the modelled schedule (`auto`), the fastest of the schedules whose chunk cuts the "
-             "longest sequence into 1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48 or 64 pieces (`grid best`), the "
+             "Per batch: the modelled schedule (`auto`: its chunk length, in 32-key tiles, and the merge of its "
+             "split sequences, `f` inside the split launch, `2` a second launch), the fastest of the schedules "
+             "whose chunk cuts the longest sequence into 1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48 or 64 pieces, "
+             "each with either merge (`grid best`), the "
              "uniform launch planned for the longest sequence (`uniform plan`) and the fastest uniform split "
              "count (`uniform best`).  Times in microseconds per call, HIP-graph replay, medians of 5 "
              "interleaved replays.  `fit`: the batches the schedule model was fitted to; `check`: drawn "
@@ -509,15 +527,14 @@ def schedule_sweep_summary(path: str) -> None:
              "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     stats = {}
     for r in d["rows"]:
-        cu = {int(k): v for k, v in r["chunk_us"].items()}
+        gb = min(us for by in r["chunk_us_by_combine"].values() for us in by.values())
         uu = {int(k): v for k, v in r["uniform_us"].items()}
-        gb = min(cu.values())
         ub = min(uu, key=uu.get)
         up = uu[r["uniform_plan_splits"]]
         a = r["auto_us"]
         stats.setdefault(r["set"], []).append((a / gb, up / a, uu[ub] / a))
         lines.append(f"| {r['set']} | {r['batch']} | {r['B']} | {r['H_Q']}/{r['H_KV']} | {r['keys']} | "
-                     f"{r['auto_chunk']} | {a:.2f} | {gb:.2f} | {a / gb:.3f} | {up:.2f} ({r['uniform_plan_splits']}) "
+                     f"{r['auto_chunk']} {'f' if r.get('auto_combine') else '2'} | {a:.2f} | {gb:.2f} | {a / gb:.3f} | {up:.2f} ({r['uniform_plan_splits']}) "
                      f"| {uu[ub]:.2f} ({ub}) | {up / a:.2f} | {uu[ub] / a:.3f} |")
     lines.append("")
     for k, v in stats.items():
@@ -556,7 +573,7 @@ def cu_margin_run(args, da, torch, np) -> dict:
     def decode_fn(margin):
         sched, meta = da.da_make_schedule(lens, H_Q, H_KV, 8192, cu_margin=margin)
         md = meta.cuda()
-        ws = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+        ws = torch.zeros(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
         return sched, lambda s: da.da_decode_attn_scheduled(q, k, v, sched, md, cu_seqlens_k=cu, out=out,
                                                             workspace=ws, stream=s)
 
@@ -760,7 +777,7 @@ def ragged_only(args, da, torch, np):
     out = torch.empty(B, H_Q, 128, dtype=torch.bfloat16, device="cuda")
     sched, meta = da.da_make_schedule(lens, H_Q, H_KV, L)
     meta_dev = meta.cuda()
-    ws = torch.empty(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
     K = args.highload_steps
     var = Timed(torch, lambda i: da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out,
                                                              workspace=ws), K)
@@ -1305,7 +1322,10 @@ def main():
     allv = [heur, base, paper_s1] + list(pol.values()) + sweep + two + unpacked
     validate(torch, OracleFull(np, inp), allv, sh.name)
     validate(torch, OracleRows(np, torch, q, copies[0][0], copies[0][1], [0]), cold, sh.name + " cold")
-    interleave(torch, allv + cold, args.rounds)
+    # the cold-cache pair streams 512 MiB per replay through L2 and the MALL: timed on its own, so that
+    # its evictions do not land between the warm launches' replays
+    interleave(torch, allv, args.rounds)
+    interleave(torch, cold, args.rounds)
     sweep_us = {1: round(base.median, 3), **{x.plan.num_splits: round(x.median, 3) for x in sweep}}
     best_s = min(sweep_us, key=sweep_us.get)
     detail = {"workload": sh.name, "heuristic_us": round(heur.median, 3), "plan": plan_brief(heur.plan),

@@ -312,6 +312,10 @@ typedef struct da_schedule {
   int32_t seq_offset;            /* byte offset of the per-sequence table in the metadata */
   int32_t meta_bytes;            /* metadata bytes written */
   int32_t kv_nontemporal;        /* as in da_plan, for the K/V of all B sequences */
+  int32_t combine;               /* 1: the chunk states of each split sequence are merged inside
+                                    the split launch by the last workgroup of each of its head
+                                    tiles (arrival counters in the workspace, as in da_plan);
+                                    0: by a second launch.  0 when no sequence is split */
 } da_schedule;
 
 /* Upper bound on the metadata bytes da_make_schedule writes for this shape
@@ -347,7 +351,10 @@ int da_make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_
 
 /* Workspace bytes da_decode_attn_scheduled needs for `sched`: 0 when no
  * sequence is split.  Layout (256-byte aligned regions): Otilde fp32
- * [state_rows, H_Q, D] | m fp32 [state_rows, H_Q] | l fp32 [state_rows, H_Q]. */
+ * [state_rows, H_Q, D] | m fp32 [state_rows, H_Q] | l fp32 [state_rows, H_Q],
+ * and the DA_ARRIVAL_BYTES counter region at the end of the buffer passed,
+ * as for da_decode_attn: zero before the first call, and every call leaves
+ * it zero, so one zero-filled buffer serves uniform and scheduled calls. */
 size_t da_schedule_workspace_bytes(const da_schedule* sched);
 
 /* Decode attention driven by a per-sequence schedule: the same result as
@@ -366,7 +373,8 @@ size_t da_schedule_workspace_bytes(const da_schedule* sched);
  *              clamped to the sequence and each sequence's last chunk runs
  *              to its end: only the balance changes
  *   workspace  >= da_schedule_workspace_bytes(sched)
- * At most two launches (the combine only when some sequence is split), no
+ * One launch, or two (the combine launch when some sequence is split and
+ * sched->combine is 0); no
  * allocation, graph-capturable; results bit-identical across runs for a
  * fixed schedule. */
 int da_decode_attn_scheduled(const void* q, const void* k, const void* v,

@@ -67,7 +67,8 @@ class DaPlan(ctypes.Structure):
 class DaSchedule(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "B", "H_Q", "H_KV", "L_K_max", "pack_gqa", "heads_per_tile", "tiles", "num_items", "chunk_tiles",
-        "max_splits", "state_rows", "num_cus", "kv_fetch", "seq_offset", "meta_bytes", "kv_nontemporal")]
+        "max_splits", "state_rows", "num_cus", "kv_fetch", "seq_offset", "meta_bytes", "kv_nontemporal",
+        "combine")]
 
     def as_dict(self) -> dict:
         return {name: int(getattr(self, name)) for name, _ in self._fields_}

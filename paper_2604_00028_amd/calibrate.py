@@ -286,17 +286,22 @@ def planner_regret(sweep: dict, c: Dict[str, float]) -> Dict[str, Dict[str, obje
 # its own model (schedule_time in csrc/plan.cpp): sequences cut into
 # ceil(T_b / c) chunks of 32-key tiles, workgroups dealt longest first to the
 # CUs, and a wave step costing tau(A) = (t_tile^p + (A x 64 KiB / R)^p)^(1/p)
-# while A CUs are still busy.  Its 16-column constants are fitted to a sweep
-# of timed schedules (bench.py --schedule-sweep); the 32-column ones carry the
-# warm uniform model's ratios between the two tile widths.
+# while A CUs are still busy, plus the merge of the split sequences: a second
+# launch, merge0 + merge1 max_s, or inside the split launch, fused0 + fused1
+# max_s hpt / 8 + fused2 (batches - 1), as in the uniform model.  The
+# scheduler takes the chunk length and merge the model puts fastest.  Its
+# 16-column constants are fitted to a sweep of timed schedules, every chunk
+# length with either merge (bench.py --schedule-sweep); the 32-column ones
+# carry the warm uniform model's ratios between the two tile widths.
 
-SCHED_NAMES = ["base", "t_tile", "t_staged", "hbm_rate", "pnorm", "tail", "merge0", "merge1"]
+SCHED_NAMES = ["base", "t_tile", "t_staged", "hbm_rate", "pnorm", "tail", "merge0", "merge1", "fused0", "fused1",
+               "fused2"]
 # tail scales the summed steps, which t_tile and hbm_rate already scale: it
 # is held at 1 (a free tail leaves the fit one degree of freedom with no
 # information, along which it drifts).
 SCHED_HELD = {"tail": 1.0}
 SCHED_START = dict(base=3.19, t_tile=0.9375, t_staged=0.8113, hbm_rate=11.144e6, pnorm=1.194, tail=1.289,
-                   merge0=2.703, merge1=0.2368)
+                   merge0=2.703, merge1=0.2368, fused0=1.5, fused1=0.1, fused2=0.5)
 MAX_SPLITS = 64
 
 
@@ -305,7 +310,7 @@ def seq_splits(T: int, c: int) -> int:
 
 
 def schedule_time(sc: Dict[str, float], warm: Dict[str, float], tiles_of, H_Q: int, hpt: int, c: int,
-                  cus: int = CUS) -> float:
+                  combine: int = 0, cus: int = CUS) -> float:
     """Modelled microseconds of a schedule with target chunk c tiles (the
     arithmetic of schedule_time in csrc/plan.cpp)."""
     wide = hpt > 16
@@ -314,6 +319,7 @@ def schedule_time(sc: Dict[str, float], warm: Dict[str, float], tiles_of, H_Q: i
     t_tile = sc["t_tile"] * ratio("tt0", "tt1")
     t_staged = sc["t_staged"] * ratio("ts0", "ts1")
     merge1 = sc["merge1"] * ratio("merge1_0", "merge1_1")
+    fused1 = sc["fused1"] * ratio("fused1_0", "fused1_1")
     tps = H_Q // hpt
     t_max = max(tiles_of) if len(tiles_of) else 0
     q_max = max(c, -(-t_max // MAX_SPLITS))
@@ -367,7 +373,11 @@ def schedule_time(sc: Dict[str, float], warm: Dict[str, float], tiles_of, H_Q: i
         prev = sh
     t = base + sc["tail"] * steps + 2.0 * state_rows * H_Q * STATE_BYTES / sc["hbm_rate"]
     if state_rows > 0:
-        t += sc["merge0"] + merge1 * max_s
+        if combine:
+            n = 4 if wide else 8
+            t += sc["fused0"] + fused1 * max_s * hpt / 8.0 + sc["fused2"] * ((max_s + n - 1) // n - 1)
+        else:
+            t += sc["merge0"] + merge1 * max_s
     return t
 
 
@@ -381,9 +391,15 @@ def schedule_batches_by_name():
             for name, lens, H_Q, H_KV in schedule_batches(kind)}
 
 
+def chunk_times(row: dict) -> Dict[tuple, float]:
+    """(chunk, merge) -> microseconds of a sweep row: every timed chunk
+    length with each merge it was timed with."""
+    return {(int(c), int(k)): float(us) for c, by in row["chunk_us_by_combine"].items() for k, us in by.items()}
+
+
 def schedule_points(sweep: dict, kinds=("fit",)):
-    """(tiles_of, H_Q, hpt, c, us, batch best) for every timed chunk length of
-    the sweep's batches of the given sets."""
+    """(tiles_of, H_Q, hpt, c, combine, us, batch best) for every timed
+    chunk length and merge of the sweep's batches of the given sets."""
     batches = schedule_batches_by_name()
     pts = []
     for r in sweep["rows"]:
@@ -391,17 +407,18 @@ def schedule_points(sweep: dict, kinds=("fit",)):
             continue
         lens, H_Q, _ = batches[(r["set"], r["batch"])]
         tiles_of = [-(-L // 32) for L in lens]
-        best = min(r["chunk_us"].values())
-        for c, us in r["chunk_us"].items():
-            pts.append((tiles_of, H_Q, int(r["chunk_hpt"][c]), int(c), float(us), best))
+        ct = chunk_times(r)
+        best = min(ct.values())
+        for (c, k), us in ct.items():
+            pts.append((tiles_of, H_Q, int(r["chunk_hpt"][str(c)]), c, k, us, best))
     return pts
 
 
 def fit_schedule(sweep: dict, warm: Dict[str, float]) -> Dict[str, float]:
     """Schedule-model constants fitted to the sweep's "fit" batches (log-error
-    least squares over chunk lengths within 1.6x of each batch's fastest)."""
+    least squares over the launches within 1.6x of each batch's fastest)."""
     from scipy.optimize import least_squares
-    pts = [p for p in schedule_points(sweep) if p[4] <= WINDOW * p[5]]
+    pts = [p for p in schedule_points(sweep) if p[5] <= WINDOW * p[6]]
     free = [n for n in SCHED_NAMES if n not in SCHED_HELD]
 
     def consts(x):
@@ -411,35 +428,51 @@ def fit_schedule(sweep: dict, warm: Dict[str, float]) -> Dict[str, float]:
 
     def resid(x):
         sc = consts(x)
-        return np.array([math.log(schedule_time(sc, warm, t, H_Q, hpt, c)) - math.log(us)
-                         for t, H_Q, hpt, c, us, _ in pts])
+        return np.array([math.log(schedule_time(sc, warm, t, H_Q, hpt, c, k)) - math.log(us)
+                         for t, H_Q, hpt, c, k, us, _ in pts])
 
     x0 = np.log([SCHED_START[n] for n in free])
     res = least_squares(resid, x0, method="trf", xtol=1e-10, ftol=1e-10, gtol=1e-10, max_nfev=2000)
     return {n: float(f"{v:.6g}") for n, v in consts(res.x).items()}
 
 
-def choose_chunk(sc: Dict[str, float], warm: Dict[str, float], lens, H_Q: int, hpt: int, cus: int = CUS) -> int:
-    """The chunk length da_make_schedule picks for unequal lengths at head
-    tile width hpt: the fastest modelled of the longest sequence cut into
-    1..64 pieces, the longer chunk on a tie."""
+def choose_chunk(sc: Dict[str, float], warm: Dict[str, float], lens, H_Q: int, hpt: int, cus: int = CUS,
+                 max_arrival_tiles: int = 4096):
+    """The chunk length and merge da_make_schedule picks for unequal lengths
+    at head tile width hpt: the fastest modelled of the longest sequence cut
+    into 1..64 pieces, each with either merge (inside the split launch only
+    while the tiles have arrival counters); on a tie the longer chunk and the
+    second launch.  (chunk, combine)."""
     tiles_of = [-(-L // 32) for L in lens]
     t_max = max(tiles_of)
-    c, best, prev = t_max, schedule_time(sc, warm, tiles_of, H_Q, hpt, t_max, cus), t_max
+    combs = (0, 1) if len(lens) * (H_Q // hpt) <= max_arrival_tiles else (0,)
+
+    def best_of(cand):
+        ts = [(schedule_time(sc, warm, tiles_of, H_Q, hpt, cand, k, cus), k) for k in combs]
+        t, k = ts[0]
+        for tk, kk in ts[1:]:
+            if tk < t:
+                t, k = tk, kk
+        return t, k
+
+    best, comb = best_of(t_max)
+    c, prev = t_max, t_max
     for s in range(2, MAX_SPLITS + 1):
         cand = -(-t_max // s)
         if cand == prev:
             continue
         prev = cand
-        t = schedule_time(sc, warm, tiles_of, H_Q, hpt, cand, cus)
+        t, k = best_of(cand)
         if t < best:
-            best, c = t, cand
-    return c
+            best, c, comb = t, cand, k
+    return c, comb
 
 
 def schedule_regret(sweep: dict, sc: Dict[str, float], warm: Dict[str, float]) -> Dict[str, object]:
-    """The modelled chunk against the fastest timed one, per batch (both
-    sets), at the tile width the sweep timed."""
+    """The modelled chunk and merge against the fastest timed launch, per
+    batch (both sets), at the tile width the sweep timed.  A chunk the sweep
+    did not time is read at the next longer timed one (with the same merge
+    where that was timed)."""
     batches = schedule_batches_by_name()
     out = {}
     for kind in ("fit", "check"):
@@ -448,12 +481,13 @@ def schedule_regret(sweep: dict, sc: Dict[str, float], warm: Dict[str, float]) -
             if r["set"] != kind:
                 continue
             lens, H_Q, _ = batches[(kind, r["batch"])]
-            cu = {int(c): us for c, us in r["chunk_us"].items()}
+            ct = chunk_times(r)
             hpt = int(r["auto_hpt"])
-            c = choose_chunk(sc, warm, lens, H_Q, hpt)
-            timed = [x for x in cu if x >= c]
-            got = cu[min(timed)] if timed else cu[max(cu)]
-            r_all.append(got / min(cu.values()))
+            c, k = choose_chunk(sc, warm, lens, H_Q, hpt)
+            timed = sorted({x for x, _ in ct if x >= c})
+            cc = timed[0] if timed else max(x for x, _ in ct)
+            got = ct.get((cc, k), ct.get((cc, 0)))
+            r_all.append(got / min(ct.values()))
         out[kind] = {"batches": len(r_all), "mean": float(np.mean(r_all)), "worst": float(np.max(r_all))}
     return out
 
@@ -470,11 +504,13 @@ def model_literal(c: Dict[str, float]) -> str:
 def schedule_literal(sc: Dict[str, float], warm: Dict[str, float]) -> str:
     r = lambda k0, k1: warm[k1] / warm[k0]
     f = lambda x: repr(float(f"{x:.6g}"))
-    return "{{{b0}, {b1}}}, {{{t0}, {t1}}}, {{{s0}, {s1}}}, {rate}, {p}, {tail}, {m0}, {{{m10}, {m11}}}".format(
+    return ("{{{b0}, {b1}}}, {{{t0}, {t1}}}, {{{s0}, {s1}}}, {rate}, {p}, {tail}, {m0}, {{{m10}, {m11}}}, {f0}, "
+            "{{{f10}, {f11}}}, {f2}").format(
         b0=f(sc["base"]), b1=f(sc["base"] * r("base0", "base1")), t0=f(sc["t_tile"]),
         t1=f(sc["t_tile"] * r("tt0", "tt1")), s0=f(sc["t_staged"]), s1=f(sc["t_staged"] * r("ts0", "ts1")),
         rate=f(sc["hbm_rate"]), p=f(sc["pnorm"]), tail=f(sc["tail"]), m0=f(sc["merge0"]), m10=f(sc["merge1"]),
-        m11=f(sc["merge1"] * r("merge1_0", "merge1_1")))
+        m11=f(sc["merge1"] * r("merge1_0", "merge1_1")), f0=f(sc["fused0"]), f10=f(sc["fused1"]),
+        f11=f(sc["fused1"] * r("fused1_0", "fused1_1")), f2=f(sc["fused2"]))
 
 
 def header_text(models: Dict[str, Dict[str, float]], schedule: Dict[str, float] = None) -> str:
@@ -550,8 +586,8 @@ def write_summary(models, sched) -> None:
     lines += ["## Per-sequence schedule", "",
               f"* Sweep: {len(sw['rows'])} mixed-length batches, {sw.get('validated', 0)} launches validated, "
               f"{len(sw.get('invalid', []))} invalid.",
-              f"* The modelled chunk against the fastest of 12 timed chunk lengths (a chunk the sweep did not time is "
-              f"read at the next longer timed one): fitted batches {reg['fit']['mean']:.4f}x on average, "
+              f"* The modelled chunk and merge against the fastest of 12 timed chunk lengths, each timed with either "
+              f"merge (a chunk the sweep did not time is read at the next longer timed one): fitted batches {reg['fit']['mean']:.4f}x on average, "
               f"{reg['fit']['worst']:.3f}x at worst; batches never fitted {reg['check']['mean']:.4f}x, "
               f"{reg['check']['worst']:.3f}x at worst.", "", "| constant | value |", "|---|---|"]
     lines += [f"| {n} | {v:.6g} |" for n, v in sorted(sched.items())]

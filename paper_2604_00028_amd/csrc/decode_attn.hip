@@ -145,6 +145,7 @@ struct Params {
   int page_size, max_pages, num_pages;
   Div div_page;         // page_size
   const int32_t* work;  // nullable: per-sequence schedule, int32x4 {tile, first, end, state row} per workgroup
+  const int32_t* seqs;  // schedule, kFused: int32x2 [B] {first chunk-state row or -1, chunk count}
   int state_rows;       // chunk-state rows of the schedule
   int B, H_Q, H_KV, L_K, g, hpt, tiles_per_seq, tiles, s, mode;
   int xcd_group;        // 1: consecutive tiles share an XCD (packing off)
@@ -286,7 +287,9 @@ __device__ __forceinline__ void merge_rows(const float* o_part, const float* m_p
 
 // The single-launch merge: the last workgroup of a tile merges the tile's
 // s chunk states for its hpt <= 32 rows (query heads), with every thread
-// holding float4 output columns.  The states were written in this launch by
+// holding float4 output columns.  Chunk i of the tile's head h is state row
+// srow0 + i * cstride + h (state_rows rows in all); its output row is orow0
+// + h.  The states were written in this launch by
 // other workgroups with device-scope stores and are read with device-scope
 // loads.  Per output element the operations and their order are those of
 // merge_rows (maximum over non-empty chunks, then the weights, L and O
@@ -294,21 +297,23 @@ __device__ __forceinline__ void merge_rows(const float* o_part, const float* m_p
 // code is kept short and rolled: it runs once per tile, on cold
 // instruction caches.  `lds` holds at least 3 x 64 x 32 floats.
 template <int NT, int W>
-__device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t row0_tile, int tid) {
+__device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t srow0, int64_t cstride, int s,
+                                           int64_t orow0, int64_t state_rows, int tid) {
   constexpr int T = 64 * W;              // threads
   constexpr int R = T / 32;              // thread t stages row t % 32 of chunks t / 32 + R u
   constexpr int IPT = NT * 16 * 32 / T;  // float4 columns per thread (hpt * 32 items over T threads)
   constexpr int CB = 16 / IPT;           // chunks of columns loaded at once
   static_assert(CB == da::kFusedBatch[NT - 1], "the planner prices the merge in batches of CB chunks");
   constexpr uint32_t kOut = 0xfffffff0u; // an offset past every buffer: reads zero, touches nothing
-  const int hpt = p.hpt, s = p.s;
+  const int hpt = p.hpt;
   // 32-bit offsets: the chunk states of a call stay below 2 GiB (checked on the host), and the
   // buffer ranges end with them, so out-of-range rows and chunks read as zeros
-  const uint32_t rows = (uint32_t)p.B * (uint32_t)p.H_Q;
-  const uint32_t r0 = (uint32_t)row0_tile;
-  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(p.m_part, (uint32_t)s * rows * 4u);
-  const __amdgpu_buffer_rsrc_t lrs = make_rsrc(p.l_part, (uint32_t)s * rows * 4u);
-  const __amdgpu_buffer_rsrc_t ors = make_rsrc(p.o_part, (uint32_t)s * rows * (uint32_t)D * 4u);
+  const uint32_t rows = (uint32_t)cstride;  // state rows between two chunks of one head
+  const uint32_t r0 = (uint32_t)srow0;
+  const uint32_t nrows = (uint32_t)state_rows;
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(p.m_part, nrows * 4u);
+  const __amdgpu_buffer_rsrc_t lrs = make_rsrc(p.l_part, nrows * 4u);
+  const __amdgpu_buffer_rsrc_t ors = make_rsrc(p.o_part, nrows * (uint32_t)D * 4u);
   // chunk rows are padded to 64 + CB so that a batch reads them unconditionally
   float* lm = lds;                               // [64 + CB chunks][32 rows] maxima
   float* ll = lds + (DA_MAX_SPLITS + CB) * 32;   // [64 + CB][32] sums
@@ -336,7 +341,7 @@ __device__ __forceinline__ void merge_tile(const Params& p, float* lds, int64_t 
   auto store_item = [&](int j, float M, float L, const f32x4& o) {
     const int item = tid + T * j, h = item >> 5, c = item & 31;
     if (h >= hpt) return;
-    const int64_t row = row0_tile + h;
+    const int64_t row = orow0 + h;
     const float inv = L > 0.f ? 1.0f / L : 0.f;
     *reinterpret_cast<uint2*>(p.out + row * D + 4 * c) =
         make_uint2(pack_bf16x2(o[0] * inv, o[1] * inv), pack_bf16x2(o[2] * inv, o[3] * inv));
@@ -1021,7 +1026,7 @@ split_partial_kernel(Params p) {
             make_uint2(pack_bf16x2(o[bb][0] * inv, o[bb][1] * inv), pack_bf16x2(o[bb][2] * inv, o[bb][3] * inv));
       }
       if (p.lse && wave == 0 && quad == 0 && nb0 == 0) p.lse[row] = Lw > 0.f ? mval + logf(Lw) : -INFINITY;
-    } else if (SCH || p.mode == kPartials) {
+    } else if (p.mode == kPartials) {
 #pragma unroll
       for (int bb = 0; bb < NBW; ++bb) {
         const int nn = nb0 + wave * NBW + bb;
@@ -1051,35 +1056,51 @@ split_partial_kernel(Params p) {
     }
   }
 
-  if constexpr (!SCH) {
-    if (p.mode == kFused) {
-      // Single-launch merge.  Hand-off: every wave waits until its chunk
-      // state stores have completed (they are device-scope, written through
-      // L2), then thread 0 takes an arrival ticket for the tile.  The
-      // workgroup that takes the last of the tile's s x VS tickets has seen
-      // every other workgroup's ticket, each taken after that workgroup's
-      // stores completed, so device-scope loads now return all the states.
-      // This is the agent-scope release/acquire sequence of the AMDGPU memory
-      // model without its L2 write-back and invalidate, which only non-atomic
-      // data needs; the chunk states are written and read with device-scope
-      // (sc1) accesses only.  No workgroup waits for another.  The last one
-      // sets the counter back to zero for the next call.
-      __shared__ int s_last;
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      if (tid == 0) {
-        const uint32_t n = (uint32_t)p.s * VS;
-        // counters sit a cache line apart: atomics on one line are serialised
-        uint32_t* counter = p.arrivals + (size_t)tile * da::kArrivalStride;
-        const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool last = prev + 1u == n;
-        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last ? 1 : 0;
-      }
-      __syncthreads();
-      if (!s_last) return;
-      merge_tile<NT, W>(p, reinterpret_cast<float*>(smem), row0_tile, tid);
+  if (p.mode == kFused && !direct) {
+    // Single-launch merge.  Hand-off: every wave waits until its chunk
+    // state stores have completed (they are device-scope, written through
+    // L2), then thread 0 takes an arrival ticket for the tile.  The
+    // workgroup that takes the last of the tile's tickets (s x VS, or a
+    // scheduled sequence's chunk count) has seen every other workgroup's
+    // ticket, each taken after that workgroup's stores completed, so
+    // device-scope loads now return all the states.  This is the agent-scope
+    // release/acquire sequence of the AMDGPU memory model without its L2
+    // write-back and invalidate, which only non-atomic data needs; the chunk
+    // states are written and read with device-scope (sc1) accesses only.  No
+    // workgroup waits for another.  The last one sets the counter back to
+    // zero for the next call.
+    int s_m;
+    int64_t srow_m, cstride, nrows;
+    uint32_t n;
+    if constexpr (SCH) {
+      // the sequence's chunks are state rows first, first + 1, ... (uniform across the workgroup)
+      const int first = p.seqs[2 * b], chunks = p.seqs[2 * b + 1];
+      s_m = chunks;
+      n = (uint32_t)chunks;
+      srow_m = (int64_t)first * p.H_Q + head0;
+      cstride = p.H_Q;
+      nrows = (int64_t)p.state_rows * p.H_Q;
+    } else {
+      s_m = p.s;
+      n = (uint32_t)p.s * VS;
+      srow_m = row0_tile;
+      cstride = rows;
+      nrows = (int64_t)p.s * rows;
     }
+    __shared__ int s_last;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+      // counters sit a cache line apart: atomics on one line are serialised
+      uint32_t* counter = p.arrivals + (size_t)tile * da::kArrivalStride;
+      const uint32_t prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const bool last = prev + 1u == n;
+      if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = last ? 1 : 0;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    merge_tile<NT, W>(p, reinterpret_cast<float*>(smem), srow_m, cstride, s_m, row0_tile, nrows, tid);
   }
 }
 
@@ -1606,7 +1627,8 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
       sched->max_splits > DA_MAX_SPLITS || sched->state_rows < 0 || sched->kv_fetch < 0 || sched->kv_fetch > 2 ||
       sched->kv_nontemporal < 0 || sched->kv_nontemporal > 1 ||
       (int64_t)sched->seq_offset != (int64_t)sched->num_items * 16 ||
-      (sched->max_splits > 1) != (sched->state_rows > 0))
+      (sched->max_splits > 1) != (sched->state_rows > 0) || sched->combine < 0 || sched->combine > 1 ||
+      (sched->combine == 1 && (sched->state_rows == 0 || sched->tiles > da::kMaxArrivalTiles)))
     return da::fail(DA_ERR_ARG, "schedule does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   if (!meta_dev) return da::fail(DA_ERR_NULL, "meta_dev must be non-NULL");
   if (!aligned(meta_dev, 16)) return da::fail(DA_ERR_ALIGN, "meta_dev must be 16-byte aligned");
@@ -1649,20 +1671,23 @@ int da_decode_attn_scheduled(const void* q, const void* k, const void* v, const 
   p.xcd_group = 0;  // the schedule orders its workgroups itself
   p.work = static_cast<const int32_t*>(meta_dev);
   p.state_rows = sched->state_rows;
-  p.mode = kPartials;
+  p.mode = sched->combine ? kFused : kPartials;
   p.out = static_cast<uint16_t*>(out);
   p.lse = lse_out;
+  const int32_t* seqs =
+      reinterpret_cast<const int32_t*>(static_cast<const unsigned char*>(meta_dev) + sched->seq_offset);
+  p.seqs = seqs;
   if (need) {
     const da::WorkspaceLayout wl = da::workspace_layout(sched->state_rows, H_Q, D, 1);
     unsigned char* ws = static_cast<unsigned char*>(workspace);
     p.o_part = reinterpret_cast<float*>(ws + wl.o_off);
     p.m_part = reinterpret_cast<float*>(ws + wl.m_off);
     p.l_part = reinterpret_cast<float*>(ws + wl.l_off);
+    // the arrival counters: the fixed region at the end of the caller's buffer
+    p.arrivals = reinterpret_cast<uint32_t*>(ws + da::arrival_offset(workspace_bytes));
   }
   rc = launch_partial(p, pl, static_cast<hipStream_t>(stream));
-  if (rc || !need) return rc;
-  const int32_t* seqs =
-      reinterpret_cast<const int32_t*>(static_cast<const unsigned char*>(meta_dev) + sched->seq_offset);
+  if (rc || !need || sched->combine) return rc;
   return launch_combine(p.o_part, p.m_part, p.l_part, static_cast<uint16_t*>(out), lse_out, sched->max_splits,
                         (int64_t)B * H_Q, static_cast<hipStream_t>(stream), seqs, H_Q);
 }

@@ -342,7 +342,7 @@ StepCost::StepCost(const ScheduleModel& m, int wide, int cus) : direct((size_t)c
 // its workgroups' steps.  Shares run out in increasing order, and while A
 // CUs are busy a step costs tau(A) = (t^p + (A x 64 KiB / rate)^p)^(1/p).
 double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t* tiles_of, int B, int H_Q,
-                     int hpt, int64_t c, int cus) {
+                     int hpt, int64_t c, int cus, int combine) {
   const int wide = hpt > 16 ? 1 : 0;
   const int64_t tps = H_Q / hpt;
   // Workgroups per step count: sequence b gives `big` chunks of q + 1 tiles
@@ -408,8 +408,15 @@ double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t
     prev = sh;
   }
   double t = m.base[wide] + m.tail * steps + 2.0 * (double)state_rows * H_Q * (kHeadDim + 2) * 4.0 / m.hbm_rate;
-  if (state_rows > 0) t += m.merge0 + m.merge1[wide] * max_s;
+  if (state_rows > 0) t += schedule_merge_time(m, hpt, max_s, combine);
   return t;
+}
+
+double schedule_merge_time(const ScheduleModel& m, int hpt, int max_s, int combine) {
+  const int wide = hpt > 16 ? 1 : 0;
+  if (!combine) return m.merge0 + m.merge1[wide] * max_s;
+  const int n = kFusedBatch[wide];
+  return m.fused0 + m.fused1[wide] * max_s * (hpt / 8.0) + m.fused2 * ((max_s + n - 1) / n - 1);
 }
 
 namespace {
@@ -443,33 +450,53 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   }
   bool equal = true;
   for (int b = 1; b < B; ++b) equal = equal && seq_lens[b] == seq_lens[0];
-  // Chunk length (in tiles) for head tiles of h heads, and its modelled
-  // time.  Equal lengths take the uniform plan's split count.  Otherwise the
-  // candidates are the longest sequence cut into 1..64 pieces; the fastest
-  // modelled one wins, on a tie the longer chunk.
-  auto choose_chunk = [&](int h, double* t) -> int64_t {
+  // Chunk length (in tiles) for head tiles of h heads, the merge of the
+  // split sequences (*comb), and the modelled time.  Equal lengths take the
+  // uniform plan's split count and merge.  Otherwise the candidates are the
+  // longest sequence cut into 1..64 pieces, each with either merge (inside
+  // the split launch only while the tiles have arrival counters); the
+  // fastest modelled one wins, on a tie the longer chunk and the second
+  // launch.
+  auto choose_chunk = [&](int h, double* t, int* comb) -> int64_t {
     const ScheduleModel& m = mi355x_schedule_model();
     const StepCost step(m, h > 16 ? 1 : 0, cus);
+    const int max_comb = (int64_t)B * (H_Q / h) <= kMaxArrivalTiles ? 1 : 0;
+    auto best_of = [&](int64_t cand, int* cb) {
+      double bt = schedule_time(m, step, T.data(), B, H_Q, h, cand, cus, 0);
+      *cb = 0;
+      for (int k = 1; k <= max_comb; ++k) {
+        const double tk = schedule_time(m, step, T.data(), B, H_Q, h, cand, cus, k);
+        if (tk < bt) {
+          bt = tk;
+          *cb = k;
+        }
+      }
+      return bt;
+    };
     if (chunk_tiles > 0) {
-      *t = schedule_time(m, step, T.data(), B, H_Q, h, chunk_tiles, cus);
+      *t = best_of(chunk_tiles, comb);
       return chunk_tiles;
     }
     if (equal) {
-      const int s = t_max > 0 ? mi355x_splits(mi355x_model(), B, H_Q, H_KV, seq_lens[0], h, cus) : 1;
-      *t = model_time(mi355x_model(), B, H_Q, H_KV, seq_lens[0], h, s, cus);
+      const CostModel& u = mi355x_model();
+      const int s = t_max > 0 ? mi355x_splits(u, B, H_Q, H_KV, seq_lens[0], h, cus) : 1;
+      *comb = fused_merge(u, h, s, (int64_t)B * (H_Q / h)) ? 1 : 0;
+      *t = model_time(u, B, H_Q, H_KV, seq_lens[0], h, s, cus, 1, *comb == 1);
       return t_max > 0 ? (t_max + s - 1) / s : 1;
     }
     int64_t c = t_max;
-    double best = schedule_time(m, step, T.data(), B, H_Q, h, c, cus);
+    double best = best_of(c, comb);
     int64_t prev = c;
     for (int s = 2; s <= kMaxSplits; ++s) {
       const int64_t cand = (t_max + s - 1) / s;
       if (cand == prev) continue;
       prev = cand;
-      const double ts = schedule_time(m, step, T.data(), B, H_Q, h, cand, cus);
+      int cb = 0;
+      const double ts = best_of(cand, &cb);
       if (ts < best) {
         best = ts;
         c = cand;
+        *comb = cb;
       }
     }
     *t = best;
@@ -479,13 +506,15 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   // the uniform plan (narrow only when modelled at least 1% faster).
   int hpt = heads_per_tile(H_Q, H_KV, pack);
   double t_wide = 0.0, t_narrow = 0.0;
-  int64_t c = choose_chunk(hpt, &t_wide);
+  int comb = 0, comb_narrow = 0;
+  int64_t c = choose_chunk(hpt, &t_wide, &comb);
   const int narrow = pack == 1 ? heads_per_tile(H_Q, H_KV, pack, kNarrowHeadsPerTile) : hpt;
   if (narrow != hpt) {
-    const int64_t c_narrow = choose_chunk(narrow, &t_narrow);
+    const int64_t c_narrow = choose_chunk(narrow, &t_narrow, &comb_narrow);
     if (t_narrow < kSplitGain * t_wide) {
       hpt = narrow;
       c = c_narrow;
+      comb = comb_narrow;
     }
   }
   const int tps = H_Q / hpt;
@@ -525,6 +554,7 @@ int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max
   }
   out->seq_offset = (int32_t)seq_off;
   out->meta_bytes = (int32_t)need;
+  out->combine = rows > 0 ? comb : 0;
   {
     double key_rows = 0.0;
     for (int b = 0; b < B; ++b) key_rows += (double)seq_lens[b] * H_KV;
@@ -658,7 +688,7 @@ int da_make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_
 
 size_t da_schedule_workspace_bytes(const da_schedule* s) {
   if (!s || s->state_rows <= 0 || s->H_Q <= 0) return 0;
-  return da::workspace_layout(s->state_rows, s->H_Q, da::kHeadDim, 1).states;
+  return da::workspace_layout(s->state_rows, s->H_Q, da::kHeadDim, 1).total;
 }
 
 size_t da_workspace_bytes(int B, int H_Q, int d, int num_splits) {

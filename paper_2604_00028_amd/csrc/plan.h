@@ -141,8 +141,15 @@ struct ScheduleModel {
   double tail;              // scale of the summed steps
   double merge0;            // combine launch, fixed part (some sequence split)
   double merge1[2];         // ... per chunk of the most-split sequence
+  double fused0;            // merge inside the split launch, fixed part (some sequence split)
+  double fused1[2];         // ... per chunk of the most-split sequence and 8 heads of a tile
+  double fused2;            // ... per batch of kFusedBatch chunks after the first
 };
 const ScheduleModel& mi355x_schedule_model();
+
+// The merge term of a schedule whose most-split sequence has max_s chunks:
+// a second launch (combine 0) or inside the split launch (combine 1).
+double schedule_merge_time(const ScheduleModel& m, int hpt, int max_s, int combine);
 
 // Cost of one wave step while `busy` CUs stream (index busy = 1..cus), for
 // K through registers (direct) and straight into LDS (staged).
@@ -151,10 +158,11 @@ struct StepCost {
   StepCost(const ScheduleModel& m, int wide, int cus);
 };
 
-// Modelled time (us) of a schedule with target chunk c tiles; `tiles_of`
-// holds the 32-key tile count of each sequence.
+// Modelled time (us) of a schedule with target chunk c tiles whose split
+// sequences are merged as `combine` says; `tiles_of` holds the 32-key tile
+// count of each sequence.
 double schedule_time(const ScheduleModel& m, const StepCost& step, const int64_t* tiles_of, int B, int H_Q,
-                     int hpt, int64_t c, int cus);
+                     int hpt, int64_t c, int cus, int combine);
 
 int make_schedule(const int32_t* seq_lens, int B, int H_Q, int H_KV, int L_K_max, int d, int pack_gqa,
                   int num_cus, int cu_margin, int chunk_tiles, void* meta, size_t meta_bytes, da_schedule* out);

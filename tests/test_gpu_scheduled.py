@@ -296,3 +296,82 @@ def test_device_lengths_differ_from_scheduled(page):
         torch.cuda.synchronize()
         assert_parity(out, O, f"lengths differ page={page} chunk={c}")
         check_lse(lse_t, lse)
+
+
+@pytest.mark.parametrize("page", [None, 32])
+@pytest.mark.parametrize("B,H_Q,H_KV,lengths,c", [
+    (4, 8, 1, [0, 1, 1000, 33], 1),        # 32 chunks: batches of 8 through LDS
+    (3, 128, 2, [700, 2100, 3], 2),        # 32-head tiles or 16-head ones, 17 chunks
+    (2, 12, 4, [300, 95], 4),              # 3 chunks: one batch in registers
+    (3, 32, 1, [300, 40, 511], 1),         # 16 chunks
+    (2, 8, 1, [4096, 32], 2),              # 64 chunks, the most a sequence takes
+    (5, 64, 8, [2000, 17, 0, 900, 4100], 0),
+])
+def test_scheduled_merge_in_launch(B, H_Q, H_KV, lengths, c, page):
+    """The chunk states of split sequences merged by the last workgroup of
+    each head tile inside the split launch, or by the combine launch: both
+    against the oracle, with the same bits (the merge takes the same
+    operations in the same order either way), twice in a row (the arrival
+    counters return to zero)."""
+    sh = custom_shape(B, H_Q, H_KV, max(lengths), varlen=True)
+    inp = make_inputs(sh, seed=B * 13 + H_Q + c, lengths=lengths)
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    kw = dict(cu_seqlens_k=cu)
+    if page is not None:
+        pg = paged_layout(inp, page, seed=page + 1)
+        k, v = to_dev(pg.k_cache), to_dev(pg.v_cache)
+        kw = dict(block_table=torch.from_numpy(pg.block_table).cuda(), seq_lens=torch.from_numpy(pg.seq_lens).cuda())
+    sched, meta = da.da_make_schedule(lengths, H_Q, H_KV, max(lengths), chunk_tiles=c)
+    assert sched.state_rows > 0
+    meta_dev = meta.cuda()
+    got = {}
+    for comb in (sched.combine, 1 - sched.combine, sched.combine, 1):
+        sched.combine = comb
+        say(f"scheduled merge combine={comb} B{B}-H{H_Q}-KV{H_KV} chunk={c} page={page} {sched.as_dict()}")
+        lse_t = torch.empty(B, H_Q, dtype=torch.float32, device="cuda")
+        out = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, lse_out=lse_t, **kw)
+        torch.cuda.synchronize()
+        assert_parity(out, O, f"scheduled merge combine={comb} ({sched.as_dict()})")
+        check_lse(lse_t, lse)
+        if got:
+            first = next(iter(got.values()))
+            assert torch.equal(out.view(torch.int16), first[0].view(torch.int16)), comb
+            assert torch.equal(lse_t, first[1]), comb
+        got[len(got)] = (out, lse_t)
+
+
+@pytest.mark.parametrize("comb", [0, 1])
+def test_scheduled_merge_graph_replay(comb):
+    """A captured scheduled launch with either merge, replayed with eager
+    calls in between: every replay gives the eager bits (the in-launch
+    merge's counters are reset by the kernel itself, no memset node)."""
+    lens = [2000, 17, 0, 900, 4100, 333]
+    sh = custom_shape(len(lens), 64, 8, max(lens), varlen=True)
+    inp = make_inputs(sh, seed=99, lengths=lens)
+    q, k, v, cu = dev_inputs(inp)
+    sched, meta = da.da_make_schedule(lens, 64, 8, max(lens), chunk_tiles=3)
+    assert sched.state_rows > 0
+    sched.combine = comb
+    meta_dev = meta.cuda()
+    say(f"scheduled merge graph replay combine={comb}")
+    eager = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu)
+    torch.cuda.synchronize()
+    out = torch.empty_like(eager)
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream):
+        da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out)
+    torch.cuda.current_stream().wait_stream(stream)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out)
+    for r in range(4):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), f"replay {r}"
+        again = da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu)
+        torch.cuda.synchronize()
+        assert torch.equal(again.view(torch.int16), eager.view(torch.int16))

@@ -202,10 +202,30 @@ def test_schedule_head_tile_width_checked():
 def test_schedule_workspace_bytes():
     s, _ = da.da_make_schedule([8192, 100], 16, 2, num_cus=CUS, chunk_tiles=16)
     assert s.state_rows == 16
-    # Otilde [16 rows, 16 heads, 128] | m [16, 16] | l [16, 16], 256-byte aligned
-    assert da.da_schedule_workspace_bytes(s) == 16 * 16 * 128 * 4 + 2 * 1024
+    # Otilde [16 rows, 16 heads, 128] | m [16, 16] | l [16, 16], 256-byte aligned, then the
+    # arrival counter region the merge inside the split launch counts in
+    assert da.da_schedule_workspace_bytes(s) == 16 * 16 * 128 * 4 + 2 * 1024 + (1 << 20)
     one, _ = da.da_make_schedule([100, 100], 16, 2, num_cus=CUS)
-    assert one.state_rows == 0 and da.da_schedule_workspace_bytes(one) == 0
+    assert one.state_rows == 0 and da.da_schedule_workspace_bytes(one) == 0 and one.combine == 0
+
+
+def test_schedule_merge_choice():
+    """A schedule merges its split sequences inside the split launch when
+    the MI355X model prices that below a second launch for its longest
+    split count: the same choice as a uniform plan of that split count."""
+    for lens, H_Q, H_KV, c in (([8192, 100], 16, 2, 16), ([4096, 64, 900], 64, 8, 4), ([32768] + [256] * 7, 8, 1, 0),
+                               ([20000, 10], 8, 1, 4)):
+        s, _ = da.da_make_schedule(lens, H_Q, H_KV, num_cus=CUS, chunk_tiles=c)
+        assert s.state_rows > 0
+        plan = da.da_make_plan(len(lens), H_Q, H_KV, max(lens), num_splits=s.max_splits, pack_gqa=s.pack_gqa,
+                               num_cus=CUS)
+        want = 1 if plan.heads_per_tile == s.heads_per_tile and plan.combine == 1 else None
+        if want is not None:
+            assert s.combine == want, (lens, s.as_dict())
+        assert s.combine in (0, 1)
+    # 4096-key sequence in 32-key tiles of 1: 64 chunks, beyond the register batch -- priced, still a choice
+    s, _ = da.da_make_schedule([4096, 32], 8, 1, num_cus=CUS, chunk_tiles=2)
+    assert s.max_splits == 64 and s.combine in (0, 1)
 
 
 def scheduled(lib, sched, meta=FAKE, q=FAKE, k=FAKE, v=FAKE, cu=None, bt=None, sl=None, page=64, mp=4, npg=4,
@@ -233,7 +253,7 @@ def test_scheduled_argument_errors():
     # a schedule that does not describe this launch
     for field, val in (("tiles", 3), ("heads_per_tile", 4), ("max_splits", 65), ("num_items", 1),
                        ("seq_offset", 0), ("state_rows", 0), ("kv_fetch", 3), ("pack_gqa", 5),
-                       ("kv_nontemporal", 2), ("kv_nontemporal", -1)):
+                       ("kv_nontemporal", 2), ("kv_nontemporal", -1), ("combine", 2), ("combine", -1)):
         bad = bnd.DaSchedule.from_buffer_copy(s)
         setattr(bad, field, val)
         assert scheduled(lib, bad, ws=FAKE, ws_bytes=need) == bnd.DA_ERR_ARG, field
