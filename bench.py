@@ -44,7 +44,8 @@ if ROOT not in sys.path:
 METRIC = "decode-attention µs/call + achieved HBM GB/s (% of peak), heuristic vs num_splits=1"
 HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_00028_amd", "csrc", f) for f in ("decode_attn.hip", "plan.cpp")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_00028_amd", "csrc", f)
+                  for f in ("decode_attn.hip", "plan.cpp", "plan.h", "cost_model.inc")]
 SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
 LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
@@ -234,7 +235,7 @@ def algorithmic_bytes(B, H_Q, H_KV, L, D=128):
 
 def kernel_source_sha() -> str:
     """Hash of the sources that decide which kernel runs and what it reads:
-    the kernels and the planner that picks the variant."""
+    the kernels, and the planner and its constants that pick the variant."""
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
         h.update(open(path, "rb").read())
@@ -521,7 +522,9 @@ def schedule_sweep_summary(path: str) -> None:
              "uniform launch planned for the longest sequence (`uniform plan`) and the fastest uniform split "
              "count (`uniform best`).  Times in microseconds per call, HIP-graph replay, medians of 5 "
              "interleaved replays.  `fit`: the batches the schedule model was fitted to; `check`: drawn "
-             "afterwards and never fitted.", "",
+             "afterwards and never fitted.  `auto` is what the library made with the constants compiled in when "
+             "the sweep ran (fitted to an earlier sweep of the same batches); calibration_summary.md evaluates the "
+             "constants fitted to this sweep.", "",
              "| set | batch | B | H_Q/H_KV | keys | auto chunk | auto | grid best | auto/grid | uniform plan (s) "
              "| uniform best (s) | plan/auto | best/auto |",
              "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
