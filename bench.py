@@ -857,11 +857,11 @@ def occupancy_summary(d: str) -> None:
              "Commands (MI355X, one GPU), for each case and pass:", "", "```",
              "cd /tmp && export TMPDIR=/tmp && cd $REPO",
              "rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_BUSY_CU_CYCLES SQ_WAVE_CYCLES SQ_WAVES --kernel-trace --stats \\",
-             "    --output-format csv -d gpurun_out/occ_raw_<case> -o run -- \\",
+             "    --output-format csv -d $OUT/occ_raw_<case> -o run -- \\",
              "    python3 bench.py --only <workload> <flags> --steps 20 --rounds 1 --highload-steps 3",
-             "rocprofv3 --pmc MeanOccupancyPerActiveCU --output-format csv -d gpurun_out/occ_occ_<case> -o run -- \\",
+             "rocprofv3 --pmc MeanOccupancyPerActiveCU --output-format csv -d $OUT/occ_occ_<case> -o run -- \\",
              "    python3 bench.py --only <workload> <flags> --steps 20 --rounds 1 --highload-steps 3",
-             "python3 bench.py --occupancy-summary gpurun_out   # writes this file", "```", "",
+             "python3 bench.py --occupancy-summary $OUT   # writes this file", "```", "",
              "Per split-kernel dispatch, mean over the dispatches of the run. GRBM_GUI_ACTIVE comes summed over the "
              "8 XCDs and is divided by 8. Busy CUs = SQ_BUSY_CU_CYCLES / GPU-active cycles (the profiler's "
              "SIMD_UTILIZATION without the division by the CU count); over the kernel's own duration = "
@@ -1021,8 +1021,8 @@ def regression_summary(path: str) -> None:
         "Command (MI355X, one GPU):",
         "",
         "```",
-        "python3 bench.py --regression gpurun_out/regression.json --rounds 5",
-        "python3 bench.py --regression-summary gpurun_out/regression.json   # writes this file",
+        "python3 bench.py --regression $OUT/regression.json --rounds 5",
+        "python3 bench.py --regression-summary $OUT/regression.json   # writes this file",
         "```",
         "",
         f"* Shapes: {n}.",
