@@ -134,7 +134,9 @@ typedef struct da_plan {
  *            HIP attribute query, cached per device); > 0 = no device access
  *   cu_margin compute units to leave free (the paper's sm_margin, Section 3.1)
  *   policy   da_policy
- * Host-only integer/float arithmetic; deterministic for equal arguments. */
+ * Host-only integer/float arithmetic; deterministic for equal arguments.
+ * The chosen split count keeps the chunk states below 2 GiB (they are
+ * addressed with 32-bit offsets). */
 int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
                      int cu_margin, int policy, da_plan* out);
 
@@ -155,7 +157,10 @@ double da_model_time(int policy, int B, int H_Q, int H_KV, int L_K, int heads_pe
  * (num_splits <= 0 or pack_gqa == -1 leave that choice to the policy;
  * pack_gqa 0, 1 or 2 as in da_plan).
  * Fills every field of `out` for the resulting launch; num_cus as for
- * da_choose_splits. */
+ * da_choose_splits.  Errors: DA_ERR_SHAPE for a shape the library does not
+ * take, or a forced num_splits > 1 whose chunk states (num_splits x B x H_Q
+ * x d x 4 bytes) would reach 2 GiB; DA_ERR_SPLITS for num_splits > 64;
+ * DA_ERR_ARG for pack_gqa, policy, num_cus or cu_margin out of range. */
 int da_make_plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa,
                  int num_cus, int cu_margin, int policy, da_plan* out);
 

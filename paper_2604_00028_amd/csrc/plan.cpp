@@ -246,6 +246,14 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   const int g = H_Q / H_KV;
   const int pack = pack_gqa >= 0 ? pack_gqa : (g > 1 ? 1 : 0);
   int hpt = heads_per_tile(H_Q, H_KV, pack);
+  // Chunk states are addressed with 32-bit byte offsets: a split launch
+  // keeps them below 2 GiB.  A forced split count beyond that is refused; a
+  // chosen one is capped (where it could bind, the chip is full anyway).
+  const int64_t split_bytes = (int64_t)B * H_Q * kHeadDim * 4;
+  const int max_s = (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (((int64_t)1 << 31) - 1) / split_bytes));
+  if (num_splits > 1 && num_splits > max_s)
+    return fail(DA_ERR_SHAPE, "num_splits=%d: %lld bytes of chunk state exceed 2 GiB", num_splits,
+                (long long)num_splits * split_bytes);
   int s = num_splits;
   if (policy == DA_POLICY_PAPER || policy == DA_POLICY_EVOLVED) {
     if (s <= 0 && policy == DA_POLICY_PAPER)
@@ -283,6 +291,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
       s = s_wide;
     }
   }
+  s = std::min(s, max_s);
   int vs = 1;
   if (policy == DA_POLICY_MI355X || policy == DA_POLICY_STREAMED) {
     double t = 0.0;

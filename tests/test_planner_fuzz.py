@@ -37,8 +37,15 @@ def shapes(draw):
 def test_every_plan_is_a_launch_the_library_accepts(shape, policy, s, pack, margin):
     B, H_Q, H_KV, L = shape
     cus = 256
-    plan = da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pack, num_cus=cus, cu_margin=margin,
-                           policy=policy)
+    state_bytes = lambda n: n * B * H_Q * 128 * 4
+    try:
+        plan = da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pack, num_cus=cus, cu_margin=margin,
+                               policy=policy)
+    except bnd.DecodeAttnError as e:
+        # a forced split whose chunk states would pass 2 GiB is refused
+        assert e.code == bnd.DA_ERR_SHAPE and s > 1 and state_bytes(s) >= 1 << 31, (shape, s)
+        return
+    assert plan.num_splits == 1 or state_bytes(plan.num_splits) < 1 << 31
     g = H_Q // H_KV
     # fields
     assert 1 <= plan.num_splits <= 64 and (s == 0 or plan.num_splits == s)
