@@ -90,3 +90,71 @@ def test_random_shape_parity(case):
             out, lse_t = run(q, k, v, cu, L, other)
             assert torch.equal(out.view(torch.int16), results["forced"][0].view(torch.int16))
             assert torch.equal(lse_t, results["forced"][1])
+
+
+def draw_paged_case(i: int):
+    c = draw_case(1000 + i)
+    rng = np.random.default_rng(30_000 + i)
+    c["page"] = int(rng.choice([32, 64, 96, 256]))
+    c["varlen"] = True
+    if c["lengths"] is None:
+        c["lengths"] = [int(x) for x in rng.integers(0, c["L"] + 1, size=c["B"])]
+        c["lengths"][0] = c["L"]
+    c["chunk"] = int(rng.choice([0, 0, 1, 2, 5, 40]))
+    return c
+
+
+PAGED_CASES = [draw_paged_case(i) for i in range(60)]
+
+
+@pytest.mark.parametrize("case", PAGED_CASES, ids=lambda c: f"B{c['B']}-H{c['H_Q']}-KV{c['H_KV']}-L{c['L']}"
+                                                            f"-page{c['page']}-s{c['s']}-c{c['chunk']}")
+def test_random_paged_and_scheduled_parity(case):
+    """The same draws over a paged cache: the planned paged entry point with
+    the planner's plan and a forced split count, and the per-sequence
+    schedule (modelled or forced chunk length) with both merges, against the
+    oracle on the contiguous keys; the schedule's two merges give the same
+    bits."""
+    from workloads import paged_layout
+    from tests.gpu_helpers import to_dev
+    c = case
+    sh = custom_shape(c["B"], c["H_Q"], c["H_KV"], c["L"], varlen=True)
+    inp = make_inputs(sh, seed=c["seed"], lengths=c["lengths"])
+    O, lse = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    pg = paged_layout(inp, c["page"], seed=c["seed"] % 1000 + 1)
+    q = to_dev(inp.q)
+    kc, vc = to_dev(pg.k_cache), to_dev(pg.v_cache)
+    bt, sl = torch.from_numpy(pg.block_table).cuda(), torch.from_numpy(pg.seq_lens).cuda()
+    L = c["L"]
+    fin = np.isfinite(lse)
+
+    def check(out, lse_t, what):
+        assert_parity(out, O, what)
+        lg = lse_t.cpu().numpy().astype(np.float64)
+        assert np.array_equal(np.isfinite(lg), fin)
+        assert np.max(np.abs(lg[fin] - lse[fin]), initial=0.0) <= LSE_TOL
+
+    plans = {"planned": da.da_choose_splits(c["B"], c["H_Q"], c["H_KV"], L),
+             "forced": da.da_make_plan(c["B"], c["H_Q"], c["H_KV"], L, num_splits=c["s"], pack_gqa=c["pack"])}
+    for name, plan in plans.items():
+        say(f"random paged {c} {name} {plan.as_dict()}")
+        lse_t = torch.empty(c["B"], c["H_Q"], dtype=torch.float32, device="cuda")
+        out = da.da_decode_attn_paged_planned(q, kc, vc, bt, sl, L, plan, lse_out=lse_t)
+        torch.cuda.synchronize()
+        check(out, lse_t, f"paged {name} {plan.as_dict()}")
+    sched, meta = da.da_make_schedule(c["lengths"], c["H_Q"], c["H_KV"], L, pack_gqa=c["pack"], chunk_tiles=c["chunk"])
+    meta_dev = meta.cuda()
+    combs = (sched.combine, 1 - sched.combine) if sched.state_rows > 0 and sched.tiles <= 4096 else (sched.combine,)
+    first = None
+    for comb in combs:
+        sched.combine = comb
+        say(f"random scheduled {c} {sched.as_dict()}")
+        lse_t = torch.empty(c["B"], c["H_Q"], dtype=torch.float32, device="cuda")
+        out = da.da_decode_attn_scheduled(q, kc, vc, sched, meta_dev, block_table=bt, seq_lens=sl, lse_out=lse_t)
+        torch.cuda.synchronize()
+        check(out, lse_t, f"scheduled {sched.as_dict()}")
+        if first is None:
+            first = (out, lse_t)
+        else:
+            assert torch.equal(out.view(torch.int16), first[0].view(torch.int16))
+            assert torch.equal(lse_t, first[1])
