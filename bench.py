@@ -699,22 +699,25 @@ def read_probe_run(torch, steps: int = 20) -> dict:
     decode kernel's achieved bandwidth is set against."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2604_00028_amd", "libhbm_probe.so"))
-    lib.hbm_read_probe.restype = ctypes.c_int
-    lib.hbm_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
-                                   ctypes.c_int, ctypes.c_void_p]
+    for f in (lib.hbm_read_probe, lib.hbm_read_probe_waves):
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                      ctypes.c_void_p]
     n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device="cuda")
     src.fill_(3)
     sink = torch.empty(max(PROBE_GRID) * 256, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
     grid = {}
-    for wgs in PROBE_GRID:
+    # the grid-stride front at 1-16 workgroups per CU, and one region per wave at one workgroup per CU (the
+    # decode kernel's pattern at high load), with and without the nontemporal hint
+    configs = [(f"wg{w}", lib.hbm_read_probe, w) for w in PROBE_GRID] + [("waves256", lib.hbm_read_probe_waves, 256)]
+    for tag, fn, wgs in configs:
         for nt in (0, 1):
             def launch():
-                rc = lib.hbm_read_probe(src.data_ptr(), n, sink.data_ptr(), sink.numel() * 4, wgs, nt,
-                                        stream.cuda_stream)
+                rc = fn(src.data_ptr(), n, sink.data_ptr(), sink.numel() * 4, wgs, nt, stream.cuda_stream)
                 if rc != 0:
-                    raise RuntimeError(f"hbm_read_probe failed ({rc})")
+                    raise RuntimeError(f"read probe {tag} failed ({rc})")
             launch()
             launch()
             a = torch.cuda.Event(enable_timing=True)
@@ -725,11 +728,11 @@ def read_probe_run(torch, steps: int = 20) -> dict:
             b.record(stream)
             torch.cuda.synchronize()
             us = a.elapsed_time(b) * 1000.0 / steps
-            grid[f"wg{wgs}_{'nt' if nt else 'plain'}"] = round(n / (us * 1e-6) / 1e9, 1)
-    best = max(grid, key=grid.get)
+            grid[f"{tag}_{'nt' if nt else 'plain'}"] = round(n / (us * 1e-6) / 1e9, 1)
+    best = max((k for k in grid if k.startswith("wg")), key=grid.get)
     del src, sink
     return {"bytes": n, "best_gbps": grid[best], "best": best, "frac_of_peak": round(grid[best] / HBM_PEAK_GBS, 4),
-            "gbps": grid}
+            "wave_regions_1wg_per_cu_gbps": grid["waves256_nt"], "gbps": grid}
 
 
 def only_run(args, da, torch, np, dev):

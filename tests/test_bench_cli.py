@@ -92,3 +92,9 @@ def test_read_probe_library_checks_its_arguments():
     assert f(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 0, None) == 1          # sink too small for the grid
     assert f(p, 1 << 20, p, 1 << 20, 0, 0, None) == 1                      # no workgroups
     assert f(p, 1 << 20, p, 1 << 20, 256, 2, None) == 1                    # hint not 0 or 1
+    g = lib.hbm_read_probe_waves
+    g.restype = ctypes.c_int
+    g.argtypes = f.argtypes
+    assert g(None, 1 << 20, p, 1 << 20, 256, 0, None) == 1                 # no source
+    assert g(p, 1 << 20, p, 1 << 20, 3, 0, None) == 1                      # regions do not divide the buffer
+    assert g(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 0, None) == 1          # sink too small
