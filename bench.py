@@ -78,10 +78,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--lk", type=int, default=8192, help="with --only long: L_K of the B=1 Llama-70B GQA shape")
+    ap.add_argument("--shape", default="1,32,1,512", help="with --only shape: B,H_Q,H_KV,L_K (fixed layout)")
     ap.add_argument("--occupancy-summary", metavar="DIR", default=None,
                     help="summarise rocprofv3 occupancy counter runs DIR/occ_<pass>_<case> into "
                          "profiles/occupancy_heuristic_vs_s1.md")
-    ap.add_argument("--only", choices=("headline", "highload", "long", "ragged", "copy", "readprobe"), default=None,
+    ap.add_argument("--only", choices=("headline", "highload", "long", "shape", "ragged", "copy", "readprobe"),
+                    default=None,
                     help="time only the planned launch of one workload, a plain 1 GiB device copy (the reference "
                          "for HBM traffic counters) or the 1 GiB read probe, for profiler runs")
     ap.add_argument("--num-splits", type=int, default=0, help="with --only: force num_splits")
@@ -752,16 +754,26 @@ def only_run(args, da, torch, np, dev):
     if args.only == "long":
         sh = custom_shape(1, 64, 8, args.lk)
         inp = make_inputs(sh, seed=3000 + args.lk)
+    elif args.only == "shape":
+        B, H_Q, H_KV, L = (int(x) for x in args.shape.split(","))
+        sh = custom_shape(B, H_Q, H_KV, L, name=f"b{B}_h{H_Q}_kv{H_KV}_l{L}")
+        inp = make_inputs(sh, seed=5000 + B * 7 + L)
     else:
         sh = config_shapes(2)[3] if args.only == "headline" else config_shapes(5)[0]
         inp = make_inputs(sh)
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
+    # the oracle on every row, or on two sampled sequences of a 1 GiB call
+    oracle = OracleRows(np, torch, q, k, v, [0, sh.B - 1]) if args.only == "highload" else OracleFull(np, inp)
     del inp
     K = args.highload_steps if args.only == "highload" else args.steps
     plan = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, 128, args.num_splits, args.pack_gqa)
     if args.combine >= 0:
         plan = with_combine(da, plan, args.combine)
     var = Variant(args.only, da, torch, q, k, v, sh.L_K, 0, -1, K, plan=plan)
+    validate(torch, oracle, [var], sh.name)
+    if VALIDATION["invalid"]:
+        log(f"{sh.name}: the launch disagrees with the oracle")
+        sys.exit(3)
     interleave(torch, [var], args.rounds)
     nbytes = algorithmic_bytes(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
     gbs = nbytes / (var.median * 1e-6) / 1e9
@@ -786,7 +798,12 @@ def ragged_only(args, da, torch, np):
     ws = torch.zeros(max(da.da_schedule_workspace_bytes(sched), 256), dtype=torch.uint8, device="cuda")
     K = args.highload_steps
     var = Timed(torch, lambda i: da.da_decode_attn_scheduled(q, k, v, sched, meta_dev, cu_seqlens_k=cu, out=out,
-                                                             workspace=ws), K)
+                                                             workspace=ws), K, out, "scheduled")
+    longest = max(range(B), key=lambda b: lens[b])
+    validate(torch, OracleVarlen(np, torch, q, k, v, lens, [0, longest]), [var], name)
+    if VALIDATION["invalid"]:
+        log(f"{name}: the launch disagrees with the oracle")
+        sys.exit(3)
     interleave(torch, [var], args.rounds)
     gbs = ab(B, H_Q, H_KV, tot, varlen=True) / (var.median * 1e-6) / 1e9
     print(json.dumps({"workload": name, "us_per_call": round(var.median, 3), "chunk_tiles": sched.chunk_tiles,
