@@ -1,7 +1,9 @@
 """fp64 CPU oracle for split-KV single-query decode attention.
 
 TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
-benchmark's CPU-baseline leg may import this package.  The product path (the
+benchmark may import this package: the benchmark times it as the CPU
+baseline and checks every launch it times against it before timing (a
+check beside the measurement, never a step of it).  The product path (the
 HIP library and its Python binding) never imports, calls or links it, and it
 shares no code with that path: it takes bf16 bit patterns from the seeded
 input generators and computes everything itself, in float64.
