@@ -45,7 +45,7 @@ METRIC = "decode-attention µs/call + achieved HBM GB/s (% of peak), heuristic v
 HBM_PEAK_GBS = 8000.0
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2604_00028_amd", "csrc", f)
-                  for f in ("decode_attn.hip", "plan.cpp", "plan.h", "cost_model.inc")]
+                  for f in ("decode_attn.hip", "plan.cpp", "plan.h", "cost_model.inc", "split_table.inc")]
 SWEEP = (1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48, 64)
 HIGHLOAD_SWEEP = (1, 2, 3, 4, 6, 8, 12, 16)
 LONG_SWEEP = (1, 2, 4, 8, 12, 16, 24)
@@ -305,6 +305,21 @@ def low_head_run(args, da, torch, np, dev) -> dict:
     return res
 
 
+def table_holds(which: str, B: int, H_Q: int, H_KV: int, L: int) -> bool:
+    """Whether the generated split table ("warm" or "streamed") holds the shape."""
+    from paper_2604_00028_amd import calibrate as cal
+    if not hasattr(table_holds, "shapes"):
+        t = cal.parse_table(open(cal.TABLE_SPLIT).read())
+        table_holds.shapes = {w: {e[:4] for e in t[w]} for w in ("warm", "streamed")}
+    return (B, H_Q, H_KV, L) in table_holds.shapes[which]
+
+
+def launch_key(p) -> tuple:
+    """What a plan launches: every field but pack_gqa, which only names the
+    packing its tile width comes from."""
+    return tuple(v for k, v in sorted(p.as_dict().items()) if k != "pack_gqa")
+
+
 def plan_brief(p) -> str:
     """s, heads per tile, V slices and merge of a plan, e.g. 's4 h8 v4 fused'."""
     merge = "" if p.num_splits == 1 else (" fused" if p.combine else " 2-launch")
@@ -340,7 +355,8 @@ def streamed_run(args, da, torch) -> dict:
     """K/V streamed from HBM: every call of a timed replay reads its own copy
     of the cache (>= 1 GiB per replay, more than L2 + MALL hold), as each
     layer's cache is evicted by the rest of a decode step.  num_splits = 1,
-    the warm-calibrated policy, the streamed policy and fixed splits."""
+    the warm-calibrated policy, the streamed policy, the streamed split
+    table's plan and fixed splits."""
     res = {}
     for B, H_Q, H_KV, L in STREAMED_SHAPES:
         kvb = 2 * B * L * H_KV * 256
@@ -361,10 +377,13 @@ def streamed_run(args, da, torch) -> dict:
         var = {s: Variant(str(s), da, torch, q, K[0], V[0], L, s, 1, steps, kv_copies=kvs, plan=plans[s])
                for s in splits}
         wv = Variant("warm", da, torch, q, K[0], V[0], L, 0, -1, steps, kv_copies=kvs, plan=warm)
+        # the streamed split table's plan (the launch its sweep measured fastest on this shape, if it holds it)
+        tab = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_TABLE_STREAMED)
+        tv = Variant("table", da, torch, q, K[0], V[0], L, 0, -1, steps, kv_copies=kvs, plan=tab)
         import numpy as np
-        validate(torch, OracleRows(np, torch, q, K[0], V[0], range(min(B, 2))), list(var.values()) + [wv],
+        validate(torch, OracleRows(np, torch, q, K[0], V[0], range(min(B, 2))), list(var.values()) + [wv, tv],
                  f"streamed B={B} H_Q={H_Q} H_KV={H_KV} L_K={L}")
-        interleave(torch, list(var.values()) + [wv], args.rounds)
+        interleave(torch, list(var.values()) + [wv, tv], args.rounds)
         us = {s: round(v.median, 3) for s, v in var.items()}
         iqr = lambda v: [round(x, 3) for x in np.percentile(v.times, [25, 75])]
         best = min(us, key=us.get)
@@ -378,8 +397,11 @@ def streamed_run(args, da, torch) -> dict:
             "streamed_speedup_vs_s1": round(us[1] / us[cold.num_splits], 3),
             "streamed_speedup_vs_warm_policy": round(wv.median / us[cold.num_splits], 3),
             "best_fixed": best, "best_fixed_us": us[best],
-            "streamed_vs_best": round(us[cold.num_splits] / us[best], 3), "sweep_us": us}
-        del K, V, kvs, var, wv
+            "streamed_vs_best": round(us[cold.num_splits] / us[best], 3),
+            "table_plan": plan_brief(tab), "table_held": table_holds("streamed", B, H_Q, H_KV, L),
+            "table_us": round(tv.median, 3),
+            "table_vs_best": round(tv.median / us[best], 3), "sweep_us": us}
+        del K, V, kvs, var, wv, tv
     return res
 
 
@@ -960,11 +982,13 @@ def regression_run(args, da, torch) -> None:
                 paper = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_PAPER)
                 evolved = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_EVOLVED)
                 heur = da.da_choose_splits(B, H_Q, H_KV, L)
+                table = da.da_choose_splits(B, H_Q, H_KV, L, policy=da.POLICY_TABLE)
                 splits = sorted({s for s in REG_SWEEP if s == 1 or s * 8 <= L})
                 variants = {s: Variant(f"s{s}", da, torch, q, k, v, L, s, 1, K) for s in splits}
                 own = {"heuristic": Variant("heuristic", da, torch, q, k, v, L, 0, -1, K, plan=heur),
                        "paper": Variant("paper", da, torch, q, k, v, L, 0, -1, K, plan=paper),
                        "evolved": Variant("evolved", da, torch, q, k, v, L, 0, -1, K, plan=evolved),
+                       "table": Variant("table", da, torch, q, k, v, L, 0, -1, K, plan=table),
                        "s1_paper_launch": Variant("s1_paper_launch", da, torch, q, k, v, L, 1, 2, K),
                        # the same launch as s = 1 once more: how far apart two identical launches time
                        "s1_repeat": Variant("s1_repeat", da, torch, q, k, v, L, 0, -1, K, plan=variants[1].plan)}
@@ -985,6 +1009,11 @@ def regression_run(args, da, torch) -> None:
                        "s1_us": sw[1], "s1_iqr": iqr(variants[1]), "s1_repeat_us": round(own["s1_repeat"].median, 3),
                        "paper_splits": paper.num_splits, "paper_us": round(own["paper"].median, 3),
                        "evolved_splits": evolved.num_splits, "evolved_us": round(own["evolved"].median, 3),
+                       "table_plan": plan_brief(table), "table_us": round(own["table"].median, 3),
+                       "table_iqr": iqr(own["table"]),
+                       "table_held": table_holds("warm", B, H_Q, H_KV, L),
+                       # the heuristic's launch is the paper's one-split launch itself (pack_gqa only names it)
+                       "same_launch_as_s1_paper": launch_key(heur) == launch_key(own["s1_paper_launch"].plan),
                        "best_fixed": best, "best_fixed_us": sw[best], "sweep_us": sw}
                 results.append(row)
                 log(f"B={B} H_KV={H_KV} L_K={L}: heuristic {row['heuristic_plan']} {row['heuristic_us']} us, "
@@ -1022,8 +1051,25 @@ def regression_summary(path: str) -> None:
     slower_p1 = [r for r in rows if beyond(r, "s1_paper_launch")]
     slower_s1 = [r for r in rows if beyond(r, "s1")]
     under99_p1 = sum(x > 1 / 0.99 for x in r_p1)
+    same_p1 = [r for r in rows if r.get("same_launch_as_s1_paper")]
+    under99_same = sum(r["heuristic_us"] / r["s1_paper_launch_us"] > 1 / 0.99 for r in same_p1)
     over5 = sum(x > 1.05 for x in r_best)
     bnd = [r for r in rows if r["L_K"] in (576, 640, 768)]
+    held = [r for r in rows if r.get("table_held")]
+    table_lines = []
+    if held:
+        t_h = [r["table_us"] / r["heuristic_us"] for r in held]
+        t_b = [r["table_us"] / min(r["best_fixed_us"], r["heuristic_us"]) for r in held]
+        h_b = [r["heuristic_us"] / min(r["best_fixed_us"], r["table_us"]) for r in held]
+        diff = [r for r in held if r["table_plan"] != r["heuristic_plan"]]
+        table_lines = [
+            f"* Policy TABLE (the configuration-specific split table, learned from the calibration sweep, which "
+            f"was timed in another run) on the {len(held)} shapes it holds: a plan other than the heuristic's in {len(diff)}; "
+            f"its time over the heuristic's mean {statistics.mean(t_h):.3f}x, best {min(t_h):.3f}x, worst "
+            f"{max(t_h):.3f}x; over the faster of the heuristic and the best fixed split: within 5% in "
+            f"{sum(x <= 1.05 for x in t_b)} of {len(held)}, worst {max(t_b):.3f}x (the heuristic over the faster of "
+            f"the table and the best fixed split: within 5% in {sum(x <= 1.05 for x in h_b)}, worst "
+            f"{max(h_b):.3f}x). Every other shape the table plans as the heuristic does."]
     lines = [
         f"# Regression matrix: {n} decode shapes (the paper's Section 5.3 sweep and its L_K >= 640 boundary) "
         "on MI355X",
@@ -1034,8 +1080,9 @@ def regression_summary(path: str) -> None:
         "the MI355X heuristic; one split launched as the paper launches it (`pack_gqa = 2`: one workgroup per",
         "KV head with the whole group, no V slices); one split as the planner makes it (its tile width and V",
         "slices); the paper's policy (policy PAPER); the evolved single-batch setting of its Fig. 1 (policy",
-        "EVOLVED); and fixed splits s in {1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8) as the library plans",
-        "them. Every launch was checked against the fp64 oracle (sampled sequences) before it was timed:",
+        "EVOLVED); the configuration-specific split table (policy TABLE); and fixed splits s in",
+        "{1, 2, 3, 4, 6, 8, 12, 16, 24, 32} (s <= L_K / 8) as the library plans them. Every launch was checked",
+        "against the fp64 oracle (sampled sequences) before it was timed:",
         f"{d.get('validated', 0)} launches, {len(d.get('invalid', []))} invalid.",
         "",
         "Command (MI355X, one GPU):",
@@ -1053,7 +1100,11 @@ def regression_summary(path: str) -> None:
         f"* Heuristic vs one split as the paper launches it: at least 0.99x its speed in {n - under99_p1} of {n} "
         f"shapes (worst {max(r_p1):.3f}x its time); slower beyond noise in {len(slower_p1)}; "
         f"faster by more than 1% in {sum(x < 0.99 for x in r_p1)}; mean {statistics.mean(r_p1):.3f}x its time, "
-        f"best {min(r_p1):.3f}x.",
+        f"best {min(r_p1):.3f}x." + (
+            f" In {len(same_p1)} shapes the heuristic's launch is the paper's launch itself (the same kernel, grid "
+            f"and cache hint; only the name of the packing differs), so their gap is the noise of timing one launch "
+            f"twice; {under99_same} of the shapes under 0.99x are among them." if "same_launch_as_s1_paper" in rows[0]
+            else ""),
         f"* Heuristic vs one split as the planner makes it: worst {max(r_s1):.3f}x its time; slower beyond noise in "
         f"{len(slower_s1)}; faster by more than 1% in {sum(x < 0.99 for x in r_s1)}.",
         f"* Heuristic vs the best fixed split: within 5% in {n - over5} of {n}; worst {max(r_best):.3f}x, "
@@ -1067,19 +1118,22 @@ def regression_summary(path: str) -> None:
         f"{max(r['heuristic_us'] / r['s1_paper_launch_us'] for r in bnd):.3f}x its time; vs the paper's policy "
         f"{min(r['heuristic_us'] / r['paper_us'] for r in bnd):.3f}x to "
         f"{max(r['heuristic_us'] / r['paper_us'] for r in bnd):.3f}x." if bnd else "",
+        *table_lines,
         "",
         "IQR columns: 25th-75th percentile of the per-replay microseconds.",
         "",
         "| B | H_KV | L_K | heuristic plan | us (IQR) | s = 1 paper launch us (IQR) | vs it | s = 1 planned us | "
-        "paper s | paper us | evolved s | evolved us | best s | best us | vs best |",
-        "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
+        "paper s | paper us | evolved s | evolved us | table plan | table us | best s | best us | vs best |",
+        "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|",
     ]
     for r, a, c in zip(rows, r_p1, r_best):
         hi, pi = r["heuristic_iqr"], r["s1_paper_launch_iqr"]
+        tp = (r["table_plan"] + (" (held)" if r["table_held"] else "")) if "table_plan" in r else ""
         lines.append(f"| {r['B']} | {r['H_KV']} | {r['L_K']} | {r['heuristic_plan']} | {r['heuristic_us']} "
                      f"({hi[0]}-{hi[1]}) | {r['s1_paper_launch_us']} ({pi[0]}-{pi[1]}) | {1 / a:.2f}x | "
                      f"{r['s1_us']} | {r['paper_splits']} | {r['paper_us']} | {r['evolved_splits']} | "
-                     f"{r['evolved_us']} | {r['best_fixed']} | {r['best_fixed_us']} | {c:.3f} |")
+                     f"{r['evolved_us']} | {tp} | {r.get('table_us', '')} | {r['best_fixed']} | "
+                     f"{r['best_fixed_us']} | {c:.3f} |")
     open(PROFILE_REGRESSION, "w").write("\n".join(lines) + "\n")
     print(f"wrote {PROFILE_REGRESSION}")
 
@@ -1330,7 +1384,7 @@ def main():
     pol = {name: Variant(name, da, torch, q, k, v, sh.L_K, 0, -1, Kl,
                          plan=da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K, policy=code))
            for name, code in (("paper", da.POLICY_PAPER), ("evolved", da.POLICY_EVOLVED),
-                              ("streamed", da.POLICY_STREAMED))}
+                              ("streamed", da.POLICY_STREAMED), ("table", da.POLICY_TABLE))}
     sweep = [Variant(f"s{x}", da, torch, q, k, v, sh.L_K, x, 1, Kl) for x in SWEEP if x != 1]
     # the same split counts with the chunk states merged by a second launch
     two = [Variant(f"s{x}_two_launch", da, torch, q, k, v, sh.L_K, 0, -1, Kl,
@@ -1434,6 +1488,9 @@ def main():
             "vs_best_fixed_worst": max(r["vs_best_fixed"] for r in low.values())}
     if streamed:
         result["streamed_summary"] = {n: r["streamed_speedup_vs_s1"] for n, r in streamed.items()}
+        result["streamed_vs_best_summary"] = {
+            "streamed_policy": {n: r["streamed_vs_best"] for n, r in streamed.items()},
+            "table_streamed_policy": {n: r["table_vs_best"] for n, r in streamed.items()}}
     result["high_load_summary"] = {"us": high["us_per_call"], "gbs": round(achieved, 1),
                                    "frac": round(achieved / HBM_PEAK_GBS, 4), "plan": high["plan"],
                                    "s1_paper_launch_us": high["s1_paper_launch_us"],

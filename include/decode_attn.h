@@ -75,11 +75,21 @@ typedef enum da_policy {
   DA_POLICY_EVOLVED = 2, /* the evolved single-batch setting the paper's search found (Section 3,
                            Fig. 1): batch 1 -> 12 splits, 16 below 256 keys, GQA packing on;
                            larger batches use the MI355X cost model */
-  DA_POLICY_STREAMED = 3 /* the MI355X cost model calibrated with K/V read from HBM on every call
+  DA_POLICY_STREAMED = 3, /* the MI355X cost model calibrated with K/V read from HBM on every call
                             (no cache reuse between calls, as in a decode step through all
                             layers); it splits earlier, e.g. 4 splits at B=1, H_KV=8, L_K=512,
                             and marks K/V loads nontemporal at any size where one workgroup
                             reads each key.  Its plans run through da_decode_attn_planned. */
+  DA_POLICY_TABLE = 4,   /* configuration-specific split table learned offline (the paper's future
+                            work, Sections 3.3, 4.1 and 4.2: split counts per configuration instead
+                            of one rule): a shape (B, H_Q, H_KV, L_K_max) that the calibration
+                            sweep with K/V resident timed gets the launch measured fastest on it
+                            (split count, tile width, V slices, merge; a launch with fewer splits
+                            within 1% of it preferred); every other shape, a forced num_splits,
+                            pack_gqa 0 or 2, or a CU count other than the sweep's (after
+                            cu_margin) is planned as DA_POLICY_MI355X plans it */
+  DA_POLICY_TABLE_STREAMED = 5 /* the same over the sweep with K/V read from HBM on every call;
+                            falls back to DA_POLICY_STREAMED, whose cache hint it uses */
 } da_policy;
 
 /* A launch plan: the scheduler metadata decided on the host before launch
@@ -113,8 +123,9 @@ typedef struct da_plan {
                              128/v_slices of the output dims (1, 2 or 4; more than 1 only with
                              kv_fetch 2 and pack_gqa 1, or pack_gqa 0 when H_Q = H_KV).  The
                              policies MI355X and STREAMED choose it where a launch keeps one
-                             workgroup per CU and its K/V fit in L2; results are the same bits
-                             for every value. */
+                             workgroup per CU and its K/V fit in L2 (the TABLE policies where
+                             it was measured fastest); results are the same bits for every
+                             value. */
   int32_t combine;        /* how num_splits > 1 chunk states are merged (the final reduction of
                              Sections 3.1 and 5.3): 0 a second kernel launch; 1 inside the split
                              launch, by the last workgroup of each tile to finish (an arrival
@@ -126,8 +137,9 @@ typedef struct da_plan {
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split
  * policy that counts work tiles against the available compute units).
- * Policies MI355X and STREAMED also choose the packed tile width (see
- * da_plan); PAPER and EVOLVED keep the whole group in one tile.
+ * Policies MI355X, STREAMED and the two TABLE policies also choose the
+ * packed tile width (see da_plan); PAPER and EVOLVED keep the whole group in
+ * one tile.
  *   L_K_max  longest sequence in the batch (host-known, as with precomputed
  *            scheduler metadata, Section 5.1)
  *   num_cus  compute units to plan for; 0 = query the current device (one
@@ -145,8 +157,8 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
  * tiles against the compute units; here the count of workgroups per CU, the
  * 32-key tiles each wave walks, the HBM rate and the merge of the chunk
  * states are priced with measured constants).  policy DA_POLICY_STREAMED
- * uses the constants for K/V read from HBM on every call, any other value
- * those of DA_POLICY_MI355X.  heads_per_tile, v_slices and combine as in
+ * or DA_POLICY_TABLE_STREAMED uses the constants for K/V read from HBM on
+ * every call, any other value those of DA_POLICY_MI355X.  heads_per_tile, v_slices and combine as in
  * da_plan; num_cus > 0.  Host only.  Returns -1 for arguments that describe
  * no launch (heads_per_tile not dividing H_Q, num_splits outside 1..64,
  * v_slices not 1, 2 or 4, combine not 0 or 1, non-positive sizes). */

@@ -34,6 +34,8 @@ POLICY_MI355X = 0
 POLICY_PAPER = 1
 POLICY_EVOLVED = 2
 POLICY_STREAMED = 3
+POLICY_TABLE = 4
+POLICY_TABLE_STREAMED = 5
 
 # Every symbol include/decode_attn.h declares.
 EXPORTS = (

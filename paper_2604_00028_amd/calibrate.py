@@ -1,7 +1,7 @@
 """Calibration of the planner's cost models from measured sweeps.
 
     python -m paper_2604_00028_amd.calibrate            # fit and print
-    python -m paper_2604_00028_amd.calibrate --write    # also regenerate csrc/cost_model.inc
+    python -m paper_2604_00028_amd.calibrate --write    # also regenerate csrc/cost_model.inc and split_table.inc
 
 The split policy (paper Section 4) replaces the paper's H100 rule with a cost
 model over num_splits in [1, 64]; its constants are measured on MI355X.  The
@@ -492,6 +492,124 @@ def schedule_regret(sweep: dict, sc: Dict[str, float], warm: Dict[str, float]) -
     return out
 
 
+# ---------------------------------------------------------------- configuration-specific split table
+#
+# The configurations the sweeps timed are planned from what was measured on
+# them rather than from the model: for each shape (B, H_Q, H_KV, L_K) the
+# launch the planner may choose (choosable) that ran fastest, except that a
+# launch with fewer chunks within TABLE_GAIN of it is preferred, as the model
+# takes a split only when it pays at least 1%.  Policies TABLE and
+# TABLE_STREAMED look a shape up by exact match and plan every other shape
+# with the model.  A nearest-configuration lookup for shapes between the
+# timed ones was measured on the sweeps themselves, each shape planned from
+# its neighbours with that shape left out (table_holdout): it did worse than
+# the model, so the table is used only where it was measured.
+
+TABLE_GAIN = 1.01
+TABLE_SPLIT = os.path.join(HERE, "csrc", "split_table.inc")
+
+
+def table_pick(sh: dict):
+    """The launch the table keeps for one timed shape: (hpt, s, vs, combine)."""
+    t = {(h, s, v, c): us for h, s, v, c, us in choosable(sh)}
+    best = min(t.values())
+    near = [k for k, us in t.items() if us <= TABLE_GAIN * best]
+    return min(near, key=lambda k: (k[1], t[k]))
+
+
+def split_table(sweep: dict) -> List[tuple]:
+    """(B, H_Q, H_KV, L_K, hpt, s, vs, combine) for every shape of a sweep,
+    sorted by shape."""
+    return sorted((sh["B"], sh["H_Q"], sh["H_KV"], sh["L"]) + tuple(table_pick(sh)) for sh in sweep["shapes"])
+
+
+def table_holdout(sweep: dict, c: Dict[str, float]) -> Dict[str, object]:
+    """Each timed shape planned from the nearest other timed shape with the
+    same group size H_Q / H_KV (distance |log2 of the ratio of B x H_KV| +
+    |log2 of the ratio of L_K|, each at most 1; else the model), against the
+    model's own plan; times read from the shape's own launches as regret()
+    reads them."""
+    shapes = sweep["shapes"]
+    picks = [table_pick(sh) for sh in shapes]
+    model = {(r["B"], r["H_Q"], r["H_KV"], r["L"]): r for r in regret(sweep, lambda B, H, K, L: plan_mi355x(c, B, H, K, L))["rows"]}
+    out_t, out_m, fallback = [], [], 0
+    for i, sh in enumerate(shapes):
+        t = {(h, s, v, cc): us for h, s, v, cc, us in choosable(sh)}
+        best = min(t.values())
+        g = sh["H_Q"] // sh["H_KV"]
+        near = None
+        for j, o in enumerate(shapes):
+            if j == i or o["H_Q"] // o["H_KV"] != g:
+                continue
+            db = abs(math.log2(sh["B"] * sh["H_KV"] / (o["B"] * o["H_KV"])))
+            dl = abs(math.log2(sh["L"] / o["L"]))
+            if db <= 1 and dl <= 1 and (near is None or (db + dl, db) < near[0]):
+                near = ((db + dl, db), picks[j])
+        m = model[(sh["B"], sh["H_Q"], sh["H_KV"], sh["L"])]["us"] / best
+        out_m.append(m)
+        got = None
+        if near is not None:
+            h, s, v, cc = near[1]
+            same = [k for k in t if k[0] == h and k[2] == v and k[3] == cc and k[1] <= s]
+            if same:
+                got = t[max(same, key=lambda k: k[1])] / best
+        if got is None:
+            fallback += 1
+            got = m
+        out_t.append(got)
+    st = lambda r: {"mean_vs_best": float(np.mean(r)), "worst_vs_best": float(np.max(r)),
+                    "within_5pct": int(sum(x <= 1.05 for x in r))}
+    return {"shapes": len(shapes), "nearest": st(out_t), "model": st(out_m), "fallback": fallback}
+
+
+def table_summary_line(sweep: dict, c: Dict[str, float], which: str) -> str:
+    h = table_holdout(sweep, c)
+    n, t, m = h["shapes"], h["nearest"], h["model"]
+    differ = sum(tuple(e[4:]) != tuple(r["plan"]) for e, r in
+                 zip(split_table(sweep), sorted(regret(sweep, lambda B, H, K, L: plan_mi355x(c, B, H, K, L))["rows"],
+                                                key=lambda r: (r["B"], r["H_Q"], r["H_KV"], r["L"]))))
+    return (f"* Split table (policy {'TABLE' if which == 'warm' else 'TABLE_STREAMED'}): one entry per shape, the "
+            f"fastest launch measured there (fewer chunks preferred within {TABLE_GAIN - 1:.0%}); it differs from the "
+            f"model's choice on {differ} of {n} shapes. Planned from the nearest other swept shape instead (each shape "
+            f"left out in turn), a shape lands {t['mean_vs_best']:.4f}x its fastest on average, {t['worst_vs_best']:.3f}x "
+            f"at worst, within 5% on {t['within_5pct']}, against {m['mean_vs_best']:.4f}x, {m['worst_vs_best']:.3f}x and "
+            f"{m['within_5pct']} for the model: so the library looks the table up by exact shape only.")
+
+
+def table_literal(rows: List[tuple]) -> str:
+    return ", ".join("{" + ", ".join(str(int(x)) for x in r) + "}" for r in rows)
+
+
+def table_text(tables: Dict[str, List[tuple]], cus: int) -> str:
+    lines = ["// Configuration-specific split table: for every shape the calibration",
+             "// sweeps timed, the launch that ran fastest there (a launch with fewer",
+             "// chunks within 1% of it preferred), as {B, H_Q, H_KV, L_K, heads per tile,",
+             "// num_splits, v_slices, combine}, sorted by shape; measured with",
+             "// DA_SPLIT_TABLE_CUS compute units.  Generated by",
+             "// `python -m paper_2604_00028_amd.calibrate --write` from the sweeps",
+             "// profiles/calibration_{warm,streamed}.json; do not edit by hand.",
+             f"#define DA_SPLIT_TABLE_CUS {cus}",
+             f"#define DA_SPLIT_TABLE_WARM {{{table_literal(tables['warm'])}}}",
+             f"#define DA_SPLIT_TABLE_STREAMED {{{table_literal(tables['streamed'])}}}"]
+    return "\n".join(lines + [""])
+
+
+def parse_table(text: str) -> Dict[str, List[tuple]]:
+    """The entries of each table in a generated split_table.inc."""
+    import re
+    out = {}
+    for which, macro in (("warm", "DA_SPLIT_TABLE_WARM"), ("streamed", "DA_SPLIT_TABLE_STREAMED")):
+        m = re.search(rf"#define {macro} (.*)", text)
+        out[which] = [tuple(int(x) for x in e.split(",")) for e in re.findall(r"\{([-0-9, ]+)\}", m.group(1))]
+    m = re.search(r"#define DA_SPLIT_TABLE_CUS (\d+)", text)
+    out["cus"] = int(m.group(1))
+    return out
+
+
+def tables_all() -> Dict[str, List[tuple]]:
+    return {which: split_table(json.load(open(path))) for which, path in SWEEPS.items()}
+
+
 def model_literal(c: Dict[str, float]) -> str:
     f = lambda n: repr(float(c[n]))
     return ("{{{b0}, {b1}}}, {{{tt0}, {tt1}}}, {{{ts0}, {ts1}}}, {m0}, {{{m10}, {m11}}}, {f0}, {{{f10}, {f11}}}, "
@@ -578,6 +696,7 @@ def write_summary(models, sched) -> None:
                   f"counts the sweep did not time (read at the nearest timed count below, which overstates them); "
                   f"{a['mean_vs_best']:.4f}x on average, {a['worst_vs_best']:.3f}x at worst, within 5% on "
                   f"{a['within_5pct']}. The regression matrix times the library's own choices.",
+                  table_summary_line(sweep, c, which),
                   "", "| constant | value |", "|---|---|"]
         lines += [f"| {n} | {v:.6g} |" for n, v in sorted(c.items())]
         lines.append("")
@@ -598,7 +717,7 @@ def write_summary(models, sched) -> None:
 
 def main() -> None:
     ap = argparse.ArgumentParser()
-    ap.add_argument("--write", action="store_true", help="regenerate csrc/cost_model.inc")
+    ap.add_argument("--write", action="store_true", help="regenerate csrc/cost_model.inc and csrc/split_table.inc")
     ap.add_argument("--summary", action="store_true", help="write profiles/calibration_summary.md")
     args = ap.parse_args()
     models = fit_all()
@@ -611,10 +730,17 @@ def main() -> None:
     sched = fit_schedule_all(models)
     print("schedule", json.dumps(sched),
           json.dumps(schedule_regret(json.load(open(SCHEDULE_SWEEP)), sched, models["warm"])))
+    for which, c in models.items():
+        print(which, "table held out", json.dumps(table_holdout(json.load(open(SWEEPS[which])), c)))
     if args.write:
         with open(HEADER, "w") as f:
             f.write(header_text(models, sched))
         print(f"wrote {HEADER}")
+        cus = {json.load(open(path))["device_cus"] for path in SWEEPS.values()}
+        assert len(cus) == 1, "sweeps taken with different CU counts"
+        with open(TABLE_SPLIT, "w") as f:
+            f.write(table_text(tables_all(), cus.pop()))
+        print(f"wrote {TABLE_SPLIT}")
     if args.summary:
         write_summary(models, sched)
 

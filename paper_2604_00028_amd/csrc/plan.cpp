@@ -106,6 +106,31 @@ const CostModel& mi355x_streamed_model() {
   return m;
 }
 
+// The configuration-specific split tables (generated beside the model
+// constants from the same sweeps), sorted by shape.
+#include "split_table.inc"
+
+namespace {
+const TableEntry kTableWarm[] = DA_SPLIT_TABLE_WARM;
+const TableEntry kTableStreamed[] = DA_SPLIT_TABLE_STREAMED;
+
+bool shape_less(const TableEntry& a, const TableEntry& b) {
+  if (a.B != b.B) return a.B < b.B;
+  if (a.H_Q != b.H_Q) return a.H_Q < b.H_Q;
+  if (a.H_KV != b.H_KV) return a.H_KV < b.H_KV;
+  return a.L_K < b.L_K;
+}
+}  // namespace
+
+const TableEntry* table_entry(bool streamed, int B, int H_Q, int H_KV, int L_K) {
+  const TableEntry* first = streamed ? kTableStreamed : kTableWarm;
+  const TableEntry* last =
+      first + (streamed ? sizeof(kTableStreamed) / sizeof(kTableStreamed[0]) : sizeof(kTableWarm) / sizeof(kTableWarm[0]));
+  const TableEntry key = {B, H_Q, H_KV, L_K, 0, 0, 0, 0};
+  const TableEntry* e = std::lower_bound(first, last, key, shape_less);
+  return e != last && !shape_less(key, *e) ? e : nullptr;
+}
+
 // Whether s > 1 chunk states are merged inside the split launch by the last
 // workgroup of each tile (da_plan.combine 1) rather than by a second launch:
 // whichever merge the model prices lower.
@@ -236,8 +261,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   if (rc) return rc;
   if (num_splits > kMaxSplits) return fail(DA_ERR_SPLITS, "num_splits=%d exceeds %d", num_splits, kMaxSplits);
   if (pack_gqa < -1 || pack_gqa > 2) return fail(DA_ERR_ARG, "pack_gqa=%d not in {-1,0,1,2}", pack_gqa);
-  if (policy != DA_POLICY_MI355X && policy != DA_POLICY_PAPER && policy != DA_POLICY_EVOLVED &&
-      policy != DA_POLICY_STREAMED)
+  if (policy < DA_POLICY_MI355X || policy > DA_POLICY_TABLE_STREAMED)
     return fail(DA_ERR_ARG, "unknown policy %d", policy);
   if (num_cus <= 0) return fail(DA_ERR_ARG, "num_cus=%d must be positive here", num_cus);
   if (cu_margin < 0 || cu_margin >= num_cus)
@@ -254,8 +278,40 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   if (num_splits > 1 && num_splits > max_s)
     return fail(DA_ERR_SHAPE, "num_splits=%d: %lld bytes of chunk state exceed 2 GiB", num_splits,
                 (long long)num_splits * split_bytes);
+  const bool streamed = policy == DA_POLICY_STREAMED || policy == DA_POLICY_TABLE_STREAMED;
   int s = num_splits;
-  if (policy == DA_POLICY_PAPER || policy == DA_POLICY_EVOLVED) {
+  int vs = 1, comb = 0;
+  bool from_table = false;
+  if (policy == DA_POLICY_TABLE || policy == DA_POLICY_TABLE_STREAMED) {
+    // A shape the calibration sweep timed, on as many CUs as it had, with
+    // the split count and tile width left to the policy, takes the launch
+    // measured fastest there; any other goes to the cost model.
+    const TableEntry* e = num_splits <= 0 && pack == (g > 1 ? 1 : 0) && cus == DA_SPLIT_TABLE_CUS
+                              ? table_entry(streamed, B, H_Q, H_KV, L_K_max)
+                              : nullptr;
+    if (e) {
+      const int64_t tiles = (int64_t)B * H_Q / e->hpt;
+      da_plan t = {};
+      t.pack_gqa = pack;
+      t.v_slices = e->vs;
+      t.kv_fetch = launch_grid(tiles * e->s, e->vs) <= cus ? kLoneFetch : 0;
+      const bool ok = heads_per_tile_valid(H_Q, H_KV, pack, e->hpt) && e->s >= 1 && e->s <= max_s &&
+                      (e->vs == 1 || e->vs == 2 || e->vs == 4) && v_slices_valid(H_Q, H_KV, t) &&
+                      (e->combine == 0 || (e->combine == 1 && e->s > 1 && tiles <= kMaxArrivalTiles));
+      if (!ok) e = nullptr;
+    }
+    if (e) {
+      hpt = e->hpt;
+      s = e->s;
+      vs = e->vs;
+      comb = e->combine;
+      from_table = true;
+    }
+    policy = streamed ? DA_POLICY_STREAMED : DA_POLICY_MI355X;
+  }
+  if (from_table) {
+    // planned above
+  } else if (policy == DA_POLICY_PAPER || policy == DA_POLICY_EVOLVED) {
     if (s <= 0 && policy == DA_POLICY_PAPER)
       s = paper_splits(B, H_KV, L_K_max, H_Q, hpt, cus);
     else if (s <= 0 && B == 1)
@@ -291,18 +347,17 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
       s = s_wide;
     }
   }
-  s = std::min(s, max_s);
-  int vs = 1;
-  if (policy == DA_POLICY_MI355X || policy == DA_POLICY_STREAMED) {
-    double t = 0.0;
-    vs = best_vslices(policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model(), B, H_Q, H_KV,
-                      L_K_max, hpt, s, cus, pack == 1 || (pack == 0 && hpt == g), &t);
+  if (!from_table) {
+    s = std::min(s, max_s);
+    const CostModel& m = streamed ? mi355x_streamed_model() : mi355x_model();
+    if (policy == DA_POLICY_MI355X || policy == DA_POLICY_STREAMED) {
+      double t = 0.0;
+      vs = best_vslices(m, B, H_Q, H_KV, L_K_max, hpt, s, cus, pack == 1 || (pack == 0 && hpt == g), &t);
+    }
+    comb = fused_merge(m, hpt, s, (int64_t)B * H_Q / hpt) ? 1 : 0;
   }
   out->num_splits = s;
-  out->combine = fused_merge(policy == DA_POLICY_STREAMED ? mi355x_streamed_model() : mi355x_model(), hpt, s,
-                             (int64_t)B * H_Q / hpt)
-                     ? 1
-                     : 0;
+  out->combine = comb;
   out->pack_gqa = pack;
   out->heads_per_tile = hpt;
   out->tiles = (int32_t)((int64_t)B * H_Q / hpt);
@@ -317,8 +372,7 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   // STREAMED plans for K/V that are not resident whatever their size.  The
   // V slices of a chunk all read its keys, as the head tiles of a group do.
   const int readers = (g / hpt) * vs;
-  out->kv_nontemporal = policy == DA_POLICY_STREAMED ? (readers == 1 ? 1 : 0)
-                                                     : kv_nontemporal((double)B * L_K_max * H_KV, readers);
+  out->kv_nontemporal = streamed ? (readers == 1 ? 1 : 0) : kv_nontemporal((double)B * L_K_max * H_KV, readers);
   return DA_OK;
 }
 
@@ -669,7 +723,9 @@ double da_model_time(int policy, int B, int H_Q, int H_KV, int L_K, int heads_pe
       H_Q % heads_per_tile != 0 || num_splits < 1 || num_splits > da::kMaxSplits ||
       (v_slices != 1 && v_slices != 2 && v_slices != 4) || combine < 0 || combine > 1 || num_cus <= 0)
     return -1.0;
-  const da::CostModel& m = policy == DA_POLICY_STREAMED ? da::mi355x_streamed_model() : da::mi355x_model();
+  const da::CostModel& m = policy == DA_POLICY_STREAMED || policy == DA_POLICY_TABLE_STREAMED
+                               ? da::mi355x_streamed_model()
+                               : da::mi355x_model();
   return da::model_time(m, B, H_Q, H_KV, L_K, heads_per_tile, num_splits, num_cus, v_slices, combine == 1);
 }
 

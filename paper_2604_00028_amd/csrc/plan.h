@@ -40,9 +40,9 @@ bool heads_per_tile_valid(int H_Q, int H_KV, int pack, int hpt);
 inline int64_t chunk_start(int64_t L, int s, int i) { return (L * i) / s; }
 
 // Constants of the MI355X cost model (times in microseconds, rates in bytes
-// per microsecond), fitted to a measured split sweep over 72 shapes
-// (B, H_Q, H_KV, L_K) x 12 split counts.  Exposed so tests can check the
-// model's properties.
+// per microsecond), fitted to measured sweeps of every launch the planner
+// can choose over 120-132 shapes (B, H_Q, H_KV, L_K).  Exposed so tests can
+// check the model's properties.
 struct CostModel {
   double base[2];          // launch, first loads and epilogue (16-column / 32-column head tiles)
   double t_tile[2];        // one 32-key tile on one wave, K fetched into the operand layout
@@ -113,6 +113,17 @@ int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave);
 // one group), marks its K/V loads nontemporal (da_plan.kv_nontemporal): only
 // when they exceed DA_RESIDENT_BYTES and one workgroup reads each row.
 int kv_nontemporal(double key_rows, int readers);
+
+// One entry of the configuration-specific split table (policies TABLE and
+// TABLE_STREAMED): the launch measured fastest on one shape of a calibration
+// sweep.
+struct TableEntry {
+  int32_t B, H_Q, H_KV, L_K;           // the shape
+  int32_t hpt, s, vs, combine;         // heads per tile, num_splits, v_slices, combine
+};
+// The entry for exactly (B, H_Q, H_KV, L_K) in the resident (streamed =
+// false) or streamed table, or nullptr.
+const TableEntry* table_entry(bool streamed, int B, int H_Q, int H_KV, int L_K);
 
 int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_gqa, int num_cus,
          int cu_margin, int policy, da_plan* out);

@@ -469,7 +469,9 @@ def test_cu_margin_and_plan_errors():
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=7)
     with pytest.raises(da.DecodeAttnError):
-        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=4)
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=6)
+    with pytest.raises(da.DecodeAttnError):
+        da.da_choose_splits(1, 8, 1, 512, num_cus=256, policy=-1)
     with pytest.raises(da.DecodeAttnError):
         da.da_choose_splits(1, 8, 3, 512, num_cus=256)
     with pytest.raises(da.DecodeAttnError):

@@ -92,3 +92,31 @@ def test_planned_equals_planning_entry(shape):
         a = da.da_decode_attn(q, k, v, lse_out=lse, num_splits=s, pack_gqa=pack)
         torch.cuda.synchronize()
         assert same_bits((a, lse), planned(q, k, v, cu, shape.L_K, plan))
+
+
+@pytest.mark.parametrize("B,H_Q,H_KV,L", [
+    (1, 64, 8, 384),     # streamed table: 4 splits, 4 V slices, merged in the launch
+    (1, 64, 8, 512),
+    (1, 8, 1, 640),      # 6 splits, 4 V slices
+    (1, 32, 1, 768),     # a group of 32 in 16-head tiles
+    (16, 32, 4, 512),    # streamed table: 4 splits, nontemporal
+    (4, 256, 32, 256),
+])
+def test_table_policy_plans(B, H_Q, H_KV, L):
+    """Plans of the configuration-specific split tables on shapes they hold:
+    oracle parity, and the same bits as the same split count and tile width
+    launched one workgroup per chunk with K/V through registers."""
+    sh = custom_shape(B, H_Q, H_KV, L)
+    inp = make_inputs(sh, seed=B * 37 + L)
+    O, _ = decode_attention(inp.q, inp.k, inp.v, inp.lengths, inp.cu_seqlens_k)
+    q, k, v, cu = dev_inputs(inp)
+    for pol in (da.POLICY_TABLE, da.POLICY_TABLE_STREAMED):
+        plan = da.da_choose_splits(B, H_Q, H_KV, L, policy=pol)
+        say(f"table policy {pol} B{B}-H{H_Q}-KV{H_KV}-L{L} {plan.as_dict()}")
+        got = planned(q, k, v, cu, L, plan)
+        assert_parity(got[0], O, f"table policy {pol} {plan.as_dict()}")
+        p = da.DaPlan.from_buffer_copy(plan)
+        p.v_slices, p.kv_fetch, p.kv_nontemporal = 1, 1, 0
+        p.grid = p.tiles * p.num_splits
+        say(f"same split, registers {p.as_dict()}")
+        assert same_bits(planned(q, k, v, cu, L, p), got), (plan.as_dict(), p.as_dict())

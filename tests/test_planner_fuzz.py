@@ -12,10 +12,14 @@ from hypothesis import strategies as st
 
 import paper_2604_00028_amd as da
 from paper_2604_00028_amd import _binding as bnd
+from paper_2604_00028_amd import calibrate as cal
 
 FAKE = 1 << 20
 P = ctypes.c_void_p
-POLICIES = [da.POLICY_MI355X, da.POLICY_STREAMED, da.POLICY_PAPER, da.POLICY_EVOLVED]
+POLICIES = [da.POLICY_MI355X, da.POLICY_STREAMED, da.POLICY_PAPER, da.POLICY_EVOLVED, da.POLICY_TABLE,
+            da.POLICY_TABLE_STREAMED]
+# the shapes the split tables hold, so that the TABLE policies' own plans are drawn too
+TABLE_SHAPES = sorted({e[:4] for t in ("warm", "streamed") for e in cal.tables_all()[t]})
 
 
 def launch_grid(chunks, vs):
@@ -32,8 +36,8 @@ def shapes(draw):
 
 
 @settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.too_slow])
-@given(shapes(), st.sampled_from(POLICIES), st.integers(0, 64), st.sampled_from([-1, 0, 1, 2]),
-       st.sampled_from([0, 0, 17, 200]))
+@given(st.one_of(shapes(), st.sampled_from(TABLE_SHAPES)), st.sampled_from(POLICIES),
+       st.one_of(st.just(0), st.integers(0, 64)), st.sampled_from([-1, -1, 0, 1, 2]), st.sampled_from([0, 0, 17, 200]))
 def test_every_plan_is_a_launch_the_library_accepts(shape, policy, s, pack, margin):
     B, H_Q, H_KV, L = shape
     cus = 256
