@@ -321,9 +321,11 @@ def launch_key(p) -> tuple:
 
 
 def plan_brief(p) -> str:
-    """s, heads per tile, V slices and merge of a plan, e.g. 's4 h8 v4 fused'."""
+    """s, heads per tile, V slices, merge and (when not four) waves per
+    workgroup of a plan, e.g. 's4 h8 v4 fused' or 's1 h8 v1 w2'."""
     merge = "" if p.num_splits == 1 else (" fused" if p.combine else " 2-launch")
-    return f"s{p.num_splits} h{p.heads_per_tile} v{p.v_slices}{merge}"
+    waves = "" if p.group_waves == 4 else f" w{p.group_waves}"
+    return f"s{p.num_splits} h{p.heads_per_tile} v{p.v_slices}{merge}{waves}"
 
 
 class OracleFull:
@@ -711,35 +713,39 @@ def copy_run(args, torch):
                       "us_per_copy": round(us, 2), "gbps": round(2 * n / (us * 1e-6) / 1e9, 1)}), flush=True)
 
 
-PROBE_GRID = (256, 512, 1024, 2048, 4096)
+# (workgroups, loads per thread) of the grid-stride probe, and of the one-region-per-wave probe
+PROBE_GRID = ((256, 4), (256, 8), (256, 16), (512, 4), (512, 8), (1024, 4), (2048, 4), (4096, 4))
+PROBE_WAVES = ((256, 8), (256, 16))
 
 
 def read_probe_run(torch, steps: int = 20) -> dict:
     """The HBM read ceiling: a kernel that only reads 1 GiB with 16-byte
-    loads (libhbm_probe.so, csrc/hbm_probe.hip), at 1-16 workgroups per CU,
-    with and without the nontemporal hint; microseconds per launch from HIP
-    events around `steps` launches on the current stream, after two warm-up
-    launches.  The fastest configuration's rate is the practical ceiling the
-    decode kernel's achieved bandwidth is set against."""
+    loads (libhbm_probe.so, csrc/hbm_probe.hip), at 1-16 workgroups per CU
+    and 4-16 loads per thread in flight, with and without the nontemporal
+    hint; microseconds per launch from HIP events around `steps` launches on
+    the current stream, after two warm-up launches.  The fastest
+    configuration's rate is the practical ceiling the decode kernel's
+    achieved bandwidth is set against."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2604_00028_amd", "libhbm_probe.so"))
     for f in (lib.hbm_read_probe, lib.hbm_read_probe_waves):
         f.restype = ctypes.c_int
         f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
-                      ctypes.c_void_p]
+                      ctypes.c_int, ctypes.c_void_p]
     n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device="cuda")
     src.fill_(3)
-    sink = torch.empty(max(PROBE_GRID) * 256, dtype=torch.int32, device="cuda")
+    sink = torch.empty(max(w for w, _ in PROBE_GRID) * 256, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
     grid = {}
     # the grid-stride front at 1-16 workgroups per CU, and one region per wave at one workgroup per CU (the
     # decode kernel's pattern at high load), with and without the nontemporal hint
-    configs = [(f"wg{w}", lib.hbm_read_probe, w) for w in PROBE_GRID] + [("waves256", lib.hbm_read_probe_waves, 256)]
-    for tag, fn, wgs in configs:
+    configs = [(f"wg{w}x{u}", lib.hbm_read_probe, w, u) for w, u in PROBE_GRID] + \
+              [(f"waves{w}x{u}", lib.hbm_read_probe_waves, w, u) for w, u in PROBE_WAVES]
+    for tag, fn, wgs, loads in configs:
         for nt in (0, 1):
             def launch():
-                rc = fn(src.data_ptr(), n, sink.data_ptr(), sink.numel() * 4, wgs, nt, stream.cuda_stream)
+                rc = fn(src.data_ptr(), n, sink.data_ptr(), sink.numel() * 4, wgs, loads, nt, stream.cuda_stream)
                 if rc != 0:
                     raise RuntimeError(f"read probe {tag} failed ({rc})")
             launch()
@@ -753,10 +759,10 @@ def read_probe_run(torch, steps: int = 20) -> dict:
             torch.cuda.synchronize()
             us = a.elapsed_time(b) * 1000.0 / steps
             grid[f"{tag}_{'nt' if nt else 'plain'}"] = round(n / (us * 1e-6) / 1e9, 1)
-    best = max((k for k in grid if k.startswith("wg")), key=grid.get)
+    best = max(grid, key=grid.get)
     del src, sink
     return {"bytes": n, "best_gbps": grid[best], "best": best, "frac_of_peak": round(grid[best] / HBM_PEAK_GBS, 4),
-            "wave_regions_1wg_per_cu_gbps": grid["waves256_nt"], "gbps": grid}
+            "wave_regions_1wg_per_cu_gbps": max(grid["waves256x8_nt"], grid["waves256x16_nt"]), "gbps": grid}
 
 
 def only_run(args, da, torch, np, dev):
@@ -1237,6 +1243,7 @@ def calibration_plans(da, B, H_Q, H_KV, L, s, which, cus):
                 p = da.DaPlan.from_buffer_copy(base)
                 p.heads_per_tile, p.tiles, p.v_slices, p.grid = w, tiles, vs, grid
                 p.kv_fetch, p.kv_nontemporal, p.combine = fetch, nt, comb
+                p.group_waves = 4    # the model prices four-wave launches (two waves are a rule on top)
                 out.append(p)
     return out
 
@@ -1508,6 +1515,9 @@ def with_combine(da, plan, combine):
     launch: 0; inside the split launch: 1)."""
     p = da.DaPlan.from_buffer_copy(plan)
     p.combine = combine if p.num_splits > 1 else 0
+    if p.combine == 1 and p.group_waves == 2:
+        # the in-launch merge runs in four-wave launches: one workgroup per CU, K/V straight into LDS
+        p.group_waves, p.kv_fetch = 4, 2
     return p
 
 

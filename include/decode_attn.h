@@ -109,7 +109,13 @@ typedef struct da_plan {
                              v_slices * 8 * ceil(tiles * num_splits / 8) (a chunk's slices share an
                              XCD; the workgroups past the last chunk return at once) */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
-  int32_t group_waves;    /* wave64s per workgroup (4); each takes a contiguous part of the chunk */
+  int32_t group_waves;    /* wave64s per workgroup, each taking a contiguous part of the chunk: 4, or 2
+                             where the launch fills at least 3/4 of the CUs with one workgroup each,
+                             one workgroup reads each key and chunks hold >= 512 keys (fewer loads
+                             in flight read HBM faster there); with 2, kv_fetch is 0 or 1, v_slices
+                             1 and combine 0.  Entry points that plan for themselves and read the
+                             lengths on the device (cu_seqlens_k, paged seq_lens) launch four, as
+                             their sequences may be far shorter than L_K_max. */
   int32_t kv_fetch;       /* how K/V tiles reach the matrix cores: 0 K straight into the operand
                              layout, V through registers to LDS (chunks of one 32-key tile per
                              wave); 1 both row-contiguous into registers, then through LDS (several
@@ -244,7 +250,8 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
  * of this shape: num_splits outside 1..64, a heads_per_tile its pack_gqa
  * cannot produce, tiles != B*H_Q/heads_per_tile, a grid other than the one
  * the da_plan.grid comment gives for its tiles, num_splits and v_slices,
- * group_waves != 4, kv_fetch outside 0..2, kv_nontemporal outside 0..1,
+ * group_waves other than 4 or 2 (2 only with kv_fetch 0 or 1, v_slices 1 and
+ * combine 0), kv_fetch outside 0..2, kv_nontemporal outside 0..1,
  * num_cus < 1, v_slices other than 1, 2 or 4, or v_slices > 1 with a
  * kv_fetch other than 2, with pack_gqa 2, or unpacked with H_Q != H_KV),
  * all before any device access. */

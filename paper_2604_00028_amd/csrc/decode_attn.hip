@@ -1056,7 +1056,9 @@ split_partial_kernel(Params p) {
     }
   }
 
-  if (p.mode == kFused && !direct) {
+  // Two-wave kernels never merge in the launch (their plans use the second
+  // launch; the merge's batches are sized for four waves).
+  if constexpr (W == 4) if (p.mode == kFused && !direct) {
     // Single-launch merge.  Hand-off: every wave waits until its chunk
     // state stores have completed (they are device-scope, written through
     // L2), then thread 0 takes an arrival ticket for the tile.  The
@@ -1202,7 +1204,23 @@ const void* kernel_ptr() {
 }
 
 template <bool PG, bool SCH, bool NTL>
-const void* pick_kernel(int NT, int FETCH, int VS) {
+const void* pick_kernel(int NT, int FETCH, int VS, int W) {
+  if (W == 2) {
+    // two waves, K/V through registers: uniform and paged launches without V slices
+    if constexpr (SCH) {
+      return nullptr;
+    } else {
+      if (VS != 1) return nullptr;
+      switch (FETCH * 2 + NT - 1) {
+        case 0: return kernel_ptr<1, 2, kFetchDirect, PG, SCH, NTL>();
+        case 1: return kernel_ptr<2, 2, kFetchDirect, PG, SCH, NTL>();
+        case 2: return kernel_ptr<1, 2, kFetchStaged, PG, SCH, NTL>();
+        case 3: return kernel_ptr<2, 2, kFetchStaged, PG, SCH, NTL>();
+        default: return nullptr;
+      }
+    }
+  }
+  if (W != 4) return nullptr;
   if (VS != 1) {
     // V slices: direct-to-LDS fetch of uniform launches only
     if constexpr (SCH) {
@@ -1230,23 +1248,27 @@ const void* pick_kernel(int NT, int FETCH, int VS) {
 }
 
 template <bool NTL>
-const void* pick_kernel(bool paged, bool scheduled, int NT, int FETCH, int VS) {
+const void* pick_kernel(bool paged, bool scheduled, int NT, int FETCH, int VS, int W) {
   if (paged)
-    return scheduled ? pick_kernel<true, true, NTL>(NT, FETCH, VS) : pick_kernel<true, false, NTL>(NT, FETCH, VS);
-  return scheduled ? pick_kernel<false, true, NTL>(NT, FETCH, VS) : pick_kernel<false, false, NTL>(NT, FETCH, VS);
+    return scheduled ? pick_kernel<true, true, NTL>(NT, FETCH, VS, W)
+                     : pick_kernel<true, false, NTL>(NT, FETCH, VS, W);
+  return scheduled ? pick_kernel<false, true, NTL>(NT, FETCH, VS, W) : pick_kernel<false, false, NTL>(NT, FETCH, VS, W);
 }
 
 int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   const int W = pl.group_waves;
   const int NT = pl.heads_per_tile <= 16 ? 1 : 2;
   const int FETCH = pl.kv_fetch;
-  if (W != 4) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
+  if (W != 4 && W != 2) return da::fail(DA_ERR_ARG, "plan asks for %d waves per workgroup", W);
+  if (W == 2 && (pl.combine != 0 || pl.v_slices != 1 || FETCH == kFetchLds))
+    return da::fail(DA_ERR_ARG, "two-wave launches take K/V through registers, one V slice and no in-launch merge");
   if (pl.kv_nontemporal != 0 && pl.kv_nontemporal != 1)
     return da::fail(DA_ERR_ARG, "plan asks for K/V cache hint %d", pl.kv_nontemporal);
   const bool paged = prm.block_table != nullptr, scheduled = prm.work != nullptr;
-  const void* fn = pl.kv_nontemporal ? pick_kernel<true>(paged, scheduled, NT, FETCH, pl.v_slices)
-                                     : pick_kernel<false>(paged, scheduled, NT, FETCH, pl.v_slices);
-  if (!fn) return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d with %d V slices", FETCH, pl.v_slices);
+  const void* fn = pl.kv_nontemporal ? pick_kernel<true>(paged, scheduled, NT, FETCH, pl.v_slices, W)
+                                     : pick_kernel<false>(paged, scheduled, NT, FETCH, pl.v_slices, W);
+  if (!fn)
+    return da::fail(DA_ERR_ARG, "plan asks for K/V fetch mode %d with %d V slices and %d waves", FETCH, pl.v_slices, W);
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
   if (rc) return rc;
@@ -1311,7 +1333,7 @@ int check_plan(const da_plan* pl, int B, int H_Q, int H_KV) {
   if (pl->num_splits < 1 || pl->num_splits > DA_MAX_SPLITS || !da::heads_per_tile_valid(H_Q, H_KV, pl->pack_gqa, hpt) ||
       (int64_t)pl->tiles != (int64_t)B * (H_Q / hpt) ||
       (int64_t)pl->grid != da::launch_grid((int64_t)pl->tiles * pl->num_splits, pl->v_slices) ||
-      pl->group_waves != 4 || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
+      !da::group_waves_valid(*pl) || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
       pl->kv_nontemporal > 1 || pl->num_cus < 1 || !da::v_slices_valid(H_Q, H_KV, *pl) || pl->combine < 0 ||
       pl->combine > 1 || (pl->combine == 1 && (pl->num_splits < 2 || pl->tiles > da::kMaxArrivalTiles)))
     return da::fail(DA_ERR_ARG, "plan does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
@@ -1348,10 +1370,12 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
   rc = ensure_gfx950(&cus);
   if (rc) return rc;
   da_plan pl;
-  if (given)
+  if (given) {
     pl = *given;
-  else
+  } else {
     rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+    if (p.cu || p.seq_lens) da::four_waves(&pl, L_K_max);  // lengths known only on the device
+  }
   if (rc) return rc;
   const int s = pl.num_splits;
   const bool fused = s > 1 && pl.combine == 1;
@@ -1554,6 +1578,7 @@ int da_decode_attn_noalloc(const void* q, const void* k, const void* v, const in
   da_plan pl;
   rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
+  if (cu_seqlens_k) da::four_waves(&pl, L_K_max);  // lengths known only on the device
   rc = fits(pl.num_splits);
   if (rc) return rc;
   unsigned char* ws = nullptr;
@@ -1712,6 +1737,7 @@ int da_split_partials(const void* q, const void* k, const void* v, const int32_t
   da_plan pl;
   rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
   if (rc) return rc;
+  if (cu_seqlens_k) da::four_waves(&pl, L_K_max);  // lengths known only on the device
   Params p = make_params(q, k, v, cu_seqlens_k, B, H_Q, H_KV, L_K_max, softmax_scale, pl);
   p.mode = kPartials;
   p.o_part = o_part;

@@ -196,15 +196,27 @@ static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
   return mi355x_splits(mi355x_model(), B, H_Q, H_KV, L_K, hpt, cus);
 }
 
-int group_waves(int64_t grid, int cus) {
-  // Four wave64s, one per SIMD.  Eight (two per SIMD, with K staged)
-  // measured about 15% faster per key on a lone workgroup per CU with a
-  // long chunk, but 0.6-1.5 us slower at chunks of a few hundred keys; the
-  // split count is the better lever for long sequences, and with it chosen
-  // the chunks stay short.
-  (void)grid;
-  (void)cus;
-  return 4;
+int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int combine) {
+  // Four wave64s, one per SIMD, by default.  Where the launch fills at
+  // least three quarters of the CUs with one workgroup each, every key row
+  // is read by one workgroup and the chunks hold at least 512 keys, two
+  // waves, each walking half the chunk with one tile in flight through
+  // registers, read HBM faster than four waves with two direct-to-LDS
+  // stages each: the chip then keeps about a quarter of the loads in flight
+  // (8 instead of 32 MiB), and HBM serves the smaller set of streams closer
+  // to its peak.  Measured on MI355X in one process per comparison: 1 GiB
+  // of K/V at one split 1.8-6.2% faster (B=32, H_Q=64, H_KV=8, L_K=8192:
+  // 157.9 -> 151.7 us), 1.9-8.3% at 128-512 MiB, 4.2% and 7.4% with 192
+  // and 224 of 256 CUs busy, 2.5-8.4% at 2-4 splits merged by a second
+  // launch; neutral at 512 keys per chunk; slower below that (0.84-0.91x at
+  // 128-256 keys), with 160 or 128 of 256 CUs busy (0.98x, 0.95x) and where
+  // two workgroups share each key (16-head tiles of a 32-head group: 0.91x).
+  // The in-launch merge is sized for four waves, so two-wave plans merge by
+  // a second launch.  Eight waves (two per SIMD, with K staged) measured
+  // slower at chunks of a few hundred keys.
+  return vs == 1 && readers == 1 && combine == 0 && grid <= cus && 4 * grid >= 3 * (int64_t)cus && chunk >= 512
+             ? 2
+             : 4;
 }
 
 int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
@@ -219,6 +231,13 @@ int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
   // (36 KB, three workgroups per CU) wins by up to 30%.
   if (grid <= cus) return kLoneFetch;
   return tiles_per_wave >= 2 ? 1 : 0;
+}
+
+void four_waves(da_plan* pl, int L_K_max) {
+  if (pl->group_waves != 2) return;
+  const int64_t chunk = ((int64_t)L_K_max + pl->num_splits - 1) / pl->num_splits;
+  pl->group_waves = 4;
+  pl->kv_fetch = kv_fetch(pl->grid, pl->num_cus, ((chunk + 3) / 4 + 31) / 32);
 }
 
 bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl) {
@@ -364,14 +383,18 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   out->v_slices = vs;
   out->grid = (int32_t)launch_grid((int64_t)out->tiles * s, vs);
   out->num_cus = cus;
-  out->group_waves = group_waves(out->grid, cus);
-  {
-    const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
-    out->kv_fetch = kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
-  }
   // STREAMED plans for K/V that are not resident whatever their size.  The
   // V slices of a chunk all read its keys, as the head tiles of a group do.
   const int readers = (g / hpt) * vs;
+  {
+    const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
+    out->group_waves = group_waves(out->grid, cus, chunk, readers, vs, comb);
+    // two waves: K through registers, straight into the operand layout
+    // where key rows hold one KV head (contiguous 256-byte rows, measured
+    // 1-3% faster there) and through LDS otherwise
+    out->kv_fetch = out->group_waves == 2 ? (H_KV == 1 ? 0 : 1)
+                                          : kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
+  }
   out->kv_nontemporal = streamed ? (readers == 1 ? 1 : 0) : kv_nontemporal((double)B * L_K_max * H_KV, readers);
   return DA_OK;
 }

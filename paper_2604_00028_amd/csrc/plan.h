@@ -98,8 +98,22 @@ inline int64_t launch_grid(int64_t chunks, int vs) {
   return vs == 1 ? chunks : (int64_t)vs * 8 * ((chunks + 7) / 8);
 }
 
-// Waves per workgroup for a launch of `grid` workgroups on `cus` CUs.
-int group_waves(int64_t grid, int cus);
+// Waves per workgroup (da_plan.group_waves) for a launch of `grid`
+// workgroups on `cus` CUs over chunks of `chunk` keys, each key row read by
+// `readers` workgroups, with vs V slices and merge `combine`: 2 or 4.
+int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int combine);
+
+// A plan made inside an entry point whose sequence lengths are read on the
+// device (cu_seqlens_k, paged seq_lens): the sequences may be far shorter
+// than L_K_max, so a two-wave plan, which pays only where every workgroup
+// streams a long chunk, becomes the four-wave launch of the same grid.
+void four_waves(da_plan* pl, int L_K_max);
+
+// Whether a plan's wave count fits the rest of it: 4, or 2 with K/V through
+// registers (kv_fetch 0 or 1), one V slice and no in-launch merge.
+inline bool group_waves_valid(const da_plan& pl) {
+  return pl.group_waves == 4 || (pl.group_waves == 2 && pl.kv_fetch != 2 && pl.v_slices == 1 && pl.combine == 0);
+}
 
 // How K/V tiles reach the matrix cores for a launch of `grid` workgroups on
 // `cus` CUs whose waves walk up to `tiles_per_wave` 32-key tiles

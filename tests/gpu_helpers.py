@@ -43,3 +43,12 @@ def assert_parity(gpu_out: torch.Tensor, ref: np.ndarray, what: str = "") -> Non
     assert np.all(np.isfinite(g)), f"{what}: non-finite output"
     mx, mean = errors(g, ref)
     assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max-abs {mx:.3e} mean-abs {mean:.3e}"
+
+
+def fit_waves(p):
+    """Keep an edited plan's wave count valid: two waves only with K/V through
+    registers (kv_fetch 0 or 1), one V slice and the merge in a second
+    launch; four otherwise."""
+    if p.group_waves == 2 and (p.kv_fetch == 2 or p.v_slices != 1 or p.combine != 0):
+        p.group_waves = 4
+    return p

@@ -363,6 +363,53 @@ def test_planned_entry_checks_the_plan():
         assert call(plan, ws_bytes=states) == bnd.DA_ERR_WORKSPACE, comb
 
 
+def test_two_waves_where_long_chunks_fill_the_chip():
+    """Four waves per workgroup, or two (K/V through registers, no in-launch
+    merge) where the launch fills at least 3/4 of the CUs with one workgroup
+    each, one workgroup reads each key and chunks hold at least 512 keys."""
+    def plan(*shape, **kw):
+        return da.da_choose_splits(*shape, num_cus=256, **kw)
+    p = plan(32, 64, 8, 8192)                      # the 1 GiB high-load call
+    assert (p.group_waves, p.kv_fetch, p.v_slices, p.combine, p.grid) == (2, 1, 1, 0, 256), p.as_dict()
+    assert plan(256, 8, 1, 8192).kv_fetch == 0     # key rows of one KV head: K into the operand layout
+    assert plan(24, 64, 8, 8192).group_waves == 2  # 192 of 256 CUs
+    assert plan(20, 64, 8, 8192).group_waves == 4  # 160 of 256
+    assert plan(8, 256, 32, 512).group_waves == 2  # chunks of 512 keys
+    assert plan(8, 256, 32, 256).group_waves == 4  # 256
+    assert plan(1, 64, 8, 512).group_waves == 4    # 32 workgroups with V slices
+    assert plan(32, 64, 8, 8192, cu_margin=64).group_waves == 4   # more workgroups than the 192 CUs
+    # two 16-head workgroups read each key of a group of 32
+    p = da.da_make_plan(32, 128, 4, 8192, num_splits=1, pack_gqa=1, num_cus=256)
+    assert p.heads_per_tile == 16 and p.group_waves == 4
+    assert da.da_make_plan(64, 128, 4, 8192, num_splits=1, pack_gqa=2, num_cus=256).group_waves == 2
+    # a split merged in the launch keeps four waves; merged by a second launch it takes two
+    p = da.da_make_plan(16, 64, 8, 8192, num_splits=2, pack_gqa=1, num_cus=256)
+    assert p.combine == 1 and p.group_waves == 4
+    p = plan(16, 128, 4, 8192)
+    assert (p.num_splits, p.combine, p.group_waves) == (4, 0, 2), p.as_dict()
+    # the planned entry point takes two waves only with K/V through registers, one V slice, no in-launch merge
+    lib = da.load()
+    FAKE = 1 << 20
+    P = ctypes.c_void_p
+    two = da.da_make_plan(8, 256, 32, 1024, num_splits=1, pack_gqa=1, num_cus=256)
+    assert two.group_waves == 2
+    call = lambda pl: lib.da_decode_attn_planned(P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), None, 8, 256, 32, 1024,
+                                                 128, 0.0, ctypes.byref(pl), P(FAKE), 1 << 30, None)
+    for fetch in (0, 1):
+        ok = bnd.DaPlan.from_buffer_copy(two)
+        ok.kv_fetch = fetch
+        assert call(ok) == bnd.DA_ERR_HIP        # accepted: fails only at the device query here
+    for field, val in (("kv_fetch", 2), ("group_waves", 3), ("group_waves", 1)):
+        bad = bnd.DaPlan.from_buffer_copy(two)
+        setattr(bad, field, val)
+        assert call(bad) == bnd.DA_ERR_ARG, (field, val)
+    split = da.da_make_plan(8, 256, 32, 1024, num_splits=2, pack_gqa=1, num_cus=256)
+    split.group_waves, split.kv_fetch, split.combine = 2, 1, 1
+    assert split.grid == 512 and call(split) == bnd.DA_ERR_ARG     # in-launch merge with two waves
+    split.combine = 0
+    assert call(split) == bnd.DA_ERR_HIP
+
+
 def test_paged_planned_entry_checks_arguments():
     lib = da.load()
     FAKE = 1 << 20

@@ -84,17 +84,20 @@ def test_read_probe_library_checks_its_arguments():
     f = lib.hbm_read_probe
     f.restype = ctypes.c_int
     f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
-                  ctypes.c_void_p]
+                  ctypes.c_int, ctypes.c_void_p]
     p = ctypes.c_void_p(0x1000)
-    assert f(None, 1 << 20, p, 1 << 20, 256, 0, None) == 1                 # no source
-    assert f(p, 1 << 20, None, 1 << 20, 256, 0, None) == 1                 # no sink
-    assert f(p, (1 << 20) + 8, p, 1 << 20, 256, 0, None) == 1              # not whole 16-byte vectors
-    assert f(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 0, None) == 1          # sink too small for the grid
-    assert f(p, 1 << 20, p, 1 << 20, 0, 0, None) == 1                      # no workgroups
-    assert f(p, 1 << 20, p, 1 << 20, 256, 2, None) == 1                    # hint not 0 or 1
+    assert f(None, 1 << 20, p, 1 << 20, 256, 4, 0, None) == 1              # no source
+    assert f(p, 1 << 20, None, 1 << 20, 256, 4, 0, None) == 1              # no sink
+    assert f(p, (1 << 20) + 8, p, 1 << 20, 256, 4, 0, None) == 1           # not whole 16-byte vectors
+    assert f(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 4, 0, None) == 1       # sink too small for the grid
+    assert f(p, 1 << 20, p, 1 << 20, 0, 4, 0, None) == 1                   # no workgroups
+    assert f(p, 1 << 20, p, 1 << 20, 256, 4, 2, None) == 1                 # hint not 0 or 1
+    for loads in (0, 2, 12, 32):
+        assert f(p, 1 << 20, p, 1 << 20, 256, loads, 0, None) == 1         # loads not 4, 8 or 16
     g = lib.hbm_read_probe_waves
     g.restype = ctypes.c_int
     g.argtypes = f.argtypes
-    assert g(None, 1 << 20, p, 1 << 20, 256, 0, None) == 1                 # no source
-    assert g(p, 1 << 20, p, 1 << 20, 3, 0, None) == 1                      # regions do not divide the buffer
-    assert g(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 0, None) == 1          # sink too small
+    assert g(None, 1 << 20, p, 1 << 20, 256, 8, 0, None) == 1              # no source
+    assert g(p, 1 << 20, p, 1 << 20, 3, 8, 0, None) == 1                   # regions do not divide the buffer
+    assert g(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 8, 0, None) == 1       # sink too small
+    assert g(p, 1 << 20, p, 1 << 20, 256, 4, 0, None) == 1                 # loads not 8 or 16

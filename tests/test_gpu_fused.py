@@ -12,7 +12,7 @@ import torch
 import paper_2604_00028_amd as da
 from oracle import decode_attention
 from workloads import config_shapes, custom_shape, make_inputs
-from tests.gpu_helpers import assert_parity, dev_inputs, say
+from tests.gpu_helpers import assert_parity, dev_inputs, fit_waves, say
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,7 @@ def edited(plan, combine=None, vs=None, fetch=None, hpt=None, B=None, H_Q=None):
         p.combine = combine
     chunks = p.tiles * p.num_splits
     p.grid = chunks if p.v_slices == 1 else p.v_slices * 8 * -(-chunks // 8)
-    return p
+    return fit_waves(p)
 
 
 ARRIVAL_BYTES = 1 << 20

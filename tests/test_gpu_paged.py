@@ -215,8 +215,18 @@ def test_highload_paged_full_size():
         assert np.max(np.abs(lse_t.cpu().numpy()[picks] - lse)) <= LSE_TOL
         assert torch.isfinite(out.float()).all()
     for s in (1, 4):
-        say(f"highload paged vs contiguous s={s}")
-        a = da.da_decode_attn(q, k, v, L_K_max=sh.L_K, num_splits=s, pack_gqa=1)
+        # the planned launch (two waves at one split here) and its four-wave form, on both layouts;
+        # the paged entry point, which reads the lengths on the device, launches the four-wave form
+        plan = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, num_splits=s, pack_gqa=1)
+        four = da.DaPlan.from_buffer_copy(plan)
+        if four.group_waves == 2:
+            four.group_waves, four.kv_fetch = 4, 2     # one workgroup per CU: K/V straight into LDS
+        for p in (plan, four):
+            say(f"highload paged vs contiguous s={s} {p.as_dict()}")
+            a = da.da_decode_attn_planned(q, k, v, p, None, L_K_max=sh.L_K)
+            b = da.da_decode_attn_paged_planned(q, kc, vc, bt, sl, sh.L_K, p)
+            torch.cuda.synchronize()
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), p.as_dict()
         b, _ = run_paged(q, kc, vc, bt, sl, sh.L_K, s, 1)
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
@@ -244,12 +254,16 @@ def test_paged_planned_plans_of_every_kind(B, H_Q, H_KV, lengths, page):
     plans += [da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pk) for s in (1, 4) for pk in (0, 1, 2)]
     g = H_Q // H_KV
     for plan in plans:
-        ref = run_paged(q, kc, vc, bt, sl, L, plan.num_splits, plan.pack_gqa)
+        # the entry point's own plan for this split count and packing, and its bits per wave count
+        ref_plan = da.da_make_plan(B, H_Q, H_KV, L, num_splits=plan.num_splits, pack_gqa=plan.pack_gqa)
+        by_waves = {ref_plan.group_waves: run_paged(q, kc, vc, bt, sl, L, plan.num_splits, plan.pack_gqa)}
         vss = (1, 2, 4) if plan.pack_gqa == 1 or (plan.pack_gqa == 0 and g == 1) else (1,)
-        for fetch, vs in [(0, 1), (1, 1)] + [(2, v) for v in vss]:
+        for fetch, vs, waves in [(0, 1, 4), (1, 1, 4), (0, 1, 2), (1, 1, 2)] + [(2, v, 4) for v in vss]:
             for hint in (0, 1):
                 p = da.DaPlan.from_buffer_copy(plan)
-                p.kv_fetch, p.kv_nontemporal, p.v_slices = fetch, hint, vs
+                p.kv_fetch, p.kv_nontemporal, p.v_slices, p.group_waves = fetch, hint, vs, waves
+                if waves == 2:
+                    p.combine = 0    # two-wave launches merge by a second launch
                 chunks = p.tiles * p.num_splits
                 p.grid = chunks if vs == 1 else vs * 8 * -(-chunks // 8)
                 say(f"paged planned B{B}-H{H_Q}-KV{H_KV}-{lengths} page={page} {p.as_dict()}")
@@ -258,6 +272,8 @@ def test_paged_planned_plans_of_every_kind(B, H_Q, H_KV, lengths, page):
                 torch.cuda.synchronize()
                 assert_parity(out, O, f"paged planned {p.as_dict()}")
                 check_lse(lse_t, lse)
-                # neither the tile width, the fetch path, V slices nor the hint change the bits
+                # neither the tile width, the fetch path, V slices nor the hint change the bits; the wave
+                # count cuts the chunk differently, so two-wave launches are compared among themselves
+                ref = by_waves.setdefault(p.group_waves, (out, lse_t))
                 assert torch.equal(out.view(torch.int16), ref[0].view(torch.int16)), p.as_dict()
                 assert torch.equal(lse_t, ref[1]), p.as_dict()

@@ -65,6 +65,35 @@ def test_highload_parity_sampled_sequences():
         assert torch.isfinite(out.float()).all()
 
 
+def test_two_wave_launches_at_full_load_sampled_sequences():
+    """1 GiB of pure-MQA K/V (B=256, H_Q=8, H_KV=1, L_K=8192), which the
+    planner launches with two waves per workgroup and K straight into the
+    operand layout: oracle parity on sampled sequences through both register
+    fetch paths, the same bits for both, and the same bits on a repeat."""
+    sh = custom_shape(256, 8, 1, 8192)
+    inp = make_inputs(sh, seed=43)
+    q, k, v, _ = dev_inputs(inp)
+    picks = [0, 101, 255]
+    O, lse = decode_attention(inp.q[picks], inp.k[picks], inp.v[picks])
+    plan = da.da_choose_splits(sh.B, sh.H_Q, sh.H_KV, sh.L_K)
+    assert (plan.group_waves, plan.kv_fetch, plan.num_splits) == (2, 0, 1), plan.as_dict()
+    first = None
+    for fetch in (0, 1, 0):
+        p = da.DaPlan.from_buffer_copy(plan)
+        p.kv_fetch = fetch
+        say(f"two-wave full load fetch={fetch} {p.as_dict()}")
+        lse_t = torch.empty(sh.B, sh.H_Q, dtype=torch.float32, device="cuda")
+        out = da.da_decode_attn_planned(q, k, v, p, None, lse_out=lse_t)
+        torch.cuda.synchronize()
+        assert_parity(out[picks], O, f"two-wave full load fetch={fetch}")
+        assert np.max(np.abs(lse_t.cpu().numpy()[picks] - lse)) <= LSE_TOL
+        assert torch.isfinite(out.float()).all()
+        if first is None:
+            first = out
+        else:
+            assert torch.equal(out.view(torch.int16), first.view(torch.int16)), fetch
+
+
 def test_streaming_wide_group_sampled_sequences():
     """537 MB of K/V (streaming loads) with groups of 32 heads in one
     workgroup (two 16-column tiles), through each K/V fetch path; the oracle

@@ -54,11 +54,16 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
         vss = (1, 2, 4) if plan.pack_gqa == 1 or (plan.pack_gqa == 0 and g == 1) else (1,)
         # packed groups of more than 16 heads: both tile widths
         widths = {plan.heads_per_tile} | ({16, 32} if plan.pack_gqa == 1 and g > 16 else set())
-        for w, fetch, vs in [(w, f, v) for w in sorted(widths) for f, v in [(0, 1), (1, 1)] + [(2, v) for v in vss]]:
+        # four waves with every fetch path; two (K/V through registers, one V slice) with the merge
+        # in a second launch
+        combos = [(f, v, 4) for f, v in [(0, 1), (1, 1)] + [(2, v) for v in vss]] + [(0, 1, 2), (1, 1, 2)]
+        for w, fetch, vs, waves in [(w, f, v, n) for w in sorted(widths) for f, v, n in combos]:
             for hint in (0, 1):
                 p = da.DaPlan.from_buffer_copy(plan)
                 p.heads_per_tile, p.tiles = w, B * H_Q // w
-                p.kv_fetch, p.kv_nontemporal, p.v_slices = fetch, hint, vs
+                p.kv_fetch, p.kv_nontemporal, p.v_slices, p.group_waves = fetch, hint, vs, waves
+                if waves == 2:
+                    p.combine = 0
                 chunks = p.tiles * p.num_splits
                 p.grid = chunks if vs == 1 else vs * 8 * -(-chunks // 8)
                 say(f"planned B{B}-H{H_Q}-KV{H_KV}-L{L} {p.as_dict()}")
@@ -67,12 +72,12 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
                 lg = got[1].cpu().numpy().astype(np.float64)
                 fin = np.isfinite(lse)
                 assert np.max(np.abs(lg[fin] - lse[fin]), initial=0.0) <= LSE_TOL
-                key = (p.num_splits, p.heads_per_tile)
+                key = (p.num_splits, p.heads_per_tile, p.group_waves)
                 if key in first:
                     assert same_bits(got, first[key]), (key, p.as_dict())
                 else:
                     first[key] = got
-                if p.num_splits > 1:
+                if p.num_splits > 1 and p.group_waves == 4:
                     # the other merge (a second launch, or inside the split launch): the same bits
                     p.combine = 1 - p.combine
                     say(f"planned, other merge {p.as_dict()}")
