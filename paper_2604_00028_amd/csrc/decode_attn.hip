@@ -13,15 +13,19 @@
 // 3.1 and 5.3).
 //
 // gfx950 mapping:
-//  * W = 4 wave64s per workgroup, one per SIMD.  The chunk is cut into W
-//    contiguous key ranges, one per wave; each wave walks its range in tiles
-//    of 32 keys, and the W wave states are merged through LDS in one step,
-//    each wave producing a quarter of the output dims.
+//  * W wave64s per workgroup: 4, one per SIMD, or 2 where one workgroup per
+//    CU streams long chunks over most of the chip (fewer loads in flight
+//    read HBM faster there).  The chunk is cut into W contiguous key
+//    ranges, one per wave; each wave walks its range in tiles of 32 keys,
+//    and the W wave states are merged through LDS in one step, each wave
+//    producing 128 / W of the output dims.
 //  * Scores S^T[key, head] = K . Q^T on MFMA v_mfma_f32_16x16x32_bf16: keys
 //    are the 16 rows, the packed query heads the 16 columns (two column
-//    tiles when a KV head serves up to 32 query heads).  K is fetched in
-//    whole 128-byte lines (8 keys per load instruction) and moved into the
-//    MFMA A-operand layout with one DPP lane rotation per dword.
+//    tiles when a KV head serves up to 32 query heads).  K reaches the
+//    A-operand layout one of three ways (FETCH): loaded straight into it
+//    (each lane reads 64 bytes of one key row), row-contiguous into
+//    registers and then through LDS, or row-contiguous straight into LDS
+//    (buffer loads with the LDS destination), two tiles in flight per wave.
 //  * Online softmax on the MFMA result layout: every lane holds 8 scores of
 //    one head column; the tile max and sum over the 4 row groups take two
 //    v_permlane16/32_swap steps; exp2 on the hardware v_exp_f32 with the
@@ -635,8 +639,8 @@ split_partial_kernel(Params p) {
   // lanes read one 256-byte row) for its LDS stage.  K either comes the same
   // way and takes its own LDS stage (KS), from which it is read back in the
   // MFMA A layout, or is fetched straight into that layout: lane (row r,
-  // group q) loads the 64 bytes of dims [32q, 32q+32) of key r, so
-  // neighbouring lanes read different rows, which the memory pipeline
+  // group q) loads dims [32j + 8q, +8) of key r for j = 0..3 (64 bytes of
+  // one row), so neighbouring lanes read different rows, which the memory pipeline
   // serves at about half the rate of row-contiguous lanes.  The per-lane
   // byte offsets are fixed; tile t moves the descriptor base by t*32 rows
   // and shrinks its record count to match (scalar work only).

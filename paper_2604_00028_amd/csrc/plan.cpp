@@ -60,7 +60,9 @@ const CostModel& mi355x_model() {
 //   T = (compute^p + stream^p)^(1/p) + merge_time
 // Every workgroup has four waves, one per SIMD, and walks a quarter of its
 // chunk each; workgroups that share a CU share its SIMDs.  The soft maximum
-// reflects that a CU's tile loop slows as the chip nears its HBM rate.
+// reflects that a CU's tile loop slows as the chip nears its HBM rate.  The
+// two-wave launch (group_waves) is a measured rule applied after the model
+// has chosen; the model prices the four-wave launch.
 double model_time(const CostModel& m, int B, int H_Q, int H_KV, int L_K, int hpt, int s, int cus, int vs,
                   bool fused) {
   const int wide = hpt > 16 ? 1 : 0;
@@ -388,7 +390,25 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   const int readers = (g / hpt) * vs;
   {
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
-    out->group_waves = group_waves(out->grid, cus, chunk, readers, vs, comb);
+    int waves = group_waves(out->grid, cus, chunk, readers, vs, comb);
+    if (waves == 4 && comb == 1 && !from_table && group_waves(out->grid, cus, chunk, readers, vs, 0) == 2) {
+      // Two waves merge by a second launch.  They take it where the share of
+      // the split launch they save (kTwoWaveGain) is modelled to outweigh
+      // what the second launch adds over the merge inside the launch:
+      // measured at 1 GiB, 2 splits 84.3 -> 83.3 us and at 256 MiB, 4 splits
+      // 43.7 -> 43.1 us, while 4 splits at 128 MiB stayed faster merged in
+      // the launch (22.8 against 23.6 us).  Table plans keep the merge
+      // their sweep measured.
+      const CostModel& m = streamed ? mi355x_streamed_model() : mi355x_model();
+      const double t_in = model_time(m, B, H_Q, H_KV, L_K_max, hpt, s, cus, vs, true);
+      const double t_two = model_time(m, B, H_Q, H_KV, L_K_max, hpt, s, cus, vs, false);
+      if (kTwoWaveGain * t_two < t_in) {
+        comb = 0;
+        out->combine = 0;
+        waves = 2;
+      }
+    }
+    out->group_waves = waves;
     // two waves: K through registers, straight into the operand layout
     // where key rows hold one KV head (contiguous 256-byte rows, measured
     // 1-3% faster there) and through LDS otherwise

@@ -109,6 +109,12 @@ int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int c
 // streams a long chunk, becomes the four-wave launch of the same grid.
 void four_waves(da_plan* pl, int L_K_max);
 
+// Time factor of a two-wave launch against the four-wave one where the
+// two-wave rule applies: the least gain measured at 1-4 splits (1.8-2.5%),
+// rounded up to what the planner counts on when it gives up the in-launch
+// merge for two waves.
+constexpr double kTwoWaveGain = 0.97;
+
 // Whether a plan's wave count fits the rest of it: 4, or 2 with K/V through
 // registers (kv_fetch 0 or 1), one V slice and no in-launch merge.
 inline bool group_waves_valid(const da_plan& pl) {

@@ -382,11 +382,19 @@ def test_two_waves_where_long_chunks_fill_the_chip():
     p = da.da_make_plan(32, 128, 4, 8192, num_splits=1, pack_gqa=1, num_cus=256)
     assert p.heads_per_tile == 16 and p.group_waves == 4
     assert da.da_make_plan(64, 128, 4, 8192, num_splits=1, pack_gqa=2, num_cus=256).group_waves == 2
-    # a split merged in the launch keeps four waves; merged by a second launch it takes two
+    # split plans: two waves merge by a second launch, taken over the in-launch merge where the modelled
+    # call is long enough for the two waves' gain to pay for the second launch (about 24 us and up)
     p = da.da_make_plan(16, 64, 8, 8192, num_splits=2, pack_gqa=1, num_cus=256)
-    assert p.combine == 1 and p.group_waves == 4
+    assert (p.combine, p.group_waves, p.kv_fetch) == (0, 2, 1), p.as_dict()
+    p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=1, num_cus=256)
+    assert (p.combine, p.group_waves, p.kv_fetch) == (1, 4, 2), p.as_dict()
     p = plan(16, 128, 4, 8192)
     assert (p.num_splits, p.combine, p.group_waves) == (4, 0, 2), p.as_dict()
+    p = plan(128, 8, 1, 8192)
+    assert (p.num_splits, p.combine, p.group_waves, p.kv_fetch) == (2, 0, 2, 0), p.as_dict()
+    for pol in (da.POLICY_MI355X, da.POLICY_STREAMED, da.POLICY_PAPER, da.POLICY_EVOLVED):
+        p = plan(8, 64, 8, 8192, policy=pol)
+        assert p.group_waves == 4 or p.combine == 0, (pol, p.as_dict())
     # the planned entry point takes two waves only with K/V through registers, one V slice, no in-launch merge
     lib = da.load()
     FAKE = 1 << 20

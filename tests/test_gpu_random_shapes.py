@@ -12,7 +12,7 @@ import torch
 import paper_2604_00028_amd as da
 from oracle import decode_attention
 from workloads import custom_shape, make_inputs
-from tests.gpu_helpers import assert_parity, dev_inputs, say
+from tests.gpu_helpers import assert_parity, dev_inputs, fit_waves, say
 
 pytestmark = pytest.mark.gpu
 
@@ -72,6 +72,7 @@ def test_random_shape_parity(case):
         forced.v_slices, forced.kv_fetch = 1, c["fetch"]
         forced.grid = forced.tiles * forced.num_splits
     forced.kv_nontemporal = c["hint"]
+    fit_waves(forced)       # two waves only with K/V through registers and one V slice
     plans["forced"] = forced
     results = {}
     for name, plan in plans.items():
