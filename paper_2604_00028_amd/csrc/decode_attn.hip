@@ -1378,9 +1378,9 @@ int run_decode(Params p, int B, int H_Q, int H_KV, int L_K_max, int d, float sof
     pl = *given;
   } else {
     rc = da::plan(B, H_Q, H_KV, L_K_max, d, num_splits, pack_gqa, cus, 0, DA_POLICY_MI355X, &pl);
+    if (rc) return rc;
     if (p.cu || p.seq_lens) da::four_waves(&pl, L_K_max);  // lengths known only on the device
   }
-  if (rc) return rc;
   const int s = pl.num_splits;
   const bool fused = s > 1 && pl.combine == 1;
   rc = check_workspace(s);

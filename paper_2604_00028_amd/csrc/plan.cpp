@@ -240,6 +240,9 @@ void four_waves(da_plan* pl, int L_K_max) {
   const int64_t chunk = ((int64_t)L_K_max + pl->num_splits - 1) / pl->num_splits;
   pl->group_waves = 4;
   pl->kv_fetch = kv_fetch(pl->grid, pl->num_cus, ((chunk + 3) / 4 + 31) / 32);
+  // and the merge a four-wave plan takes (these entry points plan with policy MI355X)
+  if (pl->num_splits > 1)
+    pl->combine = fused_merge(mi355x_model(), pl->heads_per_tile, pl->num_splits, pl->tiles) ? 1 : 0;
 }
 
 bool v_slices_valid(int H_Q, int H_KV, const da_plan& pl) {

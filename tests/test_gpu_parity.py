@@ -94,6 +94,35 @@ def test_two_wave_launches_at_full_load_sampled_sequences():
             assert torch.equal(out.view(torch.int16), first.view(torch.int16)), fetch
 
 
+def test_device_lengths_launch_four_waves():
+    """Where the planner gives a fixed-length batch two waves (B=32, H_Q=64,
+    H_KV=8, L_K=1024: 256 workgroups of 1024 keys), the same batch passed
+    with cu_seqlens_k (lengths read on the device) runs the four-wave
+    launch: its bits are those of the four-wave plan on the fixed layout,
+    and both match the oracle on sampled sequences."""
+    sh = custom_shape(32, 64, 8, 1024)
+    inp = make_inputs(sh, seed=47)
+    q, k, v, _ = dev_inputs(inp)
+    picks = [0, 31]
+    O, _ = decode_attention(inp.q[picks], inp.k[picks], inp.v[picks])
+    two = da.da_choose_splits(32, 64, 8, 1024)
+    assert (two.group_waves, two.num_splits) == (2, 1), two.as_dict()
+    four = da.DaPlan.from_buffer_copy(two)
+    four.group_waves, four.kv_fetch = 4, 2
+    cu = torch.arange(0, 33 * 1024, 1024, dtype=torch.int32, device="cuda")
+    say("device lengths: four waves")
+    a = da.da_decode_attn_planned(q, k, v, two, None)
+    b = da.da_decode_attn_planned(q, k, v, four, None)
+    c = da.da_decode_attn(q, k.view(-1, 8, 128), v.view(-1, 8, 128), cu, L_K_max=1024)
+    torch.cuda.synchronize()
+    for out, what in ((a, "two waves"), (b, "four waves"), (c, "varlen")):
+        assert_parity(out[picks], O, what)
+    assert torch.equal(c.view(torch.int16), b.view(torch.int16))
+    d = da.da_decode_attn(q, k, v)                       # the fixed layout plans two waves
+    torch.cuda.synchronize()
+    assert torch.equal(d.view(torch.int16), a.view(torch.int16))
+
+
 def test_streaming_wide_group_sampled_sequences():
     """537 MB of K/V (streaming loads) with groups of 32 heads in one
     workgroup (two 16-column tiles), through each K/V fetch path; the oracle
