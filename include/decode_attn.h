@@ -165,7 +165,8 @@ int da_choose_splits(int B, int H_Q, int H_KV, int L_K_max, int d, int num_cus,
  * states are priced with measured constants).  policy DA_POLICY_STREAMED
  * or DA_POLICY_TABLE_STREAMED uses the constants for K/V read from HBM on
  * every call, any other value those of DA_POLICY_MI355X.  heads_per_tile, v_slices and combine as in
- * da_plan; num_cus > 0.  Host only.  Returns -1 for arguments that describe
+ * da_plan; the launch is priced with four waves per workgroup (the planner
+ * applies its two-wave rule to the model's choice); num_cus > 0.  Host only.  Returns -1 for arguments that describe
  * no launch (heads_per_tile not dividing H_Q, num_splits outside 1..64,
  * v_slices not 1, 2 or 4, combine not 0 or 1, non-positive sizes). */
 double da_model_time(int policy, int B, int H_Q, int H_KV, int L_K, int heads_per_tile, int num_splits,
