@@ -129,8 +129,9 @@ class Variant:
         self.steps = steps
         s_res, p_res = self.plan.num_splits, self.plan.pack_gqa
         kvs = kv_copies if kv_copies else [(k, v)]
-        # the same launch on the same data: variants with equal keys pool their timings
-        self.key = (tuple(self.plan.as_dict().items()), q.data_ptr(), kvs[0][0].data_ptr(), len(kvs),
+        # the same launch on the same data: variants with equal keys pool their timings (pack_gqa only
+        # names the packing a tile width comes from, so plans that differ in it alone are one launch)
+        self.key = (launch_key(self.plan), q.data_ptr(), kvs[0][0].data_ptr(), len(kvs),
                     None if cu is None else cu.data_ptr())
 
         def call(i):
