@@ -918,7 +918,11 @@ def occupancy_summary(d: str) -> None:
              "longest case. For kernels of a few microseconds the GPU-active window also spans the dispatch, "
              "so the first figure reads low. MeanOccupancyPerActiveCU is the profiler's derived metric. "
              "Occupancy = 4 x SQ_WAVE_CYCLES / (GPU-active cycles x 256 CUs x 32 waves), the profiler's "
-             "OccupancyPercent.", "",
+             "OccupancyPercent. The busy count follows the SIMDs of a CU that hold a wave: the high-load "
+             "heuristic runs one workgroup of two waves per CU (every CU busy, two of its four SIMDs), so it "
+             "reads about half the CUs. Kernel times under counter collection vary from box to box for the "
+             "short launches (the L_K=8192 heuristic case took 8.8 us in an earlier take on another box); the "
+             "benchmark's graph-replay times are the reference.", "",
              "| case | workgroups | waves | kernel us | GPU-active cycles | busy CUs (GPU-active) | busy CUs "
              "(kernel time) | MeanOccupancyPerActiveCU | occupancy |",
              "|---|---|---|---|---|---|---|---|---|"]
