@@ -102,6 +102,11 @@ def parse():
                          "on mixed-length batches and write the results to OUT_JSON")
     ap.add_argument("--schedule-sweep-summary", metavar="IN_JSON", default=None,
                     help="summarise a --schedule-sweep result into profiles/schedule_mixed_length_batches.md")
+    ap.add_argument("--waves-sweep", metavar="OUT_JSON", default=None,
+                    help="time one-split launches of two waves per workgroup against four on shapes of 192-576 "
+                         "workgroups (the planner's own wave count and the other one) and write OUT_JSON")
+    ap.add_argument("--waves-sweep-summary", metavar="IN_JSON", default=None,
+                    help="summarise a --waves-sweep result into profiles/two_waves_vs_four_waves.md")
     ap.add_argument("--calibrate", metavar="OUT_JSON", default=None,
                     help="time every launch the planner can choose (split count, tile width, V slices, merge) over "
                          "the calibration shapes, each output checked against the oracle, and write the sweep that "
@@ -1149,6 +1154,111 @@ def regression_summary(path: str) -> None:
     print(f"wrote {PROFILE_REGRESSION}")
 
 
+# ---------------------------------------------------------------- two waves against four
+
+PROFILE_WAVES = os.path.join(ROOT, "profiles", "two_waves_vs_four_waves.md")
+# (B, H_Q, H_KV, L_K), all planned unsplit with one V slice and one workgroup reading each key: 192-256
+# workgroups (one per CU), 264-320 (the two-wave rule's upper range) and 384-576 (past it, four waves)
+WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8, 1, 4096),
+                (33, 64, 8, 1024), (36, 64, 8, 1024), (40, 64, 8, 512), (39, 64, 8, 2048), (40, 64, 8, 2048),
+                (300, 8, 1, 512), (300, 8, 1, 1024), (300, 16, 1, 2048), (80, 32, 4, 2048), (80, 64, 4, 1024),
+                (17, 128, 16, 512), (20, 128, 16, 1024),
+                (48, 64, 8, 1024), (56, 64, 8, 1024), (64, 64, 8, 1024), (72, 64, 8, 1024), (384, 8, 1, 1024),
+                (448, 8, 1, 1024))
+
+
+def wave_forms(da, plan, H_KV):
+    """(two-wave, four-wave) forms of a one-split plan, one of them the plan
+    itself: four waves fetch straight into LDS with one workgroup per CU and
+    through registers into LDS where CUs hold more (chunks of >= 512 keys);
+    two waves fetch through registers, K straight into the operand layout
+    where key rows hold one KV head and each CU holds one workgroup."""
+    other = da.DaPlan.from_buffer_copy(plan)
+    lone = plan.grid <= plan.num_cus
+    if plan.group_waves == 2:
+        other.group_waves, other.kv_fetch = 4, 2 if lone else 1
+        return plan, other
+    other.group_waves, other.combine = 2, 0
+    other.kv_fetch = 0 if H_KV == 1 and lone else 1
+    return other, plan
+
+
+def waves_sweep_run(args, da, torch, np) -> None:
+    """Each shape of WAVES_SHAPES launched with two and with four waves per
+    workgroup (the planner's plan and its other wave count, same split,
+    tile and merge), each output checked against the oracle on the first
+    and last sequence, then timed as graph-replayed calls interleaved over
+    rounds."""
+    rows = []
+    gen = torch.Generator(device="cuda")
+    for B, H_Q, H_KV, L in WAVES_SHAPES:
+        gen.manual_seed(B * 100000 + H_KV * 10000 + L)
+        q = torch.randn((B, H_Q, 128), generator=gen, device="cuda").to(torch.bfloat16)
+        k = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
+        v = torch.randn((B, L, H_KV, 128), generator=gen, device="cuda").to(torch.bfloat16)
+        plan = da.da_choose_splits(B, H_Q, H_KV, L)
+        if plan.num_splits != 1 or plan.v_slices != 1 or plan.heads_per_tile != H_Q // H_KV:
+            log(f"waves sweep: B={B} H_Q={H_Q} H_KV={H_KV} L_K={L} planned {plan_brief(plan)}; skipped")
+            continue
+        two, four = wave_forms(da, plan, H_KV)
+        est_us = 5.0 + 2.0 * B * L * H_KV * 256 / 5e6
+        K = int(max(10, min(100, 2000.0 / est_us)))
+        vs = [Variant("two", da, torch, q, k, v, L, 0, -1, K, plan=two),
+              Variant("four", da, torch, q, k, v, L, 0, -1, K, plan=four)]
+        validate(torch, OracleRows(np, torch, q, k, v, [0, B - 1]), vs, f"waves B={B} H_Q={H_Q} H_KV={H_KV} L_K={L}")
+        interleave(torch, vs, args.rounds)
+        iqr = lambda x: [round(t, 3) for t in np.percentile(x.times, [25, 75])]
+        row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L, "grid": plan.grid, "cus": plan.num_cus,
+               "planned_waves": plan.group_waves, "two_fetch": two.kv_fetch, "four_fetch": four.kv_fetch,
+               "two_us": round(vs[0].median, 3), "two_iqr": iqr(vs[0]),
+               "four_us": round(vs[1].median, 3), "four_iqr": iqr(vs[1]),
+               "two_over_four": round(vs[0].median / vs[1].median, 4)}
+        rows.append(row)
+        log(f"waves B={B} H_Q={H_Q} H_KV={H_KV} L_K={L} grid {plan.grid}: two {row['two_us']} four "
+            f"{row['four_us']} ({row['two_over_four']})")
+        del q, k, v, vs
+        torch.cuda.empty_cache()
+    json.dump({"rows": rows, "validated": VALIDATION["validated"], "invalid": VALIDATION["invalid"],
+               "kernel_source_sha256": kernel_source_sha(), "rounds": args.rounds},
+              open(args.waves_sweep, "w"), indent=1)
+    print(json.dumps({"waves_shapes": len(rows), "validated": VALIDATION["validated"],
+                      "invalid": len(VALIDATION["invalid"])}), flush=True)
+    if VALIDATION["invalid"]:
+        sys.exit(3)
+
+
+def waves_sweep_summary(path: str) -> None:
+    d = json.load(open(path))
+    rows = d["rows"]
+    fetch = {0: "operand layout", 1: "registers to LDS", 2: "direct to LDS"}
+    lines = ["# Two waves per workgroup against four, one-split launches of 192-576 workgroups", "",
+             "Each shape launched with the planner's wave count and with the other one (same split, tile and merge; "
+             "the fetch path each wave count takes there), every output checked against the oracle on the first "
+             f"and last sequence ({d['validated']} launches validated, {len(d['invalid'])} invalid), then timed as "
+             f"graph-replayed calls interleaved over {d['rounds']} rounds: median us per call (IQR).", "",
+             "Command (MI355X, one GPU):", "", "```",
+             "cd $REPO && python3 bench.py --waves-sweep $OUT/waves.json --rounds %d" % d["rounds"],
+             "python3 bench.py --waves-sweep-summary $OUT/waves.json", "```", "",
+             "| B | H_Q | H_KV | L_K | workgroups / CUs | planned | two waves us (fetch) | four waves us (fetch) | "
+             "two / four |", "|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        ti, fi = r["two_iqr"], r["four_iqr"]
+        lines.append(f"| {r['B']} | {r['H_Q']} | {r['H_KV']} | {r['L_K']} | {r['grid']} / {r['cus']} | "
+                     f"{r['planned_waves']} | {r['two_us']} ({ti[0]}-{ti[1]}, {fetch[r['two_fetch']]}) | "
+                     f"{r['four_us']} ({fi[0]}-{fi[1]}, {fetch[r['four_fetch']]}) | {r['two_over_four']:.3f} |")
+    by = lambda lo, hi: [r["two_over_four"] for r in rows if lo < r["grid"] / r["cus"] <= hi]
+    lines += [""]
+    for name, lo, hi in (("up to one workgroup per CU", 0, 1.0), ("up to 5/4 (the two-wave rule)", 1.0, 1.25),
+                         ("past 5/4", 1.25, 99)):
+        x = by(lo, hi)
+        if x:
+            lines.append(f"* {name}: two / four {min(x):.3f}-{max(x):.3f} over {len(x)} shapes.")
+    planned_right = sum((r["two_over_four"] < 1) == (r["planned_waves"] == 2) for r in rows)
+    lines.append(f"* The planner's wave count is the faster one on {planned_right} of {len(rows)} shapes.")
+    open(PROFILE_WAVES, "w").write("\n".join(lines) + "\n")
+    print(f"wrote {PROFILE_WAVES}")
+
+
 # ---------------------------------------------------------------- validation
 
 class OracleRows:
@@ -1322,6 +1432,9 @@ def main():
     if args.schedule_sweep_summary:
         schedule_sweep_summary(args.schedule_sweep_summary)
         return
+    if args.waves_sweep_summary:
+        waves_sweep_summary(args.waves_sweep_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the decode kernel shards by "
               f"(sequence, KV head) with no exchange, so no multi-GPU figure is produced.", file=sys.stderr)
@@ -1349,6 +1462,9 @@ def main():
         return
     if args.calibrate:
         calibrate_run(args, da, torch, np)
+        return
+    if args.waves_sweep:
+        waves_sweep_run(args, da, torch, np)
         return
 
     # ---------------- headline: the high-load shape (B=32, H_Q=64, H_KV=8, L_K=8192, 1 GiB of K/V)
@@ -1521,8 +1637,9 @@ def with_combine(da, plan, combine):
     p = da.DaPlan.from_buffer_copy(plan)
     p.combine = combine if p.num_splits > 1 else 0
     if p.combine == 1 and p.group_waves == 2:
-        # the in-launch merge runs in four-wave launches: one workgroup per CU, K/V straight into LDS
-        p.group_waves, p.kv_fetch = 4, 2
+        # the in-launch merge runs in four-wave launches: K/V straight into LDS with one workgroup per CU,
+        # through registers into LDS where some CUs hold two (two-wave chunks hold at least 512 keys)
+        p.group_waves, p.kv_fetch = 4, 2 if p.grid <= p.num_cus else 1
     return p
 
 

@@ -199,24 +199,29 @@ static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
 }
 
 int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int combine) {
-  // Four wave64s, one per SIMD, by default.  Where the launch fills at
-  // least three quarters of the CUs with one workgroup each, every key row
-  // is read by one workgroup and the chunks hold at least 512 keys, two
-  // waves, each walking half the chunk with one tile in flight through
-  // registers, read HBM faster than four waves with two direct-to-LDS
-  // stages each: the chip then keeps about a quarter of the loads in flight
-  // (8 instead of 32 MiB), and HBM serves the smaller set of streams closer
-  // to its peak.  Measured on MI355X in one process per comparison: 1 GiB
-  // of K/V at one split 1.8-6.2% faster (B=32, H_Q=64, H_KV=8, L_K=8192:
-  // 157.9 -> 151.7 us), 1.9-8.3% at 128-512 MiB, 4.2% and 7.4% with 192
-  // and 224 of 256 CUs busy, 2.5-8.4% at 2-4 splits merged by a second
-  // launch; neutral at 512 keys per chunk; slower below that (0.84-0.91x at
-  // 128-256 keys), with 160 or 128 of 256 CUs busy (0.98x, 0.95x) and where
-  // two workgroups share each key (16-head tiles of a 32-head group: 0.91x).
-  // The in-launch merge is sized for four waves, so two-wave plans merge by
-  // a second launch.  Eight waves (two per SIMD, with K staged) measured
-  // slower at chunks of a few hundred keys.
-  return vs == 1 && readers == 1 && combine == 0 && grid <= cus && 4 * grid >= 3 * (int64_t)cus && chunk >= 512
+  // Four wave64s, one per SIMD, by default.  Where the launch puts one
+  // workgroup on at least three quarters of the CUs and two on at most a
+  // quarter of them, every key row is read by one workgroup and the chunks
+  // hold at least 512 keys, two waves, each walking half the chunk with one
+  // tile in flight through registers, read HBM faster than four waves with
+  // two direct-to-LDS stages each: the chip then keeps about a quarter of
+  // the loads in flight (8 instead of 32 MiB), and HBM serves the smaller
+  // set of streams closer to its peak.  Measured on MI355X in one process
+  // per comparison: 1 GiB of K/V at one split 1.8-6.2% faster (B=32,
+  // H_Q=64, H_KV=8, L_K=8192: 157.9 -> 151.7 us), 1.9-8.3% at 128-512 MiB,
+  // 4.2% and 7.4% with 192 and 224 of 256 CUs busy, 2.5-8.4% at 2-4 splits
+  // merged by a second launch; neutral at 512 keys per chunk; slower below
+  // that (0.84-0.91x at 128-256 keys), with 160 or 128 of 256 CUs busy
+  // (0.98x, 0.95x) and where two workgroups share each key (16-head tiles
+  // of a 32-head group: 0.91x).  Past one workgroup per CU (against four
+  // waves fetching through LDS): 264-320 workgroups on 256 CUs 0.5-3%
+  // faster with 8 KV heads and 3-9% with one, 384-512 within 1% with 8 KV
+  // heads (0.97-1.0x with one), 576 slower (1.02-1.03x).  The in-launch
+  // merge is sized for four waves, so two-wave plans merge by a second
+  // launch.  Eight waves (two per SIMD, with K staged) measured slower at
+  // chunks of a few hundred keys.
+  return vs == 1 && readers == 1 && combine == 0 && 4 * grid <= 5 * (int64_t)cus && 4 * grid >= 3 * (int64_t)cus &&
+                 chunk >= 512
              ? 2
              : 4;
 }
@@ -413,9 +418,10 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     }
     out->group_waves = waves;
     // two waves: K through registers, straight into the operand layout
-    // where key rows hold one KV head (contiguous 256-byte rows, measured
-    // 1-3% faster there) and through LDS otherwise
-    out->kv_fetch = out->group_waves == 2 ? (H_KV == 1 ? 0 : 1)
+    // where key rows hold one KV head and each CU holds one workgroup
+    // (contiguous 256-byte rows, measured 1-3% faster there) and through LDS
+    // otherwise (with one KV head on 300 workgroups: 5% faster)
+    out->kv_fetch = out->group_waves == 2 ? (H_KV == 1 && out->grid <= cus ? 0 : 1)
                                           : kv_fetch(out->grid, cus, ((chunk + 3) / 4 + 31) / 32);
   }
   out->kv_nontemporal = streamed ? (readers == 1 ? 1 : 0) : kv_nontemporal((double)B * L_K_max * H_KV, readers);

@@ -233,9 +233,12 @@ def test_fetch_mode_follows_workgroups_per_cu():
     # (the paper's packing, pack_gqa = 2, so that no V slices multiply the grid)
     # direct-to-LDS with two tiles in flight when every workgroup has a CU to
     # itself; K and V through registers into LDS (two workgroups per CU) otherwise
-    for s, fetch in [(1, 2), (4, 2), (5, 1), (16, 1), (64, 0)]:
+    for s, fetch in [(1, 2), (4, 2), (6, 1), (16, 1), (64, 0)]:
         p = da.da_make_plan(8, 64, 8, 4096, num_splits=s, pack_gqa=2, num_cus=256)   # 64 tiles
         assert p.grid == 64 * s and p.kv_fetch == fetch and p.group_waves == 4, (s, p.as_dict())
+    # 320 workgroups over chunks of 820 keys: two waves, K and V through registers into LDS
+    p = da.da_make_plan(8, 64, 8, 4096, num_splits=5, pack_gqa=2, num_cus=256)
+    assert (p.grid, p.kv_fetch, p.group_waves, p.combine) == (320, 1, 2, 0), p.as_dict()
     p = da.da_make_plan(8, 64, 8, 4096, num_splits=4, pack_gqa=2, num_cus=256, cu_margin=1)
     assert p.kv_fetch == 1
     # one 32-key tile per wave (chunks of at most 128 keys): the operand-layout fetch
@@ -365,8 +368,8 @@ def test_planned_entry_checks_the_plan():
 
 def test_two_waves_where_long_chunks_fill_the_chip():
     """Four waves per workgroup, or two (K/V through registers, no in-launch
-    merge) where the launch fills at least 3/4 of the CUs with one workgroup
-    each, one workgroup reads each key and chunks hold at least 512 keys."""
+    merge) where the launch has 3/4 to 5/4 as many workgroups as CUs, one
+    workgroup reads each key and chunks hold at least 512 keys."""
     def plan(*shape, **kw):
         return da.da_choose_splits(*shape, num_cus=256, **kw)
     p = plan(32, 64, 8, 8192)                      # the 1 GiB high-load call
@@ -377,7 +380,14 @@ def test_two_waves_where_long_chunks_fill_the_chip():
     assert plan(8, 256, 32, 512).group_waves == 2  # chunks of 512 keys
     assert plan(8, 256, 32, 256).group_waves == 4  # 256
     assert plan(1, 64, 8, 512).group_waves == 4    # 32 workgroups with V slices
-    assert plan(32, 64, 8, 8192, cu_margin=64).group_waves == 4   # more workgroups than the 192 CUs
+    assert plan(32, 64, 8, 8192, cu_margin=64).group_waves == 4   # 256 workgroups on 192 CUs
+    # past one workgroup per CU, up to 5/4 of them: K/V through LDS, also with one KV head
+    for shape in ((40, 64, 8, 1024), (300, 8, 1, 1024)):
+        p = plan(*shape)
+        assert (p.grid, p.group_waves, p.kv_fetch) == (shape[0] * shape[2], 2, 1), (shape, p.as_dict())
+    assert plan(34, 64, 8, 1024, cu_margin=32).group_waves == 2   # 272 workgroups on 224 CUs
+    assert plan(36, 64, 8, 1024, cu_margin=32).group_waves == 4   # 288 on 224
+    assert plan(48, 64, 8, 1024).group_waves == 4                 # 384 on 256
     # two 16-head workgroups read each key of a group of 32
     p = da.da_make_plan(32, 128, 4, 8192, num_splits=1, pack_gqa=1, num_cus=256)
     assert p.heads_per_tile == 16 and p.group_waves == 4

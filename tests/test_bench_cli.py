@@ -1,5 +1,6 @@
 """The benchmark's command-line contract that holds without a GPU: one GPU
-only, and the oracle's CPU baseline record."""
+only, the oracle's CPU baseline record, the validation of timed launches and
+the host side of the measurement helpers."""
 
 import os
 import subprocess
@@ -101,3 +102,44 @@ def test_read_probe_library_checks_its_arguments():
     assert g(p, 1 << 20, p, 1 << 20, 3, 8, 0, None) == 1                   # regions do not divide the buffer
     assert g(p, 1 << 20, p, 256 * 256 * 4 - 4, 256, 8, 0, None) == 1       # sink too small
     assert g(p, 1 << 20, p, 1 << 20, 256, 4, 0, None) == 1                 # loads not 8 or 16
+
+
+def test_wave_forms_pair_each_plan_with_its_other_wave_count():
+    """The wave-count sweep launches every shape with two and with four waves
+    per workgroup: the planner's plan and a valid plan of the other count
+    (same split, tile and merge), with the fetch path that count takes."""
+    sys.path.insert(0, ROOT)
+    import bench
+    import paper_2604_00028_amd as da
+    for B, H_Q, H_KV, L in bench.WAVES_SHAPES:
+        plan = da.da_choose_splits(B, H_Q, H_KV, L, num_cus=256)
+        assert plan.num_splits == 1 and plan.v_slices == 1 and plan.heads_per_tile == H_Q // H_KV
+        two, four = bench.wave_forms(da, plan, H_KV)
+        assert (two.group_waves, four.group_waves) == (2, 4)
+        assert plan.group_waves == 2 and two is plan or plan.group_waves == 4 and four is plan
+        lone = plan.grid <= 256
+        assert two.combine == 0 and two.kv_fetch == (0 if H_KV == 1 and lone else 1)
+        assert four.kv_fetch == (2 if lone else 1)
+        for p in (two, four):
+            assert (p.num_splits, p.grid, p.heads_per_tile, p.v_slices) == (1, plan.grid, plan.heads_per_tile, 1)
+
+
+def test_waves_sweep_summary(tmp_path, monkeypatch):
+    sys.path.insert(0, ROOT)
+    import json
+    import bench
+    row = lambda grid, planned, ratio: {"B": grid // 8, "H_Q": 64, "H_KV": 8, "L_K": 1024, "grid": grid,
+                                        "cus": 256, "planned_waves": planned, "two_fetch": 1, "four_fetch": 1,
+                                        "two_us": 10 * ratio, "two_iqr": [9.9, 10.1], "four_us": 10.0,
+                                        "four_iqr": [9.9, 10.1], "two_over_four": ratio}
+    src = tmp_path / "waves.json"
+    src.write_text(json.dumps({"rows": [row(256, 2, 0.96), row(320, 2, 0.99), row(512, 4, 1.01), row(576, 4, 0.995)],
+                               "validated": 8, "invalid": [], "rounds": 7}))
+    out = tmp_path / "waves.md"
+    monkeypatch.setattr(bench, "PROFILE_WAVES", str(out))
+    bench.waves_sweep_summary(str(src))
+    text = out.read_text()
+    assert "python3 bench.py --waves-sweep $OUT/waves.json --rounds 7" in text
+    assert "| 40 | 64 | 8 | 1024 | 320 / 256 | 2 | 9.9 (9.9-10.1, registers to LDS) |" in text
+    assert "up to 5/4 (the two-wave rule): two / four 0.990-0.990 over 1 shapes" in text
+    assert "faster one on 3 of 4 shapes" in text

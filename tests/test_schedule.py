@@ -134,9 +134,10 @@ def test_equal_lengths_match_the_uniform_plan():
             if plan.v_slices > 1:
                 plan = da.da_make_plan(B, H_Q, H_KV, L, num_splits=0, pack_gqa=2, num_cus=CUS)
             assert set(seqs[:, 1]) == {plan.num_splits}, (B, H_Q, H_KV, L)
-            # schedules keep four waves per workgroup; where the plan takes two (a full chip of long
-            # chunks), the four-wave launch of one workgroup per CU fetches straight into LDS
-            fetch = plan.kv_fetch if plan.group_waves == 4 else 2
+            # schedules keep four waves per workgroup; where the plan takes two (about a chip of long
+            # chunks), the four-wave launch fetches straight into LDS with one workgroup per CU and
+            # through registers where some CUs hold two
+            fetch = plan.kv_fetch if plan.group_waves == 4 else (2 if plan.grid <= CUS else 1)
             assert sched.num_items == plan.grid and sched.kv_fetch == fetch, (B, H_Q, H_KV, L)
 
 
