@@ -109,7 +109,8 @@ typedef struct da_plan {
                              v_slices * 8 * ceil(tiles * num_splits / 8) (a chunk's slices share an
                              XCD; the workgroups past the last chunk return at once) */
   int32_t num_cus;        /* compute units the plan was made for (after cu_margin) */
-  int32_t group_waves;    /* wave64s per workgroup, each taking a contiguous part of the chunk: 4, or 2
+  int32_t group_waves;    /* wave64s per workgroup, each taking a contiguous part of the chunk (with 2
+                             waves and H_KV <= 4, every other 32-key tile of it): 4, or 2
                              where the launch has between 3/4 and 5/4 as many workgroups as CUs,
                              one workgroup reads each key and chunks hold >= 512 keys (fewer loads
                              in flight read HBM faster there); with 2, kv_fetch is 0 or 1, v_slices

@@ -202,7 +202,8 @@ int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int c
   // Four wave64s, one per SIMD, by default.  Where the launch puts one
   // workgroup on at least three quarters of the CUs and two on at most a
   // quarter of them, every key row is read by one workgroup and the chunks
-  // hold at least 512 keys, two waves, each walking half the chunk with one
+  // hold at least 512 keys, two waves, each walking half the chunk (every
+  // other 32-key tile of it where key rows hold at most 4 KV heads) with one
   // tile in flight through registers, read HBM faster than four waves with
   // two direct-to-LDS stages each: the chip then keeps about a quarter of
   // the loads in flight (8 instead of 32 MiB), and HBM serves the smaller

@@ -34,6 +34,7 @@ def same_bits(a, b):
     (2, 128, 2, 300, False),    # a group of 64
     (4, 32, 4, 200, True),      # varlen GQA
     (5, 8, 1, 2049, False),     # ragged tail
+    (2, 16, 2, 45, False),      # chunks shorter than a tile per wave (two waves: the second may have none)
 ])
 def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
     """Plans from each policy, with and without a CU margin and with every
