@@ -1158,13 +1158,16 @@ def regression_summary(path: str) -> None:
 
 PROFILE_WAVES = os.path.join(ROOT, "profiles", "two_waves_vs_four_waves.md")
 # (B, H_Q, H_KV, L_K), all planned unsplit with one V slice and one workgroup reading each key: 192-256
-# workgroups (one per CU), 264-320 (the two-wave rule's upper range) and 384-576 (past it, four waves)
+# workgroups (one per CU), 264-320 (the two-wave rule's upper range), 384-576 with 2-8 KV heads (past it,
+# four waves) and pure MQA at 384-768 (two waves over chunks of >= 1024 keys, four over 512)
 WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8, 1, 4096),
                 (33, 64, 8, 1024), (36, 64, 8, 1024), (40, 64, 8, 512), (39, 64, 8, 2048), (40, 64, 8, 2048),
                 (300, 8, 1, 512), (300, 8, 1, 1024), (300, 16, 1, 2048), (80, 32, 4, 2048), (80, 64, 4, 1024),
                 (17, 128, 16, 512), (20, 128, 16, 1024),
-                (48, 64, 8, 1024), (56, 64, 8, 1024), (64, 64, 8, 1024), (72, 64, 8, 1024), (384, 8, 1, 1024),
-                (448, 8, 1, 1024))
+                (48, 64, 8, 1024), (56, 64, 8, 1024), (64, 64, 8, 1024), (72, 64, 8, 1024), (192, 16, 2, 1024),
+                (96, 32, 4, 4096),
+                (384, 8, 1, 1024), (448, 8, 1, 1024), (512, 16, 1, 4096), (640, 8, 1, 1024), (768, 32, 1, 2048),
+                (640, 8, 1, 512))
 
 
 def wave_forms(da, plan, H_KV):
@@ -1246,11 +1249,12 @@ def waves_sweep_summary(path: str) -> None:
         lines.append(f"| {r['B']} | {r['H_Q']} | {r['H_KV']} | {r['L_K']} | {r['grid']} / {r['cus']} | "
                      f"{r['planned_waves']} | {r['two_us']} ({ti[0]}-{ti[1]}, {fetch[r['two_fetch']]}) | "
                      f"{r['four_us']} ({fi[0]}-{fi[1]}, {fetch[r['four_fetch']]}) | {r['two_over_four']:.3f} |")
-    by = lambda lo, hi: [r["two_over_four"] for r in rows if lo < r["grid"] / r["cus"] <= hi]
     lines += [""]
-    for name, lo, hi in (("up to one workgroup per CU", 0, 1.0), ("up to 5/4 (the two-wave rule)", 1.0, 1.25),
-                         ("past 5/4", 1.25, 99)):
-        x = by(lo, hi)
+    for name, lo, hi, mqa in (("up to one workgroup per CU", 0, 1.0, None),
+                              ("up to 5/4 (the two-wave rule)", 1.0, 1.25, None),
+                              ("past 5/4, 2-16 KV heads", 1.25, 99, False), ("past 5/4, pure MQA", 1.25, 99, True)):
+        x = [r["two_over_four"] for r in rows if lo < r["grid"] / r["cus"] <= hi and
+             (mqa is None or (r["H_KV"] == 1) == mqa)]
         if x:
             lines.append(f"* {name}: two / four {min(x):.3f}-{max(x):.3f} over {len(x)} shapes.")
     planned_right = sum((r["two_over_four"] < 1) == (r["planned_waves"] == 2) for r in rows)

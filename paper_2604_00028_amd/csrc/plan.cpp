@@ -198,7 +198,7 @@ static int paper_splits(int B, int H_KV, int L_K, int H_Q, int hpt, int cus) {
   return mi355x_splits(mi355x_model(), B, H_Q, H_KV, L_K, hpt, cus);
 }
 
-int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int combine) {
+int group_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int vs, int combine) {
   // Four wave64s, one per SIMD, by default.  Where the launch puts one
   // workgroup on at least three quarters of the CUs and two on at most a
   // quarter of them, every key row is read by one workgroup and the chunks
@@ -217,12 +217,16 @@ int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int c
   // of a 32-head group: 0.91x).  Past one workgroup per CU (against four
   // waves fetching through LDS): 264-320 workgroups on 256 CUs 0.5-3%
   // faster with 8 KV heads and 3-9% with one, 384-512 within 1% with 8 KV
-  // heads (0.97-1.0x with one), 576 slower (1.02-1.03x).  The in-launch
-  // merge is sized for four waves, so two-wave plans merge by a second
-  // launch.  Eight waves (two per SIMD, with K staged) measured slower at
-  // chunks of a few hundred keys.
-  return vs == 1 && readers == 1 && combine == 0 && 4 * grid <= 5 * (int64_t)cus && 4 * grid >= 3 * (int64_t)cus &&
-                 chunk >= 512
+  // heads (0.97-1.0x with one), 576 slower (1.02-1.03x).  Pure MQA (key
+  // rows of one head, whose two waves take alternate tiles) keeps the gain
+  // further: at 384-768 workgroups with chunks of 1024-8192 keys 0.94-1.0x
+  // (2.6% on average over 21 shapes), while at 512-key chunks (0.997-1.026x)
+  // and at 1024-1536 workgroups (0.92-1.09x) it is no longer steady.  The
+  // in-launch merge is sized for four waves, so two-wave plans merge by a
+  // second launch.  Eight waves (two per SIMD, with K staged) measured
+  // slower at chunks of a few hundred keys.
+  const int64_t top = H_KV == 1 && chunk >= 1024 ? 3 * (int64_t)cus : 5 * (int64_t)cus / 4;
+  return vs == 1 && readers == 1 && combine == 0 && grid <= top && 4 * grid >= 3 * (int64_t)cus && chunk >= 512
              ? 2
              : 4;
 }
@@ -399,8 +403,8 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   const int readers = (g / hpt) * vs;
   {
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
-    int waves = group_waves(out->grid, cus, chunk, readers, vs, comb);
-    if (waves == 4 && comb == 1 && !from_table && group_waves(out->grid, cus, chunk, readers, vs, 0) == 2) {
+    int waves = group_waves(out->grid, cus, chunk, H_KV, readers, vs, comb);
+    if (waves == 4 && comb == 1 && !from_table && group_waves(out->grid, cus, chunk, H_KV, readers, vs, 0) == 2) {
       // Two waves merge by a second launch.  They take it where the share of
       // the split launch they save (kTwoWaveGain) is modelled to outweigh
       // what the second launch adds over the merge inside the launch:

@@ -99,9 +99,10 @@ inline int64_t launch_grid(int64_t chunks, int vs) {
 }
 
 // Waves per workgroup (da_plan.group_waves) for a launch of `grid`
-// workgroups on `cus` CUs over chunks of `chunk` keys, each key row read by
-// `readers` workgroups, with vs V slices and merge `combine`: 2 or 4.
-int group_waves(int64_t grid, int cus, int64_t chunk, int readers, int vs, int combine);
+// workgroups on `cus` CUs over chunks of `chunk` keys of rows holding H_KV
+// heads, each key row read by `readers` workgroups, with vs V slices and
+// merge `combine`: 2 or 4.
+int group_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int vs, int combine);
 
 // A plan made inside an entry point whose sequence lengths are read on the
 // device (cu_seqlens_k, paged seq_lens): the sequences may be far shorter

@@ -388,6 +388,12 @@ def test_two_waves_where_long_chunks_fill_the_chip():
     assert plan(34, 64, 8, 1024, cu_margin=32).group_waves == 2   # 272 workgroups on 224 CUs
     assert plan(36, 64, 8, 1024, cu_margin=32).group_waves == 4   # 288 on 224
     assert plan(48, 64, 8, 1024).group_waves == 4                 # 384 on 256
+    # pure MQA over chunks of >= 1024 keys: up to three workgroups per CU
+    for B, L, waves in ((384, 1024, 2), (768, 2048, 2), (769, 2048, 4), (640, 512, 4), (1024, 2048, 4)):
+        p = plan(B, 8, 1, L)
+        assert (p.num_splits, p.grid, p.group_waves) == (1, B, waves), (B, L, p.as_dict())
+        assert p.kv_fetch == (1 if waves == 2 else p.kv_fetch)
+    assert plan(192, 16, 2, 1024).group_waves == 4                # 2 KV heads: 384 on 256
     # two 16-head workgroups read each key of a group of 32
     p = da.da_make_plan(32, 128, 4, 8192, num_splits=1, pack_gqa=1, num_cus=256)
     assert p.heads_per_tile == 16 and p.group_waves == 4

@@ -142,4 +142,5 @@ def test_waves_sweep_summary(tmp_path, monkeypatch):
     assert "python3 bench.py --waves-sweep $OUT/waves.json --rounds 7" in text
     assert "| 40 | 64 | 8 | 1024 | 320 / 256 | 2 | 9.9 (9.9-10.1, registers to LDS) |" in text
     assert "up to 5/4 (the two-wave rule): two / four 0.990-0.990 over 1 shapes" in text
+    assert "past 5/4, 2-16 KV heads: two / four 0.995-1.010 over 2 shapes" in text
     assert "faster one on 3 of 4 shapes" in text

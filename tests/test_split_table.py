@@ -70,9 +70,11 @@ def test_swept_shapes_are_planned_from_the_table(which):
         chunk = -(-L // s)
         tpw = -(-(-(-chunk // 4)) // 32)
         readers = (H_Q // H_KV // hpt) * vs
-        # two waves where the launch has 3/4 to 5/4 as many workgroups as CUs, one workgroup reads each
-        # key, chunks hold >= 512 keys and no merge runs in the launch; the sweep timed four waves
-        two = vs == 1 and readers == 1 and comb == 0 and 192 <= p.grid <= 320 and chunk >= 512
+        # two waves where the launch has 3/4 to 5/4 as many workgroups as CUs (3 times as many for pure
+        # MQA over chunks of >= 1024 keys), one workgroup reads each key, chunks hold >= 512 keys and no
+        # merge runs in the launch; the sweep timed four waves
+        top = 768 if H_KV == 1 and chunk >= 1024 else 320
+        two = vs == 1 and readers == 1 and comb == 0 and 192 <= p.grid <= top and chunk >= 512
         assert p.group_waves == (2 if two else 4), sh
         fetch = (0 if H_KV == 1 and p.grid <= 256 else 1) if two else (2 if p.grid <= 256 else (1 if tpw >= 2 else 0))
         assert p.kv_fetch == fetch, sh
