@@ -120,9 +120,11 @@ typedef struct da_plan {
                              their sequences may be far shorter than L_K_max. */
   int32_t kv_fetch;       /* how K/V tiles reach the matrix cores: 0 K straight into the operand
                              layout, V through registers to LDS (chunks of one 32-key tile per
-                             wave); 1 both row-contiguous into registers, then through LDS (several
-                             workgroups per CU); 2 both row-contiguous straight into LDS, two tiles
-                             in flight per wave (at most one workgroup per CU) */
+                             wave, or two waves over rows of one KV head with at most one workgroup
+                             per CU); 1 both row-contiguous into registers, then through LDS
+                             (several workgroups per CU, or two waves); 2 both row-contiguous
+                             straight into LDS, two tiles in flight per wave (four waves, at most
+                             one workgroup per CU) */
   int32_t kv_nontemporal; /* 1: K/V loads carry the nontemporal (streaming) cache hint, chosen when
                              one call's K/V exceed DA_RESIDENT_BYTES and cannot stay in L2 and the
                              MALL between calls, and one workgroup reads each key (heads_per_tile

@@ -13,9 +13,9 @@
 // 3.1 and 5.3).
 //
 // gfx950 mapping:
-//  * W wave64s per workgroup: 4, one per SIMD, or 2 where one workgroup per
-//    CU streams long chunks over most of the chip (fewer loads in flight
-//    read HBM faster there).  The chunk is cut into W contiguous key
+//  * W wave64s per workgroup: 4, one per SIMD, or 2 where about one
+//    workgroup per CU (up to three for pure MQA) streams long chunks over
+//    most of the chip (fewer loads in flight read HBM faster there).  The chunk is cut into W contiguous key
 //    ranges, one per wave, or, with two waves over key rows of at most
 //    1 KiB (H_KV <= 4), its 32-key tiles alternate between the waves; each
 //    wave walks its tiles in key order, and the W wave states are merged
