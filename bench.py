@@ -103,7 +103,7 @@ def parse():
     ap.add_argument("--schedule-sweep-summary", metavar="IN_JSON", default=None,
                     help="summarise a --schedule-sweep result into profiles/schedule_mixed_length_batches.md")
     ap.add_argument("--waves-sweep", metavar="OUT_JSON", default=None,
-                    help="time one-split launches of two waves per workgroup against four on shapes of 192-576 "
+                    help="time one-split launches of two waves per workgroup against four on shapes of 192-1024 "
                          "workgroups (the planner's own wave count and the other one) and write OUT_JSON")
     ap.add_argument("--waves-sweep-summary", metavar="IN_JSON", default=None,
                     help="summarise a --waves-sweep result into profiles/two_waves_vs_four_waves.md")
@@ -327,11 +327,13 @@ def launch_key(p) -> tuple:
 
 
 def plan_brief(p) -> str:
-    """s, heads per tile, V slices, merge and (when not four) waves per
-    workgroup of a plan, e.g. 's4 h8 v4 fused' or 's1 h8 v1 w2'."""
+    """s, heads per tile, V slices, merge, (when not four) waves per
+    workgroup and (when held to one) workgroups per CU of a plan, e.g.
+    's4 h8 v4 fused', 's1 h8 v1 w2' or 's1 h8 v1 w2 1/cu'."""
     merge = "" if p.num_splits == 1 else (" fused" if p.combine else " 2-launch")
     waves = "" if p.group_waves == 4 else f" w{p.group_waves}"
-    return f"s{p.num_splits} h{p.heads_per_tile} v{p.v_slices}{merge}{waves}"
+    per_cu = " 1/cu" if getattr(p, "wg_per_cu", 0) == 1 else ""
+    return f"s{p.num_splits} h{p.heads_per_tile} v{p.v_slices}{merge}{waves}{per_cu}"
 
 
 class OracleFull:
@@ -1159,7 +1161,8 @@ def regression_summary(path: str) -> None:
 PROFILE_WAVES = os.path.join(ROOT, "profiles", "two_waves_vs_four_waves.md")
 # (B, H_Q, H_KV, L_K), all planned unsplit with one V slice and one workgroup reading each key: 192-256
 # workgroups (one per CU), 264-320 (the two-wave rule's upper range), 384-576 with 2-8 KV heads (past it,
-# four waves) and pure MQA at 384-768 (two waves over chunks of >= 1024 keys, four over 512)
+# four waves, or two held to one workgroup per CU over 2-4 full rounds of chunks of >= 2048 keys) and pure
+# MQA at 384-768 (two waves over chunks of >= 1024 keys, four over 512)
 WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8, 1, 4096),
                 (33, 64, 8, 1024), (36, 64, 8, 1024), (40, 64, 8, 512), (39, 64, 8, 2048), (40, 64, 8, 2048),
                 (300, 8, 1, 512), (300, 8, 1, 1024), (300, 16, 1, 2048), (80, 32, 4, 2048), (80, 64, 4, 1024),
@@ -1167,7 +1170,8 @@ WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8
                 (48, 64, 8, 1024), (56, 64, 8, 1024), (64, 64, 8, 1024), (72, 64, 8, 1024), (192, 16, 2, 1024),
                 (96, 32, 4, 4096),
                 (384, 8, 1, 1024), (448, 8, 1, 1024), (512, 16, 1, 4096), (640, 8, 1, 1024), (768, 32, 1, 2048),
-                (640, 8, 1, 512))
+                (640, 8, 1, 512), (60, 64, 8, 2048), (64, 64, 8, 4096), (96, 64, 8, 2048), (128, 32, 4, 8192),
+                (128, 64, 8, 4096), (128, 64, 8, 2048))
 
 
 def wave_forms(da, plan, H_KV):
@@ -1175,8 +1179,10 @@ def wave_forms(da, plan, H_KV):
     itself: four waves fetch straight into LDS with one workgroup per CU and
     through registers into LDS where CUs hold more (chunks of >= 512 keys);
     two waves fetch through registers, K straight into the operand layout
-    where key rows hold one KV head and each CU holds one workgroup."""
+    where key rows hold one KV head and each CU holds one workgroup.  The
+    form that is not the plan lets CUs hold several workgroups at once."""
     other = da.DaPlan.from_buffer_copy(plan)
+    other.wg_per_cu = 0  # the other form lets CUs hold several workgroups
     lone = plan.grid <= plan.num_cus
     if plan.group_waves == 2:
         other.group_waves, other.kv_fetch = 4, 2 if lone else 1
@@ -1213,6 +1219,7 @@ def waves_sweep_run(args, da, torch, np) -> None:
         iqr = lambda x: [round(t, 3) for t in np.percentile(x.times, [25, 75])]
         row = {"B": B, "H_Q": H_Q, "H_KV": H_KV, "L_K": L, "grid": plan.grid, "cus": plan.num_cus,
                "planned_waves": plan.group_waves, "two_fetch": two.kv_fetch, "four_fetch": four.kv_fetch,
+               "two_per_cu": two.wg_per_cu,
                "two_us": round(vs[0].median, 3), "two_iqr": iqr(vs[0]),
                "four_us": round(vs[1].median, 3), "four_iqr": iqr(vs[1]),
                "two_over_four": round(vs[0].median / vs[1].median, 4)}
@@ -1234,7 +1241,7 @@ def waves_sweep_summary(path: str) -> None:
     d = json.load(open(path))
     rows = d["rows"]
     fetch = {0: "operand layout", 1: "registers to LDS", 2: "direct to LDS"}
-    lines = ["# Two waves per workgroup against four, one-split launches of 192-576 workgroups", "",
+    lines = ["# Two waves per workgroup against four, one-split launches of 192-1024 workgroups", "",
              "Each shape launched with the planner's wave count and with the other one (same split, tile and merge; "
              "the fetch path each wave count takes there), every output checked against the oracle on the first "
              f"and last sequence ({d['validated']} launches validated, {len(d['invalid'])} invalid), then timed as "
@@ -1246,8 +1253,9 @@ def waves_sweep_summary(path: str) -> None:
              "two / four |", "|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
         ti, fi = r["two_iqr"], r["four_iqr"]
+        held = ", one workgroup per CU" if r.get("two_per_cu") else ""
         lines.append(f"| {r['B']} | {r['H_Q']} | {r['H_KV']} | {r['L_K']} | {r['grid']} / {r['cus']} | "
-                     f"{r['planned_waves']} | {r['two_us']} ({ti[0]}-{ti[1]}, {fetch[r['two_fetch']]}) | "
+                     f"{r['planned_waves']} | {r['two_us']} ({ti[0]}-{ti[1]}, {fetch[r['two_fetch']]}{held}) | "
                      f"{r['four_us']} ({fi[0]}-{fi[1]}, {fetch[r['four_fetch']]}) | {r['two_over_four']:.3f} |")
     lines += [""]
     for name, lo, hi, mqa in (("up to one workgroup per CU", 0, 1.0, None),

@@ -143,6 +143,14 @@ typedef struct da_plan {
                              at most DA_ARRIVAL_BYTES / DA_ARRIVAL_STRIDE tiles).  Both give the same bits.  0 when
                              num_splits == 1.  The policies pick the merge their cost model
                              prices lower. */
+  int32_t wg_per_cu;      /* 0: each CU holds as many of the launch's workgroups at once as its LDS
+                             and registers allow; 1: one at a time (the launch asks for more than
+                             half of a CU's LDS), so that a grid of a few times the CU count runs
+                             in rounds of one workgroup per CU.  The policies set 1 on two-wave
+                             plans of 2-4 such rounds over chunks of >= 2048 keys (4096 for four
+                             rounds) with H_KV >= 2, where it keeps the chip's loads in flight at
+                             the one-workgroup-per-CU level.  It changes where workgroups run,
+                             never the result. */
 } da_plan;
 
 /* Choose num_splits and pack_gqa (paper Section 4: a sequence-aware split

@@ -60,6 +60,7 @@ class DaPlan(ctypes.Structure):
         ("kv_nontemporal", ctypes.c_int32),
         ("v_slices", ctypes.c_int32),
         ("combine", ctypes.c_int32),
+        ("wg_per_cu", ctypes.c_int32),
     ]
 
     def as_dict(self) -> dict:

@@ -1298,7 +1298,10 @@ int launch_partial(const Params& prm, const da_plan& pl, hipStream_t stream) {
   int cus = 0, is950 = 0, lds = 0;
   int rc = query_device(&cus, &is950, &lds);
   if (rc) return rc;
-  const int smem = smem_bytes(W, NT, FETCH);
+  int smem = smem_bytes(W, NT, FETCH);
+  // one workgroup per CU at a time: ask for more than half of a CU's LDS
+  // (a workgroup may use all of it, so the request still fits)
+  if (pl.wg_per_cu == 1 && smem <= lds / 2) smem = lds / 2 + 1024 <= lds ? lds / 2 + 1024 : lds;
   if (smem > lds) return da::fail(DA_ERR_UNSUPPORTED, "workgroup needs %d bytes of LDS, device allows %d", smem, lds);
   void* args[] = {const_cast<Params*>(&prm)};
   hipError_t e = hipLaunchKernel(fn, dim3(pl.grid), dim3(64 * W), args, smem, stream);
@@ -1361,7 +1364,8 @@ int check_plan(const da_plan* pl, int B, int H_Q, int H_KV) {
       (int64_t)pl->grid != da::launch_grid((int64_t)pl->tiles * pl->num_splits, pl->v_slices) ||
       !da::group_waves_valid(*pl) || pl->kv_fetch < 0 || pl->kv_fetch > 2 || pl->kv_nontemporal < 0 ||
       pl->kv_nontemporal > 1 || pl->num_cus < 1 || !da::v_slices_valid(H_Q, H_KV, *pl) || pl->combine < 0 ||
-      pl->combine > 1 || (pl->combine == 1 && (pl->num_splits < 2 || pl->tiles > da::kMaxArrivalTiles)))
+      pl->combine > 1 || (pl->combine == 1 && (pl->num_splits < 2 || pl->tiles > da::kMaxArrivalTiles)) ||
+      pl->wg_per_cu < 0 || pl->wg_per_cu > 1)
     return da::fail(DA_ERR_ARG, "plan does not describe a launch of B=%d H_Q=%d H_KV=%d", B, H_Q, H_KV);
   return DA_OK;
 }

@@ -231,6 +231,22 @@ int group_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int
              : 4;
 }
 
+bool round_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int vs, int combine) {
+  // Past the two-wave range of group_waves a four-wave launch keeps two or
+  // more workgroups on each CU, 16-32 MiB of loads in flight.  Two-wave
+  // workgroups held to one per CU keep 8 MiB in flight and run the grid in
+  // rounds; each round start costs a ramp, so the rounds must be few, full
+  // and long.  Measured on MI355X against the four-wave launch, in one
+  // process per comparison (2 KV heads and more): 480-512 workgroups
+  // (two rounds) 0.966-1.0x, 768 (three) 0.966-0.99x, 1024 (four) over
+  // chunks of 4096-8192 keys 0.967-0.987x but 1.009-1.014x over 2048, and
+  // 1.02-1.04x at 576 (a quarter-full third round).  Pure MQA keeps its own
+  // two-wave range (group_waves), which shares CUs.
+  if (vs != 1 || readers != 1 || combine != 0 || H_KV < 2 || 4 * grid <= 5 * (int64_t)cus) return false;
+  const int64_t rounds = (grid + cus - 1) / cus;
+  return rounds >= 2 && rounds <= 4 && 8 * (rounds * cus - grid) <= cus && chunk >= (rounds == 4 ? 4096 : 2048);
+}
+
 int kv_fetch(int64_t grid, int cus, int64_t tiles_per_wave) {
   // A workgroup with a CU to itself streams fastest with K and V loaded
   // straight into LDS, two tiles in flight per wave (144 KB of LDS).  When
@@ -249,6 +265,7 @@ void four_waves(da_plan* pl, int L_K_max) {
   if (pl->group_waves != 2) return;
   const int64_t chunk = ((int64_t)L_K_max + pl->num_splits - 1) / pl->num_splits;
   pl->group_waves = 4;
+  pl->wg_per_cu = 0;
   pl->kv_fetch = kv_fetch(pl->grid, pl->num_cus, ((chunk + 3) / 4 + 31) / 32);
   // and the merge a four-wave plan takes (these entry points plan with policy MI355X)
   if (pl->num_splits > 1)
@@ -404,7 +421,10 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
   {
     const int64_t chunk = ((int64_t)L_K_max + s - 1) / s;
     int waves = group_waves(out->grid, cus, chunk, H_KV, readers, vs, comb);
-    if (waves == 4 && comb == 1 && !from_table && group_waves(out->grid, cus, chunk, H_KV, readers, vs, 0) == 2) {
+    bool rounds = waves == 4 && round_waves(out->grid, cus, chunk, H_KV, readers, vs, comb);
+    const bool two_c0 = group_waves(out->grid, cus, chunk, H_KV, readers, vs, 0) == 2;
+    const bool rounds_c0 = !two_c0 && round_waves(out->grid, cus, chunk, H_KV, readers, vs, 0);
+    if (waves == 4 && !rounds && comb == 1 && !from_table && (two_c0 || rounds_c0)) {
       // Two waves merge by a second launch.  They take it where the share of
       // the split launch they save (kTwoWaveGain) is modelled to outweigh
       // what the second launch adds over the merge inside the launch:
@@ -419,9 +439,12 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
         comb = 0;
         out->combine = 0;
         waves = 2;
+        rounds = rounds_c0;
       }
     }
+    if (rounds) waves = 2;
     out->group_waves = waves;
+    out->wg_per_cu = rounds ? 1 : 0;
     // two waves: K through registers, straight into the operand layout
     // where key rows hold one KV head and each CU holds one workgroup
     // (contiguous 256-byte rows, measured 1-3% faster there) and through LDS

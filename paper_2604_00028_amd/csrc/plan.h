@@ -104,6 +104,11 @@ inline int64_t launch_grid(int64_t chunks, int vs) {
 // merge `combine`: 2 or 4.
 int group_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int vs, int combine);
 
+// Whether a launch of `grid` workgroups that group_waves gives four waves
+// runs faster as two-wave workgroups held to one per CU (da_plan.wg_per_cu),
+// in 2-4 rounds over the CUs.
+bool round_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int vs, int combine);
+
 // A plan made inside an entry point whose sequence lengths are read on the
 // device (cu_seqlens_k, paged seq_lens): the sequences may be far shorter
 // than L_K_max, so a two-wave plan, which pays only where every workgroup

@@ -48,7 +48,7 @@ def assert_parity(gpu_out: torch.Tensor, ref: np.ndarray, what: str = "") -> Non
 def fit_waves(p):
     """Keep an edited plan's wave count valid: two waves only with K/V through
     registers (kv_fetch 0 or 1), one V slice and the merge in a second
-    launch; four otherwise."""
+    launch; four otherwise (sharing CUs, as four-wave plans do)."""
     if p.group_waves == 2 and (p.kv_fetch == 2 or p.v_slices != 1 or p.combine != 0):
-        p.group_waves = 4
+        p.group_waves, p.wg_per_cu = 4, 0
     return p

@@ -394,6 +394,19 @@ def test_two_waves_where_long_chunks_fill_the_chip():
         assert (p.num_splits, p.grid, p.group_waves) == (1, B, waves), (B, L, p.as_dict())
         assert p.kv_fetch == (1 if waves == 2 else p.kv_fetch)
     assert plan(192, 16, 2, 1024).group_waves == 4                # 2 KV heads: 384 on 256
+    # two waves held to one workgroup per CU, in 2-4 nearly full rounds of long chunks (2+ KV heads)
+    for shape, held in (((64, 64, 8, 4096), 1), ((60, 64, 8, 2048), 1), ((96, 64, 8, 2048), 1),
+                        ((128, 64, 8, 4096), 1), ((64, 64, 8, 1024), 0), ((72, 64, 8, 2048), 0),
+                        ((128, 64, 8, 2048), 0), ((160, 64, 8, 4096), 0)):
+        p = plan(*shape)
+        assert p.num_splits == 1 and (p.group_waves, p.wg_per_cu) == ((2, 1) if held else (4, 0)), (shape, p.as_dict())
+        assert not held or p.kv_fetch == 1
+    p = plan(512, 8, 1, 4096)                                     # pure MQA: two waves sharing CUs
+    assert (p.group_waves, p.wg_per_cu) == (2, 0), p.as_dict()
+    p = da.da_make_plan(64, 64, 8, 4096, num_splits=1, num_cus=256, cu_margin=32)   # 512 on 224 CUs: a
+    assert (p.group_waves, p.wg_per_cu) == (4, 0), p.as_dict()                     # third round, 2/7 full
+    p = da.da_make_plan(56, 64, 8, 4096, num_splits=1, num_cus=256, cu_margin=32)   # 448 on 224: two rounds
+    assert (p.group_waves, p.wg_per_cu, p.kv_fetch) == (2, 1, 1), p.as_dict()
     # two 16-head workgroups read each key of a group of 32
     p = da.da_make_plan(32, 128, 4, 8192, num_splits=1, pack_gqa=1, num_cus=256)
     assert p.heads_per_tile == 16 and p.group_waves == 4

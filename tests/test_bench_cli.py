@@ -116,9 +116,11 @@ def test_wave_forms_pair_each_plan_with_its_other_wave_count():
         assert plan.num_splits == 1 and plan.v_slices == 1 and plan.heads_per_tile == H_Q // H_KV
         two, four = bench.wave_forms(da, plan, H_KV)
         assert (two.group_waves, four.group_waves) == (2, 4)
+        assert four.wg_per_cu == 0 and (two is plan or two.wg_per_cu == 0)
         assert plan.group_waves == 2 and two is plan or plan.group_waves == 4 and four is plan
         lone = plan.grid <= 256
         assert two.combine == 0 and two.kv_fetch == (0 if H_KV == 1 and lone else 1)
+        assert plan.wg_per_cu == 0 or (plan.group_waves == 2 and plan.grid > 320)
         assert four.kv_fetch == (2 if lone else 1)
         for p in (two, four):
             assert (p.num_splits, p.grid, p.heads_per_tile, p.v_slices) == (1, plan.grid, plan.heads_per_tile, 1)

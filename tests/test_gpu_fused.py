@@ -73,8 +73,10 @@ def test_fused_matches_oracle_and_two_launch(shape):
     for s, pack in [(2, 1), (3, 1), (4, 1), (8, 1), (16, 1), (64, 1), (3, 0), (4, 2), (6, 2)]:
         base = da.da_make_plan(B, H_Q, H_KV, L, num_splits=s, pack_gqa=pack)
         say(f"fused {shape.name} s={s} pack={pack} {base.as_dict()}")
-        two = run_plan(q, k, v, cu, L, edited(base, combine=0))
-        one = run_plan(q, k, v, cu, L, edited(base, combine=1))
+        # both merges on the launch the in-launch merge runs on (four waves)
+        fused = edited(base, combine=1)
+        two = run_plan(q, k, v, cu, L, edited(fused, combine=0))
+        one = run_plan(q, k, v, cu, L, fused)
         check(*one, O, lse, f"fused {shape.name} s={s} pack={pack}")
         assert same_bits(one, two), f"fused vs two-launch {shape.name} s={s} pack={pack}"
 
@@ -166,9 +168,10 @@ def test_fused_empty_and_short_sequences():
     for s in (2, 8, 64):
         base = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, num_splits=s, pack_gqa=1)
         say(f"fused short/empty s={s}")
-        got = run_plan(q, k, v, cu, sh.L_K, edited(base, combine=1))
+        fused = edited(base, combine=1)
+        got = run_plan(q, k, v, cu, sh.L_K, fused)
         check(*got, O, lse, f"fused short/empty s={s}")
-        assert same_bits(got, run_plan(q, k, v, cu, sh.L_K, edited(base, combine=0)))
+        assert same_bits(got, run_plan(q, k, v, cu, sh.L_K, edited(fused, combine=0)))
         assert torch.all(got[0][0] == 0) and torch.all(got[0][5] == 0)
         assert torch.all(torch.isneginf(got[1][0])) and torch.all(torch.isneginf(got[1][5]))
 
@@ -185,9 +188,16 @@ def test_fused_highload_sampled_sequences():
     for s in (2, 4, 16):
         base = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, num_splits=s, pack_gqa=1)
         say(f"fused highload s={s} {base.as_dict()}")
-        one = run_plan(q, k, v, cu, sh.L_K, edited(base, combine=1))
+        fused = edited(base, combine=1)
+        one = run_plan(q, k, v, cu, sh.L_K, fused)
         assert_parity(one[0][picks], O, f"fused highload s={s}")
         assert np.max(np.abs(one[1].cpu().numpy()[picks] - lse)) <= LSE_TOL
         assert torch.isfinite(one[0].float()).all()
-        two = run_plan(q, k, v, cu, sh.L_K, edited(base, combine=0))
+        two = run_plan(q, k, v, cu, sh.L_K, edited(fused, combine=0))
         assert same_bits(one, two)
+        if base.group_waves == 2:
+            # the planner's own launch (two waves, at two splits held to one workgroup per CU)
+            say(f"highload planned s={s} {base.as_dict()}")
+            own = run_plan(q, k, v, cu, sh.L_K, base)
+            assert_parity(own[0][picks], O, f"highload planned s={s}")
+            assert np.max(np.abs(own[1].cpu().numpy()[picks] - lse)) <= LSE_TOL

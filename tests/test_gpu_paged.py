@@ -220,7 +220,8 @@ def test_highload_paged_full_size():
         plan = da.da_make_plan(sh.B, sh.H_Q, sh.H_KV, sh.L_K, num_splits=s, pack_gqa=1)
         four = da.DaPlan.from_buffer_copy(plan)
         if four.group_waves == 2:
-            four.group_waves, four.kv_fetch = 4, 2     # one workgroup per CU: K/V straight into LDS
+            # K/V straight into LDS with one workgroup per CU, through registers where CUs hold more
+            four.group_waves, four.kv_fetch, four.wg_per_cu = 4, 2 if four.grid <= four.num_cus else 1, 0
         for p in (plan, four):
             say(f"highload paged vs contiguous s={s} {p.as_dict()}")
             a = da.da_decode_attn_planned(q, k, v, p, None, L_K_max=sh.L_K)

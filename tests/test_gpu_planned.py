@@ -78,6 +78,12 @@ def test_plans_of_every_kind(B, H_Q, H_KV, L, varlen):
                     assert same_bits(got, first[key]), (key, p.as_dict())
                 else:
                     first[key] = got
+                if hint == 0:
+                    # one workgroup per CU at a time: where workgroups run, not what they compute
+                    p.wg_per_cu = 1
+                    say(f"planned, one workgroup per CU {p.as_dict()}")
+                    assert same_bits(planned(q, k, v, cu, L, p), got), p.as_dict()
+                    p.wg_per_cu = 0
                 if p.num_splits > 1 and p.group_waves == 4:
                     # the other merge (a second launch, or inside the split launch): the same bits
                     p.combine = 1 - p.combine

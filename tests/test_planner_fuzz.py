@@ -62,10 +62,18 @@ def test_every_plan_is_a_launch_the_library_accepts(shape, policy, s, pack, marg
     assert plan.num_cus == cus - margin and plan.kv_fetch in (0, 1, 2) and plan.kv_nontemporal in (0, 1)
     # two waves only for a launch of 3/4 to 5/4 as many workgroups as CUs, long chunks, keys read once
     assert plan.group_waves in (2, 4)
-    if plan.group_waves == 2:
+    C, chunk = cus - margin, -(-L // plan.num_splits)
+    assert plan.wg_per_cu in (0, 1) and (plan.wg_per_cu == 0 or plan.group_waves == 2)
+    if plan.group_waves == 2 and plan.wg_per_cu == 1:
+        # two waves held to one workgroup per CU: 2-4 nearly full rounds of long chunks, 2+ KV heads
+        rounds = -(-plan.grid // C)
+        assert 4 * plan.grid > 5 * C and 2 <= rounds <= 4 and 8 * (rounds * C - plan.grid) <= C and H_KV >= 2
+        assert chunk >= (4096 if rounds == 4 else 2048) and plan.kv_fetch == 1
+        assert plan.v_slices == 1 and plan.combine == 0 and plan.heads_per_tile == g
+    elif plan.group_waves == 2:
         assert plan.kv_fetch in (0, 1) and plan.v_slices == 1 and plan.combine == 0
-        top = 3 * (cus - margin) if H_KV == 1 and -(-L // plan.num_splits) >= 1024 else 5 * (cus - margin) // 4
-        assert 4 * plan.grid >= 3 * (cus - margin) and plan.grid <= top
+        top = 3 * C if H_KV == 1 and chunk >= 1024 else 5 * C // 4
+        assert 4 * plan.grid >= 3 * C and plan.grid <= top
         assert plan.kv_fetch == (0 if H_KV == 1 and plan.grid <= cus - margin else 1)
         assert -(-L // plan.num_splits) >= 512 and plan.heads_per_tile == g
     if g > 1 and plan.pack_gqa == 1:

@@ -19,7 +19,7 @@ SWEEPS = {"warm": os.path.join(ROOT, "profiles", "calibration_warm.json"),
           "streamed": os.path.join(ROOT, "profiles", "calibration_streamed.json")}
 POLICY = {"warm": (da.POLICY_TABLE, da.POLICY_MI355X), "streamed": (da.POLICY_TABLE_STREAMED, da.POLICY_STREAMED)}
 FIELDS = ("num_splits", "pack_gqa", "heads_per_tile", "tiles", "grid", "num_cus", "group_waves", "kv_fetch",
-          "kv_nontemporal", "v_slices", "combine")
+          "kv_nontemporal", "v_slices", "combine", "wg_per_cu")
 
 
 def fastest(shape):
@@ -75,7 +75,12 @@ def test_swept_shapes_are_planned_from_the_table(which):
         # merge runs in the launch; the sweep timed four waves
         top = 768 if H_KV == 1 and chunk >= 1024 else 320
         two = vs == 1 and readers == 1 and comb == 0 and 192 <= p.grid <= top and chunk >= 512
-        assert p.group_waves == (2 if two else 4), sh
+        # or two waves held to one workgroup per CU over 2-4 nearly full rounds of long chunks
+        rounds = -(-p.grid // 256)
+        held = (not two and vs == 1 and readers == 1 and comb == 0 and H_KV >= 2 and p.grid > 320 and
+                2 <= rounds <= 4 and 8 * (rounds * 256 - p.grid) <= 256 and chunk >= (4096 if rounds == 4 else 2048))
+        two = two or held
+        assert p.group_waves == (2 if two else 4) and p.wg_per_cu == int(held), sh
         fetch = (0 if H_KV == 1 and p.grid <= 256 else 1) if two else (2 if p.grid <= 256 else (1 if tpw >= 2 else 0))
         assert p.kv_fetch == fetch, sh
         nt = readers == 1 if which == "streamed" else (readers == 1 and B * L * H_KV * 512 > 288 << 20)
