@@ -425,7 +425,8 @@ int plan(int B, int H_Q, int H_KV, int L_K_max, int d, int num_splits, int pack_
     const bool two_c0 = group_waves(out->grid, cus, chunk, H_KV, readers, vs, 0) == 2;
     const bool rounds_c0 = !two_c0 && round_waves(out->grid, cus, chunk, H_KV, readers, vs, 0);
     if (waves == 4 && !rounds && comb == 1 && !from_table && (two_c0 || rounds_c0)) {
-      // Two waves merge by a second launch.  They take it where the share of
+      // Two waves (sharing CUs, or held to one workgroup per CU in rounds)
+      // merge by a second launch.  They take it where the share of
       // the split launch they save (kTwoWaveGain) is modelled to outweigh
       // what the second launch adds over the merge inside the launch:
       // measured at 1 GiB, 2 splits 84.3 -> 83.3 us and at 256 MiB, 4 splits

@@ -113,7 +113,7 @@ bool round_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, in
 // device (cu_seqlens_k, paged seq_lens): the sequences may be far shorter
 // than L_K_max, so a two-wave plan, which pays only where every workgroup
 // streams a long chunk, becomes the four-wave launch of the same grid (with
-// the fetch path and merge policy MI355X gives four waves).
+// the fetch path and merge policy MI355X gives four waves, sharing CUs).
 void four_waves(da_plan* pl, int L_K_max);
 
 // Time factor of a two-wave launch against the four-wave one where the
