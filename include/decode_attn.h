@@ -257,7 +257,7 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
  * passed explicitly).  The plan comes from da_make_plan or da_choose_splits
  * for this B, H_Q and H_KV, with any policy and cu_margin, and may be edited
  * within its valid values. The launch uses exactly its split count, head
- * tiles, K/V fetch path and cache hint.  Other arguments and the workspace
+ * tiles, K/V fetch path, cache hint and workgroups per CU.  Other arguments and the workspace
  * need (for plan->num_splits) as in da_decode_attn.  Errors as there, plus
  * DA_ERR_NULL (plan NULL) and DA_ERR_ARG (the plan does not describe a launch
  * of this shape: num_splits outside 1..64, a heads_per_tile its pack_gqa
@@ -266,8 +266,9 @@ int da_decode_attn(const void* q, const void* k, const void* v, const int32_t* c
  * group_waves other than 4 or 2 (2 only with kv_fetch 0 or 1, v_slices 1 and
  * combine 0), kv_fetch outside 0..2, kv_nontemporal outside 0..1,
  * num_cus < 1, v_slices other than 1, 2 or 4, or v_slices > 1 with a
- * kv_fetch other than 2, with pack_gqa 2, or unpacked with H_Q != H_KV),
- * all before any device access. */
+ * kv_fetch other than 2, with pack_gqa 2, or unpacked with H_Q != H_KV,
+ * combine outside 0..1 or 1 with one split, wg_per_cu outside 0..1), all
+ * before any device access. */
 int da_decode_attn_planned(const void* q, const void* k, const void* v, const int32_t* cu_seqlens_k,
                            void* out, float* lse_out, int B, int H_Q, int H_KV, int L_K_max, int d,
                            float softmax_scale, const da_plan* plan, void* workspace,
