@@ -1162,7 +1162,8 @@ PROFILE_WAVES = os.path.join(ROOT, "profiles", "two_waves_vs_four_waves.md")
 # (B, H_Q, H_KV, L_K), all planned unsplit with one V slice and one workgroup reading each key: 192-256
 # workgroups (one per CU), 264-320 (the two-wave rule's upper range), 384-576 with 2-8 KV heads (past it,
 # four waves, or two held to one workgroup per CU over 2-4 full rounds of chunks of >= 2048 keys) and pure
-# MQA at 384-768 (two waves over chunks of >= 1024 keys, four over 512)
+# MQA at 384-1152 (two waves up to 768 over chunks of >= 1024 keys and up to 1024 over >= 2048, four over 512
+# and past 1024)
 WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8, 1, 4096),
                 (33, 64, 8, 1024), (36, 64, 8, 1024), (40, 64, 8, 512), (39, 64, 8, 2048), (40, 64, 8, 2048),
                 (300, 8, 1, 512), (300, 8, 1, 1024), (300, 16, 1, 2048), (80, 32, 4, 2048), (80, 64, 4, 1024),
@@ -1171,7 +1172,7 @@ WAVES_SHAPES = ((24, 64, 8, 8192), (28, 64, 8, 2048), (32, 64, 8, 8192), (256, 8
                 (96, 32, 4, 4096),
                 (384, 8, 1, 1024), (448, 8, 1, 1024), (512, 16, 1, 4096), (640, 8, 1, 1024), (768, 32, 1, 2048),
                 (640, 8, 1, 512), (60, 64, 8, 2048), (64, 64, 8, 4096), (96, 64, 8, 2048), (128, 32, 4, 8192),
-                (128, 64, 8, 4096), (128, 64, 8, 2048))
+                (128, 64, 8, 4096), (128, 64, 8, 2048), (1024, 16, 1, 2048), (1152, 8, 1, 4096))
 
 
 def wave_forms(da, plan, H_KV):

@@ -112,7 +112,8 @@ typedef struct da_plan {
   int32_t group_waves;    /* wave64s per workgroup, each taking a contiguous part of the chunk (with 2
                              waves and H_KV <= 4, every other 32-key tile of it): 4, or 2
                              where the launch has between 3/4 and 5/4 as many workgroups as CUs (3
-                             times as many for H_KV = 1 with chunks of >= 1024 keys), one
+                             times as many for H_KV = 1 with chunks of >= 1024 keys, 4 times with
+                             >= 2048), one
                              workgroup reads each key and chunks hold >= 512 keys (fewer loads
                              in flight read HBM faster there); with 2, kv_fetch is 0 or 1, v_slices
                              1 and combine 0.  Entry points that plan for themselves and read the

@@ -220,12 +220,16 @@ int group_waves(int64_t grid, int cus, int64_t chunk, int H_KV, int readers, int
   // heads (0.97-1.0x with one), 576 slower (1.02-1.03x).  Pure MQA (key
   // rows of one head, whose two waves take alternate tiles) keeps the gain
   // further: at 384-768 workgroups with chunks of 1024-8192 keys 0.94-1.0x
-  // (2.6% on average over 21 shapes), while at 512-key chunks (0.997-1.026x)
-  // and at 1024-1536 workgroups (0.92-1.09x) it is no longer steady.  The
+  // (2.6% on average over 21 shapes), at 800-1024 with chunks of 2048-8192
+  // keys 0.92-1.04x (2.2% on average over 31 shapes), while at 512-key
+  // chunks (0.997-1.026x) and past four workgroups per CU (1.0-1.09x at
+  // 1152-1536) it is no longer steady.  The
   // in-launch merge is sized for four waves, so two-wave plans merge by a
   // second launch.  Eight waves (two per SIMD, with K staged) measured
   // slower at chunks of a few hundred keys.
-  const int64_t top = H_KV == 1 && chunk >= 1024 ? 3 * (int64_t)cus : 5 * (int64_t)cus / 4;
+  const int64_t top = H_KV == 1 && chunk >= 2048   ? 4 * (int64_t)cus
+                      : H_KV == 1 && chunk >= 1024 ? 3 * (int64_t)cus
+                                                   : 5 * (int64_t)cus / 4;
   return vs == 1 && readers == 1 && combine == 0 && grid <= top && 4 * grid >= 3 * (int64_t)cus && chunk >= 512
              ? 2
              : 4;

@@ -388,8 +388,9 @@ def test_two_waves_where_long_chunks_fill_the_chip():
     assert plan(34, 64, 8, 1024, cu_margin=32).group_waves == 2   # 272 workgroups on 224 CUs
     assert plan(36, 64, 8, 1024, cu_margin=32).group_waves == 4   # 288 on 224
     assert plan(48, 64, 8, 1024).group_waves == 4                 # 384 on 256
-    # pure MQA over chunks of >= 1024 keys: up to three workgroups per CU
-    for B, L, waves in ((384, 1024, 2), (768, 2048, 2), (769, 2048, 4), (640, 512, 4), (1024, 2048, 4)):
+    # pure MQA over chunks of >= 1024 keys: up to three workgroups per CU, four over >= 2048
+    for B, L, waves in ((384, 1024, 2), (768, 1024, 2), (769, 1024, 4), (1024, 2048, 2), (1025, 2048, 4),
+                        (640, 512, 4)):
         p = plan(B, 8, 1, L)
         assert (p.num_splits, p.grid, p.group_waves) == (1, B, waves), (B, L, p.as_dict())
         assert p.kv_fetch == (1 if waves == 2 else p.kv_fetch)

@@ -72,7 +72,7 @@ def test_every_plan_is_a_launch_the_library_accepts(shape, policy, s, pack, marg
         assert plan.v_slices == 1 and plan.combine == 0 and plan.heads_per_tile == g
     elif plan.group_waves == 2:
         assert plan.kv_fetch in (0, 1) and plan.v_slices == 1 and plan.combine == 0
-        top = 3 * C if H_KV == 1 and chunk >= 1024 else 5 * C // 4
+        top = (4 * C if chunk >= 2048 else 3 * C if chunk >= 1024 else 5 * C // 4) if H_KV == 1 else 5 * C // 4
         assert 4 * plan.grid >= 3 * C and plan.grid <= top
         assert plan.kv_fetch == (0 if H_KV == 1 and plan.grid <= cus - margin else 1)
         assert -(-L // plan.num_splits) >= 512 and plan.heads_per_tile == g

@@ -73,7 +73,7 @@ def test_swept_shapes_are_planned_from_the_table(which):
         # two waves where the launch has 3/4 to 5/4 as many workgroups as CUs (3 times as many for pure
         # MQA over chunks of >= 1024 keys), one workgroup reads each key, chunks hold >= 512 keys and no
         # merge runs in the launch; the sweep timed four waves
-        top = 768 if H_KV == 1 and chunk >= 1024 else 320
+        top = (1024 if chunk >= 2048 else 768 if chunk >= 1024 else 320) if H_KV == 1 else 320
         two = vs == 1 and readers == 1 and comb == 0 and 192 <= p.grid <= top and chunk >= 512
         # or two waves held to one workgroup per CU over 2-4 nearly full rounds of long chunks
         rounds = -(-p.grid // 256)
